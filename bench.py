@@ -1,0 +1,243 @@
+"""Benchmark of the speculative-decoding verify step on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload full_depth_bf16]
+
+A step is one molt_verify_step call: the whole hot path (embedding, 48 decoder layers
+with paged attention and top-8 routed MoE, final norm, LM head, fused accept/resample
+sampler) over one batch of B = 128 sequences with k = 4 drafts at context 8192, vocab
+151936, bf16, random-init weights of that shape and seeded synthetic inputs, all
+resident in HBM before the timed region. Drafts follow the method's serving setup:
+q_i = softmax(target row i-1 + N(0, 0.5^2)) and x_i ~ q_i, built with untimed passes.
+
+Prints one JSON line: verified tokens/s (= B*(1+k) positions scored per second), the
+roofline of the dominant kernel (paged attention, HBM-bound; its average launch time
+measured with HIP events on the library's stream during the timed region), and the
+CPU oracle timed on a bounded sample of the same workload (cpu_baseline).
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+import torch
+
+import workloads
+
+HBM_PEAK_GBS = 8000.0
+BF16_PEAK_TFLOPS = 2500.0
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def attention_bytes(w, ctx):
+    """Algorithmic bytes of one attention launch: every cached K and V vector of every
+    (sequence, kv head) read once, q read once, the output written once."""
+    e = 2 if w.dtype == "bf16" else 4
+    kv = int(np.sum(ctx.astype(np.int64) + w.k + 1)) * w.n_kv_heads * w.head_dim * e * 2
+    T = w.batch * (w.k + 1)
+    qo = 2 * T * w.n_q_heads * w.head_dim * e
+    return kv + qo
+
+
+def build(w, seed, molt):
+    dev = "cuda"
+    layout = workloads.make_kv_layout(w, seed)
+    layers, kcs, vcs = [], [], []
+    for l in range(w.n_layers):
+        layers.append(workloads.make_layer_weights(w, seed, l, device=dev))
+        kc, vc = workloads.make_kv_cache(w, layout, seed, l, device=dev)
+        kcs.append(kc)
+        vcs.append(vc)
+        if l % 8 == 0 or l == w.n_layers - 1:
+            log(f"[bench] layer {l + 1}/{w.n_layers} generated, "
+                f"{torch.cuda.memory_allocated() / 2**30:.1f} GiB resident")
+    head = workloads.make_head_weights(w, seed, device=dev)
+    model = molt.Model(layers, head, n_q_heads=w.n_q_heads, n_kv_heads=w.n_kv_heads,
+                       head_dim=w.head_dim, top_k=w.top_k, rms_eps=w.rms_eps, rope_theta=w.rope_theta)
+    kv = molt.KVCache(kcs, vcs, torch.from_numpy(layout.block_tables).to(dev),
+                      torch.from_numpy(layout.context_lens).to(dev))
+    return layout, layers, head, model, kv
+
+
+def make_drafts(w, seed, molt, model, kv, ws):
+    """Autoregressive drafts: q_i = softmax(target row i-1 + N(0, sigma^2)), x_i ~ q_i.
+    Row i-1 only depends on tokens 0..i-1 (causal), so pass i fixes draft i."""
+    dev = "cuda"
+    B, k, V = w.batch, w.k, w.vocab
+    g = np.random.Generator(np.random.Philox(workloads._seed(seed, w.name, "last")))
+    tokens = torch.from_numpy(g.integers(0, V, (B, k + 1)).astype(np.int32)).to(dev)
+    q = torch.empty(B, k, V, dtype=torch.float32, device=dev)
+    u = workloads.make_uniforms(B, k, seed, device=dev)
+    gen = workloads.rng(seed, w.name, "draft-sample", device=dev)
+    for i in range(1, k + 1):
+        out = molt.verify_step(model, kv, tokens, u, None, workspace=ws)
+        row = out["logits"][:, i - 1]
+        noise = torch.randn(B, V, generator=gen, device=dev) * w.draft_sigma
+        qi = torch.softmax(row + noise, dim=-1)
+        q[:, i - 1] = qi
+        tokens[:, i] = torch.multinomial(qi, 1, generator=gen).squeeze(1).int()
+        log(f"[bench] draft position {i}/{k} built")
+    return tokens, q, u
+
+
+def cpu_baseline(w, layout, layers, head, kv, tokens, q, u, sample_layers=2):
+    """Oracle on a bounded sample: sequence 0 (1+k positions) through `sample_layers` of
+    the layers, then the LM head and the sampler; the per-layer time is scaled to all
+    layers. Returns (positions/s, seconds measured, description)."""
+    import oracle.model as omodel
+    from oracle import sampler as osamp
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        threads = os.cpu_count() or 1
+
+    def host(t):
+        t = t.detach().cpu()
+        return t.view(torch.int16).numpy().view(np.uint16) if t.dtype == torch.bfloat16 else t.numpy()
+
+    cfg = dict(dtype=w.dtype, expert_dtype=w.expert_dtype, n_layers=sample_layers,
+               n_q_heads=w.n_q_heads, n_kv_heads=w.n_kv_heads, head_dim=w.head_dim, top_k=w.top_k,
+               rms_eps=w.rms_eps, rope_theta=w.rope_theta, block_size=16)
+    b = 0
+    blocks = layout.block_tables[b][layout.block_tables[b] >= 0]
+    lw = [{k_: (None if v is None else host(v)) for k_, v in layers[l].items()} for l in range(sample_layers)]
+    caches = []
+    for l in range(sample_layers):
+        idx = torch.from_numpy(blocks).long().cuda()
+        kc = omodel.widen_cache(host(kv.k_caches[l][idx]), w.dtype)
+        vc = omodel.widen_cache(host(kv.v_caches[l][idx]), w.dtype)
+        caches.append((kc, vc))
+    bt = np.arange(len(blocks))[None, :]
+    ctx = layout.context_lens[b:b + 1]
+    hh = {k_: host(v) for k_, v in head.items()}
+    toks = host(tokens)[b:b + 1]
+    t0 = time.perf_counter()
+    x = omodel.embed(toks, hh, cfg)
+    x, _ = omodel.decoder_forward(x, lambda l: lw[l], caches, bt, ctx, w.k, cfg)
+    t1 = time.perf_counter()
+    logits = omodel.lm_logits(x, hh, cfg).reshape(1, w.k + 1, -1)
+    osamp.spec_accept(logits, toks[:, 1:], host(u)[b:b + 1], host(q)[b:b + 1])
+    t2 = time.perf_counter()
+    per_step = (t1 - t0) * (w.n_layers / sample_layers) + (t2 - t1)
+    value = (w.k + 1) / per_step
+    desc = (f"1 of {w.batch} sequences ({w.k + 1} positions) through {sample_layers} of {w.n_layers} "
+            f"layers ({t1 - t0:.2f} s, scaled x{w.n_layers / sample_layers:g}) + LM head + sampler "
+            f"({t2 - t1:.2f} s); float64 NumPy oracle")
+    return value, t2 - t0, threads, desc
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="full_depth_bf16", choices=sorted(workloads.WORKLOADS))
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="only run a 1 GiB device-to-device copy (HBM counter calibration)")
+    a = ap.parse_args()
+    if a.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for {a.gpus}): the verify step shards by "
+              "sequence with no communication, so each GPU's share is this single-GPU workload.",
+              file=sys.stderr)
+        sys.exit(2)
+    if a.calibrate_copy:
+        src = torch.empty(2 ** 30, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"calibration": "copy", "bytes_read": 2 ** 30, "bytes_written": 2 ** 30,
+                          "launches": 5}))
+        return
+    import paper_2607_21653_amd as molt
+    molt.load()
+    w = workloads.WORKLOADS[a.workload]
+    if not w.full_model:
+        sys.exit(f"{a.workload} is a single-layer workload; the bench step is the full verify step")
+    t_setup = time.time()
+    layout, layers, head, model, kv = build(w, a.seed, molt)
+    B, k, V = w.batch, w.k, w.vocab
+    ws = torch.empty(molt.verify_step_workspace_size(model, B, k, layout.block_tables.shape[1]),
+                     dtype=torch.uint8, device="cuda")
+    if w.draft == "perturbed":
+        tokens, q, u = make_drafts(w, a.seed, molt, model, kv, ws)
+    else:
+        tokens = torch.from_numpy(workloads.make_step_tokens(w, a.seed)).cuda()
+        q = workloads.make_softmax_q(B, k, V, a.seed, device="cuda")
+        u = workloads.make_uniforms(B, k, a.seed, device="cuda")
+    out = {"tokens": torch.empty(B, k + 1, dtype=torch.int32, device="cuda"),
+           "n_accepted": torch.empty(B, dtype=torch.int32, device="cuda"),
+           "logprobs": torch.empty(B, k + 1, dtype=torch.float32, device="cuda"),
+           "logits": torch.empty(B, k + 1, V, dtype=torch.float32, device="cuda")}
+    log(f"[bench] setup {time.time() - t_setup:.1f} s; warmup {a.warmup} steps")
+    for _ in range(a.warmup):
+        molt.verify_step(model, kv, tokens, u, q, workspace=ws, out=out)
+    torch.cuda.synchronize()
+    log(f"[bench] timing {a.steps} steps")
+    molt.profile_enable(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(a.steps):
+        molt.verify_step(model, kv, tokens, u, q, workspace=ws, out=out)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    molt.profile_enable(False)
+    ms = (t1 - t0) * 1e3 / a.steps
+    groups = {g: molt.profile_read(g) for g in molt._lib.PROF_GROUPS}
+    n_acc = out["n_accepted"].cpu().numpy()
+    positions = B * (k + 1)
+    value = positions / (ms / 1e3)
+    emitted = float((n_acc + 1).sum()) / (ms / 1e3)
+
+    attn_ms, attn_n = groups["attention"]
+    attn_avg = attn_ms / max(attn_n, 1)
+    abytes = attention_bytes(w, layout.context_lens)
+    achieved = abytes / (attn_avg / 1e3) / 1e9
+    lm_ms, lm_n = groups["lm_head"]
+    lm_flops = 2.0 * positions * V * w.d_model
+    per_group = {g: {"avg_ms": (t / n if n else None), "launches": n, "share_of_step":
+                     (t / a.steps / ms if n else None)} for g, (t, n) in groups.items()}
+    res = {
+        "metric": "verified tokens/s per MI355X (verify step) + % HBM/MFMA roofline",
+        "value": round(value, 1),
+        "unit": "verified tokens/s",
+        "n_gpus": 1,
+        "steps": a.steps,
+        "warmup": a.warmup,
+        "ms_per_step": round(ms, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.dtype,
+        "data": "synthetic (seeded random-init weights, KV and drafts; no checkpoint or dataset)",
+        "config": {"workload": w.name, "layers": w.n_layers, "batch": B, "k": k,
+                   "context": int(layout.context_lens.max()), "vocab": V, "d_model": w.d_model,
+                   "heads": f"{w.n_q_heads}q/{w.n_kv_heads}kv x {w.head_dim}",
+                   "experts": f"{w.n_experts} top-{w.top_k}, ffn {w.d_ff}", "block": 16,
+                   "drafts": f"q = softmax(target + N(0, {w.draft_sigma}^2))" if w.draft == "perturbed" else "uniform"},
+        "roofline": {"kernel": "paged attention (attn_mfma_kernel + split merge), per layer launch",
+                     "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                     "algorithmic_bytes_per_launch": abytes, "avg_launch_ms": round(attn_avg, 4)},
+        "emitted_tokens_per_s": round(emitted, 1),
+        "mean_accepted_fraction": round(float(n_acc.mean()) / k, 4) if k else None,
+        "kernel_groups": per_group,
+        "lm_head_tflops": round(lm_flops / (lm_ms / max(lm_n, 1) / 1e3) / 1e12, 1) if lm_n else None,
+    }
+    if not a.no_cpu_baseline:
+        log("[bench] timing the CPU oracle on a bounded sample")
+        v, secs, threads, desc = cpu_baseline(w, layout, layers, head, kv, tokens, q, u)
+        res["cpu_baseline"] = {"value": round(v, 3), "unit": "verified tokens/s", "cores": threads,
+                               "kind": "oracle", "sample": desc, "seconds": round(secs, 2)}
+    print(json.dumps(res))
+
+
+if __name__ == "__main__":
+    main()

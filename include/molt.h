@@ -1,0 +1,265 @@
+/*
+ * molt.h -- C ABI of the MI355X (gfx950) speculative-decoding verify step.
+ *
+ * The method: a mixture-of-experts policy served with speculative decoding. Its
+ * serving engine drafts k tokens per sequence and verifies them with the target
+ * model; k = 0 disables speculation (paper Sec. 4.1, table of scaling controls:
+ * number of speculative tokens). Verification runs one target forward pass over
+ * the 1+k positions of every sequence (paged-KV attention, top-K routed expert
+ * FFNs, LM head) and then applies the speculative accept rule min(1, p/q) with a
+ * residual resample at temperature 1 and no truncation (Sec. 5.3, Sec. 5.4). The
+ * engine returns the emitted token IDs and their behavior log-probabilities
+ * (Sec. 4.2, Eq. 1) and, for routing replay, the experts each token used
+ * (Sec. 4.1; route records travel with every experience, Sec. 4.4).
+ *
+ * Conventions for every entry point:
+ *  - Pointers are DEVICE pointers unless marked "host". Arrays are row-major.
+ *  - The caller owns every buffer. The library allocates no device memory: each
+ *    call takes a caller-provided workspace of at least *_workspace_size() bytes
+ *    (256-byte aligned start recommended; any alignment is accepted).
+ *  - Calls are asynchronous on `stream` and never synchronise. Results are valid
+ *    after the stream is synchronised. The library keeps no state between calls
+ *    (weights and KV cache may be overwritten between calls, e.g. on a weight
+ *    refit).
+ *  - Arguments are validated on the host BEFORE anything is enqueued; a
+ *    validation failure enqueues nothing and returns a negative status, with a
+ *    message available from molt_last_error() (thread-local). Values that live
+ *    in device memory (token IDs, block IDs, context lengths) cannot be checked
+ *    on the host: out-of-range values there give undefined results, except where
+ *    a function states otherwise.
+ *  - A failed kernel launch returns MOLT_ERR_HIP with the HIP error string.
+ *  - Calls that share a workspace must not overlap in time.
+ *
+ * Cache layout (PagedAttention-style blocks of 16 tokens, block table per
+ * sequence; the paper's rollout engines use vLLM's paged cache, Sec. 2):
+ *    K cache  [num_blocks, n_kv_heads, 16, head_dim]   one token's head vector contiguous
+ *    V cache  [num_blocks, n_kv_heads, head_dim, 16]   the 16 tokens of a dim contiguous
+ * Position p of sequence b lives in block block_tables[b * max_blocks_per_seq + p / 16],
+ * slot p % 16. context_lens[b] counts tokens already cached; the 1+k new tokens
+ * take positions context_lens[b] .. context_lens[b] + k. After a step the caller
+ * advances context_lens[b] by n_accepted[b] + 1; slots of rejected drafts are
+ * overwritten by the next step.
+ */
+#ifndef MOLT_H
+#define MOLT_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct ihipStream_t* molt_stream_t; /* the same type as hipStream_t */
+
+typedef enum {
+  MOLT_OK = 0,
+  MOLT_ERR_INVALID_ARG = -1, /* NULL required pointer, bad size, bad combination  */
+  MOLT_ERR_UNSUPPORTED = -2, /* valid request this build does not implement       */
+  MOLT_ERR_WORKSPACE = -3,   /* workspace missing or smaller than *_workspace_size */
+  MOLT_ERR_HIP = -4          /* a HIP runtime call or kernel launch failed         */
+} molt_status;
+
+typedef enum {
+  MOLT_F32 = 0,     /* IEEE binary32                                            */
+  MOLT_BF16 = 1,    /* bfloat16 (upper half of binary32), round-to-nearest-even */
+  MOLT_FP8_E4M3 = 2 /* OCP fp8 e4m3fn: bias 7, max +-448, no inf               */
+} molt_dtype;
+
+/* Message of the last failed call on this thread ("" if none). Valid until the
+ * next call on the same thread. */
+const char* molt_last_error(void);
+
+/* ABI version of this header (major * 100 + minor). */
+int molt_version(void);
+
+/* ------------------------------------------------------------------------------
+ * molt_spec_accept -- speculative accept / residual resample (Sec. 4.1 control
+ * table: k speculative tokens; Sec. 4.2: token IDs and behavior log-probs
+ * recorded at generation time; Sec. 5.3/5.4: temperature 1, no top-p/top-k).
+ * The rule is the published speculative-sampling rule (Leviathan et al. 2023,
+ * Chen et al. 2023): draft i (1..k) is judged by logits row i-1 and kept iff
+ *       u[b, i-1] * q_i(x_i) * S < exp(l_x - m)      (i.e. u < p/q), strict,
+ * with m = max_t l_t and S = sum_t exp(l_t - m) of that row. At the first
+ * rejection the final token is drawn from norm(max(0, p - q)); if all k pass, a
+ * bonus token is drawn from row k. The draw uses u[b, k] and an integer inverse
+ * CDF: R_t = floor(r_t * 2^62), Tot = sum R_t, target = (Tot * floor(u * 2^32)) >> 32,
+ * token = first t with prefix(R)_t > target (zero residual mass falls back to p).
+ *
+ *   logits         [B, k+1, V] f32   target logits (row j scores position j)
+ *   draft_probs    [B, k, V]   f32   q of each draft position; NULL = one-hot q at
+ *                                    the draft (greedy drafting)
+ *   draft_tokens   [B, k]      i32   drafts in [0, V); an out-of-range draft is
+ *                                    rejected (never read through); NULL iff k == 0
+ *   uniforms       [B, k+1]    f32   in [0, 1): k accept tests, then the final draw
+ *   out_tokens     [B, k+1]    i32   emitted tokens: n accepted drafts, then the
+ *                                    final token; the rest -1
+ *   out_num_accepted [B]       i32   n in [0, k]
+ *   out_logprobs   [B, k+1]    f32   log p_j(token_j) of each emitted token at its
+ *                                    row; the rest NaN. May be NULL.
+ * Errors: INVALID_ARG for NULL required pointers, B < 1, k < 0, V < 1 or
+ * B*(k+1)*V >= 2^62; WORKSPACE for a short workspace. Rows whose logits are all
+ * -inf or contain NaN give undefined tokens.
+ * ---------------------------------------------------------------------------- */
+size_t molt_spec_accept_workspace_size(int B, int k, int V);
+int molt_spec_accept(const float* logits, const float* draft_probs, const int32_t* draft_tokens,
+                     const float* uniforms, int B, int k, int V, int32_t* out_tokens,
+                     int32_t* out_num_accepted, float* out_logprobs, void* workspace,
+                     size_t workspace_bytes, molt_stream_t stream);
+
+/* ------------------------------------------------------------------------------
+ * molt_moe_layer -- top-K routed SwiGLU mixture-of-experts on normalised input
+ * (the MoE policy of Sec. 5.4; expert choices are the route records kept for
+ * routing replay, Sec. 4.1):
+ *   g = x W_r^T (+ router_bias)                 f32 router logits [T, E]
+ *   ids, w = top-K of g (descending, ties to the lower expert ID, -0 == +0),
+ *            softmax over the K selected logits
+ *   out[t] = sum_{j<K} w[t,j] * FFN_{ids[t,j]}(x[t])   (slot order, f32)
+ *   FFN_e(x) = (silu(x W_g,e^T) * (x W_u,e^T)) W_d,e^T, SwiGLU product stored in
+ *            act_dtype before the down projection.
+ * fp8 experts: x and the SwiGLU product are quantised per row (s = amax/448,
+ * codes = e4m3(v / s), saturating, round-to-nearest-even); products are rescaled
+ * by s_row * s_channel.
+ *
+ *   x            [T, d]        act_dtype (F32 or BF16)
+ *   w_router     [E, d]        act_dtype
+ *   router_bias  [E]           f32, or NULL (added to the logits before top-K)
+ *   w_gate_up    [E, 2F, d]    w_dtype: rows 0..F-1 gate, F..2F-1 up
+ *   w_down       [E, d, F]     w_dtype
+ *   s_gate_up    [E, 2F] f32, s_down [E, d] f32: per-output-channel scales, required
+ *                iff w_dtype == FP8_E4M3, else ignored
+ *   replay_ids   [T, K] i32 or NULL: use these experts (distinct, in [0, E)) and take
+ *                only their weights from the router (routing replay)
+ *   out          [T, d] f32    the weighted expert sum (no residual)
+ *   out_ids, out_weights [T, K] i32 / f32: route records, may be NULL
+ *   out_counts [E], out_offsets [E+1], out_perm [T*K] i32: the stable (expert,
+ *                token, slot) grouping, may be NULL
+ * Supported: (act, w) in {(F32, F32), (BF16, BF16), (BF16, FP8_E4M3)}; d % 64 == 0,
+ * F % 64 == 0, 1 <= K <= E <= 256, K <= 16. T >= 1.
+ * ---------------------------------------------------------------------------- */
+size_t molt_moe_layer_workspace_size(int T, int d, int E, int K, int F, molt_dtype act_dtype,
+                                     molt_dtype w_dtype);
+int molt_moe_layer(const void* x, const void* w_router, const float* router_bias,
+                   const void* w_gate_up, const void* w_down, const float* s_gate_up,
+                   const float* s_down, int T, int d, int E, int K, int F, molt_dtype act_dtype,
+                   molt_dtype w_dtype, const int32_t* replay_ids, float* out, int32_t* out_ids,
+                   float* out_weights, int32_t* out_counts, int32_t* out_offsets,
+                   int32_t* out_perm, void* workspace, size_t workspace_bytes,
+                   molt_stream_t stream);
+
+/* ------------------------------------------------------------------------------
+ * molt_paged_attention -- multi-query paged decode attention of the verify step
+ * (PagedAttention cache, Sec. 2). Token t = b*(1+k) + j is query position j of
+ * sequence b and attends to positions 0 .. context_lens[b] + j (its own included);
+ * query head h reads kv head h / (Hq/Hkv); scores scaled by 1/sqrt(D); softmax in
+ * f32. The cache must already hold the 1+k new positions.
+ *
+ *   q             [T, Hq, D]  dtype           T = B*(1+k)
+ *   k_cache, v_cache          dtype, layouts above
+ *   block_tables  [B, max_blocks_per_seq] i32;  context_lens [B] i32
+ *   out           [T, Hq*D]   dtype
+ * Supported: dtype F32 or BF16, D in {64, 128}, Hq % Hkv == 0, Hq/Hkv*(1+k) <= 128.
+ * context_lens[b] + k + 1 <= 16 * max_blocks_per_seq is the caller's duty.
+ * ---------------------------------------------------------------------------- */
+size_t molt_paged_attention_workspace_size(int B, int k, int n_q_heads, int n_kv_heads,
+                                           int head_dim, int max_blocks_per_seq);
+int molt_paged_attention(const void* q, const void* k_cache, const void* v_cache,
+                         const int32_t* block_tables, const int32_t* context_lens, int B, int k,
+                         int n_q_heads, int n_kv_heads, int head_dim, int max_blocks_per_seq,
+                         molt_dtype dtype, void* out, void* workspace, size_t workspace_bytes,
+                         molt_stream_t stream);
+
+/* ------------------------------------------------------------------------------
+ * Model description: a HOST struct holding device pointers; read only during a
+ * call. Per-layer members are HOST arrays of n_layers device pointers.
+ * Pre-norm decoder (Sec. 5.3/5.4 run MoE decoders):
+ *   x += Attn(RMSNorm(x)); x += MoE(RMSNorm(x))    per layer, x f32
+ * RMSNorm(x) = x / sqrt(mean(x^2) + rms_eps) * g, rounded to dtype.
+ * RoPE: rotate-half pairs (i, i + D/2), inverse frequency rope_theta^(-2i/D),
+ * angle = position * inv_freq, evaluated in f64.
+ * dtype F32 requires expert_dtype F32; dtype BF16 allows BF16 or FP8_E4M3 experts.
+ * ---------------------------------------------------------------------------- */
+typedef struct molt_model {
+  int n_layers, d_model, n_q_heads, n_kv_heads, head_dim, n_experts, top_k, d_ff, vocab;
+  float rms_eps, rope_theta;
+  molt_dtype dtype;        /* activations, embeddings, attention/router/LM-head weights, KV */
+  molt_dtype expert_dtype; /* expert weights                                              */
+  const void* embed;       /* [V, d] dtype (needed by molt_verify_step)                   */
+  const float* final_norm; /* [d]                                                         */
+  const void* lm_head;     /* [V, d] dtype                                                */
+  const float* const* attn_norm;   /* [L] -> [d]                                          */
+  const void* const* w_qkv;        /* [L] -> [(Hq + 2 Hkv) D, d]: q heads, k heads, v heads */
+  const void* const* w_o;          /* [L] -> [d, Hq D]                                    */
+  const float* const* moe_norm;    /* [L] -> [d]                                          */
+  const void* const* w_router;     /* [L] -> [E, d]                                       */
+  const float* const* router_bias; /* NULL, or [L] -> [E] f32 (entries may be NULL)       */
+  const void* const* w_gate_up;    /* [L] -> [E, 2F, d]                                   */
+  const void* const* w_down;       /* [L] -> [E, d, F]                                    */
+  const float* const* s_gate_up;   /* [L] -> [E, 2F] f32, fp8 experts only, else NULL     */
+  const float* const* s_down;      /* [L] -> [E, d] f32                                   */
+} molt_model;
+
+typedef struct molt_kv {
+  void* const* k_cache;        /* HOST array [n_layers] of device K caches (layout above) */
+  void* const* v_cache;        /* HOST array [n_layers] of device V caches                */
+  const int32_t* block_tables; /* [B, max_blocks_per_seq] physical block IDs              */
+  const int32_t* context_lens; /* [B] tokens already cached                               */
+  int max_blocks_per_seq;
+  int num_blocks;
+  int block_size; /* must be 16 */
+} molt_kv;
+
+/* ------------------------------------------------------------------------------
+ * molt_decoder_forward -- all n_layers decoder layers of the verify step on a
+ * given residual stream (token t = b*(1+k) + j at position context_lens[b] + j).
+ * Writes the new keys/values of every layer into the cache.
+ *   x           [B*(1+k), d] f32, in/out (the residual stream)
+ *   out_routes  [n_layers, B*(1+k), top_k] i32 expert IDs, or NULL
+ * Requirements as for molt_moe_layer and molt_paged_attention.
+ * ---------------------------------------------------------------------------- */
+size_t molt_decoder_workspace_size(const molt_model* m, int B, int k, int max_blocks_per_seq);
+int molt_decoder_forward(const molt_model* m, const molt_kv* kv, int B, int k, float* x,
+                         int32_t* out_routes, void* workspace, size_t workspace_bytes,
+                         molt_stream_t stream);
+
+/* ------------------------------------------------------------------------------
+ * molt_verify_step -- the whole verify step: embed tokens, run the decoder,
+ * final RMSNorm, LM head to f32 logits, then molt_spec_accept's rule.
+ *   tokens       [B, 1+k] i32: the last emitted token, then the k drafts (in [0, V))
+ *   draft_probs, uniforms, out_tokens, out_num_accepted, out_logprobs: as in
+ *                molt_spec_accept (drafts are tokens[:, 1:])
+ *   out_logits   [B, 1+k, V] f32, or NULL (then kept in the workspace)
+ *   out_routes   [n_layers, B*(1+k), top_k] i32, or NULL
+ * ---------------------------------------------------------------------------- */
+size_t molt_verify_step_workspace_size(const molt_model* m, int B, int k, int max_blocks_per_seq);
+int molt_verify_step(const molt_model* m, const molt_kv* kv, int B, int k, const int32_t* tokens,
+                     const float* draft_probs, const float* uniforms, float* out_logits,
+                     int32_t* out_tokens, int32_t* out_num_accepted, float* out_logprobs,
+                     int32_t* out_routes, void* workspace, size_t workspace_bytes,
+                     molt_stream_t stream);
+
+/* ------------------------------------------------------------------------------
+ * Kernel-group timing (a measurement aid, not part of the method). While enabled,
+ * every launch of a group is bracketed by two HIP events recorded on the call's
+ * stream; molt_profile_read synchronises on the recorded events and returns the
+ * summed elapsed time and the number of bracketed launches of one group. Events come
+ * from a pool of 4096 pairs created on the first enable (no device memory);
+ * launches beyond the pool are not timed. Process-wide state: enable, run and read
+ * from one host thread.
+ * Groups: 0 attention (+ split merge), 1 expert GEMMs (gate_up + down), 2 LM head,
+ * 3 sampler (all four passes), 4 dense projections (QKV, O, router).
+ * ---------------------------------------------------------------------------- */
+typedef enum {
+  MOLT_PROF_ATTENTION = 0,
+  MOLT_PROF_EXPERT_GEMM = 1,
+  MOLT_PROF_LM_HEAD = 2,
+  MOLT_PROF_SAMPLER = 3,
+  MOLT_PROF_PROJECTIONS = 4
+} molt_prof_group;
+int molt_profile_enable(int enable); /* 1: start (and clear), 0: stop recording */
+int molt_profile_read(int group, double* total_ms, int* launches);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* MOLT_H */

@@ -107,6 +107,7 @@ def verify_step(tokens, get_layer, head, caches, block_tables, context_lens, cfg
     s["logits"] = logits
     s["routes"] = np.stack([r["ids"] for r in routes]) if routes else None
     s["route_margin"] = np.stack([r["margin"] for r in routes]) if routes else None
+    s["route_order_margin"] = np.stack([r["order_margin"] for r in routes]) if routes else None
     return s
 
 

@@ -56,13 +56,14 @@ def moe_layer(y, w_router, w_gate_up, w_down, K, act_dtype, expert_dtype,
     F = w_gate_up.shape[1] // 2
     g = routing.router_logits_f32(y, w_router, router_bias)
     if replay_ids is None:
-        ids, wts, margin = routing.topk_route(g, K)
+        ids, wts, margin, order_margin = routing.topk_route(g, K)
     else:
         ids = np.asarray(replay_ids, dtype=np.int32).reshape(T, K)
         sel = np.take_along_axis(g.astype(np.float64), ids.astype(np.int64), axis=1)
         ev = np.exp(sel - sel.max(axis=1, keepdims=True))
         wts = (ev / ev.sum(axis=1, keepdims=True)).astype(np.float32)
         margin = np.full(T, np.inf)
+        order_margin = np.full(T, np.inf)
     counts, offsets, perm, inv = routing.permute(ids, E)
     tok = np.arange(T) if tokens is None else np.asarray(tokens)
     want = np.zeros(T, dtype=bool)
@@ -100,7 +101,7 @@ def moe_layer(y, w_router, w_gate_up, w_down, K, act_dtype, expert_dtype,
         for j in range(K):
             acc += np.float64(wts[t, j]) * o[(t, j)].astype(np.float64)
         out[i] = acc.astype(np.float32)
-    return {"out": out, "ids": ids, "weights": wts, "router_logits": g, "margin": margin,
+    return {"out": out, "ids": ids, "weights": wts, "router_logits": g, "margin": margin, "order_margin": order_margin,
             "counts": counts, "offsets": offsets, "perm": perm, "inv": inv}
 
 

@@ -25,15 +25,18 @@ def router_logits_f32(y, w_router, bias=None):
 
 
 def topk_route(logits, K):
-    """logits [T, E] float32 -> ids [T, K] int32, weights [T, K] float32, margin [T].
+    """logits [T, E] float32 -> ids [T, K] int32, weights [T, K] float32, margin [T],
+    order_margin [T].
 
-    margin[t] = gap between the K-th and (K+1)-th selected logits (inf if K == E),
-    used to classify disagreements caused by last-bit differences in the logits."""
+    margin[t] = gap between the K-th and (K+1)-th logits (inf if K == E): below it, the
+    selected set can change under last-bit differences in the logits. order_margin[t] =
+    smallest gap between adjacent selected logits: below it, the slot order can."""
     g = np.asarray(logits, dtype=np.float32)
     T, E = g.shape
     ids = np.zeros((T, K), dtype=np.int32)
     wts = np.zeros((T, K), dtype=np.float32)
     margin = np.full(T, np.inf)
+    order_margin = np.full(T, np.inf)
     for t in range(T):
         row = g[t].astype(np.float64) + 0.0       # -0.0 -> +0.0
         order = sorted(range(E), key=lambda e: (-row[e], e))
@@ -44,7 +47,9 @@ def topk_route(logits, K):
         wts[t] = (ev / ev.sum()).astype(np.float32)
         if K < E:
             margin[t] = row[order[K - 1]] - row[order[K]]
-    return ids, wts, margin
+        if K > 1:
+            order_margin[t] = float(np.min(vals[:-1] - vals[1:]))
+    return ids, wts, margin, order_margin
 
 
 def permute(ids, E):

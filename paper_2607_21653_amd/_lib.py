@@ -1,0 +1,345 @@
+"""ctypes binding of libmolt.so: argument marshalling only.
+
+Every function takes torch tensors that already live on the GPU, checks dtypes,
+shapes and contiguity, allocates outputs and the workspace with torch (device
+memory is torch's job), and calls the C entry point of the same name on torch's
+current stream. There is no fallback: if the library is missing or no GPU is
+present, the call raises."""
+import ctypes
+import os
+
+import torch
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libmolt.so")
+
+MOLT_F32, MOLT_BF16, MOLT_FP8_E4M3 = 0, 1, 2
+DTYPE_CODE = {torch.float32: MOLT_F32, torch.bfloat16: MOLT_BF16, torch.uint8: MOLT_FP8_E4M3}
+NAME_CODE = {"f32": MOLT_F32, "bf16": MOLT_BF16, "fp8": MOLT_FP8_E4M3}
+
+_lib = None
+
+c_int, c_size, c_vp, c_float = ctypes.c_int, ctypes.c_size_t, ctypes.c_void_p, ctypes.c_float
+
+
+class MoltModel(ctypes.Structure):
+    _fields_ = [(n, c_int) for n in ("n_layers", "d_model", "n_q_heads", "n_kv_heads", "head_dim",
+                                     "n_experts", "top_k", "d_ff", "vocab")] + [
+        ("rms_eps", c_float), ("rope_theta", c_float), ("dtype", c_int), ("expert_dtype", c_int),
+        ("embed", c_vp), ("final_norm", c_vp), ("lm_head", c_vp),
+        ("attn_norm", c_vp), ("w_qkv", c_vp), ("w_o", c_vp), ("moe_norm", c_vp),
+        ("w_router", c_vp), ("router_bias", c_vp), ("w_gate_up", c_vp), ("w_down", c_vp),
+        ("s_gate_up", c_vp), ("s_down", c_vp)]
+
+
+class MoltKV(ctypes.Structure):
+    _fields_ = [("k_cache", c_vp), ("v_cache", c_vp), ("block_tables", c_vp),
+                ("context_lens", c_vp), ("max_blocks_per_seq", c_int), ("num_blocks", c_int),
+                ("block_size", c_int)]
+
+
+_SIGS = {
+    "molt_last_error": (ctypes.c_char_p, []),
+    "molt_version": (c_int, []),
+    "molt_spec_accept_workspace_size": (c_size, [c_int, c_int, c_int]),
+    "molt_spec_accept": (c_int, [c_vp, c_vp, c_vp, c_vp, c_int, c_int, c_int, c_vp, c_vp, c_vp,
+                                 c_vp, c_size, c_vp]),
+    "molt_moe_layer_workspace_size": (c_size, [c_int] * 5 + [c_int, c_int]),
+    "molt_moe_layer": (c_int, [c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_int, c_int, c_int,
+                               c_int, c_int, c_int, c_int, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp,
+                               c_vp, c_vp, c_size, c_vp]),
+    "molt_paged_attention_workspace_size": (c_size, [c_int] * 6),
+    "molt_paged_attention": (c_int, [c_vp, c_vp, c_vp, c_vp, c_vp, c_int, c_int, c_int, c_int,
+                                     c_int, c_int, c_int, c_vp, c_vp, c_size, c_vp]),
+    "molt_decoder_workspace_size": (c_size, [ctypes.POINTER(MoltModel), c_int, c_int, c_int]),
+    "molt_decoder_forward": (c_int, [ctypes.POINTER(MoltModel), ctypes.POINTER(MoltKV), c_int,
+                                     c_int, c_vp, c_vp, c_vp, c_size, c_vp]),
+    "molt_profile_enable": (c_int, [c_int]),
+    "molt_profile_read": (c_int, [c_int, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(c_int)]),
+    "molt_verify_step_workspace_size": (c_size, [ctypes.POINTER(MoltModel), c_int, c_int, c_int]),
+    "molt_verify_step": (c_int, [ctypes.POINTER(MoltModel), ctypes.POINTER(MoltKV), c_int, c_int,
+                                 c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_size,
+                                 c_vp]),
+}
+
+
+class MoltError(RuntimeError):
+    pass
+
+
+def load(path=LIB_PATH):
+    """Loads the library (once). Raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise MoltError(f"{path} is missing: build it with `python -m paper_2607_21653_amd.build`")
+    lib = ctypes.CDLL(path)
+    for name, (res, args) in _SIGS.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    _lib = lib
+    return lib
+
+
+def exported_symbols():
+    return list(_SIGS)
+
+
+def _check(status, name):
+    if status != 0:
+        msg = _lib.molt_last_error().decode()
+        raise MoltError(f"{name} returned {status}: {msg}")
+
+
+def _ptr(t):
+    return None if t is None else t.data_ptr()
+
+
+def _dev(t, dtype, shape=None, name="tensor"):
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise MoltError(f"{name} must be a GPU tensor")
+    if dtype is not None and t.dtype != dtype:
+        raise MoltError(f"{name} has dtype {t.dtype}, expected {dtype}")
+    if not t.is_contiguous():
+        raise MoltError(f"{name} must be contiguous")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise MoltError(f"{name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
+    return t
+
+
+def _stream():
+    return torch.cuda.current_stream().cuda_stream
+
+
+def _workspace(nbytes, device, ws=None):
+    if nbytes == 0:
+        return None, 0
+    if ws is not None and ws.numel() >= nbytes:
+        return ws, ws.numel()
+    t = torch.empty(nbytes, dtype=torch.uint8, device=device)
+    return t, nbytes
+
+
+# ------------------------------------------------------------------ spec accept
+
+def spec_accept(logits, draft_tokens, uniforms, draft_probs=None, out=None, workspace=None):
+    """logits [B, k+1, V] f32; draft_tokens [B, k] i32; uniforms [B, k+1] f32;
+    draft_probs [B, k, V] f32 or None (one-hot q). Returns (tokens, n_accepted, logprobs)."""
+    lib = load()
+    B, kp1, V = logits.shape
+    k = kp1 - 1
+    _dev(logits, torch.float32, name="logits")
+    _dev(uniforms, torch.float32, (B, kp1), "uniforms")
+    if k > 0:
+        _dev(draft_tokens, torch.int32, (B, k), "draft_tokens")
+    _dev(draft_probs, torch.float32, (B, k, V), "draft_probs")
+    dev = logits.device
+    if out is None:
+        out = (torch.empty(B, kp1, dtype=torch.int32, device=dev),
+               torch.empty(B, dtype=torch.int32, device=dev),
+               torch.empty(B, kp1, dtype=torch.float32, device=dev))
+    toks, n, lp = out
+    ws, nb = _workspace(lib.molt_spec_accept_workspace_size(B, k, V), dev, workspace)
+    st = lib.molt_spec_accept(_ptr(logits), _ptr(draft_probs), _ptr(draft_tokens) if k > 0 else None,
+                              _ptr(uniforms), B, k, V, _ptr(toks), _ptr(n), _ptr(lp), _ptr(ws), nb,
+                              _stream())
+    _check(st, "molt_spec_accept")
+    return toks, n, lp
+
+
+# ------------------------------------------------------------------ MoE layer
+
+def moe_layer(x, w_router, w_gate_up, w_down, top_k, router_bias=None, s_gate_up=None,
+              s_down=None, replay_ids=None, want_routing=False, workspace=None):
+    """x [T, d] (f32|bf16); weights as in molt.h (fp8 experts as uint8 codes).
+    Returns out [T, d] f32, or (out, ids, weights, counts, offsets, perm) with want_routing."""
+    lib = load()
+    T, d = x.shape
+    E = w_router.shape[0]
+    F = w_gate_up.shape[1] // 2
+    act = DTYPE_CODE[x.dtype]
+    wdt = DTYPE_CODE[w_gate_up.dtype]
+    _dev(x, None, name="x")
+    _dev(w_router, x.dtype, (E, d), "w_router")
+    _dev(w_gate_up, None, (E, 2 * F, d), "w_gate_up")
+    _dev(w_down, w_gate_up.dtype, (E, d, F), "w_down")
+    _dev(router_bias, torch.float32, (E,), "router_bias")
+    _dev(s_gate_up, torch.float32, (E, 2 * F), "s_gate_up")
+    _dev(s_down, torch.float32, (E, d), "s_down")
+    _dev(replay_ids, torch.int32, (T, top_k), "replay_ids")
+    dev = x.device
+    out = torch.empty(T, d, dtype=torch.float32, device=dev)
+    ids = wts = counts = offsets = perm = None
+    if want_routing:
+        ids = torch.empty(T, top_k, dtype=torch.int32, device=dev)
+        wts = torch.empty(T, top_k, dtype=torch.float32, device=dev)
+        counts = torch.empty(E, dtype=torch.int32, device=dev)
+        offsets = torch.empty(E + 1, dtype=torch.int32, device=dev)
+        perm = torch.empty(T * top_k, dtype=torch.int32, device=dev)
+    ws, nb = _workspace(lib.molt_moe_layer_workspace_size(T, d, E, top_k, F, act, wdt), dev, workspace)
+    st = lib.molt_moe_layer(_ptr(x), _ptr(w_router), _ptr(router_bias), _ptr(w_gate_up), _ptr(w_down),
+                            _ptr(s_gate_up), _ptr(s_down), T, d, E, top_k, F, act, wdt,
+                            _ptr(replay_ids), _ptr(out), _ptr(ids), _ptr(wts), _ptr(counts),
+                            _ptr(offsets), _ptr(perm), _ptr(ws), nb, _stream())
+    _check(st, "molt_moe_layer")
+    if want_routing:
+        return out, ids, wts, counts, offsets, perm
+    return out
+
+
+# ------------------------------------------------------------------ paged attention
+
+def paged_attention(q, k_cache, v_cache, block_tables, context_lens, k, workspace=None):
+    """q [B*(1+k), Hq, D]; caches [nb, Hkv, 16, D] / [nb, Hkv, D, 16]; returns [T, Hq*D]."""
+    lib = load()
+    T, Hq, D = q.shape
+    B = context_lens.shape[0]
+    Hkv = k_cache.shape[1]
+    if T != B * (k + 1):
+        raise MoltError(f"q has {T} rows, expected B*(1+k) = {B * (k + 1)}")
+    _dev(q, None, name="q")
+    _dev(k_cache, q.dtype, name="k_cache")
+    _dev(v_cache, q.dtype, name="v_cache")
+    _dev(block_tables, torch.int32, name="block_tables")
+    _dev(context_lens, torch.int32, (B,), "context_lens")
+    maxb = block_tables.shape[1]
+    out = torch.empty(T, Hq * D, dtype=q.dtype, device=q.device)
+    ws, nb = _workspace(lib.molt_paged_attention_workspace_size(B, k, Hq, Hkv, D, maxb), q.device, workspace)
+    st = lib.molt_paged_attention(_ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(block_tables),
+                                  _ptr(context_lens), B, k, Hq, Hkv, D, maxb, DTYPE_CODE[q.dtype],
+                                  _ptr(out), _ptr(ws), nb, _stream())
+    _check(st, "molt_paged_attention")
+    return out
+
+
+# ------------------------------------------------------------------ model / decoder / step
+
+class Model:
+    """Holds the device weights of a decoder and the molt_model struct that points at them.
+    layers: list of dicts with attn_norm, w_qkv, w_o, moe_norm, w_router, w_gate_up, w_down,
+    optional router_bias, s_gate_up, s_down. head: dict with embed, final_norm, lm_head
+    (optional for the decoder-only entry point)."""
+
+    def __init__(self, layers, head=None, n_q_heads=None, n_kv_heads=None, head_dim=None,
+                 top_k=None, rms_eps=1e-6, rope_theta=1e6):
+        self.layers, self.head = layers, head or {}
+        l0 = layers[0]
+        E, twoF, d = l0["w_gate_up"].shape
+        self.dtype = l0["w_qkv"].dtype
+        m = MoltModel()
+        m.n_layers = len(layers)
+        m.d_model, m.n_q_heads, m.n_kv_heads, m.head_dim = d, n_q_heads, n_kv_heads, head_dim
+        m.n_experts, m.top_k, m.d_ff = E, top_k, twoF // 2
+        m.vocab = self.head["lm_head"].shape[0] if "lm_head" in self.head else 0
+        m.rms_eps, m.rope_theta = rms_eps, rope_theta
+        m.dtype = DTYPE_CODE[self.dtype]
+        m.expert_dtype = DTYPE_CODE[l0["w_gate_up"].dtype]
+        self._arrays = []
+
+        def arr(key, optional=False):
+            vals = [lw.get(key) for lw in layers]
+            if optional and all(v is None for v in vals):
+                return None
+            a = (c_vp * len(vals))(*[None if v is None else v.data_ptr() for v in vals])
+            self._arrays.append(a)
+            return ctypes.cast(a, c_vp)
+
+        for key in ("attn_norm", "w_qkv", "w_o", "moe_norm", "w_router", "w_gate_up", "w_down"):
+            setattr(m, key, arr(key))
+        for key in ("router_bias", "s_gate_up", "s_down"):
+            setattr(m, key, arr(key, optional=True))
+        for key in ("embed", "final_norm", "lm_head"):
+            setattr(m, key, self.head[key].data_ptr() if key in self.head else None)
+        self.struct = m
+
+
+class KVCache:
+    """Per-layer paged caches plus the block tables and context lengths (all on the GPU)."""
+
+    def __init__(self, k_caches, v_caches, block_tables, context_lens):
+        self.k_caches, self.v_caches = k_caches, v_caches
+        self.block_tables, self.context_lens = block_tables, context_lens
+        self._k = (c_vp * len(k_caches))(*[t.data_ptr() for t in k_caches])
+        self._v = (c_vp * len(v_caches))(*[t.data_ptr() for t in v_caches])
+        s = MoltKV()
+        s.k_cache = ctypes.cast(self._k, c_vp)
+        s.v_cache = ctypes.cast(self._v, c_vp)
+        s.block_tables = block_tables.data_ptr()
+        s.context_lens = context_lens.data_ptr()
+        s.max_blocks_per_seq = block_tables.shape[1]
+        s.num_blocks = k_caches[0].shape[0]
+        s.block_size = 16
+        self.struct = s
+
+
+def decoder_workspace_size(model, B, k, max_blocks):
+    return load().molt_decoder_workspace_size(ctypes.byref(model.struct), B, k, max_blocks)
+
+
+def decoder_forward(model, kv, B, k, x, want_routes=False, workspace=None):
+    """Runs every layer on the residual stream x [B*(1+k), d] f32 in place."""
+    lib = load()
+    _dev(x, torch.float32, (B * (k + 1), model.struct.d_model), "x")
+    routes = None
+    if want_routes:
+        routes = torch.empty(model.struct.n_layers, B * (k + 1), model.struct.top_k,
+                             dtype=torch.int32, device=x.device)
+    ws, nb = _workspace(decoder_workspace_size(model, B, k, kv.struct.max_blocks_per_seq), x.device, workspace)
+    st = lib.molt_decoder_forward(ctypes.byref(model.struct), ctypes.byref(kv.struct), B, k, _ptr(x),
+                                  _ptr(routes), _ptr(ws), nb, _stream())
+    _check(st, "molt_decoder_forward")
+    return routes
+
+
+def verify_step_workspace_size(model, B, k, max_blocks):
+    return load().molt_verify_step_workspace_size(ctypes.byref(model.struct), B, k, max_blocks)
+
+
+def verify_step(model, kv, tokens, uniforms, draft_probs=None, want_logits=True, want_routes=False,
+                workspace=None, out=None):
+    """tokens [B, 1+k] i32. Returns dict(tokens, n_accepted, logprobs, logits?, routes?)."""
+    lib = load()
+    B, kp1 = tokens.shape
+    k = kp1 - 1
+    V = model.struct.vocab
+    dev = tokens.device
+    _dev(tokens, torch.int32, name="tokens")
+    _dev(uniforms, torch.float32, (B, kp1), "uniforms")
+    _dev(draft_probs, torch.float32, (B, k, V), "draft_probs")
+    if out is None:
+        out = {"tokens": torch.empty(B, kp1, dtype=torch.int32, device=dev),
+               "n_accepted": torch.empty(B, dtype=torch.int32, device=dev),
+               "logprobs": torch.empty(B, kp1, dtype=torch.float32, device=dev)}
+        if want_logits:
+            out["logits"] = torch.empty(B, kp1, V, dtype=torch.float32, device=dev)
+        if want_routes:
+            out["routes"] = torch.empty(model.struct.n_layers, B * kp1, model.struct.top_k,
+                                        dtype=torch.int32, device=dev)
+    ws, nb = _workspace(verify_step_workspace_size(model, B, k, kv.struct.max_blocks_per_seq), dev, workspace)
+    st = lib.molt_verify_step(ctypes.byref(model.struct), ctypes.byref(kv.struct), B, k, _ptr(tokens),
+                              _ptr(draft_probs), _ptr(uniforms), _ptr(out.get("logits")),
+                              _ptr(out["tokens"]), _ptr(out["n_accepted"]), _ptr(out["logprobs"]),
+                              _ptr(out.get("routes")), _ptr(ws), nb, _stream())
+    _check(st, "molt_verify_step")
+    return out
+
+
+# ------------------------------------------------------------------ kernel-group timing
+
+PROF_GROUPS = {"attention": 0, "expert_gemm": 1, "lm_head": 2, "sampler": 3, "projections": 4}
+
+
+def profile_enable(on=True):
+    _check(load().molt_profile_enable(1 if on else 0), "molt_profile_enable")
+
+
+def profile_read(group):
+    """(total milliseconds, number of timed launches) of a kernel group since enable."""
+    ms, n = ctypes.c_double(0), c_int(0)
+    _check(load().molt_profile_read(PROF_GROUPS[group], ctypes.byref(ms), ctypes.byref(n)),
+           "molt_profile_read")
+    return ms.value, n.value

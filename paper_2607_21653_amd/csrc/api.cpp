@@ -1,0 +1,516 @@
+// C-ABI layer: host-side validation (before anything is enqueued), workspace
+// carving and launch sequencing for the verify step. No device allocation, no
+// synchronisation, no state kept between calls.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <string>
+
+#include "internal.h"
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+int ok() {
+  g_err.clear();
+  return MOLT_OK;
+}
+
+int hip_status(hipError_t e, const char* where) {
+  if (e != hipSuccess) return fail(MOLT_ERR_HIP, "%s: %s", where, hipGetErrorString(e));
+  return ok();
+}
+
+// ---- kernel-group timing with HIP events (opt-in, process-wide)
+struct Profiler {
+  static constexpr int kPairs = 4096;
+  bool on = false;
+  bool ready = false;
+  hipEvent_t ev[2 * kPairs];
+  int used = 0;
+  int group[kPairs];
+};
+Profiler g_prof;
+
+struct ProfScope {
+  int slot = -1;
+  hipStream_t s;
+  ProfScope(int grp, hipStream_t st) : s(st) {
+    if (!g_prof.on || g_prof.used >= Profiler::kPairs) return;
+    slot = g_prof.used++;
+    g_prof.group[slot] = grp;
+    hipEventRecord(g_prof.ev[2 * slot], s);
+  }
+  ~ProfScope() {
+    if (slot >= 0) hipEventRecord(g_prof.ev[2 * slot + 1], s);
+  }
+};
+
+#define REQUIRE(cond, ...)                                   \
+  do {                                                       \
+    if (!(cond)) return fail(MOLT_ERR_INVALID_ARG, __VA_ARGS__); \
+  } while (0)
+
+int check_ws(void* ws, size_t have, size_t need) {
+  if (need > 0 && (ws == nullptr || have < need))
+    return fail(MOLT_ERR_WORKSPACE, "workspace of %zu bytes at %p is smaller than the %zu required",
+                have, ws, need);
+  return MOLT_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* molt_last_error(void) { return g_err.c_str(); }
+
+int molt_version(void) { return 100; }
+
+// ------------------------------------------------------------------ profiling
+
+int molt_profile_enable(int enable) {
+  if (enable && !g_prof.ready) {
+    for (int i = 0; i < 2 * Profiler::kPairs; ++i) {
+      hipError_t e = hipEventCreate(&g_prof.ev[i]);
+      if (e != hipSuccess) return hip_status(e, "molt_profile_enable");
+    }
+    g_prof.ready = true;
+  }
+  if (enable) g_prof.used = 0;
+  g_prof.on = enable != 0;
+  return ok();
+}
+
+int molt_profile_read(int group, double* total_ms, int* launches) {
+  REQUIRE(total_ms && launches, "NULL output pointer");
+  double tot = 0.0;
+  int n = 0;
+  for (int i = 0; i < g_prof.used; ++i) {
+    if (g_prof.group[i] != group) continue;
+    hipError_t e = hipEventSynchronize(g_prof.ev[2 * i + 1]);
+    if (e != hipSuccess) return hip_status(e, "molt_profile_read");
+    float ms = 0.f;
+    e = hipEventElapsedTime(&ms, g_prof.ev[2 * i], g_prof.ev[2 * i + 1]);
+    if (e != hipSuccess) return hip_status(e, "molt_profile_read");
+    tot += ms;
+    ++n;
+  }
+  *total_ms = tot;
+  *launches = n;
+  return ok();
+}
+
+// ------------------------------------------------------------------ spec accept
+
+static int spec_accept_shape_ok(int B, int k, int V) {
+  REQUIRE(B >= 1, "B = %d must be >= 1", B);
+  REQUIRE(k >= 0, "k = %d must be >= 0", k);
+  REQUIRE(V >= 1, "V = %d must be >= 1", V);
+  const double rows = double(B) * (k + 1);
+  REQUIRE(rows * V < 4.0e18, "B*(k+1)*V too large");
+  const double nch = std::ceil(double(V) / molt::sampler_chunk_elems());
+  REQUIRE(rows * nch < 16777216.0, "B*(k+1)*ceil(V/%d) = %.0f exceeds 2^24 workgroups",
+          molt::sampler_chunk_elems(), rows * nch);
+  return MOLT_OK;
+}
+
+size_t molt_spec_accept_workspace_size(int B, int k, int V) {
+  if (B < 1 || k < 0 || V < 1) return 0;
+  return molt::sampler_ws_bytes(B, k, V);
+}
+
+int molt_spec_accept(const float* logits, const float* draft_probs, const int32_t* draft_tokens,
+                     const float* uniforms, int B, int k, int V, int32_t* out_tokens,
+                     int32_t* out_num_accepted, float* out_logprobs, void* workspace,
+                     size_t workspace_bytes, molt_stream_t stream) {
+  if (int r = spec_accept_shape_ok(B, k, V)) return r;
+  REQUIRE(logits, "logits is NULL");
+  REQUIRE(uniforms, "uniforms is NULL");
+  REQUIRE(k == 0 || draft_tokens, "draft_tokens is NULL with k = %d", k);
+  REQUIRE(out_tokens, "out_tokens is NULL");
+  REQUIRE(out_num_accepted, "out_num_accepted is NULL");
+  if (int r = check_ws(workspace, workspace_bytes, molt_spec_accept_workspace_size(B, k, V)))
+    return r;
+  hipError_t e;
+  {
+    ProfScope ps(MOLT_PROF_SAMPLER, reinterpret_cast<hipStream_t>(stream));
+    e = molt::launch_spec_accept(logits, draft_probs, draft_tokens, uniforms, B, k, V, out_tokens,
+                                 out_num_accepted, out_logprobs, workspace,
+                                 reinterpret_cast<hipStream_t>(stream));
+  }
+  return hip_status(e, "molt_spec_accept");
+}
+
+// ------------------------------------------------------------------ helpers
+
+static size_t dt_size(molt_dtype t) { return t == MOLT_F32 ? 4 : t == MOLT_BF16 ? 2 : 1; }
+
+static bool act_ok(molt_dtype a) { return a == MOLT_F32 || a == MOLT_BF16; }
+
+static bool pair_ok(molt_dtype act, molt_dtype w) {
+  return (act == MOLT_F32 && w == MOLT_F32) || (act == MOLT_BF16 && (w == MOLT_BF16 || w == MOLT_FP8_E4M3));
+}
+
+namespace {
+
+struct MoeWs {
+  float* g; int32_t* ids; float* w; int32_t* counts; int32_t* offsets; int32_t* perm;
+  int32_t* inv; int32_t* tiles; int32_t* n_tiles; uint8_t* xq; float* xs; void* h; uint8_t* hq;
+  float* hs; float* o; int max_tiles;
+};
+
+MoeWs carve_moe(molt::Carver& c, int T, int d, int E, int K, int F, molt_dtype act, molt_dtype w) {
+  MoeWs m{};
+  const long P = long(T) * K;
+  const int tm = molt::moe_tile_m(w);
+  m.max_tiles = molt::max_expert_tiles(T, E, K, tm);
+  m.g = c.take<float>(long(T) * E);
+  m.ids = c.take<int32_t>(P);
+  m.w = c.take<float>(P);
+  m.counts = c.take<int32_t>(E);
+  m.offsets = c.take<int32_t>(E + 1);
+  m.perm = c.take<int32_t>(P);
+  m.inv = c.take<int32_t>(P);
+  m.tiles = c.take<int32_t>(long(m.max_tiles) * 4);
+  m.n_tiles = c.take<int32_t>(1);
+  if (w == MOLT_FP8_E4M3) {
+    m.xq = c.take<uint8_t>(long(T) * d);
+    m.xs = c.take<float>(T);
+    m.hq = c.take<uint8_t>(P * F);
+    m.hs = c.take<float>(P);
+  }
+  m.h = c.take<uint8_t>(P * F * dt_size(act));
+  m.o = c.take<float>(P * d);
+  return m;
+}
+
+int moe_shape_ok(int T, int d, int E, int K, int F, molt_dtype act, molt_dtype w) {
+  REQUIRE(T >= 1, "T = %d must be >= 1", T);
+  REQUIRE(E >= 1 && E <= 256, "E = %d must be in [1, 256]", E);
+  REQUIRE(K >= 1 && K <= E && K <= 64, "K = %d must be in [1, min(E, 64)]", K);
+  REQUIRE(pair_ok(act, w), "unsupported (activation, expert) dtype pair (%d, %d)", int(act), int(w));
+  const int mult = w == MOLT_FP8_E4M3 ? 128 : 64;
+  REQUIRE(d >= mult && d % mult == 0, "d = %d must be a positive multiple of %d", d, mult);
+  REQUIRE(F >= mult && F % mult == 0, "F = %d must be a positive multiple of %d", F, mult);
+  REQUIRE(double(T) * K * (F > d ? F : d) < 2.0e9, "T*K*max(F, d) too large");
+  return MOLT_OK;
+}
+
+// Enqueues the MoE layer on normalised input x (act dtype; xq/xs = its fp8 codes when the
+// caller already quantised them). out = sum (accumulate: out += sum).
+hipError_t run_moe(const MoeWs& m, const void* x, const uint8_t* xq, const float* xs,
+                   const void* w_router, const float* bias, const void* w_gu, const void* w_d,
+                   const float* s_gu, const float* s_d, int T, int d, int E, int K, int F,
+                   molt_dtype act, molt_dtype wdt, const int32_t* replay, float* out,
+                   bool accumulate, hipStream_t s) {
+  hipError_t e;
+  {
+    ProfScope ps(MOLT_PROF_PROJECTIONS, s);
+    if ((e = molt::launch_gemm(x, w_router, m.g, T, E, d, act, false, s)) != hipSuccess) return e;
+  }
+  if ((e = molt::launch_route(m.g, bias, replay, T, E, K, m.ids, m.w, m.counts, m.offsets, m.perm,
+                              m.inv, molt::moe_tile_m(wdt), m.tiles, m.max_tiles, m.n_tiles, s)) !=
+      hipSuccess)
+    return e;
+  if (wdt == MOLT_FP8_E4M3 && xq == nullptr) {
+    if ((e = molt::launch_quant_rows_bf16(static_cast<const uint16_t*>(x), T, d, m.xq, m.xs, s)) !=
+        hipSuccess)
+      return e;
+    xq = m.xq;
+    xs = m.xs;
+  }
+  {
+    ProfScope ps(MOLT_PROF_EXPERT_GEMM, s);
+    if ((e = molt::launch_moe_gate_up(x, xq, xs, m.perm, K, w_gu, s_gu, d, F, act, wdt, m.tiles,
+                                      m.max_tiles, m.h, s)) != hipSuccess)
+      return e;
+  }
+  if (wdt == MOLT_FP8_E4M3) {
+    if ((e = molt::launch_quant_rows_bf16(static_cast<const uint16_t*>(m.h), T * K, F, m.hq, m.hs,
+                                          s)) != hipSuccess)
+      return e;
+  }
+  {
+    ProfScope ps(MOLT_PROF_EXPERT_GEMM, s);
+    if ((e = molt::launch_moe_down(m.h, m.hq, m.hs, w_d, s_d, d, F, act, wdt, m.tiles, m.max_tiles,
+                                   m.o, s)) != hipSuccess)
+      return e;
+  }
+  return molt::launch_combine(m.o, m.inv, m.w, T, K, d, out, accumulate, s);
+}
+
+hipError_t copy_out(void* dst, const void* src, size_t bytes, hipStream_t s) {
+  if (dst == nullptr || bytes == 0) return hipSuccess;
+  return hipMemcpyAsync(dst, src, bytes, hipMemcpyDeviceToDevice, s);
+}
+
+}  // namespace
+
+// ------------------------------------------------------------------ MoE layer
+
+size_t molt_moe_layer_workspace_size(int T, int d, int E, int K, int F, molt_dtype act,
+                                     molt_dtype w) {
+  if (T < 1 || E < 1 || K < 1 || d < 1 || F < 1 || !pair_ok(act, w)) return 0;
+  molt::Carver c(nullptr, 0);
+  carve_moe(c, T, d, E, K, F, act, w);
+  return c.used + 256;
+}
+
+int molt_moe_layer(const void* x, const void* w_router, const float* router_bias,
+                   const void* w_gate_up, const void* w_down, const float* s_gate_up,
+                   const float* s_down, int T, int d, int E, int K, int F, molt_dtype act_dtype,
+                   molt_dtype w_dtype, const int32_t* replay_ids, float* out, int32_t* out_ids,
+                   float* out_weights, int32_t* out_counts, int32_t* out_offsets,
+                   int32_t* out_perm, void* workspace, size_t workspace_bytes,
+                   molt_stream_t stream) {
+  if (int r = moe_shape_ok(T, d, E, K, F, act_dtype, w_dtype)) return r;
+  REQUIRE(x && w_router && w_gate_up && w_down && out, "a required pointer is NULL");
+  REQUIRE(w_dtype != MOLT_FP8_E4M3 || (s_gate_up && s_down), "fp8 experts need s_gate_up and s_down");
+  if (int r = check_ws(workspace, workspace_bytes,
+                       molt_moe_layer_workspace_size(T, d, E, K, F, act_dtype, w_dtype)))
+    return r;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  molt::Carver c(workspace, workspace_bytes);
+  MoeWs m = carve_moe(c, T, d, E, K, F, act_dtype, w_dtype);
+  hipError_t e = run_moe(m, x, nullptr, nullptr, w_router, router_bias, w_gate_up, w_down,
+                         s_gate_up, s_down, T, d, E, K, F, act_dtype, w_dtype, replay_ids, out,
+                         false, s);
+  const size_t P = size_t(T) * K;
+  if (e == hipSuccess) e = copy_out(out_ids, m.ids, P * 4, s);
+  if (e == hipSuccess) e = copy_out(out_weights, m.w, P * 4, s);
+  if (e == hipSuccess) e = copy_out(out_counts, m.counts, size_t(E) * 4, s);
+  if (e == hipSuccess) e = copy_out(out_offsets, m.offsets, size_t(E + 1) * 4, s);
+  if (e == hipSuccess) e = copy_out(out_perm, m.perm, P * 4, s);
+  return hip_status(e, "molt_moe_layer");
+}
+
+// ------------------------------------------------------------------ paged attention
+
+static int attn_shape_ok(int B, int k, int Hq, int Hkv, int D, int max_blocks, molt_dtype dt) {
+  REQUIRE(B >= 1, "B = %d must be >= 1", B);
+  REQUIRE(k >= 0, "k = %d must be >= 0", k);
+  REQUIRE(act_ok(dt), "attention dtype must be F32 or BF16");
+  REQUIRE(D == 64 || D == 128, "head_dim = %d must be 64 or 128", D);
+  REQUIRE(Hkv >= 1 && Hq >= Hkv && Hq % Hkv == 0, "n_q_heads %d must be a multiple of n_kv_heads %d", Hq, Hkv);
+  REQUIRE(dt == MOLT_F32 || (Hq / Hkv) * (k + 1) <= 128, "(Hq/Hkv)*(1+k) = %d exceeds 128", (Hq / Hkv) * (k + 1));
+  REQUIRE(max_blocks >= 1, "max_blocks_per_seq = %d must be >= 1", max_blocks);
+  REQUIRE(double(B) * Hkv * ((max_blocks + 63) / 64) < 2.0e9, "grid too large");
+  return MOLT_OK;
+}
+
+size_t molt_paged_attention_workspace_size(int B, int k, int Hq, int Hkv, int D, int max_blocks) {
+  if (B < 1 || k < 0 || Hq < 1 || Hkv < 1 || D < 1 || max_blocks < 1) return 0;
+  return molt::attention_ws_bytes(B, k, Hq, D, max_blocks);
+}
+
+int molt_paged_attention(const void* q, const void* k_cache, const void* v_cache,
+                         const int32_t* block_tables, const int32_t* context_lens, int B, int k,
+                         int Hq, int Hkv, int D, int max_blocks, molt_dtype dtype, void* out,
+                         void* workspace, size_t workspace_bytes, molt_stream_t stream) {
+  if (int r = attn_shape_ok(B, k, Hq, Hkv, D, max_blocks, dtype)) return r;
+  REQUIRE(q && k_cache && v_cache && block_tables && context_lens && out, "a required pointer is NULL");
+  const size_t need = molt_paged_attention_workspace_size(B, k, Hq, Hkv, D, max_blocks);
+  if (int r = check_ws(workspace, workspace_bytes, dtype == MOLT_F32 ? 0 : need)) return r;
+  hipError_t e;
+  {
+    ProfScope ps(MOLT_PROF_ATTENTION, reinterpret_cast<hipStream_t>(stream));
+    e = molt::launch_paged_attention(q, k_cache, v_cache, block_tables, context_lens, B, k, Hq, Hkv,
+                                     D, max_blocks, dtype, out, workspace,
+                                     reinterpret_cast<hipStream_t>(stream));
+  }
+  return hip_status(e, "molt_paged_attention");
+}
+
+// ------------------------------------------------------------------ decoder / verify step
+
+namespace {
+
+int model_ok(const molt_model* m, const molt_kv* kv, int B, int k, bool need_head) {
+  REQUIRE(m != nullptr, "model is NULL");
+  REQUIRE(m->n_layers >= 1, "n_layers = %d must be >= 1", m->n_layers);
+  REQUIRE(act_ok(m->dtype), "model dtype must be F32 or BF16");
+  if (int r = moe_shape_ok(B * (k + 1), m->d_model, m->n_experts, m->top_k, m->d_ff, m->dtype,
+                           m->expert_dtype))
+    return r;
+  REQUIRE(m->rms_eps >= 0.f, "rms_eps must be >= 0");
+  REQUIRE(m->rope_theta > 0.f, "rope_theta must be > 0");
+  REQUIRE(m->attn_norm && m->w_qkv && m->w_o && m->moe_norm && m->w_router && m->w_gate_up &&
+              m->w_down,
+          "a per-layer weight array is NULL");
+  for (int l = 0; l < m->n_layers; ++l) {
+    REQUIRE(m->attn_norm[l] && m->w_qkv[l] && m->w_o[l] && m->moe_norm[l] && m->w_router[l] &&
+                m->w_gate_up[l] && m->w_down[l],
+            "layer %d: a weight pointer is NULL", l);
+    if (m->expert_dtype == MOLT_FP8_E4M3)
+      REQUIRE(m->s_gate_up && m->s_down && m->s_gate_up[l] && m->s_down[l],
+              "layer %d: fp8 experts need s_gate_up and s_down", l);
+  }
+  if (need_head) {
+    REQUIRE(m->vocab >= 1, "vocab = %d must be >= 1", m->vocab);
+    REQUIRE(m->embed && m->lm_head && m->final_norm, "embed, final_norm and lm_head are required");
+  }
+  REQUIRE(kv != nullptr, "kv is NULL");
+  REQUIRE(kv->block_size == 16, "block_size = %d must be 16", kv->block_size);
+  REQUIRE(kv->k_cache && kv->v_cache && kv->block_tables && kv->context_lens, "a kv pointer is NULL");
+  for (int l = 0; l < m->n_layers; ++l)
+    REQUIRE(kv->k_cache[l] && kv->v_cache[l], "layer %d: cache pointer is NULL", l);
+  REQUIRE(kv->num_blocks >= 1, "num_blocks = %d must be >= 1", kv->num_blocks);
+  return attn_shape_ok(B, k, m->n_q_heads, m->n_kv_heads, m->head_dim, kv->max_blocks_per_seq,
+                       m->dtype);
+}
+
+struct DecWs {
+  void* y; uint8_t* yq; float* ys; float* qkv; void* q; void* attn; void* attn_ws; MoeWs moe;
+};
+
+DecWs carve_dec(molt::Carver& c, const molt_model* m, int B, int k, int max_blocks) {
+  DecWs w{};
+  const long T = long(B) * (k + 1);
+  const int d = m->d_model, D = m->head_dim, Hq = m->n_q_heads, Hkv = m->n_kv_heads;
+  const size_t es = dt_size(m->dtype);
+  w.y = c.take<uint8_t>(T * d * es);
+  if (m->expert_dtype == MOLT_FP8_E4M3) {
+    w.yq = c.take<uint8_t>(T * d);
+    w.ys = c.take<float>(T);
+  }
+  w.qkv = c.take<float>(T * (Hq + 2 * Hkv) * D);
+  w.q = c.take<uint8_t>(T * Hq * D * es);
+  w.attn = c.take<uint8_t>(T * Hq * D * es);
+  const size_t aws = m->dtype == MOLT_F32 ? 0 : molt::attention_ws_bytes(B, k, Hq, D, max_blocks);
+  w.attn_ws = c.take<uint8_t>(aws);
+  w.moe = carve_moe(c, int(T), d, m->n_experts, m->top_k, m->d_ff, m->dtype, m->expert_dtype);
+  return w;
+}
+
+hipError_t run_decoder(const DecWs& w, const molt_model* m, const molt_kv* kv, int B, int k,
+                       float* x, int32_t* routes, hipStream_t s) {
+  const int T = B * (k + 1);
+  const int d = m->d_model, D = m->head_dim, Hq = m->n_q_heads, Hkv = m->n_kv_heads;
+  const int K = m->top_k;
+  hipError_t e = hipSuccess;
+#define RUN(call) do { if ((e = (call)) != hipSuccess) return e; } while (0)
+  for (int l = 0; l < m->n_layers; ++l) {
+    RUN(molt::launch_rmsnorm(x, m->attn_norm[l], T, d, m->rms_eps, m->dtype, w.y, nullptr, nullptr, s));
+    {
+      ProfScope ps(MOLT_PROF_PROJECTIONS, s);
+      RUN(molt::launch_gemm(w.y, m->w_qkv[l], w.qkv, T, (Hq + 2 * Hkv) * D, d, m->dtype, false, s));
+    }
+    RUN(molt::launch_rope_kv_write(w.qkv, B, k, Hq, Hkv, D, m->rope_theta, kv->context_lens,
+                                   kv->block_tables, kv->max_blocks_per_seq, kv->num_blocks,
+                                   m->dtype, w.q, kv->k_cache[l], kv->v_cache[l], s));
+    {
+      ProfScope ps(MOLT_PROF_ATTENTION, s);
+      RUN(molt::launch_paged_attention(w.q, kv->k_cache[l], kv->v_cache[l], kv->block_tables,
+                                       kv->context_lens, B, k, Hq, Hkv, D, kv->max_blocks_per_seq,
+                                       m->dtype, w.attn, w.attn_ws, s));
+    }
+    {
+      ProfScope ps(MOLT_PROF_PROJECTIONS, s);
+      RUN(molt::launch_gemm(w.attn, m->w_o[l], x, T, d, Hq * D, m->dtype, true, s));
+    }
+    const bool fp8 = m->expert_dtype == MOLT_FP8_E4M3;
+    RUN(molt::launch_rmsnorm(x, m->moe_norm[l], T, d, m->rms_eps, m->dtype, w.y,
+                             fp8 ? w.yq : nullptr, fp8 ? w.ys : nullptr, s));
+    RUN(run_moe(w.moe, w.y, fp8 ? w.yq : nullptr, fp8 ? w.ys : nullptr, m->w_router[l],
+                m->router_bias ? m->router_bias[l] : nullptr, m->w_gate_up[l], m->w_down[l],
+                fp8 ? m->s_gate_up[l] : nullptr, fp8 ? m->s_down[l] : nullptr, T, d,
+                m->n_experts, K, m->d_ff, m->dtype, m->expert_dtype, nullptr, x, true, s));
+    if (routes) RUN(copy_out(routes + size_t(l) * T * K, w.moe.ids, size_t(T) * K * 4, s));
+  }
+#undef RUN
+  return e;
+}
+
+}  // namespace
+
+size_t molt_decoder_workspace_size(const molt_model* m, int B, int k, int max_blocks) {
+  if (!m || B < 1 || k < 0 || max_blocks < 1 || !pair_ok(m->dtype, m->expert_dtype)) return 0;
+  molt::Carver c(nullptr, 0);
+  carve_dec(c, m, B, k, max_blocks);
+  return c.used + 256;
+}
+
+int molt_decoder_forward(const molt_model* m, const molt_kv* kv, int B, int k, float* x,
+                         int32_t* out_routes, void* workspace, size_t workspace_bytes,
+                         molt_stream_t stream) {
+  if (int r = model_ok(m, kv, B, k, false)) return r;
+  REQUIRE(x, "x is NULL");
+  if (int r = check_ws(workspace, workspace_bytes,
+                       molt_decoder_workspace_size(m, B, k, kv->max_blocks_per_seq)))
+    return r;
+  molt::Carver c(workspace, workspace_bytes);
+  DecWs w = carve_dec(c, m, B, k, kv->max_blocks_per_seq);
+  return hip_status(run_decoder(w, m, kv, B, k, x, out_routes, reinterpret_cast<hipStream_t>(stream)),
+                    "molt_decoder_forward");
+}
+
+namespace {
+struct StepWs { float* x; void* yf; float* logits; void* samp; DecWs dec; };
+StepWs carve_step(molt::Carver& c, const molt_model* m, int B, int k, int max_blocks, bool own_logits) {
+  StepWs w{};
+  const long T = long(B) * (k + 1);
+  w.x = c.take<float>(T * m->d_model);
+  w.yf = c.take<uint8_t>(T * m->d_model * dt_size(m->dtype));
+  w.logits = own_logits ? c.take<float>(T * long(m->vocab)) : nullptr;
+  w.samp = c.take<uint8_t>(molt::sampler_ws_bytes(B, k, m->vocab));
+  w.dec = carve_dec(c, m, B, k, max_blocks);
+  return w;
+}
+}  // namespace
+
+size_t molt_verify_step_workspace_size(const molt_model* m, int B, int k, int max_blocks) {
+  if (!m || B < 1 || k < 0 || max_blocks < 1 || m->vocab < 1 || !pair_ok(m->dtype, m->expert_dtype))
+    return 0;
+  molt::Carver c(nullptr, 0);
+  carve_step(c, m, B, k, max_blocks, true);
+  return c.used + 256;
+}
+
+int molt_verify_step(const molt_model* m, const molt_kv* kv, int B, int k, const int32_t* tokens,
+                     const float* draft_probs, const float* uniforms, float* out_logits,
+                     int32_t* out_tokens, int32_t* out_num_accepted, float* out_logprobs,
+                     int32_t* out_routes, void* workspace, size_t workspace_bytes,
+                     molt_stream_t stream) {
+  if (int r = model_ok(m, kv, B, k, true)) return r;
+  if (int r = spec_accept_shape_ok(B, k, m->vocab)) return r;
+  REQUIRE(tokens && uniforms && out_tokens && out_num_accepted, "a required pointer is NULL");
+  if (int r = check_ws(workspace, workspace_bytes,
+                       molt_verify_step_workspace_size(m, B, k, kv->max_blocks_per_seq)))
+    return r;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  molt::Carver c(workspace, workspace_bytes);
+  StepWs w = carve_step(c, m, B, k, kv->max_blocks_per_seq, true);
+  float* logits = out_logits ? out_logits : w.logits;
+  const int T = B * (k + 1);
+  hipError_t e = molt::launch_embed(m->embed, tokens, T, m->d_model, m->vocab, m->dtype, w.x, s);
+  if (e == hipSuccess) e = run_decoder(w.dec, m, kv, B, k, w.x, out_routes, s);
+  if (e == hipSuccess)
+    e = molt::launch_rmsnorm(w.x, m->final_norm, T, m->d_model, m->rms_eps, m->dtype, w.yf,
+                             nullptr, nullptr, s);
+  if (e == hipSuccess) {
+    ProfScope ps(MOLT_PROF_LM_HEAD, s);
+    e = molt::launch_gemm(w.yf, m->lm_head, logits, T, m->vocab, m->d_model, m->dtype, false, s);
+  }
+  // drafts are tokens[:, 1:]: the sampler reads them with row stride k+1
+  if (e == hipSuccess) {
+    ProfScope ps(MOLT_PROF_SAMPLER, s);
+    e = molt::launch_spec_accept(logits, draft_probs, tokens, uniforms, B, k, m->vocab, out_tokens,
+                                 out_num_accepted, out_logprobs, w.samp, s, k + 1, 1);
+  }
+  return hip_status(e, "molt_verify_step");
+}
+
+}  // extern "C"

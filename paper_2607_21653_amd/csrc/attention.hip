@@ -1,0 +1,386 @@
+// Multi-query paged decode attention of the verify step (PagedAttention cache, paper
+// Sec. 2; k speculative tokens per sequence, Sec. 4.1). For sequence b and kv head h the
+// R = G*(1+k) query rows (G = Hq/Hkv query heads, 1+k positions) share every key/value
+// block, so each K/V byte is read once per (b, h) and reused by all R rows on MFMA.
+//
+// Work split: workgroup = (b, h, split of kBlocksPerSplit 16-token blocks), 4 wavefronts.
+// Each wavefront takes block pairs (32 keys) round-robin and keeps its own online
+// softmax. Per pair, on v_mfma_f32_16x16x32_bf16:
+//   S^T[32 keys x R] = K Q^T   (A = K rows straight from the cache: [16 keys x 32 dims]
+//                               per operand, 16 B per lane; B = Q^T held in registers)
+//   O^T[D x R]      += V^T P^T (A = V^T: the V cache stores a block as [D][16 tokens], so
+//                               a lane's 4 consecutive keys of one dim are 8 contiguous
+//                               bytes; B = P^T is exactly the S^T accumulator layout
+//                               rounded to bf16: no cross-lane shuffles)
+// The MFMA k-index is a free permutation as long as A and B agree: slot s of lane group g
+// is key 4g+s of the first block (s < 4) or of the second block (s >= 4).
+// Causality: row r = j*G + g (position j) sees keys <= ctx_b + j. Softmax in f32 with
+// exp2 of log2(e)-scaled scores. The four wavefronts merge through LDS in a fixed order;
+// splits are merged by a log-sum-exp pass (a single split writes the output directly).
+#include "device_common.h"
+#include "internal.h"
+
+namespace molt {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kWaves = 4;
+constexpr int kBlocksPerSplit = 64;  // 1024 keys per workgroup
+constexpr float kLog2e = 1.4426950408889634f;
+
+typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
+
+struct AttnParams {
+  const uint16_t* q;       // [T, Hq, D]
+  const uint16_t* kc;      // [nb, Hkv, 16, D]
+  const uint16_t* vc;      // [nb, Hkv, D, 16]
+  const int32_t* bt;       // [B, max_blocks]
+  const int32_t* ctx;      // [B]
+  uint16_t* out;           // [T, Hq * D]
+  float* part_o;           // [B, Hkv, S, R, D]
+  float* part_ml;          // [B, Hkv, S, R, 2]
+  int k, Hq, Hkv, max_blocks, splits;
+  float scale_log2;        // log2(e) / sqrt(D)
+};
+
+template <int D, int RT>
+__global__ __launch_bounds__(kThreads) void attn_mfma_kernel(AttnParams p) {
+  constexpr int DS = D / 32;      // 32-dim k-steps for S
+  constexpr int DT = D / 16;      // 16-dim tiles of O^T
+  constexpr int RP = RT * 16;     // padded rows
+  __shared__ float s_m[kWaves][RP];
+  __shared__ float s_l[kWaves][RP];
+  __shared__ float s_o[RP * D];
+
+  const int split = blockIdx.x % p.splits;
+  const int bh = blockIdx.x / p.splits;
+  const int b = bh / p.Hkv, h = bh % p.Hkv;
+  const int G = p.Hq / p.Hkv;
+  const int kp1 = p.k + 1;
+  const int R = G * kp1;
+  const int ctx = p.ctx[b];
+  const int nkeys = ctx + kp1;
+  const int nblk = (nkeys + 15) / 16;
+  const int blk0 = split * kBlocksPerSplit;
+  const int blk1 = min(blk0 + kBlocksPerSplit, nblk);
+  const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+  const int l16 = lane % 16, g4 = lane / 16;
+
+  // Q^T fragments: row r = l16 + 16 * rt; dims [32 s + 8 g4, +8)
+  bf16x8_t qf[RT][DS];
+  int rowj[RT];
+#pragma unroll
+  for (int rt = 0; rt < RT; ++rt) {
+    const int r = rt * 16 + l16;
+    const int j = r / G, gi = r % G;
+    rowj[rt] = r < R ? j : -1;
+#pragma unroll
+    for (int s = 0; s < DS; ++s) {
+      if (r < R) {
+        const uint16_t* src = p.q + ((long(b) * kp1 + j) * p.Hq + h * G + gi) * D + s * 32 + g4 * 8;
+        qf[rt][s] = *reinterpret_cast<const bf16x8_t*>(src);
+      } else {
+        for (int e = 0; e < 8; ++e) qf[rt][s][e] = __bf16(0.f);
+      }
+    }
+  }
+
+  floatx4_t o[DT][RT];
+#pragma unroll
+  for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt) o[dt][rt] = floatx4_t{0.f, 0.f, 0.f, 0.f};
+  float m_run[RT], l_run[RT];
+#pragma unroll
+  for (int rt = 0; rt < RT; ++rt) { m_run[rt] = -INFINITY; l_run[rt] = 0.f; }
+
+  const int* btab = p.bt + long(b) * p.max_blocks;
+  const long kv_blk_stride = long(p.Hkv) * 16 * D;
+  for (int pb = blk0 + 2 * wave; pb < blk1; pb += 2 * kWaves) {
+    const int pb2 = pb + 1;
+    const bool has2 = pb2 < blk1;
+    const long phys0 = btab[pb];
+    const long phys1 = has2 ? btab[pb2] : phys0;
+    // K fragments: two 16-key tiles, DS dim steps
+    bf16x8_t kf[2][DS];
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+      const long phys = t == 0 ? phys0 : phys1;
+      const uint16_t* kb = p.kc + phys * kv_blk_stride + long(h) * 16 * D + l16 * D + g4 * 8;
+#pragma unroll
+      for (int s = 0; s < DS; ++s) kf[t][s] = *reinterpret_cast<const bf16x8_t*>(kb + s * 32);
+    }
+    // V^T fragments: dim tile dt, lane dim = 16 dt + l16, keys 4 g4 .. +3 of each block
+    bf16x8_t vf[DT];
+    {
+      const uint16_t* v0 = p.vc + phys0 * kv_blk_stride + long(h) * D * 16 + l16 * 16 + g4 * 4;
+      const uint16_t* v1 = p.vc + phys1 * kv_blk_stride + long(h) * D * 16 + l16 * 16 + g4 * 4;
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) {
+        const bf16x4_t a = *reinterpret_cast<const bf16x4_t*>(v0 + dt * 16 * 16);
+        const bf16x4_t c = *reinterpret_cast<const bf16x4_t*>(v1 + dt * 16 * 16);
+        vf[dt] = bf16x8_t{a[0], a[1], a[2], a[3], c[0], c[1], c[2], c[3]};
+      }
+    }
+    // S^T tiles
+    floatx4_t st[2][RT];
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+      for (int rt = 0; rt < RT; ++rt) {
+        floatx4_t acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int s = 0; s < DS; ++s)
+          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[t][s], qf[rt][s], acc, 0, 0, 0);
+        st[t][rt] = acc;
+      }
+    // online softmax per row; lane holds keys 4 g4 + e of block pb (t=0) and pb2 (t=1)
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt) {
+      const int lim = rowj[rt] < 0 ? -1 : ctx + rowj[rt];   // last visible key position
+      float sv[8];
+      float mx = -INFINITY;
+#pragma unroll
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int kpos = (t == 0 ? pb : pb2) * 16 + g4 * 4 + e;
+          const bool vis = (t == 0 || has2) && kpos <= lim;
+          const float v = vis ? st[t][rt][e] * p.scale_log2 : -INFINITY;
+          sv[t * 4 + e] = v;
+          mx = fmaxf(mx, v);
+        }
+      mx = fmaxf(mx, __shfl_xor(mx, 16, kWave));
+      mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
+      const float m_new = fmaxf(m_run[rt], mx);
+      const float alpha = (m_new == -INFINITY) ? 1.f : exp2f(m_run[rt] - m_new);
+      float ps = 0.f;
+      bf16x8_t pf;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float pe = (sv[e] == -INFINITY) ? 0.f : exp2f(sv[e] - m_new);
+        const __bf16 pb16 = __bf16(pe);
+        pf[e] = pb16;
+        ps += float(pb16);   // the normaliser sums the same rounded weights the MFMA uses
+      }
+      l_run[rt] = l_run[rt] * alpha + ps;
+      m_run[rt] = m_new;
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) {
+        o[dt][rt] *= alpha;
+        o[dt][rt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf[dt], pf, o[dt][rt], 0, 0, 0);
+      }
+    }
+  }
+
+  // ---- merge the four wavefronts (fixed order), then write
+#pragma unroll
+  for (int rt = 0; rt < RT; ++rt) {
+    float lt = l_run[rt];
+    lt += __shfl_xor(lt, 16, kWave);
+    lt += __shfl_xor(lt, 32, kWave);
+    if (g4 == 0) {
+      s_m[wave][rt * 16 + l16] = m_run[rt];
+      s_l[wave][rt * 16 + l16] = lt;
+    }
+  }
+  __syncthreads();
+  float fac[RT];
+#pragma unroll
+  for (int rt = 0; rt < RT; ++rt) {
+    const int r = rt * 16 + l16;
+    float M = -INFINITY;
+    for (int w = 0; w < kWaves; ++w) M = fmaxf(M, s_m[w][r]);
+    fac[rt] = (s_m[wave][r] == -INFINITY) ? 0.f : exp2f(s_m[wave][r] - M);
+  }
+  // O^T accumulator element e of lane: dim 16 dt + 4 g4 + e, row 16 rt + l16
+  for (int w = 0; w < kWaves; ++w) {
+    if (wave == w) {
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const int idx = (rt * 16 + l16) * D + dt * 16 + g4 * 4 + e;
+            const float v = o[dt][rt][e] * fac[rt];
+            s_o[idx] = (w == 0) ? v : s_o[idx] + v;
+          }
+    }
+    __syncthreads();
+  }
+  // final row statistics and output
+  for (int idx = threadIdx.x; idx < R * D; idx += kThreads) {
+    const int r = idx / D, dd = idx % D;
+    float M = -INFINITY;
+    for (int w = 0; w < kWaves; ++w) M = fmaxf(M, s_m[w][r]);
+    float Lsum = 0.f;
+    for (int w = 0; w < kWaves; ++w)
+      if (s_m[w][r] != -INFINITY) Lsum += s_l[w][r] * exp2f(s_m[w][r] - M);
+    const int j = r / G, gi = r % G;
+    if (p.splits == 1) {
+      const float v = Lsum > 0.f ? s_o[idx] / Lsum : 0.f;
+      p.out[((long(b) * kp1 + j) * p.Hq + h * G + gi) * D + dd] = f32_to_bf16(v);
+    } else {
+      const long pr = (long(bh) * p.splits + split) * R + r;
+      p.part_o[pr * D + dd] = s_o[idx];
+      if (dd == 0) {
+        p.part_ml[pr * 2 + 0] = M;
+        p.part_ml[pr * 2 + 1] = Lsum;
+      }
+    }
+  }
+}
+
+// log-sum-exp merge over splits: one workgroup per (b, h, row), threads over dims
+template <int D>
+__global__ __launch_bounds__(D) void attn_merge_kernel(AttnParams p, int out_f32) {
+  const int G = p.Hq / p.Hkv;
+  const int kp1 = p.k + 1;
+  const int R = G * kp1;
+  const int r = blockIdx.x % R;
+  const int bh = blockIdx.x / R;
+  const int b = bh / p.Hkv, h = bh % p.Hkv;
+  const int nblk = (p.ctx[b] + kp1 + 15) / 16;
+  const int ns = min(p.splits, (nblk + kBlocksPerSplit - 1) / kBlocksPerSplit);
+  float M = -INFINITY;
+  for (int s = 0; s < ns; ++s) M = fmaxf(M, p.part_ml[((long(bh) * p.splits + s) * R + r) * 2]);
+  float L = 0.f, acc = 0.f;
+  for (int s = 0; s < ns; ++s) {
+    const long pr = (long(bh) * p.splits + s) * R + r;
+    const float m = p.part_ml[pr * 2];
+    if (m == -INFINITY) continue;
+    const float f = exp2f(m - M);
+    L += p.part_ml[pr * 2 + 1] * f;
+    acc += p.part_o[pr * D + threadIdx.x] * f;
+  }
+  const int j = r / G, gi = r % G;
+  const float v = L > 0.f ? acc / L : 0.f;
+  const long oi = ((long(b) * kp1 + j) * p.Hq + h * G + gi) * D + threadIdx.x;
+  if (out_f32) reinterpret_cast<float*>(p.out)[oi] = v;
+  else p.out[oi] = f32_to_bf16(v);
+}
+
+// ---------------------------------------------------------------- f32 VALU path
+// One wavefront per (token, query head); 64 keys per step, one key per lane for the
+// scores, one dim per lane for the output. Writes per-split partials like the MFMA path.
+__global__ __launch_bounds__(kWave) void attn_f32_kernel(const float* __restrict__ q,
+                                                         const float* __restrict__ kc,
+                                                         const float* __restrict__ vc,
+                                                         AttnParams p, int D) {
+  const int t = blockIdx.x / p.Hq, hq = blockIdx.x % p.Hq;
+  const int kp1 = p.k + 1;
+  const int b = t / kp1, j = t % kp1;
+  const int G = p.Hq / p.Hkv, h = hq / G;
+  const int lim = p.ctx[b] + j;   // last visible key
+  const float* qr = q + (long(t) * p.Hq + hq) * D;
+  const int* btab = p.bt + long(b) * p.max_blocks;
+  const long bs = long(p.Hkv) * 16 * D;
+  const int lane = threadIdx.x;
+  float m = -INFINITY, l = 0.f;
+  float acc[4] = {0.f, 0.f, 0.f, 0.f};   // dims lane, lane+64, ... (D <= 256)
+  const float scale = 1.0f / sqrtf(float(D));
+  for (int k0 = 0; k0 <= lim; k0 += kWave) {
+    const int kp = k0 + lane;
+    float s = -INFINITY;
+    if (kp <= lim) {
+      const float* kr = kc + btab[kp / 16] * bs + long(h) * 16 * D + (kp % 16) * D;
+      float d = 0.f;
+      for (int i = 0; i < D; ++i) d += qr[i] * kr[i];
+      s = d * scale;
+    }
+    const float mx = wave_max(s);
+    const float mn = fmaxf(m, mx);
+    const float alpha = m == -INFINITY ? 0.f : expf(m - mn);
+    const float pe = s == -INFINITY ? 0.f : expf(s - mn);
+    l = l * alpha + wave_sum(pe);
+    for (int c = 0; c < 4; ++c) acc[c] *= alpha;
+    const int nk = min(kWave, lim + 1 - k0);
+    for (int key = 0; key < nk; ++key) {
+      const float pk = __shfl(pe, key, kWave);
+      const int kk = k0 + key;
+      const float* vr = vc + btab[kk / 16] * bs + long(h) * D * 16 + (kk % 16);
+      for (int c = 0; c < 4; ++c) {
+        const int dd = lane + kWave * c;
+        if (dd < D) acc[c] += pk * vr[dd * 16];
+      }
+    }
+    m = mn;
+  }
+  float* out = reinterpret_cast<float*>(p.out) + (long(t) * p.Hq + hq) * D;
+  for (int c = 0; c < 4; ++c) {
+    const int dd = lane + kWave * c;
+    if (dd < D) out[dd] = acc[c] / l;
+  }
+}
+
+int splits_for(int max_blocks) { return (max_blocks + kBlocksPerSplit - 1) / kBlocksPerSplit; }
+
+template <int D, int RT>
+void launch_mfma(const AttnParams& p, int B, hipStream_t s) {
+  attn_mfma_kernel<D, RT><<<B * p.Hkv * p.splits, kThreads, 0, s>>>(p);
+}
+
+template <int D>
+hipError_t launch_d(const AttnParams& p, int B, int R, hipStream_t s) {
+  const int rt = (R + 15) / 16;
+  switch (rt) {
+    case 1: launch_mfma<D, 1>(p, B, s); break;
+    case 2: launch_mfma<D, 2>(p, B, s); break;
+    case 3: launch_mfma<D, 3>(p, B, s); break;
+    case 4: launch_mfma<D, 4>(p, B, s); break;
+    case 5: launch_mfma<D, 5>(p, B, s); break;
+    case 6: launch_mfma<D, 6>(p, B, s); break;
+    case 7: launch_mfma<D, 7>(p, B, s); break;
+    case 8: launch_mfma<D, 8>(p, B, s); break;
+    default: return hipErrorInvalidValue;
+  }
+  if (p.splits > 1) attn_merge_kernel<D><<<B * p.Hkv * R, D, 0, s>>>(p, 0);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+size_t attention_ws_bytes(int B, int k, int Hq, int D, int max_blocks) {
+  const int S = splits_for(max_blocks);
+  if (S <= 1) return 0;
+  const long rows = long(B) * (k + 1) * Hq;   // = B * Hkv * R
+  Carver c(nullptr, 0);
+  c.take<float>(rows * S * D);
+  c.take<float>(rows * S * 2);
+  return c.used + 256;
+}
+
+hipError_t launch_paged_attention(const void* q, const void* kc, const void* vc, const int32_t* bt,
+                                  const int32_t* ctx, int B, int k, int Hq, int Hkv, int D,
+                                  int max_blocks, molt_dtype dt, void* out, void* ws,
+                                  hipStream_t s) {
+  AttnParams p{};
+  p.q = static_cast<const uint16_t*>(q);
+  p.kc = static_cast<const uint16_t*>(kc);
+  p.vc = static_cast<const uint16_t*>(vc);
+  p.bt = bt;
+  p.ctx = ctx;
+  p.out = static_cast<uint16_t*>(out);
+  p.k = k; p.Hq = Hq; p.Hkv = Hkv; p.max_blocks = max_blocks;
+  p.scale_log2 = kLog2e / sqrtf(float(D));
+  const int R = (Hq / Hkv) * (k + 1);
+  if (dt == MOLT_F32) {
+    attn_f32_kernel<<<B * (k + 1) * Hq, kWave, 0, s>>>(static_cast<const float*>(q),
+                                                        static_cast<const float*>(kc),
+                                                        static_cast<const float*>(vc), p, D);
+    return hipGetLastError();
+  }
+  p.splits = splits_for(max_blocks);
+  if (p.splits > 1) {
+    const long rows = long(B) * (k + 1) * Hq;
+    Carver c(ws, 0);
+    p.part_o = c.take<float>(rows * p.splits * D);
+    p.part_ml = c.take<float>(rows * p.splits * 2);
+  }
+  if (D == 128) return launch_d<128>(p, B, R, s);
+  if (D == 64) return launch_d<64>(p, B, R, s);
+  return hipErrorInvalidValue;
+}
+
+}  // namespace molt

@@ -1,0 +1,124 @@
+// Device helpers shared by the gfx950 kernels: number formats, wavefront
+// reductions, MFMA operand types. 64-wide wavefronts throughout.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#define MOLT_DEV __device__ __forceinline__
+
+constexpr int kWave = 64;
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float floatx4_t __attribute__((ext_vector_type(4)));
+typedef float floatx16_t __attribute__((ext_vector_type(16)));
+typedef int int32x8_t __attribute__((ext_vector_type(8)));
+typedef int int32x4_t __attribute__((ext_vector_type(4)));
+typedef long int64x2_t __attribute__((ext_vector_type(2)));
+
+// ---------------------------------------------------------------- bf16
+
+MOLT_DEV float bf16_to_f32(uint16_t h) { return __uint_as_float(uint32_t(h) << 16); }
+
+// round to nearest, ties to even; NaN kept quiet
+MOLT_DEV uint16_t f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return uint16_t((u >> 16) | 0x40u);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return uint16_t(u >> 16);
+}
+
+MOLT_DEV float round_to_bf16(float f) { return bf16_to_f32(f32_to_bf16(f)); }
+
+// ---------------------------------------------------------------- fp8 e4m3fn (OCP)
+
+// Exact decode of an e4m3fn code (bias 7, subnormals, 0x7f/0xff NaN).
+MOLT_DEV float fp8e4m3_to_f32(uint32_t c) {
+  uint32_t s = (c & 0x80u) << 24;
+  uint32_t e = (c >> 3) & 0xfu;
+  uint32_t m = c & 0x7u;
+  if (e == 0xfu && m == 0x7u) return __uint_as_float(0x7fc00000u | s);
+  if (e == 0) return __uint_as_float(s) + (s ? -1.0f : 1.0f) * float(m) * 0.001953125f;  // m * 2^-9
+  return __uint_as_float(s | ((e + 120u) << 23) | (m << 20));
+}
+
+// float -> e4m3fn: round to nearest even, saturate finite overflow to +-448, NaN -> 0x7f.
+// Integer implementation on the binary32 encoding.
+MOLT_DEV uint32_t f32_to_fp8e4m3(float f) {
+  uint32_t u = __float_as_uint(f);
+  uint32_t sign = (u >> 24) & 0x80u;
+  uint32_t a = u & 0x7fffffffu;
+  if (a > 0x7f800000u) return 0x7fu;
+  if (a >= 0x43e00000u) return sign | 0x7eu;   // |f| >= 448 (incl. inf): saturate
+  int e = int(a >> 23) - 127;                  // unbiased exponent of |f|
+  if (e < -6) {
+    // subnormal target: value = n * 2^-9, n = rne(|f| * 2^9)
+    if (e < -11) return sign;                  // < 2^-11: rounds to 0 (2^-10 tie -> 0 handled below)
+    uint32_t mant = (a & 0x7fffffu) | 0x800000u;   // 24-bit significand, value = mant * 2^(e-23)
+    int shift = -9 - (e - 23);                 // n = mant * 2^(e-23+9) = mant >> shift
+    uint32_t n = mant >> shift;
+    uint32_t rem = mant & ((1u << shift) - 1u);
+    uint32_t half = 1u << (shift - 1);
+    if (rem > half || (rem == half && (n & 1u))) n++;
+    return sign | n;                           // n == 8 lands on the smallest normal code
+  }
+  // normal target: keep 3 mantissa bits, round to nearest even
+  uint32_t mant = a & 0x7fffffu;
+  uint32_t q = mant >> 20;
+  uint32_t rem = mant & 0xfffffu;
+  uint32_t code = (uint32_t(e + 7) << 3) | q;
+  if (rem > 0x80000u || (rem == 0x80000u && (q & 1u))) code++;
+  if (code > 0x7eu) code = 0x7eu;              // rounding past 448 saturates
+  return sign | code;
+}
+
+// ---------------------------------------------------------------- reductions
+
+MOLT_DEV float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, kWave));
+  return v;
+}
+MOLT_DEV float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
+  return v;
+}
+MOLT_DEV double wave_sum(double v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
+  return v;
+}
+MOLT_DEV unsigned long long wave_sum(unsigned long long v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
+  return v;
+}
+
+// Block-wide reductions for blocks of NW waves; `red` is LDS scratch of NW entries.
+// Every thread returns the result.
+template <int NW>
+MOLT_DEV float block_max(float v, float* red) {
+  v = wave_max(v);
+  int w = threadIdx.x / kWave, l = threadIdx.x % kWave;
+  __syncthreads();
+  if (l == 0) red[w] = v;
+  __syncthreads();
+  float r = red[0];
+#pragma unroll
+  for (int i = 1; i < NW; ++i) r = fmaxf(r, red[i]);
+  return r;
+}
+template <int NW, typename T>
+MOLT_DEV T block_sum(T v, T* red) {
+  v = wave_sum(v);
+  int w = threadIdx.x / kWave, l = threadIdx.x % kWave;
+  __syncthreads();
+  if (l == 0) red[w] = v;
+  __syncthreads();
+  T r = red[0];
+#pragma unroll
+  for (int i = 1; i < NW; ++i) r += red[i];   // fixed order: deterministic
+  return r;
+}
+
+MOLT_DEV float silu(float x) { return x / (1.0f + expf(-x)); }

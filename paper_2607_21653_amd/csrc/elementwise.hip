@@ -1,0 +1,188 @@
+// Row-wise kernels of the verify step: token embedding, RMSNorm (+ per-row fp8
+// quantisation), RoPE with the paged-KV write of the 1+k new positions, and the
+// weighted expert combine. All are HBM-bound with a few bytes per element; one
+// workgroup per token row.
+#include "device_common.h"
+#include "internal.h"
+
+namespace molt {
+namespace {
+
+constexpr int kThreads = 256;
+
+MOLT_DEV float load_act(const void* p, long i, molt_dtype dt) {
+  return dt == MOLT_BF16 ? bf16_to_f32(static_cast<const uint16_t*>(p)[i])
+                         : static_cast<const float*>(p)[i];
+}
+MOLT_DEV void store_act(void* p, long i, float v, molt_dtype dt) {
+  if (dt == MOLT_BF16) static_cast<uint16_t*>(p)[i] = f32_to_bf16(v);
+  else static_cast<float*>(p)[i] = v;
+}
+
+// x[t, :] = Emb[tokens[t], :] widened to f32 (an out-of-range token gives a zero row)
+__global__ __launch_bounds__(kThreads) void embed_kernel(const void* __restrict__ table,
+                                                         const int32_t* __restrict__ tokens, int d,
+                                                         int V, molt_dtype dt,
+                                                         float* __restrict__ x) {
+  const int t = blockIdx.x;
+  const int tok = tokens[t];
+  const bool ok = tok >= 0 && tok < V;
+  for (int i = threadIdx.x; i < d; i += kThreads)
+    x[long(t) * d + i] = ok ? load_act(table, long(tok) * d + i, dt) : 0.f;
+}
+
+// y = x / sqrt(mean(x^2) + eps) * g rounded to dt; with yq, also the per-row fp8 code
+// of y (s = amax|y| / 448, code = e4m3(y / s)).
+__global__ __launch_bounds__(kThreads) void rmsnorm_kernel(const float* __restrict__ x,
+                                                           const float* __restrict__ g, int d,
+                                                           float eps, molt_dtype dt,
+                                                           void* __restrict__ y,
+                                                           uint8_t* __restrict__ yq,
+                                                           float* __restrict__ ys) {
+  __shared__ float red[kThreads / kWave];
+  const int t = blockIdx.x;
+  const float* xr = x + long(t) * d;
+  float ss = 0.f;
+  for (int i = threadIdx.x; i < d; i += kThreads) ss += xr[i] * xr[i];
+  ss = block_sum<kThreads / kWave, float>(ss, red);
+  const float r = 1.0f / sqrtf(ss / float(d) + eps);
+  float amax = 0.f;
+  for (int i = threadIdx.x; i < d; i += kThreads) {
+    float v = xr[i] * r * g[i];
+    if (dt == MOLT_BF16) v = round_to_bf16(v);
+    store_act(y, long(t) * d + i, v, dt);
+    amax = fmaxf(amax, fabsf(v));
+  }
+  if (yq == nullptr) return;
+  amax = block_max<kThreads / kWave>(amax, red);
+  const float s = amax / 448.0f;
+  for (int i = threadIdx.x; i < d; i += kThreads) {
+    const float v = load_act(y, long(t) * d + i, dt);
+    yq[long(t) * d + i] = s > 0.f ? uint8_t(f32_to_fp8e4m3(v / s)) : uint8_t(0);
+  }
+  if (threadIdx.x == 0) ys[t] = s;
+}
+
+// per-row fp8 quantisation of bf16 rows
+__global__ __launch_bounds__(kThreads) void quant_rows_kernel(const uint16_t* __restrict__ x,
+                                                              int cols, uint8_t* __restrict__ q,
+                                                              float* __restrict__ scale) {
+  __shared__ float red[kThreads / kWave];
+  const long r = blockIdx.x;
+  float amax = 0.f;
+  for (int i = threadIdx.x; i < cols; i += kThreads) amax = fmaxf(amax, fabsf(bf16_to_f32(x[r * cols + i])));
+  amax = block_max<kThreads / kWave>(amax, red);
+  const float s = amax / 448.0f;
+  for (int i = threadIdx.x; i < cols; i += kThreads)
+    q[r * cols + i] = s > 0.f ? uint8_t(f32_to_fp8e4m3(bf16_to_f32(x[r * cols + i]) / s)) : uint8_t(0);
+  if (threadIdx.x == 0) scale[r] = s;
+}
+
+// RoPE on q and k of token t = b*(1+k)+j at position ctx[b]+j (rotate-half pairs
+// (i, i+D/2), inverse frequency theta^(-2i/D), angle and rotation in f64), then
+// q -> q_out[t, Hq, D]; k -> K cache slot; v -> V cache slot (transposed layout).
+__global__ __launch_bounds__(kThreads) void rope_kv_kernel(
+    const float* __restrict__ qkv, int k, int Hq, int Hkv, int D, float theta,
+    const int32_t* __restrict__ ctx, const int32_t* __restrict__ bt, int max_blocks, int num_blocks,
+    molt_dtype dt, void* __restrict__ q_out, void* __restrict__ kc, void* __restrict__ vc) {
+  __shared__ double cs[2][128 / 2 * 2];  // cos, sin per pair (D <= 256)
+  const int t = blockIdx.x;
+  const int b = t / (k + 1), j = t % (k + 1);
+  const long pos = long(ctx[b]) + j;
+  const int half = D / 2;
+  for (int i = threadIdx.x; i < half; i += kThreads) {
+    const double inv_freq = pow(double(theta), -2.0 * double(i) / double(D));
+    const double ang = double(pos) * inv_freq;
+    cs[0][i] = cos(ang);
+    cs[1][i] = sin(ang);
+  }
+  __syncthreads();
+  const int width = (Hq + 2 * Hkv) * D;
+  const float* row = qkv + long(t) * width;
+  const int blk = bt[long(b) * max_blocks + pos / 16];
+  const int slot = int(pos % 16);
+  const bool blk_ok = blk >= 0 && blk < num_blocks;
+  // rotations: (Hq + Hkv) heads x half pairs
+  for (int w = threadIdx.x; w < (Hq + Hkv) * half; w += kThreads) {
+    const int h = w / half, i = w % half;
+    const double a = row[h * D + i], c = row[h * D + i + half];
+    const float lo = float(a * cs[0][i] - c * cs[1][i]);
+    const float hi = float(c * cs[0][i] + a * cs[1][i]);
+    if (h < Hq) {
+      store_act(q_out, (long(t) * Hq + h) * D + i, lo, dt);
+      store_act(q_out, (long(t) * Hq + h) * D + i + half, hi, dt);
+    } else if (blk_ok) {
+      const int hk = h - Hq;
+      const long base = ((long(blk) * Hkv + hk) * 16 + slot) * D;
+      store_act(kc, base + i, lo, dt);
+      store_act(kc, base + i + half, hi, dt);
+    }
+  }
+  if (!blk_ok) return;
+  for (int w = threadIdx.x; w < Hkv * D; w += kThreads) {
+    const int hk = w / D, i = w % D;
+    const float v = row[(Hq + Hkv + hk) * D + i];
+    store_act(vc, ((long(blk) * Hkv + hk) * D + i) * 16 + slot, v, dt);
+  }
+}
+
+// out[t] (+)= sum_{j<K} w[t,j] * o[inv[t*K+j]], slot order, f32
+__global__ __launch_bounds__(kThreads) void combine_kernel(const float* __restrict__ o,
+                                                           const int32_t* __restrict__ inv,
+                                                           const float* __restrict__ w, int K,
+                                                           int d, float* __restrict__ out,
+                                                           bool accumulate) {
+  const int t = blockIdx.x;
+  for (int i = threadIdx.x * 4; i < d; i += kThreads * 4) {
+    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int j = 0; j < K; ++j) {
+      const float wj = w[long(t) * K + j];
+      const float4 v = *reinterpret_cast<const float4*>(o + long(inv[long(t) * K + j]) * d + i);
+      acc.x += wj * v.x; acc.y += wj * v.y; acc.z += wj * v.z; acc.w += wj * v.w;
+    }
+    float4* dst = reinterpret_cast<float4*>(out + long(t) * d + i);
+    if (accumulate) {
+      float4 x = *dst;
+      acc.x += x.x; acc.y += x.y; acc.z += x.z; acc.w += x.w;
+    }
+    *dst = acc;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_embed(const void* table, const int32_t* tokens, int T, int d, int V,
+                        molt_dtype dt, float* x, hipStream_t s) {
+  embed_kernel<<<T, kThreads, 0, s>>>(table, tokens, d, V, dt, x);
+  return hipGetLastError();
+}
+
+hipError_t launch_rmsnorm(const float* x, const float* g, int T, int d, float eps, molt_dtype dt,
+                          void* y, uint8_t* yq, float* ys, hipStream_t s) {
+  rmsnorm_kernel<<<T, kThreads, 0, s>>>(x, g, d, eps, dt, y, yq, ys);
+  return hipGetLastError();
+}
+
+hipError_t launch_quant_rows_bf16(const uint16_t* x, int rows, int cols, uint8_t* q, float* scale,
+                                  hipStream_t s) {
+  if (rows == 0) return hipSuccess;
+  quant_rows_kernel<<<rows, kThreads, 0, s>>>(x, cols, q, scale);
+  return hipGetLastError();
+}
+
+hipError_t launch_rope_kv_write(const float* qkv, int B, int k, int Hq, int Hkv, int D,
+                                float theta, const int32_t* ctx, const int32_t* bt, int max_blocks,
+                                int num_blocks, molt_dtype dt, void* q_out, void* k_cache,
+                                void* v_cache, hipStream_t s) {
+  rope_kv_kernel<<<B * (k + 1), kThreads, 0, s>>>(qkv, k, Hq, Hkv, D, theta, ctx, bt, max_blocks,
+                                                   num_blocks, dt, q_out, k_cache, v_cache);
+  return hipGetLastError();
+}
+
+hipError_t launch_combine(const float* o, const int32_t* inv, const float* w, int T, int K, int d,
+                          float* out, bool accumulate, hipStream_t s) {
+  combine_kernel<<<T, kThreads, 0, s>>>(o, inv, w, K, d, out, accumulate);
+  return hipGetLastError();
+}
+
+}  // namespace molt

@@ -1,0 +1,80 @@
+// Internal host-side interface between the C-ABI layer and the kernel files.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "../../include/molt.h"
+
+namespace molt {
+
+// ------------------------------------------------------------- workspace carving
+struct Carver {
+  char* base;
+  size_t used = 0;
+  size_t cap;
+  Carver(void* p, size_t c) : base(static_cast<char*>(p)), cap(c) {}
+  template <typename T>
+  T* take(size_t n) {
+    used = (used + 255) & ~size_t(255);
+    T* p = reinterpret_cast<T*>(base ? base + used : nullptr);
+    used += n * sizeof(T);
+    return p;
+  }
+};
+
+// ------------------------------------------------------------- sampler
+int sampler_chunk_elems();
+size_t sampler_ws_bytes(int B, int k, int V);
+hipError_t launch_spec_accept(const float* logits, const float* q, const int32_t* drafts,
+                              const float* u, int B, int k, int V, int32_t* out_tokens,
+                              int32_t* out_n, float* out_lp, void* ws, hipStream_t s,
+                              int draft_stride = -1, int draft_offset = 0);
+
+// ------------------------------------------------------------- elementwise
+hipError_t launch_embed(const void* table, const int32_t* tokens, int T, int d, int V,
+                        molt_dtype dt, float* x, hipStream_t s);
+// y = rmsnorm(x) * g in act dtype; optional fp8 row quantisation of y
+hipError_t launch_rmsnorm(const float* x, const float* g, int T, int d, float eps, molt_dtype dt,
+                          void* y, uint8_t* yq, float* yq_scale, hipStream_t s);
+hipError_t launch_quant_rows_bf16(const uint16_t* x, int rows, int cols, uint8_t* q, float* scale,
+                                  hipStream_t s);
+hipError_t launch_rope_kv_write(const float* qkv, int B, int k, int Hq, int Hkv, int D,
+                                float theta, const int32_t* ctx, const int32_t* bt, int max_blocks,
+                                int num_blocks, molt_dtype dt, void* q_out, void* k_cache,
+                                void* v_cache, hipStream_t s);
+hipError_t launch_combine(const float* o, const int32_t* inv, const float* w, int T, int K, int d,
+                          float* out, bool accumulate, hipStream_t s);
+
+// ------------------------------------------------------------- routing
+size_t routing_ws_bytes(int T, int E, int K, int tile_m);
+// top-K + softmax of router logits (or replay ids); stable permutation; tile table
+hipError_t launch_route(const float* logits, const float* bias, const int32_t* replay, int T,
+                        int E, int K, int32_t* ids, float* w, int32_t* counts, int32_t* offsets,
+                        int32_t* perm, int32_t* inv, int tile_m, int32_t* tiles, int max_tiles,
+                        int32_t* n_tiles, hipStream_t s);
+int max_expert_tiles(int T, int E, int K, int tile_m);
+
+// ------------------------------------------------------------- GEMMs
+// C[M, N] (f32) = A[M, K] * B[N, K]^T, A/B in dt (F32 or BF16); epilogue adds into C when
+// accumulate. Row-major, K contiguous.
+hipError_t launch_gemm(const void* A, const void* Bw, float* C, int M, int N, int K, molt_dtype dt,
+                       bool accumulate, hipStream_t s);
+// Grouped expert GEMMs over the tile table built by launch_route.
+hipError_t launch_moe_gate_up(const void* x, const uint8_t* xq, const float* xs, const int32_t* perm,
+                              int K_top, const void* w_gu, const float* s_gu, int d, int F,
+                              molt_dtype act, molt_dtype wdt, const int32_t* tiles, int max_tiles,
+                              void* h, hipStream_t s);
+hipError_t launch_moe_down(const void* h, const uint8_t* hq, const float* hs, const void* w_d,
+                           const float* s_d, int d, int F, molt_dtype act, molt_dtype wdt,
+                           const int32_t* tiles, int max_tiles, float* o, hipStream_t s);
+int moe_tile_m(molt_dtype wdt);
+
+// ------------------------------------------------------------- attention
+size_t attention_ws_bytes(int B, int k, int Hq, int D, int max_blocks);
+hipError_t launch_paged_attention(const void* q, const void* kc, const void* vc, const int32_t* bt,
+                                  const int32_t* ctx, int B, int k, int Hq, int Hkv, int D,
+                                  int max_blocks, molt_dtype dt, void* out, void* ws,
+                                  hipStream_t s);
+
+}  // namespace molt

@@ -1,0 +1,180 @@
+// Router top-K with softmax weights, and the stable token -> expert permutation
+// built from wavefront ballots and LDS prefix sums (the expert choices are the route
+// records of rollout routing replay, paper Sec. 4.1 and Sec. 4.4).
+//
+// topk_kernel: one wavefront per token. Each lane holds up to 4 router logits
+// (E <= 256) as 64-bit keys: order-preserving f32 bits (with -0 folded into +0) in
+// the high word, 0xFFFFFFFF - expert id in the low word, so the maximum key is the
+// largest logit with ties resolved to the lower expert id. K rounds of a wavefront
+// max-reduction select the experts in descending order.
+//
+// permute_kernel: one 1024-thread workgroup. Pass 1 counts pairs per expert (LDS
+// integer atomics: the totals are order-free), a serial scan gives offsets and the
+// grouped-GEMM tile table. Pass 2 walks the T*K pairs in (token, slot) order, 1024 at
+// a time: inside a wavefront, lanes holding the same expert find each other with 8
+// ballots over the expert id bits; the rank of a lane among them is a popcount of the
+// lower lanes; across the 16 wavefronts an exclusive LDS prefix per expert adds the
+// earlier wavefronts' counts. Position = offset[e] + earlier chunks + earlier
+// wavefronts + rank: the stable (expert, token, slot) order, bit-exact.
+#include "device_common.h"
+#include "internal.h"
+
+namespace molt {
+namespace {
+
+constexpr int kMaxE = 256;
+constexpr int kPermThreads = 1024;
+constexpr int kPermWaves = kPermThreads / kWave;
+
+MOLT_DEV unsigned long long route_key(float v, int e) {
+  const float c = v + 0.0f;                  // -0.0 -> +0.0
+  const uint32_t u = __float_as_uint(c);
+  const uint32_t ord = (u >> 31) ? ~u : (u | 0x80000000u);
+  return (static_cast<unsigned long long>(ord) << 32) | (0xFFFFFFFFu - uint32_t(e));
+}
+
+MOLT_DEV unsigned long long wave_max_u64(unsigned long long v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    unsigned long long w = __shfl_xor(v, o, kWave);
+    v = w > v ? w : v;
+  }
+  return v;
+}
+
+__global__ __launch_bounds__(256) void topk_kernel(const float* __restrict__ logits,
+                                                   const float* __restrict__ bias,
+                                                   const int32_t* __restrict__ replay, int T, int E,
+                                                   int K, int32_t* __restrict__ ids,
+                                                   float* __restrict__ w) {
+  const int t = blockIdx.x * 4 + threadIdx.x / kWave;
+  const int lane = threadIdx.x % kWave;
+  if (t >= T) return;
+  const float* g = logits + long(t) * E;
+  float sel_v = -INFINITY;
+  int sel_e = 0;
+  if (replay) {
+    if (lane < K) {
+      int e = replay[long(t) * K + lane];
+      if (e < 0 || e >= E) e = 0;              // out-of-range replay id: expert 0
+      sel_e = e;
+      sel_v = g[e] + (bias ? bias[e] : 0.f);
+    }
+  } else {
+    unsigned long long key[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int e = lane + kWave * i;
+      key[i] = e < E ? route_key(g[e] + (bias ? bias[e] : 0.f), e) : 0ull;
+    }
+    for (int j = 0; j < K; ++j) {
+      unsigned long long mine = key[0];
+      int which = 0;
+#pragma unroll
+      for (int i = 1; i < 4; ++i)
+        if (key[i] > mine) { mine = key[i]; which = i; }
+      const unsigned long long best = wave_max_u64(mine);
+      if (mine == best && best != 0ull) key[which] = 0ull;   // the unique owner drops it
+      const int e = int(0xFFFFFFFFu - uint32_t(best & 0xFFFFFFFFull));
+      if (lane == j) {
+        sel_e = e;
+        sel_v = g[e] + (bias ? bias[e] : 0.f);
+      }
+    }
+  }
+  // softmax over the K selected logits
+  const float m = wave_max(lane < K ? sel_v : -INFINITY);
+  const float ex = lane < K ? expf(sel_v - m) : 0.f;
+  const float sum = wave_sum(ex);
+  if (lane < K) {
+    ids[long(t) * K + lane] = sel_e;
+    w[long(t) * K + lane] = ex / sum;
+  }
+}
+
+__global__ __launch_bounds__(kPermThreads) void permute_kernel(
+    const int32_t* __restrict__ ids, int P, int E, int tile_m, int32_t* __restrict__ counts_out,
+    int32_t* __restrict__ offsets_out, int32_t* __restrict__ perm, int32_t* __restrict__ inv,
+    int4* __restrict__ tiles, int max_tiles, int32_t* __restrict__ n_tiles) {
+  __shared__ int cnt[kMaxE];
+  __shared__ int off[kMaxE + 1];
+  __shared__ int run[kMaxE];
+  __shared__ int wc[kPermWaves][kMaxE];
+  __shared__ int s_nt;
+  const int tid = threadIdx.x;
+  const int wave = tid / kWave, lane = tid % kWave;
+  for (int e = tid; e < kMaxE; e += kPermThreads) { cnt[e] = 0; run[e] = 0; }
+  __syncthreads();
+  for (int p = tid; p < P; p += kPermThreads) atomicAdd(&cnt[ids[p]], 1);
+  __syncthreads();
+  if (tid == 0) {
+    off[0] = 0;
+    int nt = 0;
+    for (int e = 0; e < E; ++e) {
+      off[e + 1] = off[e] + cnt[e];
+      for (int m0 = off[e]; m0 < off[e + 1] && nt < max_tiles; m0 += tile_m)
+        tiles[nt++] = make_int4(e, m0, min(m0 + tile_m, off[e + 1]), 0);
+    }
+    s_nt = nt;
+    *n_tiles = nt;
+  }
+  __syncthreads();
+  for (int i = s_nt + tid; i < max_tiles; i += kPermThreads) tiles[i] = make_int4(-1, 0, 0, 0);
+  for (int e = tid; e < E; e += kPermThreads) {
+    counts_out[e] = cnt[e];
+    offsets_out[e] = off[e];
+  }
+  if (tid == 0) offsets_out[E] = off[E];
+  const unsigned long long lt = (1ull << lane) - 1ull;
+  for (int base = 0; base < P; base += kPermThreads) {
+    for (int e = lane; e < kMaxE; e += kWave) wc[wave][e] = 0;
+    const int p = base + tid;
+    const bool valid = p < P;
+    const int e = valid ? ids[p] : 0;
+    unsigned long long mask = __ballot(valid);
+#pragma unroll
+    for (int bit = 0; bit < 8; ++bit) {
+      const bool on = (e >> bit) & 1;
+      const unsigned long long b = __ballot(valid && on);
+      mask &= on ? b : ~b;
+    }
+    const int rank = __popcll(mask & lt);
+    __syncthreads();
+    if (valid && rank == 0) wc[wave][e] = __popcll(mask);
+    __syncthreads();
+    if (tid < E) {
+      int s = run[tid];
+      for (int w2 = 0; w2 < kPermWaves; ++w2) {
+        const int c = wc[w2][tid];
+        wc[w2][tid] = s;
+        s += c;
+      }
+      run[tid] = s;
+    }
+    __syncthreads();
+    if (valid) {
+      const int pos = off[e] + wc[wave][e] + rank;
+      perm[pos] = p;
+      inv[p] = pos;
+    }
+    __syncthreads();
+  }
+}
+
+}  // namespace
+
+int max_expert_tiles(int T, int E, int K, int tile_m) {
+  return (T * K + tile_m - 1) / tile_m + E;
+}
+
+hipError_t launch_route(const float* logits, const float* bias, const int32_t* replay, int T,
+                        int E, int K, int32_t* ids, float* w, int32_t* counts, int32_t* offsets,
+                        int32_t* perm, int32_t* inv, int tile_m, int32_t* tiles, int max_tiles,
+                        int32_t* n_tiles, hipStream_t s) {
+  topk_kernel<<<(T + 3) / 4, 256, 0, s>>>(logits, bias, replay, T, E, K, ids, w);
+  permute_kernel<<<1, kPermThreads, 0, s>>>(ids, T * K, E, tile_m, counts, offsets, perm, inv,
+                                            reinterpret_cast<int4*>(tiles), max_tiles, n_tiles);
+  return hipGetLastError();
+}
+
+}  // namespace molt

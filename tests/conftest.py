@@ -22,3 +22,8 @@ def lib():
     import paper_2607_21653_amd as molt
     molt.load()
     return molt
+
+
+@pytest.fixture(scope="session")
+def molt_lib(lib):
+    return lib

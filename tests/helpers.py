@@ -1,0 +1,39 @@
+"""Shared test plumbing: numpy views of generated tensors for the oracle, device copies for
+the library, and the oracle's config dict for a workload. No arithmetic of the method."""
+import numpy as np
+import torch
+
+
+def host(t):
+    """numpy array of a tensor's stored values: bf16 as uint16 bit patterns, fp8 as uint8."""
+    if t is None:
+        return None
+    t = t.detach().cpu()
+    if t.dtype == torch.bfloat16:
+        return t.view(torch.int16).numpy().view(np.uint16)
+    return t.numpy()
+
+
+def dev(t):
+    return None if t is None else t.cuda().contiguous()
+
+
+def oracle_cfg(w):
+    return dict(dtype=w.dtype, expert_dtype=w.expert_dtype, n_layers=w.n_layers,
+                n_q_heads=w.n_q_heads, n_kv_heads=w.n_kv_heads, head_dim=w.head_dim,
+                top_k=w.top_k, rms_eps=w.rms_eps, rope_theta=w.rope_theta, block_size=16)
+
+
+def layer_host(lw):
+    return {k: host(v) for k, v in lw.items()}
+
+
+def model_from(w, layers, head, molt):
+    return molt.Model([{k: dev(v) for k, v in lw.items()} for lw in layers],
+                      None if head is None else {k: dev(v) for k, v in head.items()},
+                      n_q_heads=w.n_q_heads, n_kv_heads=w.n_kv_heads, head_dim=w.head_dim,
+                      top_k=w.top_k, rms_eps=w.rms_eps, rope_theta=w.rope_theta)
+
+
+def max_abs(a, b):
+    return float(np.max(np.abs(np.asarray(a, np.float64) - np.asarray(b, np.float64)))) if np.size(a) else 0.0

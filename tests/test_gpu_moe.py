@@ -1,0 +1,133 @@
+"""GPU parity of molt_moe_layer (router GEMM, top-K, ballot permutation, grouped expert
+GEMMs on MFMA, combine) against the oracle, at the 35B-A3B-like layer shape with fewer
+tokens (several 32-row tiles and ragged expert segments): routes bit-exact except where
+the oracle's K-th/(K+1)-th router-logit gap is below 1e-4 (fp32 summation order), outputs
+within 2e-2 max-abs (bf16/fp8) or 1e-4 (f32); routing on exactly representable inputs is
+bit-exact with ties; replay ids; fp8 experts with Zipf-skewed routing."""
+import numpy as np
+import pytest
+import torch
+
+import workloads
+from oracle import codecs, moe as omoe, routing as orouting
+from helpers import dev, host, max_abs
+
+pytestmark = pytest.mark.gpu
+ROUTE_GAP = 1e-4
+
+
+def _layer(w, seed, T):
+    lw = workloads.make_layer_weights(w, seed, 0)
+    x = workloads.make_hidden(w, seed, T)
+    if w.dtype == "bf16":
+        x = x.to(torch.bfloat16)
+    return lw, x
+
+
+def _oracle(w, lw, x, T, replay=None):
+    xv = omoe.widen(host(x), w.dtype)
+    return omoe.moe_layer(xv, omoe.widen(host(lw["w_router"]), w.dtype), host(lw["w_gate_up"]),
+                          host(lw["w_down"]), w.top_k, w.dtype, w.expert_dtype,
+                          host(lw["s_gate_up"]), host(lw["s_down"]), host(lw["router_bias"]), replay)
+
+
+def _gpu(molt, lw, x, K, replay=None):
+    return molt.moe_layer(dev(x), dev(lw["w_router"]), dev(lw["w_gate_up"]), dev(lw["w_down"]), K,
+                          router_bias=dev(lw["router_bias"]), s_gate_up=dev(lw["s_gate_up"]),
+                          s_down=dev(lw["s_down"]), replay_ids=dev(replay), want_routing=True)
+
+
+def _check(w, o, g, tol):
+    out, ids, wts, counts, offsets, perm = [t.cpu().numpy() for t in g]
+    near = (o["margin"] < ROUTE_GAP) | (o["order_margin"] < ROUTE_GAP)
+    assert near.mean() < 0.1, near.mean()
+    ok = ~near
+    assert (ids[ok] == o["ids"][ok]).all(), np.nonzero((ids != o["ids"]).any(1) & ok)[0][:10]
+    np.testing.assert_allclose(wts[ok], o["weights"][ok], atol=1e-5)
+    err = max_abs(out[ok], o["out"][ok])
+    print(f"max |out - oracle| = {err:.3e} over {ok.sum()} tokens ({near.sum()} near-ties)", flush=True)
+    assert err <= tol
+    if not near.any():
+        assert (counts == o["counts"]).all() and (offsets == o["offsets"]).all()
+        assert (perm == o["perm"]).all()
+
+
+@pytest.mark.parametrize("T", [1, 77, 320])
+def test_bf16_layer_shape(molt_lib, T):
+    w = workloads.LAYER_BF16
+    lw, x = _layer(w, 1, T)
+    print(f"case bf16 T={T}", flush=True)
+    _check(w, _oracle(w, lw, x, T), _gpu(molt_lib, lw, x, w.top_k), 2e-2)
+
+
+def test_fp8_zipf(molt_lib):
+    w = workloads.FP8_ZIPF
+    T = 333
+    lw, x = _layer(w, 2, T)
+    print(f"case fp8 T={T}", flush=True)
+    g = _gpu(molt_lib, lw, x, w.top_k)
+    o = _oracle(w, lw, x, T)
+    _check(w, o, g, 2e-2)
+    counts = g[3].cpu().numpy()
+    print("max/mean expert load", counts.max() / counts.mean(), flush=True)
+    assert counts.max() > 4 * counts.mean()          # skewed
+
+
+def test_f32_tiny(molt_lib):
+    w = workloads.TINY_FP32
+    lw, x = _layer(w, 3, 50)
+    _check(w, _oracle(w, lw, x, 50), _gpu(molt_lib, lw, x, w.top_k), 1e-4)
+
+
+def test_exact_routing_with_ties(molt_lib):
+    """x in {-2..2}, router weights in {-1, 0, 1}/16: every router logit is exact in f32 on
+    both sides, so routes (ties included) must agree bit for bit, and so must the permutation."""
+    w = workloads.LAYER_BF16
+    T, d, E, K = 200, w.d_model, w.n_experts, w.top_k
+    g = np.random.Generator(np.random.Philox(77))
+    x = torch.from_numpy(g.integers(-2, 3, (T, d)).astype(np.float32)).to(torch.bfloat16)
+    wr = torch.from_numpy((g.integers(-1, 2, (E, d)) / 16.0).astype(np.float32)).to(torch.bfloat16)
+    lw = workloads.make_layer_weights(w, 4, 0)
+    lw["w_router"] = wr
+    o = _oracle(w, lw, x, T)
+    gq = _gpu(molt_lib, lw, x, K)
+    ids, counts, offsets, perm = [gq[i].cpu().numpy() for i in (1, 3, 4, 5)]
+    assert (o["margin"] == 0).any()                  # ties do occur
+    assert (ids == o["ids"]).all()
+    assert (counts == o["counts"]).all() and (offsets == o["offsets"]).all() and (perm == o["perm"]).all()
+
+
+def test_replay(molt_lib):
+    w = workloads.LAYER_BF16
+    T = 64
+    lw, x = _layer(w, 5, T)
+    g = np.random.Generator(np.random.Philox(9))
+    replay = torch.from_numpy(np.stack([g.choice(w.n_experts, w.top_k, replace=False)
+                                        for _ in range(T)]).astype(np.int32))
+    o = _oracle(w, lw, x, T, host(replay))
+    gq = _gpu(molt_lib, lw, x, w.top_k, replay)
+    assert (gq[1].cpu().numpy() == host(replay)).all()
+    assert max_abs(gq[0].cpu().numpy(), o["out"]) <= 2e-2
+    np.testing.assert_allclose(gq[2].cpu().numpy(), o["weights"], atol=1e-5)
+
+
+def test_fp8_codec_on_gpu_matches_oracle(molt_lib):
+    """Every finite e4m3 code (subnormals, +-448) through the fp8 gate GEMM: a one-hot input
+    makes gate[n] = decode(code_n), so the MFMA's fp8 interpretation of each code shows up
+    directly in the output (relative tolerance 1e-2 of the output range)."""
+    w = workloads.FP8_ZIPF.scaled(n_experts=1, top_k=1, zipf=None)
+    d, F = w.d_model, w.d_ff
+    lw = workloads.make_layer_weights(w, 6, 0)
+    codes = np.array([c for c in range(256) if c not in (0x7F, 0xFF)], np.uint8)
+    wgu = np.zeros((1, 2 * F, d), np.uint8)
+    wgu[0, :len(codes), 0] = codes                   # gate rows read x[0]
+    wgu[0, F:F + len(codes), 0] = 0x38               # up = 1.0 * x[0]
+    lw["w_gate_up"] = torch.from_numpy(wgu)
+    lw["s_gate_up"] = torch.ones(1, 2 * F)
+    x = torch.zeros(4, d)
+    x[:, 0] = 1.0
+    x = x.to(torch.bfloat16)
+    o = _oracle(w, lw, x, 4)
+    gq = _gpu(molt_lib, lw, x, 1)
+    err = max_abs(gq[0].cpu().numpy(), o["out"])
+    assert err <= 1e-2 * np.abs(o["out"]).max(), err

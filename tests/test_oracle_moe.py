@@ -13,7 +13,7 @@ def test_topk_matches_stable_sort_and_ties():
     T, E, K = 200, 32, 6
     g = np.round(rng.normal(size=(T, E)) * 4) / 4          # many exact ties
     g = g.astype(np.float32)
-    ids, w, _ = routing.topk_route(g, K)
+    ids, w, _, _ = routing.topk_route(g, K)
     ref = np.argsort(-g.astype(np.float64), axis=1, kind="stable")[:, :K]
     assert (ids == ref).all()
     np.testing.assert_allclose(w.sum(axis=1), 1.0, atol=1e-6)
@@ -24,13 +24,13 @@ def test_topk_matches_stable_sort_and_ties():
 
 def test_topk_special_cases():
     g = np.zeros((3, 8), np.float32)
-    ids, w, _ = routing.topk_route(g, 3)
+    ids, w, _, _ = routing.topk_route(g, 3)
     assert (ids == [0, 1, 2]).all()
     np.testing.assert_allclose(w, 1 / 3, rtol=1e-6)
-    ids, _, _ = routing.topk_route(np.random.default_rng(1).normal(size=(4, 8)).astype(np.float32), 8)
+    ids, _, _, _ = routing.topk_route(np.random.default_rng(1).normal(size=(4, 8)).astype(np.float32), 8)
     assert (np.sort(ids, axis=1) == np.arange(8)).all()
     g = np.array([[-0.0, 0.0, -1.0, 0.0]], np.float32)      # -0.0 ties +0.0: lower id first
-    ids, _, _ = routing.topk_route(g, 2)
+    ids, _, _, _ = routing.topk_route(g, 2)
     assert ids.tolist() == [[0, 1]]
 
 
