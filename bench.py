@@ -29,6 +29,25 @@ HBM_PEAK_GBS = 8000.0
 BF16_PEAK_TFLOPS = 2500.0
 
 
+ROOT = os.path.dirname(os.path.abspath(__file__))
+
+
+def attention_traffic():
+    """Measured HBM bytes per attention launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, each
+    scaled by a 1 GiB copy's reading), only while the kernel source is the one the counters
+    were taken on; None otherwise."""
+    import hashlib
+    try:
+        rec = json.load(open(os.path.join(ROOT, "profiles", "attention_traffic.json")))
+        src = open(os.path.join(ROOT, rec["source"]), "rb").read()
+    except (OSError, ValueError, KeyError):
+        return None
+    if hashlib.sha256(src).hexdigest() != rec["source_sha256"]:
+        return None
+    return int(1024 * (rec["fetch_kib_per_dispatch"] * rec["fetch_scale"] +
+                       rec["write_kib_per_dispatch"] * rec["write_scale"]))
+
+
 def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
@@ -84,10 +103,10 @@ def make_drafts(w, seed, molt, model, kv, ws):
     return tokens, q, u
 
 
-def cpu_baseline(w, layout, layers, head, kv, tokens, q, u, sample_layers=2):
-    """Oracle on a bounded sample: sequence 0 (1+k positions) through `sample_layers` of
-    the layers, then the LM head and the sampler; the per-layer time is scaled to all
-    layers. Returns (positions/s, seconds measured, description)."""
+def cpu_baseline(w, layout, layers, head, kv, tokens, q, u, n_seq=4, sample_layers=6):
+    """Oracle on a bounded sample: `n_seq` sequences ((1+k) positions each) through
+    `sample_layers` of the layers, then the LM head and the sampler; the per-layer time is
+    scaled to all layers. Returns (positions/s, seconds measured, threads, description)."""
     import oracle.model as omodel
     from oracle import sampler as osamp
     try:
@@ -103,29 +122,34 @@ def cpu_baseline(w, layout, layers, head, kv, tokens, q, u, sample_layers=2):
     cfg = dict(dtype=w.dtype, expert_dtype=w.expert_dtype, n_layers=sample_layers,
                n_q_heads=w.n_q_heads, n_kv_heads=w.n_kv_heads, head_dim=w.head_dim, top_k=w.top_k,
                rms_eps=w.rms_eps, rope_theta=w.rope_theta, block_size=16)
-    b = 0
-    blocks = layout.block_tables[b][layout.block_tables[b] >= 0]
+    # the sample's blocks, renumbered densely
+    blk_rows = [layout.block_tables[b][layout.block_tables[b] >= 0] for b in range(n_seq)]
+    blocks = np.concatenate(blk_rows)
+    bt = np.full((n_seq, max(len(r) for r in blk_rows)), -1)
+    pos = 0
+    for b, r in enumerate(blk_rows):
+        bt[b, :len(r)] = np.arange(pos, pos + len(r))
+        pos += len(r)
     lw = [{k_: (None if v is None else host(v)) for k_, v in layers[l].items()} for l in range(sample_layers)]
     caches = []
+    idx = torch.from_numpy(blocks).long().cuda()
     for l in range(sample_layers):
-        idx = torch.from_numpy(blocks).long().cuda()
         kc = omodel.widen_cache(host(kv.k_caches[l][idx]), w.dtype)
         vc = omodel.widen_cache(host(kv.v_caches[l][idx]), w.dtype)
         caches.append((kc, vc))
-    bt = np.arange(len(blocks))[None, :]
-    ctx = layout.context_lens[b:b + 1]
+    ctx = layout.context_lens[:n_seq]
     hh = {k_: host(v) for k_, v in head.items()}
-    toks = host(tokens)[b:b + 1]
+    toks = host(tokens)[:n_seq]
     t0 = time.perf_counter()
     x = omodel.embed(toks, hh, cfg)
     x, _ = omodel.decoder_forward(x, lambda l: lw[l], caches, bt, ctx, w.k, cfg)
     t1 = time.perf_counter()
-    logits = omodel.lm_logits(x, hh, cfg).reshape(1, w.k + 1, -1)
-    osamp.spec_accept(logits, toks[:, 1:], host(u)[b:b + 1], host(q)[b:b + 1])
+    logits = omodel.lm_logits(x, hh, cfg).reshape(n_seq, w.k + 1, -1)
+    osamp.spec_accept(logits, toks[:, 1:], host(u)[:n_seq], host(q)[:n_seq])
     t2 = time.perf_counter()
     per_step = (t1 - t0) * (w.n_layers / sample_layers) + (t2 - t1)
-    value = (w.k + 1) / per_step
-    desc = (f"1 of {w.batch} sequences ({w.k + 1} positions) through {sample_layers} of {w.n_layers} "
+    value = n_seq * (w.k + 1) / per_step
+    desc = (f"{n_seq} of {w.batch} sequences ({n_seq * (w.k + 1)} positions) through {sample_layers} of {w.n_layers} "
             f"layers ({t1 - t0:.2f} s, scaled x{w.n_layers / sample_layers:g}) + LM head + sampler "
             f"({t2 - t1:.2f} s); float64 NumPy oracle")
     return value, t2 - t0, threads, desc
@@ -224,7 +248,7 @@ def main():
                    "drafts": f"q = softmax(target + N(0, {w.draft_sigma}^2))" if w.draft == "perturbed" else "uniform"},
         "roofline": {"kernel": "paged attention (attn_mfma_kernel + split merge), per layer launch",
                      "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": attention_traffic(),
                      "algorithmic_bytes_per_launch": abytes, "avg_launch_ms": round(attn_avg, 4)},
         "emitted_tokens_per_s": round(emitted, 1),
         "mean_accepted_fraction": round(float(n_acc.mean()) / k, 4) if k else None,
