@@ -313,7 +313,7 @@ static int attn_shape_ok(int B, int k, int Hq, int Hkv, int D, int max_blocks, m
 
 size_t molt_paged_attention_workspace_size(int B, int k, int Hq, int Hkv, int D, int max_blocks) {
   if (B < 1 || k < 0 || Hq < 1 || Hkv < 1 || D < 1 || max_blocks < 1) return 0;
-  return molt::attention_ws_bytes(B, k, Hq, D, max_blocks);
+  return molt::attention_ws_bytes(B, k, Hq, Hkv, D, max_blocks);
 }
 
 int molt_paged_attention(const void* q, const void* k_cache, const void* v_cache,
@@ -389,7 +389,7 @@ DecWs carve_dec(molt::Carver& c, const molt_model* m, int B, int k, int max_bloc
   w.qkv = c.take<float>(T * (Hq + 2 * Hkv) * D);
   w.q = c.take<uint8_t>(T * Hq * D * es);
   w.attn = c.take<uint8_t>(T * Hq * D * es);
-  const size_t aws = m->dtype == MOLT_F32 ? 0 : molt::attention_ws_bytes(B, k, Hq, D, max_blocks);
+  const size_t aws = m->dtype == MOLT_F32 ? 0 : molt::attention_ws_bytes(B, k, Hq, Hkv, D, max_blocks);
   w.attn_ws = c.take<uint8_t>(aws);
   w.moe = carve_moe(c, int(T), d, m->n_experts, m->top_k, m->d_ff, m->dtype, m->expert_dtype);
   return w;

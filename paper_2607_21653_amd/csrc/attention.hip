@@ -3,9 +3,12 @@
 // R = G*(1+k) query rows (G = Hq/Hkv query heads, 1+k positions) share every key/value
 // block, so each K/V byte is read once per (b, h) and reused by all R rows on MFMA.
 //
-// Work split: workgroup = (b, h, split of kBlocksPerSplit 16-token blocks), 4 wavefronts.
-// Each wavefront takes block pairs (32 keys) round-robin and keeps its own online
-// softmax. Per pair, on v_mfma_f32_16x16x32_bf16:
+// Work split: workgroup = (b, h, split of the key range), 4 wavefronts; the number of
+// splits is chosen so the grid holds ~512 workgroups (at B*Hkv >= 512 there is no split and
+// no merge pass). Each wavefront takes block pairs (32 keys) round-robin and keeps its own
+// online softmax; the next pair's fragments are loaded into a second register set while
+// the current pair computes (software pipelining through registers). Per pair, on
+// v_mfma_f32_16x16x32_bf16:
 //   S^T[32 keys x R] = K Q^T   (A = K rows straight from the cache: [16 keys x 32 dims]
 //                               per operand, 16 B per lane; B = Q^T held in registers)
 //   O^T[D x R]      += V^T P^T (A = V^T: the V cache stores a block as [D][16 tokens], so
@@ -14,8 +17,10 @@
 //                               rounded to bf16: no cross-lane shuffles)
 // The MFMA k-index is a free permutation as long as A and B agree: slot s of lane group g
 // is key 4g+s of the first block (s < 4) or of the second block (s >= 4).
-// Causality: row r = j*G + g (position j) sees keys <= ctx_b + j. Softmax in f32 with
-// exp2 of log2(e)-scaled scores. The four wavefronts merge through LDS in a fixed order;
+// Causality: row r = j*G + g (position j) sees keys <= ctx_b + j; only pairs reaching past
+// ctx_b need masks. Softmax in f32 with exp2 of log2(e)-scaled scores; the output is
+// rescaled lazily, only when a row maximum grows by more than 8 (in log2 units) over the
+// reference it was accumulated with. The four wavefronts merge through LDS in a fixed order;
 // splits are merged by a log-sum-exp pass (a single split writes the output directly).
 #include "device_common.h"
 #include "internal.h"
@@ -25,8 +30,9 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kWaves = 4;
-constexpr int kBlocksPerSplit = 64;  // 1024 keys per workgroup
 constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kNegBig = -1.0e30f;   // finite "minus infinity" for running maxima
+constexpr float kRescaleSlack = 8.0f; // probabilities may grow to 2^8 before O is rescaled
 
 typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
 
@@ -39,8 +45,15 @@ struct AttnParams {
   uint16_t* out;           // [T, Hq * D]
   float* part_o;           // [B, Hkv, S, R, D]
   float* part_ml;          // [B, Hkv, S, R, 2]
-  int k, Hq, Hkv, max_blocks, splits;
+  int k, Hq, Hkv, max_blocks, splits, blocks_per_split;
   float scale_log2;        // log2(e) / sqrt(D)
+};
+
+// K and V^T fragments of one 32-key block pair for one wavefront
+template <int D>
+struct PairFrags {
+  bf16x8_t k[2][D / 32];
+  bf16x8_t v[D / 16];
 };
 
 template <int D, int RT>
@@ -61,25 +74,30 @@ __global__ __launch_bounds__(kThreads) void attn_mfma_kernel(AttnParams p) {
   const int ctx = p.ctx[b];
   const int nkeys = ctx + kp1;
   const int nblk = (nkeys + 15) / 16;
-  const int blk0 = split * kBlocksPerSplit;
-  const int blk1 = min(blk0 + kBlocksPerSplit, nblk);
-  const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+  const int blk0 = split * p.blocks_per_split;
+  const int blk1 = min(blk0 + p.blocks_per_split, nblk);
+  // wave-uniform in a scalar register, so block-table reads become scalar loads that do not
+  // share the vector memory counter with the K/V prefetch
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+  const int lane = threadIdx.x % kWave;
   const int l16 = lane % 16, g4 = lane / 16;
+  const float c = p.scale_log2;
 
   // Q^T fragments: row r = l16 + 16 * rt; dims [32 s + 8 g4, +8)
   bf16x8_t qf[RT][DS];
-  int rowj[RT];
+  int lim[RT];   // last visible key position of the lane's row (-1: padding row)
 #pragma unroll
   for (int rt = 0; rt < RT; ++rt) {
     const int r = rt * 16 + l16;
     const int j = r / G, gi = r % G;
-    rowj[rt] = r < R ? j : -1;
+    lim[rt] = r < R ? ctx + j : -1;
 #pragma unroll
     for (int s = 0; s < DS; ++s) {
       if (r < R) {
         const uint16_t* src = p.q + ((long(b) * kp1 + j) * p.Hq + h * G + gi) * D + s * 32 + g4 * 8;
         qf[rt][s] = *reinterpret_cast<const bf16x8_t*>(src);
       } else {
+#pragma unroll
         for (int e = 0; e < 8; ++e) qf[rt][s][e] = __bf16(0.f);
       }
     }
@@ -92,37 +110,31 @@ __global__ __launch_bounds__(kThreads) void attn_mfma_kernel(AttnParams p) {
     for (int rt = 0; rt < RT; ++rt) o[dt][rt] = floatx4_t{0.f, 0.f, 0.f, 0.f};
   float m_run[RT], l_run[RT];
 #pragma unroll
-  for (int rt = 0; rt < RT; ++rt) { m_run[rt] = -INFINITY; l_run[rt] = 0.f; }
+  for (int rt = 0; rt < RT; ++rt) { m_run[rt] = kNegBig; l_run[rt] = 0.f; }
 
   const int* btab = p.bt + long(b) * p.max_blocks;
   const long kv_blk_stride = long(p.Hkv) * 16 * D;
-  for (int pb = blk0 + 2 * wave; pb < blk1; pb += 2 * kWaves) {
-    const int pb2 = pb + 1;
-    const bool has2 = pb2 < blk1;
+  const uint16_t* kbase = p.kc + long(h) * 16 * D + l16 * D + g4 * 8;
+  const uint16_t* vbase = p.vc + long(h) * D * 16 + l16 * 16 + g4 * 4;
+
+  auto load_pair = [&](PairFrags<D>& f, int pb) {
     const long phys0 = btab[pb];
-    const long phys1 = has2 ? btab[pb2] : phys0;
-    // K fragments: two 16-key tiles, DS dim steps
-    bf16x8_t kf[2][DS];
+    const long phys1 = (pb + 1 < blk1) ? btab[pb + 1] : phys0;
 #pragma unroll
-    for (int t = 0; t < 2; ++t) {
-      const long phys = t == 0 ? phys0 : phys1;
-      const uint16_t* kb = p.kc + phys * kv_blk_stride + long(h) * 16 * D + l16 * D + g4 * 8;
-#pragma unroll
-      for (int s = 0; s < DS; ++s) kf[t][s] = *reinterpret_cast<const bf16x8_t*>(kb + s * 32);
+    for (int s = 0; s < DS; ++s) {
+      f.k[0][s] = *reinterpret_cast<const bf16x8_t*>(kbase + phys0 * kv_blk_stride + s * 32);
+      f.k[1][s] = *reinterpret_cast<const bf16x8_t*>(kbase + phys1 * kv_blk_stride + s * 32);
     }
-    // V^T fragments: dim tile dt, lane dim = 16 dt + l16, keys 4 g4 .. +3 of each block
-    bf16x8_t vf[DT];
-    {
-      const uint16_t* v0 = p.vc + phys0 * kv_blk_stride + long(h) * D * 16 + l16 * 16 + g4 * 4;
-      const uint16_t* v1 = p.vc + phys1 * kv_blk_stride + long(h) * D * 16 + l16 * 16 + g4 * 4;
 #pragma unroll
-      for (int dt = 0; dt < DT; ++dt) {
-        const bf16x4_t a = *reinterpret_cast<const bf16x4_t*>(v0 + dt * 16 * 16);
-        const bf16x4_t c = *reinterpret_cast<const bf16x4_t*>(v1 + dt * 16 * 16);
-        vf[dt] = bf16x8_t{a[0], a[1], a[2], a[3], c[0], c[1], c[2], c[3]};
-      }
+    for (int dt = 0; dt < DT; ++dt) {
+      const bf16x4_t a = *reinterpret_cast<const bf16x4_t*>(vbase + phys0 * kv_blk_stride + dt * 256);
+      const bf16x4_t e = *reinterpret_cast<const bf16x4_t*>(vbase + phys1 * kv_blk_stride + dt * 256);
+      f.v[dt] = bf16x8_t{a[0], a[1], a[2], a[3], e[0], e[1], e[2], e[3]};
     }
-    // S^T tiles
+  };
+
+  auto compute_pair = [&](const PairFrags<D>& f, int pb) {
+    // S^T tiles: lane holds keys 4 g4 + e of block pb (t = 0) and pb + 1 (t = 1)
     floatx4_t st[2][RT];
 #pragma unroll
     for (int t = 0; t < 2; ++t)
@@ -131,45 +143,82 @@ __global__ __launch_bounds__(kThreads) void attn_mfma_kernel(AttnParams p) {
         floatx4_t acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int s = 0; s < DS; ++s)
-          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[t][s], qf[rt][s], acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(f.k[t][s], qf[rt][s], acc, 0, 0, 0);
         st[t][rt] = acc;
       }
-    // online softmax per row; lane holds keys 4 g4 + e of block pb (t=0) and pb2 (t=1)
+    // keys at or past pb*16 + 31 <= ctx are visible to every row: no mask needed
+    const bool full = pb * 16 + 31 <= ctx;
+    if (!full) {
+      const bool has2 = pb + 1 < blk1;
+#pragma unroll
+      for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+        for (int t = 0; t < 2; ++t)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const int kpos = (pb + t) * 16 + g4 * 4 + e;
+            if (!((t == 0 || has2) && kpos <= lim[rt])) st[t][rt][e] = -INFINITY;
+          }
+    }
+    // row maxima (raw scores; the scale is positive) across the lane's 8 keys and 4 groups
+    float mx[RT];
+    bool grow = false;
 #pragma unroll
     for (int rt = 0; rt < RT; ++rt) {
-      const int lim = rowj[rt] < 0 ? -1 : ctx + rowj[rt];   // last visible key position
-      float sv[8];
-      float mx = -INFINITY;
+      float v = fmaxf(fmaxf(fmaxf(st[0][rt][0], st[0][rt][1]), fmaxf(st[0][rt][2], st[0][rt][3])),
+                      fmaxf(fmaxf(st[1][rt][0], st[1][rt][1]), fmaxf(st[1][rt][2], st[1][rt][3])));
+      v = fmaxf(v, __shfl_xor(v, 16, kWave));
+      v = fmaxf(v, __shfl_xor(v, 32, kWave));
+      mx[rt] = v * c;
+      grow |= mx[rt] > m_run[rt] + kRescaleSlack;
+    }
+    // lazy rescale, uniform over the wavefront: only when some row's maximum has grown by
+    // more than the slack (the result is the same softmax for any reference maximum)
+    if (__builtin_amdgcn_read_exec() & __ballot(grow)) {
+#pragma unroll
+      for (int rt = 0; rt < RT; ++rt) {
+        const float m_new = fmaxf(m_run[rt], mx[rt]);
+        const float alpha = exp2f(m_run[rt] - m_new);
+        l_run[rt] *= alpha;
+        m_run[rt] = m_new;
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) o[dt][rt] *= alpha;
+      }
+    }
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt) {
+      const float nm = -m_run[rt];
+      float ps = 0.f;
+      bf16x8_t pf;
 #pragma unroll
       for (int t = 0; t < 2; ++t)
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          const int kpos = (t == 0 ? pb : pb2) * 16 + g4 * 4 + e;
-          const bool vis = (t == 0 || has2) && kpos <= lim;
-          const float v = vis ? st[t][rt][e] * p.scale_log2 : -INFINITY;
-          sv[t * 4 + e] = v;
-          mx = fmaxf(mx, v);
+          const __bf16 pb16 = __bf16(exp2f(fmaf(st[t][rt][e], c, nm)));
+          pf[t * 4 + e] = pb16;
+          ps += float(pb16);   // the normaliser sums the same rounded weights the MFMA uses
         }
-      mx = fmaxf(mx, __shfl_xor(mx, 16, kWave));
-      mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
-      const float m_new = fmaxf(m_run[rt], mx);
-      const float alpha = (m_new == -INFINITY) ? 1.f : exp2f(m_run[rt] - m_new);
-      float ps = 0.f;
-      bf16x8_t pf;
+      l_run[rt] += ps;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const float pe = (sv[e] == -INFINITY) ? 0.f : exp2f(sv[e] - m_new);
-        const __bf16 pb16 = __bf16(pe);
-        pf[e] = pb16;
-        ps += float(pb16);   // the normaliser sums the same rounded weights the MFMA uses
-      }
-      l_run[rt] = l_run[rt] * alpha + ps;
-      m_run[rt] = m_new;
-#pragma unroll
-      for (int dt = 0; dt < DT; ++dt) {
-        o[dt][rt] *= alpha;
-        o[dt][rt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf[dt], pf, o[dt][rt], 0, 0, 0);
-      }
+      for (int dt = 0; dt < DT; ++dt)
+        o[dt][rt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(f.v[dt], pf, o[dt][rt], 0, 0, 0);
+    }
+  };
+
+  // software pipeline: the next block pair's fragments load while the current one computes
+  int pb = blk0 + 2 * wave;
+  if (pb < blk1) {
+    PairFrags<D> fa, fb;
+    load_pair(fa, pb);
+    while (true) {
+      if (pb + 2 * kWaves < blk1) load_pair(fb, pb + 2 * kWaves);
+      compute_pair(fa, pb);
+      pb += 2 * kWaves;
+      if (pb >= blk1) break;
+      if (pb + 2 * kWaves < blk1) load_pair(fa, pb + 2 * kWaves);
+      compute_pair(fb, pb);
+      pb += 2 * kWaves;
+      if (pb >= blk1) break;
     }
   }
 
@@ -189,9 +238,9 @@ __global__ __launch_bounds__(kThreads) void attn_mfma_kernel(AttnParams p) {
 #pragma unroll
   for (int rt = 0; rt < RT; ++rt) {
     const int r = rt * 16 + l16;
-    float M = -INFINITY;
+    float M = kNegBig;
     for (int w = 0; w < kWaves; ++w) M = fmaxf(M, s_m[w][r]);
-    fac[rt] = (s_m[wave][r] == -INFINITY) ? 0.f : exp2f(s_m[wave][r] - M);
+    fac[rt] = exp2f(s_m[wave][r] - M);
   }
   // O^T accumulator element e of lane: dim 16 dt + 4 g4 + e, row 16 rt + l16
   for (int w = 0; w < kWaves; ++w) {
@@ -212,11 +261,10 @@ __global__ __launch_bounds__(kThreads) void attn_mfma_kernel(AttnParams p) {
   // final row statistics and output
   for (int idx = threadIdx.x; idx < R * D; idx += kThreads) {
     const int r = idx / D, dd = idx % D;
-    float M = -INFINITY;
+    float M = kNegBig;
     for (int w = 0; w < kWaves; ++w) M = fmaxf(M, s_m[w][r]);
     float Lsum = 0.f;
-    for (int w = 0; w < kWaves; ++w)
-      if (s_m[w][r] != -INFINITY) Lsum += s_l[w][r] * exp2f(s_m[w][r] - M);
+    for (int w = 0; w < kWaves; ++w) Lsum += s_l[w][r] * exp2f(s_m[w][r] - M);
     const int j = r / G, gi = r % G;
     if (p.splits == 1) {
       const float v = Lsum > 0.f ? s_o[idx] / Lsum : 0.f;
@@ -242,14 +290,13 @@ __global__ __launch_bounds__(D) void attn_merge_kernel(AttnParams p, int out_f32
   const int bh = blockIdx.x / R;
   const int b = bh / p.Hkv, h = bh % p.Hkv;
   const int nblk = (p.ctx[b] + kp1 + 15) / 16;
-  const int ns = min(p.splits, (nblk + kBlocksPerSplit - 1) / kBlocksPerSplit);
-  float M = -INFINITY;
+  const int ns = min(p.splits, (nblk + p.blocks_per_split - 1) / p.blocks_per_split);
+  float M = kNegBig;
   for (int s = 0; s < ns; ++s) M = fmaxf(M, p.part_ml[((long(bh) * p.splits + s) * R + r) * 2]);
   float L = 0.f, acc = 0.f;
   for (int s = 0; s < ns; ++s) {
     const long pr = (long(bh) * p.splits + s) * R + r;
     const float m = p.part_ml[pr * 2];
-    if (m == -INFINITY) continue;
     const float f = exp2f(m - M);
     L += p.part_ml[pr * 2 + 1] * f;
     acc += p.part_o[pr * D + threadIdx.x] * f;
@@ -314,7 +361,18 @@ __global__ __launch_bounds__(kWave) void attn_f32_kernel(const float* __restrict
   }
 }
 
-int splits_for(int max_blocks) { return (max_blocks + kBlocksPerSplit - 1) / kBlocksPerSplit; }
+// Splits of the key range: enough workgroups to fill the chip twice over (512), each split a
+// multiple of 8 blocks (4 wavefronts x one 32-key pair) and at least 32 blocks long.
+void split_plan(int B, int Hkv, int max_blocks, int& splits, int& bps) {
+  const int pairs = B * Hkv;
+  int s = (512 + pairs - 1) / pairs;
+  const int cap = (max_blocks + 31) / 32;
+  if (s > cap) s = cap;
+  if (s < 1) s = 1;
+  bps = (max_blocks + s - 1) / s;
+  bps = (bps + 7) / 8 * 8;
+  splits = (max_blocks + bps - 1) / bps;
+}
 
 template <int D, int RT>
 void launch_mfma(const AttnParams& p, int B, hipStream_t s) {
@@ -341,8 +399,9 @@ hipError_t launch_d(const AttnParams& p, int B, int R, hipStream_t s) {
 
 }  // namespace
 
-size_t attention_ws_bytes(int B, int k, int Hq, int D, int max_blocks) {
-  const int S = splits_for(max_blocks);
+size_t attention_ws_bytes(int B, int k, int Hq, int Hkv, int D, int max_blocks) {
+  int S, bps;
+  split_plan(B, Hkv, max_blocks, S, bps);
   if (S <= 1) return 0;
   const long rows = long(B) * (k + 1) * Hq;   // = B * Hkv * R
   Carver c(nullptr, 0);
@@ -371,7 +430,7 @@ hipError_t launch_paged_attention(const void* q, const void* kc, const void* vc,
                                                         static_cast<const float*>(vc), p, D);
     return hipGetLastError();
   }
-  p.splits = splits_for(max_blocks);
+  split_plan(B, Hkv, max_blocks, p.splits, p.blocks_per_split);
   if (p.splits > 1) {
     const long rows = long(B) * (k + 1) * Hq;
     Carver c(ws, 0);

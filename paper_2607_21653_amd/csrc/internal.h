@@ -71,7 +71,7 @@ hipError_t launch_moe_down(const void* h, const uint8_t* hq, const float* hs, co
 int moe_tile_m(molt_dtype wdt);
 
 // ------------------------------------------------------------- attention
-size_t attention_ws_bytes(int B, int k, int Hq, int D, int max_blocks);
+size_t attention_ws_bytes(int B, int k, int Hq, int Hkv, int D, int max_blocks);
 hipError_t launch_paged_attention(const void* q, const void* kc, const void* vc, const int32_t* bt,
                                   const int32_t* ctx, int B, int k, int Hq, int Hkv, int D,
                                   int max_blocks, molt_dtype dt, void* out, void* ws,
