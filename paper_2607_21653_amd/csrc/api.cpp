@@ -169,13 +169,14 @@ namespace {
 struct MoeWs {
   float* g; int32_t* ids; float* w; int32_t* counts; int32_t* offsets; int32_t* perm;
   int32_t* inv; int32_t* tiles; int32_t* n_tiles; uint8_t* xq; float* xs; void* h; uint8_t* hq;
-  float* hs; float* o; int max_tiles;
+  float* hs; float* o; int max_tiles; int tile_m;
 };
 
 MoeWs carve_moe(molt::Carver& c, int T, int d, int E, int K, int F, molt_dtype act, molt_dtype w) {
   MoeWs m{};
   const long P = long(T) * K;
-  const int tm = molt::moe_tile_m(w);
+  const int tm = molt::moe_tile_m(w, T, K, E);
+  m.tile_m = tm;
   m.max_tiles = molt::max_expert_tiles(T, E, K, tm);
   m.g = c.take<float>(long(T) * E);
   m.ids = c.take<int32_t>(P);
@@ -222,7 +223,7 @@ hipError_t run_moe(const MoeWs& m, const void* x, const uint8_t* xq, const float
     if ((e = molt::launch_gemm(x, w_router, m.g, T, E, d, act, false, s)) != hipSuccess) return e;
   }
   if ((e = molt::launch_route(m.g, bias, replay, T, E, K, m.ids, m.w, m.counts, m.offsets, m.perm,
-                              m.inv, molt::moe_tile_m(wdt), m.tiles, m.max_tiles, m.n_tiles, s)) !=
+                              m.inv, m.tile_m, m.tiles, m.max_tiles, m.n_tiles, s)) !=
       hipSuccess)
     return e;
   if (wdt == MOLT_FP8_E4M3 && xq == nullptr) {
@@ -235,7 +236,7 @@ hipError_t run_moe(const MoeWs& m, const void* x, const uint8_t* xq, const float
   {
     ProfScope ps(MOLT_PROF_EXPERT_GEMM, s);
     if ((e = molt::launch_moe_gate_up(x, xq, xs, m.perm, K, w_gu, s_gu, d, F, act, wdt, m.tiles,
-                                      m.max_tiles, m.h, s)) != hipSuccess)
+                                      m.max_tiles, m.tile_m, m.h, s)) != hipSuccess)
       return e;
   }
   if (wdt == MOLT_FP8_E4M3) {
@@ -246,7 +247,7 @@ hipError_t run_moe(const MoeWs& m, const void* x, const uint8_t* xq, const float
   {
     ProfScope ps(MOLT_PROF_EXPERT_GEMM, s);
     if ((e = molt::launch_moe_down(m.h, m.hq, m.hs, w_d, s_d, d, F, act, wdt, m.tiles, m.max_tiles,
-                                   m.o, s)) != hipSuccess)
+                                   m.tile_m, m.o, s)) != hipSuccess)
       return e;
   }
   return molt::launch_combine(m.o, m.inv, m.w, T, K, d, out, accumulate, s);

@@ -268,6 +268,216 @@ __global__ __launch_bounds__(kThreads) void mfma_gemm_kernel(GemmParams p) {
   }
 }
 
+// ---------------------------------------------------------------- weight-streaming grouped GEMM
+// Expert GEMMs are HBM-bound at the verify step's row counts (tens of rows per expert),
+// so the weights must stream at full bandwidth and be read once. Workgroup = BM rows of
+// one expert x 128 output columns; each of the 4 wavefronts owns 32 columns and loads its
+// weight fragments straight from global memory into registers, kPD 128-byte K slices
+// ahead (a weight element is used by exactly one wavefront: no LDS needed). The
+// activation rows (shared by the 4 wavefronts) are prefetched kPD slices ahead into
+// registers too and staged through a double-buffered LDS tile, one barrier per slice. A
+// lane's MFMA operand chunk for k-step s of a slice is bytes [64 g + 16 s, +16) (bf16,
+// g = lane / 32) or [64 g + 32 s, +32) (fp8) of its row, for both operands: each lane
+// streams 64 contiguous bytes of its weight row per slice.
+constexpr int kPD = 4;   // slices in flight per wavefront
+
+struct Slice16 { int4 c[4]; };   // 64 bytes of one row: 4 x 16 B
+
+template <int BM, bool FP8, int MODE>
+__global__ __launch_bounds__(kThreads) void moe_stream_kernel(GemmParams p) {
+  constexpr int MS = BM / 32;                        // 32-row MFMA tiles per wavefront
+  constexpr int kElem = FP8 ? 1 : 2;
+  constexpr int kBK = kRowBytes / kElem;             // K elements per slice
+  constexpr int kALoads = BM * 8 / kThreads;         // 16-byte A chunks per thread per slice
+  static_assert(kALoads >= 1, "BM too small");
+  __shared__ __attribute__((aligned(16))) uint8_t lds[2 * BM * kLdsStride];
+
+  int id = blockIdx.x;
+  const int G = gridDim.x;
+  id = (id % 8) * (G / 8) + id / 8;                   // grid is a multiple of 8: XCD-local order
+  if (id >= p.n_mtiles * p.n_ntiles) return;
+  const int mt = id % p.n_mtiles;
+  const int nt = id / p.n_mtiles;
+  const int4 tinfo = p.tiles[mt];
+  if (tinfo.x < 0) return;
+  const int expert = tinfo.x, row0 = tinfo.y, row1 = tinfo.z;
+  const long K = p.K;
+  const int nk = int(K / kBK);
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+  const int lane = threadIdx.x % kWave;
+  const int lrow = lane % 32, lg = lane / 32;
+
+  // weight row of this lane (column lrow of the wavefront's 32)
+  long brow;
+  int n0;
+  if (MODE == kGateUp) {
+    n0 = nt * (kBN / 2);
+    brow = long(expert) * 2 * p.N + (wave < 2 ? n0 + 32 * wave + lrow : p.N + n0 + 32 * (wave - 2) + lrow);
+  } else {
+    n0 = nt * kBN;
+    brow = long(expert) * p.N + n0 + 32 * wave + lrow;
+  }
+  const uint8_t* bsrc = static_cast<const uint8_t*>(p.B) + brow * K * kElem + lg * 64;
+
+  // activation rows staged by all threads: chunk c of row r = tid / 8 + 32 i. Rows past the
+  // tile read row row0 (always valid); MFMA rows are independent and those outputs are
+  // never stored, so the loads carry no branches and their count stays exact.
+  const int chunk = threadIdx.x % 8;
+  const uint8_t* a_src[kALoads];
+#pragma unroll
+  for (int i = 0; i < kALoads; ++i) {
+    const int grow = row0 + threadIdx.x / 8 + 32 * i;
+    long arow = grow < row1 ? grow : row0;
+    if (MODE == kGateUp) arow = p.perm[arow] / p.ktop;
+    a_src[i] = static_cast<const uint8_t*>(p.A) + arow * K * kElem + chunk * 16;
+  }
+
+  Slice16 wb[kPD];
+  auto wload = [&](Slice16& f, int kb) {
+    const uint8_t* src = bsrc + long(kb) * kRowBytes;
+#pragma unroll
+    for (int c = 0; c < 4; ++c) f.c[c] = *reinterpret_cast<const int4*>(src + 16 * c);
+  };
+  int4 ra[kPD][kALoads];
+  auto aload = [&](int4 (&r)[kALoads], int kb) {
+#pragma unroll
+    for (int i = 0; i < kALoads; ++i)
+      r[i] = *reinterpret_cast<const int4*>(a_src[i] + long(kb) * kRowBytes);
+  };
+  auto astore = [&](const int4 (&r)[kALoads], int buf) {
+#pragma unroll
+    for (int i = 0; i < kALoads; ++i)
+      *reinterpret_cast<int4*>(lds + buf * BM * kLdsStride +
+                               (threadIdx.x / 8 + 32 * i) * kLdsStride + chunk * 16) = r[i];
+  };
+
+  floatx16_t acc[MS];
+#pragma unroll
+  for (int i = 0; i < MS; ++i)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) acc[i][e] = 0.f;
+
+#pragma unroll
+  for (int s = 0; s < kPD; ++s)
+    if (s < nk) {
+      wload(wb[s], s);
+      aload(ra[s], s);
+    }
+  astore(ra[0], 0);
+  __syncthreads();
+
+  auto slice = [&](const Slice16& f, int buf) {
+    const uint8_t* abase = lds + buf * BM * kLdsStride + lrow * kLdsStride + lg * 64;
+    if (!FP8) {
+#pragma unroll
+      for (int s = 0; s < 4; ++s) {
+        const bf16x8_t bv = *reinterpret_cast<const bf16x8_t*>(&f.c[s]);
+        bf16x8_t av[MS];
+#pragma unroll
+        for (int i = 0; i < MS; ++i)
+          av[i] = *reinterpret_cast<const bf16x8_t*>(abase + i * 32 * kLdsStride + 16 * s);
+#pragma unroll
+        for (int i = 0; i < MS; ++i) acc[i] = mfma(av[i], bv, acc[i]);
+      }
+    } else {
+#pragma unroll
+      for (int s = 0; s < 2; ++s) {
+        const int32x8_t bv = int32x8_t{f.c[2 * s].x, f.c[2 * s].y, f.c[2 * s].z, f.c[2 * s].w,
+                                       f.c[2 * s + 1].x, f.c[2 * s + 1].y, f.c[2 * s + 1].z,
+                                       f.c[2 * s + 1].w};
+        int32x8_t av[MS];
+#pragma unroll
+        for (int i = 0; i < MS; ++i) {
+          const uint8_t* q = abase + i * 32 * kLdsStride + 32 * s;
+          const int32x4_t lo = *reinterpret_cast<const int32x4_t*>(q);
+          const int32x4_t hi = *reinterpret_cast<const int32x4_t*>(q + 16);
+          av[i] = int32x8_t{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+        }
+#pragma unroll
+        for (int i = 0; i < MS; ++i) acc[i] = mfma(av[i], bv, acc[i]);
+      }
+    }
+  };
+
+  // slice kb = kb0 + s: stage slice kb+1 (register set (s+1) % kPD) into LDS, compute slice
+  // kb from register set s, then refill set s with slice kb + kPD; one barrier per slice
+  for (int kb0 = 0; kb0 < nk; kb0 += kPD) {
+#pragma unroll
+    for (int s = 0; s < kPD; ++s) {
+      const int kb = kb0 + s;
+      if (kb < nk) {
+        if (kb + 1 < nk) astore(ra[(s + 1) % kPD], (kb + 1) & 1);
+        slice(wb[s], kb & 1);
+        if (kb + kPD < nk) {
+          wload(wb[s], kb + kPD);
+          aload(ra[s], kb + kPD);
+        }
+        __syncthreads();
+      }
+    }
+  }
+
+  // ---- epilogue: acc[i][e] is row 32 i + 8 (e/4) + 4 (lane/32) + e%4, column lane%32
+  const int lcol = lane % 32, lgrp = lane / 32;
+  if (MODE == kGateUp) {
+    // the "up" wavefronts (tile columns 64..127) park their values in LDS; the "gate"
+    // wavefronts finish h = silu(gate) * up for their columns
+    float* upbuf = reinterpret_cast<float*>(lds);   // [BM][64] fits in 2 * BM * 144 bytes
+    if (wave >= 2) {
+#pragma unroll
+      for (int i = 0; i < MS; ++i)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int r = 32 * i + 8 * (e / 4) + 4 * lgrp + (e % 4);
+          upbuf[r * 64 + 32 * (wave - 2) + lcol] = acc[i][e];
+        }
+    }
+    __syncthreads();
+    if (wave < 2) {
+      const int c = 32 * wave + lcol;
+#pragma unroll
+      for (int i = 0; i < MS; ++i)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int r = 32 * i + 8 * (e / 4) + 4 * lgrp + (e % 4);
+          const int grow = row0 + r;
+          if (grow >= row1) continue;
+          float g = acc[i][e], u = upbuf[r * 64 + c];
+          if (FP8) {
+            const float sx = p.a_scale[p.perm[grow] / p.ktop];
+            const float* sw = p.b_scale + long(expert) * p.b_scale_ld;
+            g = g * sx * sw[n0 + c];
+            u = u * sx * sw[p.N + n0 + c];
+          }
+          static_cast<uint16_t*>(p.C)[long(grow) * p.ldc + n0 + c] = f32_to_bf16(silu(g) * u);
+        }
+    }
+  } else {
+    const int c = n0 + 32 * wave + lcol;
+#pragma unroll
+    for (int i = 0; i < MS; ++i)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int r = 32 * i + 8 * (e / 4) + 4 * lgrp + (e % 4);
+        const int grow = row0 + r;
+        if (grow >= row1) continue;
+        float v = acc[i][e];
+        if (FP8) v = v * p.a_scale[grow] * p.b_scale[long(expert) * p.b_scale_ld + c];
+        static_cast<float*>(p.C)[long(grow) * p.ldc + c] = v;
+      }
+  }
+}
+
+template <bool FP8, int MODE>
+hipError_t run_stream(GemmParams p, int tile_m, hipStream_t s) {
+  int grid = p.n_mtiles * p.n_ntiles;
+  grid = (grid + 7) / 8 * 8;
+  if (tile_m == 32) moe_stream_kernel<32, FP8, MODE><<<grid, kThreads, 0, s>>>(p);
+  else if (tile_m == 64) moe_stream_kernel<64, FP8, MODE><<<grid, kThreads, 0, s>>>(p);
+  else moe_stream_kernel<128, FP8, MODE><<<grid, kThreads, 0, s>>>(p);
+  return hipGetLastError();
+}
+
 // ---------------------------------------------------------------- f32 VALU path
 // One workgroup per (row tile of 16, column tile of 64); each thread owns 4 outputs.
 template <int MODE>
@@ -324,7 +534,13 @@ hipError_t run_mfma(GemmParams p, int grid, hipStream_t s) {
 
 }  // namespace
 
-int moe_tile_m(molt_dtype wdt) { return wdt == MOLT_F32 ? 16 : 32; }
+// Row-tile height of the grouped expert GEMMs: large enough that an expert of average load
+// fits one tile (its weights are then streamed once), as small as that allows.
+int moe_tile_m(molt_dtype wdt, int T, int K, int E) {
+  if (wdt == MOLT_F32) return 16;
+  const long avg = (long(T) * K + E - 1) / E;
+  return avg <= 24 ? 32 : avg <= 56 ? 64 : 128;
+}
 
 hipError_t launch_gemm(const void* A, const void* Bw, float* C, int M, int N, int K, molt_dtype dt,
                        bool accumulate, hipStream_t s) {
@@ -350,7 +566,7 @@ hipError_t launch_gemm(const void* A, const void* Bw, float* C, int M, int N, in
 hipError_t launch_moe_gate_up(const void* x, const uint8_t* xq, const float* xs, const int32_t* perm,
                               int K_top, const void* w_gu, const float* s_gu, int d, int F,
                               molt_dtype act, molt_dtype wdt, const int32_t* tiles, int max_tiles,
-                              void* h, hipStream_t s) {
+                              int tile_m, void* h, hipStream_t s) {
   GemmParams p{};
   p.A = wdt == MOLT_FP8_E4M3 ? static_cast<const void*>(xq) : x;
   p.B = w_gu; p.C = h; p.N = F; p.K = d; p.ldc = F;
@@ -364,13 +580,14 @@ hipError_t launch_moe_gate_up(const void* x, const uint8_t* xq, const float* xs,
     return hipGetLastError();
   }
   p.n_ntiles = F / (kBN / 2);
-  if (wdt == MOLT_FP8_E4M3) return run_mfma<32, true, kGateUp>(p, max_tiles * p.n_ntiles, s);
-  return run_mfma<32, false, kGateUp>(p, max_tiles * p.n_ntiles, s);
+  if (wdt == MOLT_FP8_E4M3) return run_stream<true, kGateUp>(p, tile_m, s);
+  return run_stream<false, kGateUp>(p, tile_m, s);
 }
 
 hipError_t launch_moe_down(const void* h, const uint8_t* hq, const float* hs, const void* w_d,
                            const float* s_d, int d, int F, molt_dtype act, molt_dtype wdt,
-                           const int32_t* tiles, int max_tiles, float* o, hipStream_t s) {
+                           const int32_t* tiles, int max_tiles, int tile_m, float* o,
+                           hipStream_t s) {
   GemmParams p{};
   p.A = wdt == MOLT_FP8_E4M3 ? static_cast<const void*>(hq) : h;
   p.B = w_d; p.C = o; p.N = d; p.K = F; p.ldc = d;
@@ -383,8 +600,8 @@ hipError_t launch_moe_down(const void* h, const uint8_t* hq, const float* hs, co
     return hipGetLastError();
   }
   p.n_ntiles = d / kBN;
-  if (wdt == MOLT_FP8_E4M3) return run_mfma<32, true, kDown>(p, max_tiles * p.n_ntiles, s);
-  return run_mfma<32, false, kDown>(p, max_tiles * p.n_ntiles, s);
+  if (wdt == MOLT_FP8_E4M3) return run_stream<true, kDown>(p, tile_m, s);
+  return run_stream<false, kDown>(p, tile_m, s);
 }
 
 }  // namespace molt

@@ -64,11 +64,12 @@ hipError_t launch_gemm(const void* A, const void* Bw, float* C, int M, int N, in
 hipError_t launch_moe_gate_up(const void* x, const uint8_t* xq, const float* xs, const int32_t* perm,
                               int K_top, const void* w_gu, const float* s_gu, int d, int F,
                               molt_dtype act, molt_dtype wdt, const int32_t* tiles, int max_tiles,
-                              void* h, hipStream_t s);
+                              int tile_m, void* h, hipStream_t s);
 hipError_t launch_moe_down(const void* h, const uint8_t* hq, const float* hs, const void* w_d,
                            const float* s_d, int d, int F, molt_dtype act, molt_dtype wdt,
-                           const int32_t* tiles, int max_tiles, float* o, hipStream_t s);
-int moe_tile_m(molt_dtype wdt);
+                           const int32_t* tiles, int max_tiles, int tile_m, float* o,
+                           hipStream_t s);
+int moe_tile_m(molt_dtype wdt, int T, int K, int E);
 
 // ------------------------------------------------------------- attention
 size_t attention_ws_bytes(int B, int k, int Hq, int Hkv, int D, int max_blocks);
