@@ -170,6 +170,16 @@ int molt_paged_attention(const void* q, const void* k_cache, const void* v_cache
                          molt_stream_t stream);
 
 /* ------------------------------------------------------------------------------
+ * molt_dense_gemm -- the dense projection of the verify step's decoder (QKV, O, router,
+ * LM head): C[M, N] (f32) = A[M, K] * B[N, K]^T, or C += A * B^T with accumulate != 0
+ * (the O projection adds into the residual stream). A and B row-major in `dtype` (F32 or
+ * BF16), K contiguous, f32 accumulation. Supported: M, N, K >= 1; BF16 needs K % 64 == 0.
+ * No workspace.
+ * ---------------------------------------------------------------------------- */
+int molt_dense_gemm(const void* A, const void* B, float* C, int M, int N, int K, molt_dtype dtype,
+                    int accumulate, molt_stream_t stream);
+
+/* ------------------------------------------------------------------------------
  * Model description: a HOST struct holding device pointers; read only during a
  * call. Per-layer members are HOST arrays of n_layers device pointers.
  * Pre-norm decoder (Sec. 5.3/5.4 run MoE decoders):

@@ -48,6 +48,7 @@ _SIGS = {
     "molt_moe_layer": (c_int, [c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_int, c_int, c_int,
                                c_int, c_int, c_int, c_int, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp,
                                c_vp, c_vp, c_size, c_vp]),
+    "molt_dense_gemm": (c_int, [c_vp, c_vp, c_vp, c_int, c_int, c_int, c_int, c_int, c_vp]),
     "molt_paged_attention_workspace_size": (c_size, [c_int] * 6),
     "molt_paged_attention": (c_int, [c_vp, c_vp, c_vp, c_vp, c_vp, c_int, c_int, c_int, c_int,
                                      c_int, c_int, c_int, c_vp, c_vp, c_size, c_vp]),
@@ -189,6 +190,23 @@ def moe_layer(x, w_router, w_gate_up, w_down, top_k, router_bias=None, s_gate_up
     if want_routing:
         return out, ids, wts, counts, offsets, perm
     return out
+
+
+# ------------------------------------------------------------------ dense GEMM
+
+def dense_gemm(A, B, C=None, accumulate=False):
+    """C [M, N] f32 = A [M, K] @ B [N, K]^T (+ C when accumulate); A, B f32 or bf16."""
+    lib = load()
+    M, K = A.shape
+    N = B.shape[0]
+    _dev(A, None, name="A")
+    _dev(B, A.dtype, (N, K), "B")
+    if C is None:
+        C = torch.zeros(M, N, dtype=torch.float32, device=A.device)
+    _dev(C, torch.float32, (M, N), "C")
+    _check(lib.molt_dense_gemm(_ptr(A), _ptr(B), _ptr(C), M, N, K, DTYPE_CODE[A.dtype],
+                               1 if accumulate else 0, _stream()), "molt_dense_gemm")
+    return C
 
 
 # ------------------------------------------------------------------ paged attention

@@ -298,6 +298,23 @@ int molt_moe_layer(const void* x, const void* w_router, const float* router_bias
   return hip_status(e, "molt_moe_layer");
 }
 
+// ------------------------------------------------------------------ dense GEMM
+
+int molt_dense_gemm(const void* A, const void* B, float* C, int M, int N, int K, molt_dtype dtype,
+                    int accumulate, molt_stream_t stream) {
+  REQUIRE(A && B && C, "a required pointer is NULL");
+  REQUIRE(M >= 1 && N >= 1 && K >= 1, "M, N, K must be >= 1 (got %d, %d, %d)", M, N, K);
+  REQUIRE(act_ok(dtype), "dtype must be F32 or BF16");
+  REQUIRE(dtype == MOLT_F32 || K % 64 == 0, "bf16 needs K %% 64 == 0 (K = %d)", K);
+  hipError_t e;
+  {
+    ProfScope ps(MOLT_PROF_PROJECTIONS, reinterpret_cast<hipStream_t>(stream));
+    e = molt::launch_gemm(A, B, C, M, N, K, dtype, accumulate != 0,
+                          reinterpret_cast<hipStream_t>(stream));
+  }
+  return hip_status(e, "molt_dense_gemm");
+}
+
 // ------------------------------------------------------------------ paged attention
 
 static int attn_shape_ok(int B, int k, int Hq, int Hkv, int D, int max_blocks, molt_dtype dt) {

@@ -298,9 +298,17 @@ __global__ __launch_bounds__(kThreads) void moe_stream_kernel(GemmParams p) {
   if (id >= p.n_mtiles * p.n_ntiles) return;
   const int mt = id % p.n_mtiles;
   const int nt = id / p.n_mtiles;
-  const int4 tinfo = p.tiles[mt];
-  if (tinfo.x < 0) return;
-  const int expert = tinfo.x, row0 = tinfo.y, row1 = tinfo.z;
+  int expert = 0, row0, row1;
+  if (MODE == kDense) {
+    row0 = mt * BM;
+    row1 = min(row0 + BM, p.M);
+  } else {
+    const int4 tinfo = p.tiles[mt];
+    if (tinfo.x < 0) return;
+    expert = tinfo.x;
+    row0 = tinfo.y;
+    row1 = tinfo.z;
+  }
   const long K = p.K;
   const int nk = int(K / kBK);
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
@@ -315,7 +323,7 @@ __global__ __launch_bounds__(kThreads) void moe_stream_kernel(GemmParams p) {
     brow = long(expert) * 2 * p.N + (wave < 2 ? n0 + 32 * wave + lrow : p.N + n0 + 32 * (wave - 2) + lrow);
   } else {
     n0 = nt * kBN;
-    brow = long(expert) * p.N + n0 + 32 * wave + lrow;
+    brow = long(expert) * p.N + n0 + 32 * wave + lrow;   // dense: expert 0, N % 128 == 0
   }
   const uint8_t* bsrc = static_cast<const uint8_t*>(p.B) + brow * K * kElem + lg * 64;
 
@@ -463,7 +471,9 @@ __global__ __launch_bounds__(kThreads) void moe_stream_kernel(GemmParams p) {
         if (grow >= row1) continue;
         float v = acc[i][e];
         if (FP8) v = v * p.a_scale[grow] * p.b_scale[long(expert) * p.b_scale_ld + c];
-        static_cast<float*>(p.C)[long(grow) * p.ldc + c] = v;
+        float* dst = static_cast<float*>(p.C) + long(grow) * p.ldc + c;
+        if (MODE == kDense && p.accumulate) v += *dst;
+        *dst = v;
       }
   }
 }

@@ -44,8 +44,8 @@ def test_workspace_queries(L):
     assert L.molt_spec_accept_workspace_size(0, 4, 10) == 0
     assert L.molt_moe_layer_workspace_size(640, 2048, 128, 8, 768, 1, 1) > 640 * 8 * 2048 * 4
     assert L.molt_moe_layer_workspace_size(64, 2048, 128, 8, 768, 0, 1) == 0     # bad pair
-    assert L.molt_paged_attention_workspace_size(128, 4, 32, 4, 128, 513) > 0
-    assert L.molt_paged_attention_workspace_size(128, 4, 32, 4, 128, 64) == 0     # one split
+    assert L.molt_paged_attention_workspace_size(16, 4, 32, 4, 128, 4097) > 0    # split key range
+    assert L.molt_paged_attention_workspace_size(128, 4, 32, 4, 128, 513) == 0    # one split: none
 
 
 def _accept(L, B=2, k=1, V=10, logits=1, drafts=1, u=1, toks=1, n=1, ws=1, wsb=1 << 20):
@@ -96,7 +96,7 @@ def test_attention_validation(L):
     assert call(k=-1) == INVALID
     assert call(Hq=64, Hkv=2, k=4) == INVALID     # 160 query rows per kv head
     assert call(dt=2) == INVALID
-    assert call(mb=200, ws=None, wsb=0) == WORKSPACE
+    assert call(B=2, mb=2000, ws=None, wsb=0) == WORKSPACE
 
 
 def test_model_validation(L):

@@ -17,6 +17,19 @@ from helpers import dev, host, layer_host, max_abs, model_from, oracle_cfg
 
 pytestmark = pytest.mark.gpu
 
+# A token's route set is unique when its oracle K-th/(K+1)-th router-logit gap is clear of
+# the rounding the residual stream has picked up upstream; inside whole layers that
+# rounding moves router logits by up to a few 1e-3, so a differing set must come with an
+# oracle gap below 1e-2 (a near-tie), and such tokens are excluded from value comparison.
+ROUTE_TIE = 1e-2
+
+
+def _route_sets_agree(gpu_ids, oracle_ids, oracle_margin, max_frac=0.05):
+    same = (np.sort(gpu_ids, axis=-1) == np.sort(oracle_ids, axis=-1)).all(axis=-1)
+    assert (oracle_margin[~same] < ROUTE_TIE).all(), "a route set differs away from a tie"
+    assert (~same).mean() <= max_frac, (~same).mean()
+    return same
+
 
 def _tiny_setup(seed=0, **kw):
     w = workloads.TINY_FP32.scaled(**kw)
@@ -109,19 +122,78 @@ def test_bf16_decoder_layer(molt_lib, fp8):
     ovc = omodel.widen_cache(host(vc), w.dtype)
     xo = omodel.attention_block(host(x), lh, okc, ovc, layout.block_tables, layout.context_lens, w.k, cfg)
     xo, r = omodel.moe_block(xo, lh, cfg)
-    near = r["margin"] < 2e-3
-    assert near.mean() < 0.1
+    gr = routes.cpu().numpy()[0]
+    same = _route_sets_agree(gr, r["ids"], r["margin"])
     g = xg.cpu().numpy()
-    err = max_abs(g[~near], xo[~near])
-    d = (g[~near] - xo[~near]).astype(np.float64)
-    rel = float(np.sqrt((d * d).mean() / (xo[~near].astype(np.float64) ** 2).mean()))
-    print(f"max |x - oracle| = {err:.3e}, relative rms {rel:.2e} ({near.sum()} near-tie tokens excluded)",
+    err = max_abs(g[same], xo[same])
+    d = (g[same] - xo[same]).astype(np.float64)
+    rel = float(np.sqrt((d * d).mean() / (xo[same].astype(np.float64) ** 2).mean()))
+    print(f"max |x - oracle| = {err:.3e}, relative rms {rel:.2e} ({(~same).sum()} near-tie tokens excluded)",
           flush=True)
     assert err <= (5e-2 if fp8 else 2e-2)
     assert rel <= 1e-2
-    gr = routes.cpu().numpy()[0]
-    # the expert set is unique where the K/(K+1) gap is clear; the slot order where the
-    # adjacent gaps inside the selection are clear too
-    assert (np.sort(gr[~near], axis=1) == np.sort(r["ids"][~near], axis=1)).all()
-    ordered = ~near & (r["order_margin"] >= 2e-3)
+    # the slot order is unique where the adjacent gaps inside the selection are clear too
+    ordered = same & (r["order_margin"] >= ROUTE_TIE)
     assert (gr[ordered] == r["ids"][ordered]).all()
+
+
+def test_bf16_decoder_layer_many_tokens(molt_lib):
+    """T = 320 tokens: the dense projections run 128-row tiles with a ragged 64-row tail."""
+    w = workloads.LAYER_BF16.scaled(batch=64, k=4, ctx_lo=40, ctx_hi=300)
+    cfg = oracle_cfg(w)
+    seed = 12
+    layout = workloads.make_kv_layout(w, seed)
+    lw = workloads.make_layer_weights(w, seed, 0)
+    kc, vc = workloads.make_kv_cache(w, layout, seed, 0)
+    x = workloads.make_hidden(w, seed)
+    model = model_from(w, [lw], None, molt_lib)
+    kv = molt_lib.KVCache([dev(kc)], [dev(vc)], dev(torch.from_numpy(layout.block_tables)),
+                          dev(torch.from_numpy(layout.context_lens)))
+    xg = dev(x.clone())
+    routes = molt_lib.decoder_forward(model, kv, w.batch, w.k, xg, want_routes=True)
+    torch.cuda.synchronize()
+    lh = layer_host(lw)
+    xo = omodel.attention_block(host(x), lh, omodel.widen_cache(host(kc), w.dtype),
+                                omodel.widen_cache(host(vc), w.dtype), layout.block_tables,
+                                layout.context_lens, w.k, cfg)
+    xo, r = omodel.moe_block(xo, lh, cfg)
+    same = _route_sets_agree(routes.cpu().numpy()[0], r["ids"], r["margin"])
+    err = max_abs(xg.cpu().numpy()[same], xo[same])
+    print(f"max |x - oracle| = {err:.3e} ({(~same).sum()} near-tie tokens excluded)", flush=True)
+    assert err <= 2e-2
+
+
+def test_bf16_full_step_small_vocab(molt_lib):
+    """Whole bf16 verify step (2 layers of the 35B-A3B-like shape, vocab 4096): logits
+    within 2e-2 of the oracle in replay-free mode for sequences whose routes are clear."""
+    w = workloads.LAYER_BF16.scaled(n_layers=2, vocab=4096, batch=3, k=4, ctx_lo=30, ctx_hi=90,
+                                    full_model=True)
+    cfg = oracle_cfg(w)
+    seed = 13
+    layout = workloads.make_kv_layout(w, seed)
+    layers = [workloads.make_layer_weights(w, seed, l) for l in range(w.n_layers)]
+    head = workloads.make_head_weights(w, seed)
+    caches = [workloads.make_kv_cache(w, layout, seed, l) for l in range(w.n_layers)]
+    toks = workloads.make_step_tokens(w, 14)
+    u = workloads.make_uniforms(w.batch, w.k, 15)
+    q = workloads.make_softmax_q(w.batch, w.k, w.vocab, 16)
+    model = model_from(w, layers, head, molt_lib)
+    kv = molt_lib.KVCache([dev(c[0]) for c in caches], [dev(c[1]) for c in caches],
+                          dev(torch.from_numpy(layout.block_tables)),
+                          dev(torch.from_numpy(layout.context_lens)))
+    out = molt_lib.verify_step(model, kv, dev(torch.from_numpy(toks)), dev(u), dev(q), want_routes=True)
+    torch.cuda.synchronize()
+    lh = [layer_host(lw) for lw in layers]
+    oc = [tuple(omodel.widen_cache(host(t), w.dtype) for t in c) for c in caches]
+    o = omodel.verify_step(toks, lambda l: lh[l], layer_host(head), oc, layout.block_tables,
+                           layout.context_lens, cfg, host(q), host(u))
+    # a sequence is comparable if every token of it took the oracle's expert set in every
+    # layer (a flipped set changes the token's residual and, through attention, its sequence)
+    gr = out["routes"].cpu().numpy()
+    same = np.stack([_route_sets_agree(gr[l], o["routes"][l], o["route_margin"][l], 0.2)
+                     for l in range(w.n_layers)]).all(axis=0)
+    ok = same.reshape(w.batch, w.k + 1).all(axis=1)
+    assert ok.any()
+    err = max_abs(out["logits"].cpu().numpy()[ok], o["logits"][ok])
+    print(f"max |logits - oracle| = {err:.3e} over {ok.sum()} of {w.batch} sequences", flush=True)
+    assert err <= 2e-2
