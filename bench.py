@@ -62,12 +62,28 @@ def attention_bytes(w, ctx):
     return kv + qo
 
 
-def build(w, seed, molt):
+CPU_SAMPLE_SEQS, CPU_SAMPLE_LAYERS = 8, 12
+
+
+def host(t):
+    t = t.detach().cpu()
+    return t.view(torch.int16).numpy().view(np.uint16) if t.dtype == torch.bfloat16 else t.numpy()
+
+
+def build(w, seed, molt, keep_host=0):
+    """Generates the model on the GPU; expert weights are packed into the library's tiled
+    layout in place of the row-major ones. Row-major host copies of the first `keep_host`
+    layers are kept for the CPU baseline."""
     dev = "cuda"
     layout = workloads.make_kv_layout(w, seed)
-    layers, kcs, vcs = [], [], []
+    layers, kcs, vcs, host_layers = [], [], [], []
     for l in range(w.n_layers):
-        layers.append(workloads.make_layer_weights(w, seed, l, device=dev))
+        lw = workloads.make_layer_weights(w, seed, l, device=dev)
+        if l < keep_host:
+            host_layers.append({k_: (None if v is None else host(v)) for k_, v in lw.items()})
+        lw["w_gate_up"] = molt.pack_weights(lw["w_gate_up"])
+        lw["w_down"] = molt.pack_weights(lw["w_down"])
+        layers.append(lw)
         kc, vc = workloads.make_kv_cache(w, layout, seed, l, device=dev)
         kcs.append(kc)
         vcs.append(vc)
@@ -76,10 +92,11 @@ def build(w, seed, molt):
                 f"{torch.cuda.memory_allocated() / 2**30:.1f} GiB resident")
     head = workloads.make_head_weights(w, seed, device=dev)
     model = molt.Model(layers, head, n_q_heads=w.n_q_heads, n_kv_heads=w.n_kv_heads,
-                       head_dim=w.head_dim, top_k=w.top_k, rms_eps=w.rms_eps, rope_theta=w.rope_theta)
+                       head_dim=w.head_dim, top_k=w.top_k, rms_eps=w.rms_eps, rope_theta=w.rope_theta,
+                       packed=True)
     kv = molt.KVCache(kcs, vcs, torch.from_numpy(layout.block_tables).to(dev),
                       torch.from_numpy(layout.context_lens).to(dev))
-    return layout, layers, head, model, kv
+    return layout, host_layers, head, model, kv
 
 
 def make_drafts(w, seed, molt, model, kv, ws):
@@ -103,10 +120,12 @@ def make_drafts(w, seed, molt, model, kv, ws):
     return tokens, q, u
 
 
-def cpu_baseline(w, layout, layers, head, kv, tokens, q, u, n_seq=4, sample_layers=6):
+def cpu_baseline(w, layout, host_layers, head, kv, tokens, q, u, n_seq=CPU_SAMPLE_SEQS,
+                 sample_layers=CPU_SAMPLE_LAYERS):
     """Oracle on a bounded sample: `n_seq` sequences ((1+k) positions each) through
-    `sample_layers` of the layers, then the LM head and the sampler; the per-layer time is
-    scaled to all layers. Returns (positions/s, seconds measured, threads, description)."""
+    `sample_layers` of the layers (row-major host copies), then the LM head and the
+    sampler; the per-layer time is scaled to all layers. Returns (positions/s, seconds
+    measured, threads, description)."""
     import oracle.model as omodel
     from oracle import sampler as osamp
     try:
@@ -115,10 +134,7 @@ def cpu_baseline(w, layout, layers, head, kv, tokens, q, u, n_seq=4, sample_laye
     except Exception:
         threads = os.cpu_count() or 1
 
-    def host(t):
-        t = t.detach().cpu()
-        return t.view(torch.int16).numpy().view(np.uint16) if t.dtype == torch.bfloat16 else t.numpy()
-
+    sample_layers = min(sample_layers, len(host_layers))
     cfg = dict(dtype=w.dtype, expert_dtype=w.expert_dtype, n_layers=sample_layers,
                n_q_heads=w.n_q_heads, n_kv_heads=w.n_kv_heads, head_dim=w.head_dim, top_k=w.top_k,
                rms_eps=w.rms_eps, rope_theta=w.rope_theta, block_size=16)
@@ -130,7 +146,7 @@ def cpu_baseline(w, layout, layers, head, kv, tokens, q, u, n_seq=4, sample_laye
     for b, r in enumerate(blk_rows):
         bt[b, :len(r)] = np.arange(pos, pos + len(r))
         pos += len(r)
-    lw = [{k_: (None if v is None else host(v)) for k_, v in layers[l].items()} for l in range(sample_layers)]
+    lw = host_layers
     caches = []
     idx = torch.from_numpy(blocks).long().cuda()
     for l in range(sample_layers):
@@ -186,7 +202,8 @@ def main():
     if not w.full_model:
         sys.exit(f"{a.workload} is a single-layer workload; the bench step is the full verify step")
     t_setup = time.time()
-    layout, layers, head, model, kv = build(w, a.seed, molt)
+    layout, host_layers, head, model, kv = build(
+        w, a.seed, molt, keep_host=0 if a.no_cpu_baseline else CPU_SAMPLE_LAYERS)
     B, k, V = w.batch, w.k, w.vocab
     ws = torch.empty(molt.verify_step_workspace_size(model, B, k, layout.block_tables.shape[1]),
                      dtype=torch.uint8, device="cuda")
@@ -257,7 +274,7 @@ def main():
     }
     if not a.no_cpu_baseline:
         log("[bench] timing the CPU oracle on a bounded sample")
-        v, secs, threads, desc = cpu_baseline(w, layout, layers, head, kv, tokens, q, u)
+        v, secs, threads, desc = cpu_baseline(w, layout, host_layers, head, kv, tokens, q, u)
         res["cpu_baseline"] = {"value": round(v, 3), "unit": "verified tokens/s", "cores": threads,
                                "kind": "oracle", "sample": desc, "seconds": round(secs, 2)}
     print(json.dumps(res))

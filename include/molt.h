@@ -124,8 +124,9 @@ int molt_spec_accept(const float* logits, const float* draft_probs, const int32_
  *   x            [T, d]        act_dtype (F32 or BF16)
  *   w_router     [E, d]        act_dtype
  *   router_bias  [E]           f32, or NULL (added to the logits before top-K)
- *   w_gate_up    [E, 2F, d]    w_dtype: rows 0..F-1 gate, F..2F-1 up
- *   w_down       [E, d, F]     w_dtype
+ *   w_gate_up    [E, 2F, d]    w_dtype: rows 0..F-1 gate, F..2F-1 up; TILED layout
+ *                              (molt_pack_weights with rows = E*2F, row_bytes = d*size)
+ *   w_down       [E, d, F]     w_dtype, TILED layout (rows = E*d, row_bytes = F*size)
  *   s_gate_up    [E, 2F] f32, s_down [E, d] f32: per-output-channel scales, required
  *                iff w_dtype == FP8_E4M3, else ignored
  *   replay_ids   [T, K] i32 or NULL: use these experts (distinct, in [0, E)) and take
@@ -135,7 +136,7 @@ int molt_spec_accept(const float* logits, const float* draft_probs, const int32_
  *   out_counts [E], out_offsets [E+1], out_perm [T*K] i32: the stable (expert,
  *                token, slot) grouping, may be NULL
  * Supported: (act, w) in {(F32, F32), (BF16, BF16), (BF16, FP8_E4M3)}; d % 64 == 0,
- * F % 64 == 0, 1 <= K <= E <= 256, K <= 16. T >= 1.
+ * F % 64 == 0 (fp8: % 128), 1 <= K <= E <= 256, K <= 64. T >= 1.
  * ---------------------------------------------------------------------------- */
 size_t molt_moe_layer_workspace_size(int T, int d, int E, int K, int F, molt_dtype act_dtype,
                                      molt_dtype w_dtype);
@@ -146,6 +147,22 @@ int molt_moe_layer(const void* x, const void* w_router, const float* router_bias
                    float* out_weights, int32_t* out_counts, int32_t* out_offsets,
                    int32_t* out_perm, void* workspace, size_t workspace_bytes,
                    molt_stream_t stream);
+
+/* ------------------------------------------------------------------------------
+ * molt_pack_weights -- the expert-weight storage layout of this library (a layout
+ * choice of the implementation; the paper fixes none). A row-major byte matrix of
+ * `rows` rows and `row_bytes` bytes per row is cut into 32-row x 128-byte tiles; tile
+ * (rb, kb) takes the 4096 bytes at ((rb * row_bytes / 128) + kb) * 4096, and byte j of
+ * row r of the matrix (rb = r / 32, kb = j / 128) sits inside it at
+ *     ((j % 64) / 16) * 1024 + (((j % 128) / 64) * 32 + r % 32) * 16 + j % 16.
+ * Expert weights are packed once at load: w_gate_up as rows = E*2F, row_bytes =
+ * d * sizeof(w_dtype); w_down as rows = E*d, row_bytes = F * sizeof(w_dtype). fp8 scales
+ * stay row-major. dst receives rows*row_bytes bytes and must not overlap src.
+ * Errors: INVALID_ARG for NULL or equal pointers, rows < 1 or rows % 32 != 0,
+ * row_bytes < 128 or row_bytes % 128 != 0.
+ * ---------------------------------------------------------------------------- */
+int molt_pack_weights(const void* src, void* dst, long long rows, long long row_bytes,
+                      molt_stream_t stream);
 
 /* ------------------------------------------------------------------------------
  * molt_paged_attention -- multi-query paged decode attention of the verify step
@@ -203,8 +220,8 @@ typedef struct molt_model {
   const float* const* moe_norm;    /* [L] -> [d]                                          */
   const void* const* w_router;     /* [L] -> [E, d]                                       */
   const float* const* router_bias; /* NULL, or [L] -> [E] f32 (entries may be NULL)       */
-  const void* const* w_gate_up;    /* [L] -> [E, 2F, d]                                   */
-  const void* const* w_down;       /* [L] -> [E, d, F]                                    */
+  const void* const* w_gate_up;    /* [L] -> [E, 2F, d], tiled (molt_pack_weights)        */
+  const void* const* w_down;       /* [L] -> [E, d, F], tiled (molt_pack_weights)         */
   const float* const* s_gate_up;   /* [L] -> [E, 2F] f32, fp8 experts only, else NULL     */
   const float* const* s_down;      /* [L] -> [E, d] f32                                   */
 } molt_model;

@@ -48,6 +48,7 @@ _SIGS = {
     "molt_moe_layer": (c_int, [c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_int, c_int, c_int,
                                c_int, c_int, c_int, c_int, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp,
                                c_vp, c_vp, c_size, c_vp]),
+    "molt_pack_weights": (c_int, [c_vp, c_vp, ctypes.c_longlong, ctypes.c_longlong, c_vp]),
     "molt_dense_gemm": (c_int, [c_vp, c_vp, c_vp, c_int, c_int, c_int, c_int, c_int, c_vp]),
     "molt_paged_attention_workspace_size": (c_size, [c_int] * 6),
     "molt_paged_attention": (c_int, [c_vp, c_vp, c_vp, c_vp, c_vp, c_int, c_int, c_int, c_int,
@@ -152,13 +153,30 @@ def spec_accept(logits, draft_tokens, uniforms, draft_probs=None, out=None, work
     return toks, n, lp
 
 
+# ------------------------------------------------------------------ weight layout
+
+def pack_weights(w):
+    """Returns a tensor of w's shape and dtype holding w (row-major, last dim contiguous) in
+    the library's tiled expert-weight layout (molt_pack_weights)."""
+    lib = load()
+    _dev(w, None, name="w")
+    rows = w.numel() // w.shape[-1]
+    out = torch.empty_like(w)
+    _check(lib.molt_pack_weights(_ptr(w), _ptr(out), rows, w.shape[-1] * w.element_size(), _stream()),
+           "molt_pack_weights")
+    return out
+
+
 # ------------------------------------------------------------------ MoE layer
 
 def moe_layer(x, w_router, w_gate_up, w_down, top_k, router_bias=None, s_gate_up=None,
-              s_down=None, replay_ids=None, want_routing=False, workspace=None):
-    """x [T, d] (f32|bf16); weights as in molt.h (fp8 experts as uint8 codes).
+              s_down=None, replay_ids=None, want_routing=False, workspace=None, packed=False):
+    """x [T, d] (f32|bf16); weights as in molt.h (fp8 experts as uint8 codes), expert weights
+    row-major (packed here, per call) or already tiled with packed=True.
     Returns out [T, d] f32, or (out, ids, weights, counts, offsets, perm) with want_routing."""
     lib = load()
+    if not packed:
+        w_gate_up, w_down = pack_weights(w_gate_up), pack_weights(w_down)
     T, d = x.shape
     E = w_router.shape[0]
     F = w_gate_up.shape[1] // 2
@@ -239,11 +257,15 @@ def paged_attention(q, k_cache, v_cache, block_tables, context_lens, k, workspac
 class Model:
     """Holds the device weights of a decoder and the molt_model struct that points at them.
     layers: list of dicts with attn_norm, w_qkv, w_o, moe_norm, w_router, w_gate_up, w_down,
-    optional router_bias, s_gate_up, s_down. head: dict with embed, final_norm, lm_head
+    optional router_bias, s_gate_up, s_down (expert weights row-major, packed here; or tiled
+    already with packed=True). head: dict with embed, final_norm, lm_head
     (optional for the decoder-only entry point)."""
 
     def __init__(self, layers, head=None, n_q_heads=None, n_kv_heads=None, head_dim=None,
-                 top_k=None, rms_eps=1e-6, rope_theta=1e6):
+                 top_k=None, rms_eps=1e-6, rope_theta=1e6, packed=False):
+        if not packed:   # keep tiled copies of the expert weights (the caller keeps its own)
+            layers = [dict(lw, w_gate_up=pack_weights(lw["w_gate_up"]), w_down=pack_weights(lw["w_down"]))
+                      for lw in layers]
         self.layers, self.head = layers, head or {}
         l0 = layers[0]
         E, twoF, d = l0["w_gate_up"].shape

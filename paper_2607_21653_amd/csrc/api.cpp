@@ -77,7 +77,7 @@ extern "C" {
 
 const char* molt_last_error(void) { return g_err.c_str(); }
 
-int molt_version(void) { return 100; }
+int molt_version(void) { return 101; }
 
 // ------------------------------------------------------------------ profiling
 
@@ -168,16 +168,23 @@ namespace {
 
 struct MoeWs {
   float* g; int32_t* ids; float* w; int32_t* counts; int32_t* offsets; int32_t* perm;
-  int32_t* inv; int32_t* tiles; int32_t* n_tiles; uint8_t* xq; float* xs; void* h; uint8_t* hq;
-  float* hs; float* o; int max_tiles; int tile_m;
+  int32_t* inv; int32_t* pperm; int32_t* n_padded; int32_t* tiles; int32_t* n_tiles;
+  uint8_t* xq; float* xs; void* xt; void* h; uint8_t* hq; float* hs; float* o;
+  long max_rows; int max_tiles; int tile_m;
 };
 
+// Intermediates of the grouped GEMMs live in padded expert order (each expert's rows start
+// at a multiple of 32): the gathered activations xt and the SwiGLU product h (tiled layout
+// for bf16/fp8 experts, row-major for f32), and its fp8 codes hq/hs. The per-pair expert
+// outputs o are in pair order (token * K + slot).
 MoeWs carve_moe(molt::Carver& c, int T, int d, int E, int K, int F, molt_dtype act, molt_dtype w) {
   MoeWs m{};
   const long P = long(T) * K;
   const int tm = molt::moe_tile_m(w, T, K, E);
   m.tile_m = tm;
   m.max_tiles = molt::max_expert_tiles(T, E, K, tm);
+  m.max_rows = molt::max_padded_rows(T, E, K);
+  const long R = m.max_rows;
   m.g = c.take<float>(long(T) * E);
   m.ids = c.take<int32_t>(P);
   m.w = c.take<float>(P);
@@ -185,15 +192,18 @@ MoeWs carve_moe(molt::Carver& c, int T, int d, int E, int K, int F, molt_dtype a
   m.offsets = c.take<int32_t>(E + 1);
   m.perm = c.take<int32_t>(P);
   m.inv = c.take<int32_t>(P);
+  m.pperm = c.take<int32_t>(R);
+  m.n_padded = c.take<int32_t>(1);
   m.tiles = c.take<int32_t>(long(m.max_tiles) * 4);
   m.n_tiles = c.take<int32_t>(1);
   if (w == MOLT_FP8_E4M3) {
     m.xq = c.take<uint8_t>(long(T) * d);
     m.xs = c.take<float>(T);
-    m.hq = c.take<uint8_t>(P * F);
-    m.hs = c.take<float>(P);
+    m.hq = c.take<uint8_t>(R * F);
+    m.hs = c.take<float>(R);
   }
-  m.h = c.take<uint8_t>(P * F * dt_size(act));
+  if (w != MOLT_F32) m.xt = c.take<uint8_t>(R * d * dt_size(w));
+  m.h = c.take<uint8_t>(R * F * dt_size(act));
   m.o = c.take<float>(P * d);
   return m;
 }
@@ -211,7 +221,8 @@ int moe_shape_ok(int T, int d, int E, int K, int F, molt_dtype act, molt_dtype w
 }
 
 // Enqueues the MoE layer on normalised input x (act dtype; xq/xs = its fp8 codes when the
-// caller already quantised them). out = sum (accumulate: out += sum).
+// caller already quantised them). Expert weights are in the tiled layout. out = sum
+// (accumulate: out += sum).
 hipError_t run_moe(const MoeWs& m, const void* x, const uint8_t* xq, const float* xs,
                    const void* w_router, const float* bias, const void* w_gu, const void* w_d,
                    const float* s_gu, const float* s_d, int T, int d, int E, int K, int F,
@@ -223,34 +234,45 @@ hipError_t run_moe(const MoeWs& m, const void* x, const uint8_t* xq, const float
     if ((e = molt::launch_gemm(x, w_router, m.g, T, E, d, act, false, s)) != hipSuccess) return e;
   }
   if ((e = molt::launch_route(m.g, bias, replay, T, E, K, m.ids, m.w, m.counts, m.offsets, m.perm,
-                              m.inv, m.tile_m, m.tiles, m.max_tiles, m.n_tiles, s)) !=
-      hipSuccess)
+                              m.inv, m.pperm, m.n_padded, m.tile_m, m.tiles, m.max_tiles,
+                              m.n_tiles, s)) != hipSuccess)
     return e;
-  if (wdt == MOLT_FP8_E4M3 && xq == nullptr) {
+  const bool fp8 = wdt == MOLT_FP8_E4M3;
+  if (fp8 && xq == nullptr) {
     if ((e = molt::launch_quant_rows_bf16(static_cast<const uint16_t*>(x), T, d, m.xq, m.xs, s)) !=
         hipSuccess)
       return e;
     xq = m.xq;
     xs = m.xs;
   }
-  {
-    ProfScope ps(MOLT_PROF_EXPERT_GEMM, s);
-    if ((e = molt::launch_moe_gate_up(x, xq, xs, m.perm, K, w_gu, s_gu, d, F, act, wdt, m.tiles,
-                                      m.max_tiles, m.tile_m, m.h, s)) != hipSuccess)
+  const void* a = x;
+  if (wdt != MOLT_F32) {
+    const void* src = fp8 ? static_cast<const void*>(xq) : x;
+    if ((e = molt::launch_gather_tiled(src, m.pperm, K, m.n_padded, m.max_rows,
+                                       long(d) * dt_size(wdt), m.xt, s)) != hipSuccess)
       return e;
-  }
-  if (wdt == MOLT_FP8_E4M3) {
-    if ((e = molt::launch_quant_rows_bf16(static_cast<const uint16_t*>(m.h), T * K, F, m.hq, m.hs,
-                                          s)) != hipSuccess)
-      return e;
+    a = m.xt;
   }
   {
     ProfScope ps(MOLT_PROF_EXPERT_GEMM, s);
-    if ((e = molt::launch_moe_down(m.h, m.hq, m.hs, w_d, s_d, d, F, act, wdt, m.tiles, m.max_tiles,
-                                   m.tile_m, m.o, s)) != hipSuccess)
+    if ((e = molt::launch_moe_gate_up(a, xs, m.pperm, K, w_gu, s_gu, d, F, wdt, m.tiles,
+                                      m.n_tiles, m.max_tiles, m.tile_m, m.h, s)) != hipSuccess)
       return e;
   }
-  return molt::launch_combine(m.o, m.inv, m.w, T, K, d, out, accumulate, s);
+  if (fp8) {
+    if ((e = molt::launch_quant_rows_tiled(static_cast<const uint16_t*>(m.h), m.pperm, m.n_padded,
+                                           m.max_rows, F, m.hq, m.hs, s)) != hipSuccess)
+      return e;
+  }
+  {
+    ProfScope ps(MOLT_PROF_EXPERT_GEMM, s);
+    if ((e = molt::launch_moe_down(fp8 ? static_cast<const void*>(m.hq) : m.h, m.hs, m.pperm, w_d,
+                                   s_d, d, F, wdt, m.tiles, m.n_tiles, m.max_tiles, m.tile_m, m.o,
+                                   s)) !=
+        hipSuccess)
+      return e;
+  }
+  return molt::launch_combine(m.o, m.w, T, K, d, out, accumulate, s);
 }
 
 hipError_t copy_out(void* dst, const void* src, size_t bytes, hipStream_t s) {
@@ -296,6 +318,20 @@ int molt_moe_layer(const void* x, const void* w_router, const float* router_bias
   if (e == hipSuccess) e = copy_out(out_offsets, m.offsets, size_t(E + 1) * 4, s);
   if (e == hipSuccess) e = copy_out(out_perm, m.perm, P * 4, s);
   return hip_status(e, "molt_moe_layer");
+}
+
+// ------------------------------------------------------------------ weight layout
+
+int molt_pack_weights(const void* src, void* dst, long long rows, long long row_bytes,
+                      molt_stream_t stream) {
+  REQUIRE(src && dst, "a required pointer is NULL");
+  REQUIRE(src != dst, "packing in place is not supported");
+  REQUIRE(rows >= 1 && rows % 32 == 0, "rows = %lld must be a positive multiple of 32", rows);
+  REQUIRE(row_bytes >= 128 && row_bytes % 128 == 0,
+          "row_bytes = %lld must be a positive multiple of 128", row_bytes);
+  return hip_status(molt::launch_pack_tiled(src, dst, rows, row_bytes,
+                                            reinterpret_cast<hipStream_t>(stream)),
+                    "molt_pack_weights");
 }
 
 // ------------------------------------------------------------------ dense GEMM

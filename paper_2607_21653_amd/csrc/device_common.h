@@ -122,3 +122,17 @@ MOLT_DEV T block_sum(T v, T* red) {
 }
 
 MOLT_DEV float silu(float x) { return x / (1.0f + expf(-x)); }
+
+// ---------------------------------------------------------------- tiled operand layout
+// The grouped expert GEMMs keep their operands (expert weights, gathered activations, the
+// SwiGLU product) in a tiled byte layout. A row-major matrix of R rows (R % 32 == 0) and
+// RB bytes per row (RB % 128 == 0) is cut into 32-row x 128-byte tiles; tile (rb, kb) is
+// the 4 KB at ((rb * RB / 128) + kb) * 4096, and byte j of row r inside it sits at
+// ((j % 64) / 16) * 1024 + ((j / 64) * 32 + r) * 16 + j % 16. Lane l of a wavefront that
+// loads 16 bytes at l * 16 of each 1 KB quarter c gets row l % 32, bytes 64 (l / 32) + 16 c
+// of the slice: the MFMA operand layout, with each load instruction reading 1 KB of one
+// page instead of touching 32 rows.
+MOLT_DEV long tiled_offset(long row, long j, long row_bytes) {
+  return ((row >> 5) * (row_bytes >> 7) + (j >> 7)) * 4096 + ((j & 63) >> 4) * 1024 +
+         ((((j & 127) >> 6) << 5) + (row & 31)) * 16 + (j & 15);
+}

@@ -78,6 +78,47 @@ __global__ __launch_bounds__(kThreads) void quant_rows_kernel(const uint16_t* __
   if (threadIdx.x == 0) scale[r] = s;
 }
 
+// The same quantisation for the SwiGLU product of the grouped GEMMs: rows in padded
+// expert order, bf16 in and e4m3 codes out in the tiled layout; one wavefront per row,
+// 8 values per lane step. Padding rows (pair -1) get zero codes and scale 0.
+__global__ __launch_bounds__(kThreads) void quant_rows_tiled_kernel(
+    const uint16_t* __restrict__ h, const int32_t* __restrict__ pperm,
+    const int32_t* __restrict__ n_rows, int cols, uint8_t* __restrict__ q,
+    float* __restrict__ scale) {
+  const long r = long(blockIdx.x) * (kThreads / kWave) + threadIdx.x / kWave;
+  const int lane = threadIdx.x % kWave;
+  if (r >= *n_rows) return;
+  const bool pad = pperm[r] < 0;
+  const long rb_in = 2L * cols, rb_out = cols;
+  float amax = 0.f;
+  for (int c = lane * 8; c < cols; c += kWave * 8) {
+    const int4 v = *reinterpret_cast<const int4*>(
+        reinterpret_cast<const uint8_t*>(h) + tiled_offset(r, 2L * c, rb_in));
+    const uint32_t w[4] = {uint32_t(v.x), uint32_t(v.y), uint32_t(v.z), uint32_t(v.w)};
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      amax = fmaxf(amax, fmaxf(fabsf(bf16_to_f32(uint16_t(w[i]))), fabsf(bf16_to_f32(uint16_t(w[i] >> 16)))));
+  }
+  amax = pad ? 0.f : wave_max(amax);
+  const float s = amax / 448.0f;
+  for (int c = lane * 8; c < cols; c += kWave * 8) {
+    const int4 v = *reinterpret_cast<const int4*>(
+        reinterpret_cast<const uint8_t*>(h) + tiled_offset(r, 2L * c, rb_in));
+    const uint32_t w[4] = {uint32_t(v.x), uint32_t(v.y), uint32_t(v.z), uint32_t(v.w)};
+    uint32_t code[2] = {0u, 0u};
+    if (s > 0.f) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const uint32_t lo = f32_to_fp8e4m3(bf16_to_f32(uint16_t(w[i])) / s);
+        const uint32_t hi = f32_to_fp8e4m3(bf16_to_f32(uint16_t(w[i] >> 16)) / s);
+        code[i / 2] |= (lo | (hi << 8)) << (16 * (i % 2));
+      }
+    }
+    *reinterpret_cast<uint2*>(q + tiled_offset(r, c, rb_out)) = make_uint2(code[0], code[1]);
+  }
+  if (lane == 0) scale[r] = s;
+}
+
 // RoPE on q and k of token t = b*(1+k)+j at position ctx[b]+j (rotate-half pairs
 // (i, i+D/2), inverse frequency theta^(-2i/D), angle and rotation in f64), then
 // q -> q_out[t, Hq, D]; k -> K cache slot; v -> V cache slot (transposed layout).
@@ -126,9 +167,8 @@ __global__ __launch_bounds__(kThreads) void rope_kv_kernel(
   }
 }
 
-// out[t] (+)= sum_{j<K} w[t,j] * o[inv[t*K+j]], slot order, f32
+// out[t] (+)= sum_{j<K} w[t,j] * o[t*K+j], slot order, f32
 __global__ __launch_bounds__(kThreads) void combine_kernel(const float* __restrict__ o,
-                                                           const int32_t* __restrict__ inv,
                                                            const float* __restrict__ w, int K,
                                                            int d, float* __restrict__ out,
                                                            bool accumulate) {
@@ -137,7 +177,7 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(const float* __restri
     float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
     for (int j = 0; j < K; ++j) {
       const float wj = w[long(t) * K + j];
-      const float4 v = *reinterpret_cast<const float4*>(o + long(inv[long(t) * K + j]) * d + i);
+      const float4 v = *reinterpret_cast<const float4*>(o + (long(t) * K + j) * d + i);
       acc.x += wj * v.x; acc.y += wj * v.y; acc.z += wj * v.z; acc.w += wj * v.w;
     }
     float4* dst = reinterpret_cast<float4*>(out + long(t) * d + i);
@@ -179,9 +219,19 @@ hipError_t launch_rope_kv_write(const float* qkv, int B, int k, int Hq, int Hkv,
   return hipGetLastError();
 }
 
-hipError_t launch_combine(const float* o, const int32_t* inv, const float* w, int T, int K, int d,
-                          float* out, bool accumulate, hipStream_t s) {
-  combine_kernel<<<T, kThreads, 0, s>>>(o, inv, w, K, d, out, accumulate);
+hipError_t launch_quant_rows_tiled(const uint16_t* h, const int32_t* pperm, const int32_t* n_rows,
+                                   long max_rows, int cols, uint8_t* q, float* scale,
+                                   hipStream_t s) {
+  constexpr int rows_per_block = kThreads / kWave;
+  const long grid = (max_rows + rows_per_block - 1) / rows_per_block;
+  if (grid == 0) return hipSuccess;
+  quant_rows_tiled_kernel<<<grid, kThreads, 0, s>>>(h, pperm, n_rows, cols, q, scale);
+  return hipGetLastError();
+}
+
+hipError_t launch_combine(const float* o, const float* w, int T, int K, int d, float* out,
+                          bool accumulate, hipStream_t s) {
+  combine_kernel<<<T, kThreads, 0, s>>>(o, w, K, d, out, accumulate);
   return hipGetLastError();
 }
 

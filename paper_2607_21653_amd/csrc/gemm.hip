@@ -33,6 +33,7 @@ struct GemmParams {
   int M, N, K;             // N: output columns (gate_up: F)
   int ldc;
   const int4* tiles;       // grouped: {expert, row0, row1, -}
+  const int32_t* n_tiles_live;   // grouped (device): entries of `tiles` in use
   int n_mtiles, n_ntiles;
   const int32_t* perm;     // gate_up: permuted pair -> token * ktop + slot
   int ktop;
@@ -271,166 +272,113 @@ __global__ __launch_bounds__(kThreads) void mfma_gemm_kernel(GemmParams p) {
 // ---------------------------------------------------------------- weight-streaming grouped GEMM
 // Expert GEMMs are HBM-bound at the verify step's row counts (tens of rows per expert),
 // so the weights must stream at full bandwidth and be read once. Workgroup = BM rows of
-// one expert x 128 output columns; each of the 4 wavefronts owns 32 columns and loads its
-// weight fragments straight from global memory into registers, kPD 128-byte K slices
-// ahead (a weight element is used by exactly one wavefront: no LDS needed). The
-// activation rows (shared by the 4 wavefronts) are prefetched kPD slices ahead into
-// registers too and staged through a double-buffered LDS tile, one barrier per slice. A
-// lane's MFMA operand chunk for k-step s of a slice is bytes [64 g + 16 s, +16) (bf16,
-// g = lane / 32) or [64 g + 32 s, +32) (fp8) of its row, for both operands: each lane
-// streams 64 contiguous bytes of its weight row per slice.
-constexpr int kPD = 4;   // slices in flight per wavefront
-
-struct Slice16 { int4 c[4]; };   // 64 bytes of one row: 4 x 16 B
+// one expert x 128 output columns; each of the 4 wavefronts owns 32 output columns (32
+// weight rows) and loads its weight fragments straight from global memory into MFMA
+// operand registers, kPD 128-byte K slices ahead; a weight element is used by exactly one
+// wavefront, so no LDS and no barrier is needed in the main loop. The activation rows
+// (shared by the 4 wavefronts, served from L2) are loaded per wavefront kPA slices ahead.
+// Both operands are in the tiled layout, so every load instruction reads 1 KB of one page:
+// with row-major operands each instruction touched 32 rows, and the address translation
+// requests, not HBM, set the pace. Tiles start at multiples of 32 rows (padded expert
+// order), so each 32-row block of A is one tile column of the tiled activation buffer.
+struct Slice16 { int4 c[4]; };   // one lane's 64 bytes of a 32-row x 128-byte tile
 
 template <int BM, bool FP8, int MODE>
 __global__ __launch_bounds__(kThreads) void moe_stream_kernel(GemmParams p) {
+  static_assert(MODE == kGateUp || MODE == kDown, "grouped modes only");
   constexpr int MS = BM / 32;                        // 32-row MFMA tiles per wavefront
+  constexpr int kPD = 4;                             // weight slices in flight
+  constexpr int kPA = 2;                             // activation slices in flight
   constexpr int kElem = FP8 ? 1 : 2;
-  constexpr int kBK = kRowBytes / kElem;             // K elements per slice
-  constexpr int kALoads = BM * 8 / kThreads;         // 16-byte A chunks per thread per slice
-  static_assert(kALoads >= 1, "BM too small");
-  __shared__ __attribute__((aligned(16))) uint8_t lds[2 * BM * kLdsStride];
+  __shared__ __attribute__((aligned(16))) float upbuf[MODE == kGateUp ? BM * 64 : 1];
 
-  int id = blockIdx.x;
-  const int G = gridDim.x;
-  id = (id % 8) * (G / 8) + id / 8;                   // grid is a multiple of 8: XCD-local order
-  if (id >= p.n_mtiles * p.n_ntiles) return;
-  const int mt = id % p.n_mtiles;
-  const int nt = id / p.n_mtiles;
-  int expert = 0, row0, row1;
-  if (MODE == kDense) {
-    row0 = mt * BM;
-    row1 = min(row0 + BM, p.M);
-  } else {
-    const int4 tinfo = p.tiles[mt];
-    if (tinfo.x < 0) return;
-    expert = tinfo.x;
-    row0 = tinfo.y;
-    row1 = tinfo.z;
-  }
-  const long K = p.K;
-  const int nk = int(K / kBK);
+  // Workgroup b runs on XCD b % 8. Each XCD takes one contiguous eighth of the live
+  // (m-tile, n-tile) pairs, m-tile major: the n-tiles of one row tile run back to back on
+  // one XCD, so its activation tile is read from HBM once and then hits that XCD's L2.
+  const int total = *p.n_tiles_live * p.n_ntiles;
+  const int chunk = (total + 7) / 8;
+  const int k8 = blockIdx.x / 8;
+  const int id = (blockIdx.x % 8) * chunk + k8;
+  if (k8 >= chunk || id >= total) return;
+  const int mt = id / p.n_ntiles;
+  const int nt = id % p.n_ntiles;
+  const int4 t = p.tiles[mt];
+  const int expert = t.x, row0 = t.y, row1 = t.z;     // row0 % 32 == 0
+  const long RB = long(p.K) * kElem;                  // bytes per operand row
+  const int nk = int(RB / kRowBytes);                 // 128-byte K slices
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
   const int lane = threadIdx.x % kWave;
-  const int lrow = lane % 32, lg = lane / 32;
-
-  // weight row of this lane (column lrow of the wavefront's 32)
-  long brow;
+  // first of the wavefront's 32 weight rows (gate_up: waves 0-1 gate, 2-3 up)
+  long wrow;
   int n0;
   if (MODE == kGateUp) {
     n0 = nt * (kBN / 2);
-    brow = long(expert) * 2 * p.N + (wave < 2 ? n0 + 32 * wave + lrow : p.N + n0 + 32 * (wave - 2) + lrow);
+    wrow = long(expert) * 2 * p.N + (wave < 2 ? n0 + 32 * wave : p.N + n0 + 32 * (wave - 2));
   } else {
     n0 = nt * kBN;
-    brow = long(expert) * p.N + n0 + 32 * wave + lrow;   // dense: expert 0, N % 128 == 0
+    wrow = long(expert) * p.N + n0 + 32 * wave;
   }
-  const uint8_t* bsrc = static_cast<const uint8_t*>(p.B) + brow * K * kElem + lg * 64;
-
-  // activation rows staged by all threads: chunk c of row r = tid / 8 + 32 i. Rows past the
-  // tile read row row0 (always valid); MFMA rows are independent and those outputs are
-  // never stored, so the loads carry no branches and their count stays exact.
-  const int chunk = threadIdx.x % 8;
-  const uint8_t* a_src[kALoads];
+  const uint8_t* bsrc = static_cast<const uint8_t*>(p.B) + wrow * RB + lane * 16;
+  const uint8_t* asrc[MS];
+  const int last_block = (row1 - 1) & ~31;            // 32-row blocks past the tile end
+#pragma unroll                                        // re-read its last one
+  for (int i = 0; i < MS; ++i)
+    asrc[i] = static_cast<const uint8_t*>(p.A) + long(min(row0 + 32 * i, last_block)) * RB + lane * 16;
+  auto ld = [](Slice16& f, const uint8_t* src) {
 #pragma unroll
-  for (int i = 0; i < kALoads; ++i) {
-    const int grow = row0 + threadIdx.x / 8 + 32 * i;
-    long arow = grow < row1 ? grow : row0;
-    if (MODE == kGateUp) arow = p.perm[arow] / p.ktop;
-    a_src[i] = static_cast<const uint8_t*>(p.A) + arow * K * kElem + chunk * 16;
-  }
-
+    for (int c = 0; c < 4; ++c) f.c[c] = *reinterpret_cast<const int4*>(src + 1024 * c);
+  };
   Slice16 wb[kPD];
-  auto wload = [&](Slice16& f, int kb) {
-    const uint8_t* src = bsrc + long(kb) * kRowBytes;
+  Slice16 ab[kPA][MS];
 #pragma unroll
-    for (int c = 0; c < 4; ++c) f.c[c] = *reinterpret_cast<const int4*>(src + 16 * c);
-  };
-  int4 ra[kPD][kALoads];
-  auto aload = [&](int4 (&r)[kALoads], int kb) {
+  for (int s = 0; s < kPD; ++s) if (s < nk) ld(wb[s], bsrc + long(s) * 4096);
 #pragma unroll
-    for (int i = 0; i < kALoads; ++i)
-      r[i] = *reinterpret_cast<const int4*>(a_src[i] + long(kb) * kRowBytes);
-  };
-  auto astore = [&](const int4 (&r)[kALoads], int buf) {
+  for (int s = 0; s < kPA; ++s) if (s < nk)
 #pragma unroll
-    for (int i = 0; i < kALoads; ++i)
-      *reinterpret_cast<int4*>(lds + buf * BM * kLdsStride +
-                               (threadIdx.x / 8 + 32 * i) * kLdsStride + chunk * 16) = r[i];
-  };
-
+    for (int i = 0; i < MS; ++i) ld(ab[s][i], asrc[i] + long(s) * 4096);
   floatx16_t acc[MS];
 #pragma unroll
   for (int i = 0; i < MS; ++i)
 #pragma unroll
     for (int e = 0; e < 16; ++e) acc[i][e] = 0.f;
-
-#pragma unroll
-  for (int s = 0; s < kPD; ++s)
-    if (s < nk) {
-      wload(wb[s], s);
-      aload(ra[s], s);
-    }
-  astore(ra[0], 0);
-  __syncthreads();
-
-  auto slice = [&](const Slice16& f, int buf) {
-    const uint8_t* abase = lds + buf * BM * kLdsStride + lrow * kLdsStride + lg * 64;
+  auto slice = [&](const Slice16& w, const Slice16 (&a)[MS]) {
     if (!FP8) {
 #pragma unroll
       for (int s = 0; s < 4; ++s) {
-        const bf16x8_t bv = *reinterpret_cast<const bf16x8_t*>(&f.c[s]);
-        bf16x8_t av[MS];
+        const bf16x8_t bv = *reinterpret_cast<const bf16x8_t*>(&w.c[s]);
 #pragma unroll
-        for (int i = 0; i < MS; ++i)
-          av[i] = *reinterpret_cast<const bf16x8_t*>(abase + i * 32 * kLdsStride + 16 * s);
-#pragma unroll
-        for (int i = 0; i < MS; ++i) acc[i] = mfma(av[i], bv, acc[i]);
+        for (int i = 0; i < MS; ++i) acc[i] = mfma(*reinterpret_cast<const bf16x8_t*>(&a[i].c[s]), bv, acc[i]);
       }
     } else {
 #pragma unroll
       for (int s = 0; s < 2; ++s) {
-        const int32x8_t bv = int32x8_t{f.c[2 * s].x, f.c[2 * s].y, f.c[2 * s].z, f.c[2 * s].w,
-                                       f.c[2 * s + 1].x, f.c[2 * s + 1].y, f.c[2 * s + 1].z,
-                                       f.c[2 * s + 1].w};
-        int32x8_t av[MS];
+        const int4 w0 = w.c[2 * s], w1 = w.c[2 * s + 1];
+        const int32x8_t bv = int32x8_t{w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};
 #pragma unroll
         for (int i = 0; i < MS; ++i) {
-          const uint8_t* q = abase + i * 32 * kLdsStride + 32 * s;
-          const int32x4_t lo = *reinterpret_cast<const int32x4_t*>(q);
-          const int32x4_t hi = *reinterpret_cast<const int32x4_t*>(q + 16);
-          av[i] = int32x8_t{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+          const int4 lo = a[i].c[2 * s], hi = a[i].c[2 * s + 1];
+          acc[i] = mfma(int32x8_t{lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w}, bv, acc[i]);
         }
-#pragma unroll
-        for (int i = 0; i < MS; ++i) acc[i] = mfma(av[i], bv, acc[i]);
       }
     }
   };
-
-  // slice kb = kb0 + s: stage slice kb+1 (register set (s+1) % kPD) into LDS, compute slice
-  // kb from register set s, then refill set s with slice kb + kPD; one barrier per slice
   for (int kb0 = 0; kb0 < nk; kb0 += kPD) {
 #pragma unroll
     for (int s = 0; s < kPD; ++s) {
       const int kb = kb0 + s;
       if (kb < nk) {
-        if (kb + 1 < nk) astore(ra[(s + 1) % kPD], (kb + 1) & 1);
-        slice(wb[s], kb & 1);
-        if (kb + kPD < nk) {
-          wload(wb[s], kb + kPD);
-          aload(ra[s], kb + kPD);
-        }
-        __syncthreads();
+        slice(wb[s], ab[s % kPA]);
+        if (kb + kPD < nk) ld(wb[s], bsrc + long(kb + kPD) * 4096);
+        if (kb + kPA < nk)
+#pragma unroll
+          for (int i = 0; i < MS; ++i) ld(ab[s % kPA][i], asrc[i] + long(kb + kPA) * 4096);
       }
     }
   }
-
-  // ---- epilogue: acc[i][e] is row 32 i + 8 (e/4) + 4 (lane/32) + e%4, column lane%32
+  // accumulator element e of lane (lcol, lgrp) in tile i: row 32 i + 8 (e / 4) + 4 lgrp + e % 4
   const int lcol = lane % 32, lgrp = lane / 32;
   if (MODE == kGateUp) {
-    // the "up" wavefronts (tile columns 64..127) park their values in LDS; the "gate"
-    // wavefronts finish h = silu(gate) * up for their columns
-    float* upbuf = reinterpret_cast<float*>(lds);   // [BM][64] fits in 2 * BM * 144 bytes
+    // h = silu(gate) * up, bf16, tiled layout over padded rows; up columns go through LDS
     if (wave >= 2) {
 #pragma unroll
       for (int i = 0; i < MS; ++i)
@@ -443,6 +391,7 @@ __global__ __launch_bounds__(kThreads) void moe_stream_kernel(GemmParams p) {
     __syncthreads();
     if (wave < 2) {
       const int c = 32 * wave + lcol;
+      const long hrb = 2L * p.N;
 #pragma unroll
       for (int i = 0; i < MS; ++i)
 #pragma unroll
@@ -457,10 +406,12 @@ __global__ __launch_bounds__(kThreads) void moe_stream_kernel(GemmParams p) {
             g = g * sx * sw[n0 + c];
             u = u * sx * sw[p.N + n0 + c];
           }
-          static_cast<uint16_t*>(p.C)[long(grow) * p.ldc + n0 + c] = f32_to_bf16(silu(g) * u);
+          *reinterpret_cast<uint16_t*>(static_cast<uint8_t*>(p.C) +
+                                       tiled_offset(grow, 2L * (n0 + c), hrb)) = f32_to_bf16(silu(g) * u);
         }
     }
   } else {
+    // per-pair expert output, f32, row = pair index (token * K + slot)
     const int c = n0 + 32 * wave + lcol;
 #pragma unroll
     for (int i = 0; i < MS; ++i)
@@ -471,9 +422,7 @@ __global__ __launch_bounds__(kThreads) void moe_stream_kernel(GemmParams p) {
         if (grow >= row1) continue;
         float v = acc[i][e];
         if (FP8) v = v * p.a_scale[grow] * p.b_scale[long(expert) * p.b_scale_ld + c];
-        float* dst = static_cast<float*>(p.C) + long(grow) * p.ldc + c;
-        if (MODE == kDense && p.accumulate) v += *dst;
-        *dst = v;
+        static_cast<float*>(p.C)[long(p.perm[grow]) * p.ldc + c] = v;
       }
   }
 }
@@ -488,8 +437,42 @@ hipError_t run_stream(GemmParams p, int tile_m, hipStream_t s) {
   return hipGetLastError();
 }
 
+// ---------------------------------------------------------------- tiled-layout kernels
+// pack: row-major [rows, RB bytes] -> tiled; one thread per 16-byte chunk (reads coalesced)
+__global__ __launch_bounds__(kThreads) void pack_tiled_kernel(const uint8_t* __restrict__ src,
+                                                              uint8_t* __restrict__ dst, long rows,
+                                                              long RB) {
+  const long q = long(blockIdx.x) * kThreads + threadIdx.x;
+  const long per_row = RB / 16;
+  if (q >= rows * per_row) return;
+  const long r = q / per_row, j = (q % per_row) * 16;
+  *reinterpret_cast<int4*>(dst + tiled_offset(r, j, RB)) =
+      *reinterpret_cast<const int4*>(src + r * RB + j);
+}
+
+// gather: tiled activation rows in padded expert order, row = src[pperm[row] / ktop]
+// (zeros for padding rows); one workgroup per 4 KB tile, thread = 16-byte chunk of it
+__global__ __launch_bounds__(kThreads) void gather_tiled_kernel(
+    const uint8_t* __restrict__ src, const int32_t* __restrict__ pperm, int ktop,
+    const int32_t* __restrict__ n_rows, long RB, uint8_t* __restrict__ dst) {
+  const long tile = blockIdx.x;
+  const long nk = RB / 128;
+  const long rb = tile / nk, kb = tile % nk;
+  if (rb * 32 >= *n_rows) return;
+  const int quarter = threadIdx.x / 64, l = threadIdx.x % 64;
+  const long row = rb * 32 + (l % 32);
+  const long j = kb * 128 + (l / 32) * 64 + quarter * 16;
+  const int pair = pperm[row];
+  int4 v = make_int4(0, 0, 0, 0);
+  if (pair >= 0) v = *reinterpret_cast<const int4*>(src + long(pair / ktop) * RB + j);
+  *reinterpret_cast<int4*>(dst + tile * 4096 + threadIdx.x * 16) = v;
+}
+
 // ---------------------------------------------------------------- f32 VALU path
 // One workgroup per (row tile of 16, column tile of 64); each thread owns 4 outputs.
+// Dense: row-major operands. Grouped: weights tiled (f32 element k of row n at byte 4k),
+// activations row-major, rows in padded expert order (gate_up reads token rows through
+// the padded permutation; down writes pair rows).
 template <int MODE>
 __global__ __launch_bounds__(kThreads) void f32_gemm_kernel(GemmParams p) {
   const int id = blockIdx.x;
@@ -506,32 +489,38 @@ __global__ __launch_bounds__(kThreads) void f32_gemm_kernel(GemmParams p) {
     row1 = t.z;
   }
   const int K = p.K;
+  const long RB = 4L * K;
   const float* A = static_cast<const float*>(p.A);
-  const float* B = static_cast<const float*>(p.B);
+  const uint8_t* B = static_cast<const uint8_t*>(p.B);
+  auto w = [&](long n, int kk) { return *reinterpret_cast<const float*>(B + tiled_offset(n, 4L * kk, RB)); };
   for (int o = threadIdx.x; o < 16 * 64; o += kThreads) {
     const int r = o / 64, c = o % 64;
     const int grow = row0 + r;
     const int col = nt * 64 + c;
     if (grow >= row1 || col >= p.N) continue;
-    long arow = grow;
-    if (MODE == kGateUp) arow = p.perm[grow] / p.ktop;
-    const float* a = A + arow * K;
-    if (MODE == kGateUp) {
-      const float* bg = B + (long(expert) * 2 * p.N + col) * K;
-      const float* bu = B + (long(expert) * 2 * p.N + p.N + col) * K;
-      float g = 0.f, u = 0.f;
-      for (int kk = 0; kk < K; ++kk) {
-        g += a[kk] * bg[kk];
-        u += a[kk] * bu[kk];
-      }
-      static_cast<float*>(p.C)[long(grow) * p.ldc + col] = silu(g) * u;
-    } else {
-      const float* b = B + ((MODE == kDown ? long(expert) * p.N : 0) + col) * K;
+    if (MODE == kDense) {
+      const float* a = A + long(grow) * K;
+      const float* b = static_cast<const float*>(p.B) + long(col) * K;
       float s = 0.f;
       for (int kk = 0; kk < K; ++kk) s += a[kk] * b[kk];
       float* dst = static_cast<float*>(p.C) + long(grow) * p.ldc + col;
-      if (MODE == kDense && p.accumulate) s += *dst;
+      if (p.accumulate) s += *dst;
       *dst = s;
+    } else if (MODE == kGateUp) {
+      const float* a = A + long(p.perm[grow] / p.ktop) * K;
+      const long ng = long(expert) * 2 * p.N + col, nu = ng + p.N;
+      float g = 0.f, u = 0.f;
+      for (int kk = 0; kk < K; ++kk) {
+        g += a[kk] * w(ng, kk);
+        u += a[kk] * w(nu, kk);
+      }
+      static_cast<float*>(p.C)[long(grow) * p.ldc + col] = silu(g) * u;
+    } else {
+      const float* a = A + long(grow) * K;
+      const long n = long(expert) * p.N + col;
+      float s = 0.f;
+      for (int kk = 0; kk < K; ++kk) s += a[kk] * w(n, kk);
+      static_cast<float*>(p.C)[long(p.perm[grow]) * p.ldc + col] = s;
     }
   }
 }
@@ -573,17 +562,17 @@ hipError_t launch_gemm(const void* A, const void* Bw, float* C, int M, int N, in
   return run_mfma<32, false, kDense>(p, p.n_mtiles * p.n_ntiles, s);
 }
 
-hipError_t launch_moe_gate_up(const void* x, const uint8_t* xq, const float* xs, const int32_t* perm,
-                              int K_top, const void* w_gu, const float* s_gu, int d, int F,
-                              molt_dtype act, molt_dtype wdt, const int32_t* tiles, int max_tiles,
+hipError_t launch_moe_gate_up(const void* a, const float* a_scale, const int32_t* pperm, int K_top,
+                              const void* w_gu, const float* s_gu, int d, int F, molt_dtype wdt,
+                              const int32_t* tiles, const int32_t* n_tiles, int max_tiles,
                               int tile_m, void* h, hipStream_t s) {
   GemmParams p{};
-  p.A = wdt == MOLT_FP8_E4M3 ? static_cast<const void*>(xq) : x;
-  p.B = w_gu; p.C = h; p.N = F; p.K = d; p.ldc = F;
+  p.n_tiles_live = n_tiles;
+  p.A = a; p.B = w_gu; p.C = h; p.N = F; p.K = d; p.ldc = F;
   p.tiles = reinterpret_cast<const int4*>(tiles);
   p.n_mtiles = max_tiles;
-  p.perm = perm; p.ktop = K_top;
-  p.a_scale = xs; p.b_scale = s_gu; p.b_scale_ld = 2 * F;
+  p.perm = pperm; p.ktop = K_top;
+  p.a_scale = a_scale; p.b_scale = s_gu; p.b_scale_ld = 2 * F;
   if (wdt == MOLT_F32) {
     p.n_ntiles = (F + 63) / 64;
     f32_gemm_kernel<kGateUp><<<max_tiles * p.n_ntiles, kThreads, 0, s>>>(p);
@@ -594,16 +583,17 @@ hipError_t launch_moe_gate_up(const void* x, const uint8_t* xq, const float* xs,
   return run_stream<false, kGateUp>(p, tile_m, s);
 }
 
-hipError_t launch_moe_down(const void* h, const uint8_t* hq, const float* hs, const void* w_d,
-                           const float* s_d, int d, int F, molt_dtype act, molt_dtype wdt,
-                           const int32_t* tiles, int max_tiles, int tile_m, float* o,
-                           hipStream_t s) {
+hipError_t launch_moe_down(const void* a, const float* a_scale, const int32_t* pperm,
+                           const void* w_d, const float* s_d, int d, int F, molt_dtype wdt,
+                           const int32_t* tiles, const int32_t* n_tiles, int max_tiles,
+                           int tile_m, float* o, hipStream_t s) {
   GemmParams p{};
-  p.A = wdt == MOLT_FP8_E4M3 ? static_cast<const void*>(hq) : h;
-  p.B = w_d; p.C = o; p.N = d; p.K = F; p.ldc = d;
+  p.n_tiles_live = n_tiles;
+  p.A = a; p.B = w_d; p.C = o; p.N = d; p.K = F; p.ldc = d;
   p.tiles = reinterpret_cast<const int4*>(tiles);
   p.n_mtiles = max_tiles;
-  p.a_scale = hs; p.b_scale = s_d; p.b_scale_ld = d;
+  p.perm = pperm;
+  p.a_scale = a_scale; p.b_scale = s_d; p.b_scale_ld = d;
   if (wdt == MOLT_F32) {
     p.n_ntiles = (d + 63) / 64;
     f32_gemm_kernel<kDown><<<max_tiles * p.n_ntiles, kThreads, 0, s>>>(p);
@@ -612,6 +602,24 @@ hipError_t launch_moe_down(const void* h, const uint8_t* hq, const float* hs, co
   p.n_ntiles = d / kBN;
   if (wdt == MOLT_FP8_E4M3) return run_stream<true, kDown>(p, tile_m, s);
   return run_stream<false, kDown>(p, tile_m, s);
+}
+
+hipError_t launch_pack_tiled(const void* src, void* dst, long rows, long row_bytes, hipStream_t s) {
+  const long chunks = rows * (row_bytes / 16);
+  if (chunks == 0) return hipSuccess;
+  pack_tiled_kernel<<<(chunks + kThreads - 1) / kThreads, kThreads, 0, s>>>(
+      static_cast<const uint8_t*>(src), static_cast<uint8_t*>(dst), rows, row_bytes);
+  return hipGetLastError();
+}
+
+hipError_t launch_gather_tiled(const void* src, const int32_t* pperm, int K_top,
+                               const int32_t* n_rows, long max_rows, long row_bytes, void* dst,
+                               hipStream_t s) {
+  const long tiles = max_rows / 32 * (row_bytes / 128);
+  if (tiles == 0) return hipSuccess;
+  gather_tiled_kernel<<<tiles, kThreads, 0, s>>>(static_cast<const uint8_t*>(src), pperm, K_top,
+                                                 n_rows, row_bytes, static_cast<uint8_t*>(dst));
+  return hipGetLastError();
 }
 
 }  // namespace molt

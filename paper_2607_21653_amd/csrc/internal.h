@@ -43,32 +43,47 @@ hipError_t launch_rope_kv_write(const float* qkv, int B, int k, int Hq, int Hkv,
                                 float theta, const int32_t* ctx, const int32_t* bt, int max_blocks,
                                 int num_blocks, molt_dtype dt, void* q_out, void* k_cache,
                                 void* v_cache, hipStream_t s);
-hipError_t launch_combine(const float* o, const int32_t* inv, const float* w, int T, int K, int d,
-                          float* out, bool accumulate, hipStream_t s);
+// fp8 rows of the tiled SwiGLU product (padded expert order; n_rows on the device)
+hipError_t launch_quant_rows_tiled(const uint16_t* h, const int32_t* pperm, const int32_t* n_rows,
+                                   long max_rows, int cols, uint8_t* q, float* scale,
+                                   hipStream_t s);
+// out[t] (+)= sum_j w[t, j] o[t * K + j]
+hipError_t launch_combine(const float* o, const float* w, int T, int K, int d, float* out,
+                          bool accumulate, hipStream_t s);
 
 // ------------------------------------------------------------- routing
-size_t routing_ws_bytes(int T, int E, int K, int tile_m);
-// top-K + softmax of router logits (or replay ids); stable permutation; tile table
+// top-K + softmax of router logits (or replay ids); stable permutation (perm/inv) and its
+// padded copy (pperm: padded row -> pair or -1, n_padded rows); tile table in padded rows
 hipError_t launch_route(const float* logits, const float* bias, const int32_t* replay, int T,
                         int E, int K, int32_t* ids, float* w, int32_t* counts, int32_t* offsets,
-                        int32_t* perm, int32_t* inv, int tile_m, int32_t* tiles, int max_tiles,
-                        int32_t* n_tiles, hipStream_t s);
+                        int32_t* perm, int32_t* inv, int32_t* pperm, int32_t* n_padded,
+                        int tile_m, int32_t* tiles, int max_tiles, int32_t* n_tiles,
+                        hipStream_t s);
 int max_expert_tiles(int T, int E, int K, int tile_m);
+long max_padded_rows(int T, int E, int K);
 
 // ------------------------------------------------------------- GEMMs
 // C[M, N] (f32) = A[M, K] * B[N, K]^T, A/B in dt (F32 or BF16); epilogue adds into C when
 // accumulate. Row-major, K contiguous.
 hipError_t launch_gemm(const void* A, const void* Bw, float* C, int M, int N, int K, molt_dtype dt,
                        bool accumulate, hipStream_t s);
-// Grouped expert GEMMs over the tile table built by launch_route.
-hipError_t launch_moe_gate_up(const void* x, const uint8_t* xq, const float* xs, const int32_t* perm,
-                              int K_top, const void* w_gu, const float* s_gu, int d, int F,
-                              molt_dtype act, molt_dtype wdt, const int32_t* tiles, int max_tiles,
+// Grouped expert GEMMs over the tile table built by launch_route. bf16/fp8: A and the
+// weights in the tiled layout, gate_up writes h tiled; f32: row-major A and h, tiled
+// weights. Rows are padded-order; down writes o[pair].
+hipError_t launch_moe_gate_up(const void* a, const float* a_scale, const int32_t* pperm, int K_top,
+                              const void* w_gu, const float* s_gu, int d, int F, molt_dtype wdt,
+                              const int32_t* tiles, const int32_t* n_tiles, int max_tiles,
                               int tile_m, void* h, hipStream_t s);
-hipError_t launch_moe_down(const void* h, const uint8_t* hq, const float* hs, const void* w_d,
-                           const float* s_d, int d, int F, molt_dtype act, molt_dtype wdt,
-                           const int32_t* tiles, int max_tiles, int tile_m, float* o,
-                           hipStream_t s);
+hipError_t launch_moe_down(const void* a, const float* a_scale, const int32_t* pperm,
+                           const void* w_d, const float* s_d, int d, int F, molt_dtype wdt,
+                           const int32_t* tiles, const int32_t* n_tiles, int max_tiles,
+                           int tile_m, float* o, hipStream_t s);
+// row-major [rows, row_bytes] -> tiled layout (rows % 32 == 0, row_bytes % 128 == 0)
+hipError_t launch_pack_tiled(const void* src, void* dst, long rows, long row_bytes, hipStream_t s);
+// tiled rows in padded expert order: row = src[pperm[row] / K_top], zeros for padding
+hipError_t launch_gather_tiled(const void* src, const int32_t* pperm, int K_top,
+                               const int32_t* n_rows, long max_rows, long row_bytes, void* dst,
+                               hipStream_t s);
 int moe_tile_m(molt_dtype wdt, int T, int K, int E);
 
 // ------------------------------------------------------------- attention

@@ -16,6 +16,10 @@
 // lower lanes; across the 16 wavefronts an exclusive LDS prefix per expert adds the
 // earlier wavefronts' counts. Position = offset[e] + earlier chunks + earlier
 // wavefronts + rank: the stable (expert, token, slot) order, bit-exact.
+// The grouped GEMMs work on a padded copy of that order: every expert's rows start at a
+// multiple of 32 (padded offset poff[e] = sum of the earlier counts rounded up to 32), so
+// each 32-row block of a GEMM tile belongs to one expert; padded slots hold pair -1. The
+// tile table lists (expert, first row, end row) in padded rows.
 #include "device_common.h"
 #include "internal.h"
 
@@ -95,9 +99,11 @@ __global__ __launch_bounds__(256) void topk_kernel(const float* __restrict__ log
 __global__ __launch_bounds__(kPermThreads) void permute_kernel(
     const int32_t* __restrict__ ids, int P, int E, int tile_m, int32_t* __restrict__ counts_out,
     int32_t* __restrict__ offsets_out, int32_t* __restrict__ perm, int32_t* __restrict__ inv,
-    int4* __restrict__ tiles, int max_tiles, int32_t* __restrict__ n_tiles) {
+    int32_t* __restrict__ pperm, int32_t* __restrict__ n_padded, int4* __restrict__ tiles,
+    int max_tiles, int32_t* __restrict__ n_tiles) {
   __shared__ int cnt[kMaxE];
   __shared__ int off[kMaxE + 1];
+  __shared__ int poff[kMaxE + 1];
   __shared__ int run[kMaxE];
   __shared__ int wc[kPermWaves][kMaxE];
   __shared__ int s_nt;
@@ -109,16 +115,23 @@ __global__ __launch_bounds__(kPermThreads) void permute_kernel(
   __syncthreads();
   if (tid == 0) {
     off[0] = 0;
+    poff[0] = 0;
     int nt = 0;
     for (int e = 0; e < E; ++e) {
       off[e + 1] = off[e] + cnt[e];
-      for (int m0 = off[e]; m0 < off[e + 1] && nt < max_tiles; m0 += tile_m)
-        tiles[nt++] = make_int4(e, m0, min(m0 + tile_m, off[e + 1]), 0);
+      poff[e + 1] = poff[e] + (cnt[e] + 31) / 32 * 32;
+      for (int m0 = 0; m0 < cnt[e] && nt < max_tiles; m0 += tile_m)
+        tiles[nt++] = make_int4(e, poff[e] + m0, poff[e] + min(m0 + tile_m, cnt[e]), 0);
     }
     s_nt = nt;
     *n_tiles = nt;
+    *n_padded = poff[E];
   }
   __syncthreads();
+  for (int i = tid; i < E * 32; i += kPermThreads) {   // padding slots of each expert
+    const int e = i / 32, r = cnt[e] + i % 32;
+    if (r < poff[e + 1] - poff[e]) pperm[poff[e] + r] = -1;
+  }
   for (int i = s_nt + tid; i < max_tiles; i += kPermThreads) tiles[i] = make_int4(-1, 0, 0, 0);
   for (int e = tid; e < E; e += kPermThreads) {
     counts_out[e] = cnt[e];
@@ -156,6 +169,7 @@ __global__ __launch_bounds__(kPermThreads) void permute_kernel(
       const int pos = off[e] + wc[wave][e] + rank;
       perm[pos] = p;
       inv[p] = pos;
+      pperm[pos - off[e] + poff[e]] = p;
     }
     __syncthreads();
   }
@@ -167,13 +181,21 @@ int max_expert_tiles(int T, int E, int K, int tile_m) {
   return (T * K + tile_m - 1) / tile_m + E;
 }
 
+long max_padded_rows(int T, int E, int K) {
+  const long P = long(T) * K;
+  const long worst = P + 31L * (E < P ? E : P);   // every non-empty expert pads < 32 rows
+  return (worst + 31) / 32 * 32;
+}
+
 hipError_t launch_route(const float* logits, const float* bias, const int32_t* replay, int T,
                         int E, int K, int32_t* ids, float* w, int32_t* counts, int32_t* offsets,
-                        int32_t* perm, int32_t* inv, int tile_m, int32_t* tiles, int max_tiles,
-                        int32_t* n_tiles, hipStream_t s) {
+                        int32_t* perm, int32_t* inv, int32_t* pperm, int32_t* n_padded,
+                        int tile_m, int32_t* tiles, int max_tiles, int32_t* n_tiles,
+                        hipStream_t s) {
   topk_kernel<<<(T + 3) / 4, 256, 0, s>>>(logits, bias, replay, T, E, K, ids, w);
   permute_kernel<<<1, kPermThreads, 0, s>>>(ids, T * K, E, tile_m, counts, offsets, perm, inv,
-                                            reinterpret_cast<int4*>(tiles), max_tiles, n_tiles);
+                                            pperm, n_padded, reinterpret_cast<int4*>(tiles),
+                                            max_tiles, n_tiles);
   return hipGetLastError();
 }
 

@@ -37,3 +37,17 @@ def model_from(w, layers, head, molt):
 
 def max_abs(a, b):
     return float(np.max(np.abs(np.asarray(a, np.float64) - np.asarray(b, np.float64)))) if np.size(a) else 0.0
+
+
+def tiled_layout(mat_bytes):
+    """The library's tiled expert-weight layout, from its definition in include/molt.h
+    (molt_pack_weights), written with numpy index arithmetic: mat_bytes [rows, row_bytes]
+    uint8 -> flat uint8 of the same size."""
+    rows, rb = mat_bytes.shape
+    r = np.arange(rows)[:, None]
+    j = np.arange(rb)[None, :]
+    off = ((r // 32) * (rb // 128) + j // 128) * 4096 + ((j % 64) // 16) * 1024 \
+        + (((j % 128) // 64) * 32 + r % 32) * 16 + j % 16
+    out = np.empty(rows * rb, np.uint8)
+    out[off.ravel()] = mat_bytes.ravel()
+    return out

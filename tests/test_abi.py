@@ -35,7 +35,7 @@ def test_exports_every_declared_symbol(L):
 
 
 def test_version_and_error_string(L):
-    assert L.molt_version() == 100
+    assert L.molt_version() == 101
     assert isinstance(L.molt_last_error(), bytes)
 
 
@@ -97,6 +97,15 @@ def test_attention_validation(L):
     assert call(Hq=64, Hkv=2, k=4) == INVALID     # 160 query rows per kv head
     assert call(dt=2) == INVALID
     assert call(B=2, mb=2000, ws=None, wsb=0) == WORKSPACE
+
+
+def test_pack_validation(L):
+    p, q = ctypes.c_void_p(0x1000), ctypes.c_void_p(0x2000)
+    assert L.molt_pack_weights(None, q, 32, 128, None) == INVALID
+    assert L.molt_pack_weights(p, p, 32, 128, None) == INVALID      # in place
+    assert L.molt_pack_weights(p, q, 48, 128, None) == INVALID      # rows % 32
+    assert L.molt_pack_weights(p, q, 32, 192, None) == INVALID      # row_bytes % 128
+    assert L.molt_pack_weights(p, q, 0, 128, None) == INVALID
 
 
 def test_model_validation(L):
