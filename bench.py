@@ -71,9 +71,9 @@ def host(t):
 
 
 def build(w, seed, molt, keep_host=0):
-    """Generates the model on the GPU; expert weights are packed into the library's tiled
-    layout in place of the row-major ones. Row-major host copies of the first `keep_host`
-    layers are kept for the CPU baseline."""
+    """Generates the model on the GPU; GEMM weights are packed into the library's tiled
+    layout in place of the row-major ones. Row-major host copies of the head and of the
+    first `keep_host` layers are kept for the CPU baseline."""
     dev = "cuda"
     layout = workloads.make_kv_layout(w, seed)
     layers, kcs, vcs, host_layers = [], [], [], []
@@ -81,8 +81,8 @@ def build(w, seed, molt, keep_host=0):
         lw = workloads.make_layer_weights(w, seed, l, device=dev)
         if l < keep_host:
             host_layers.append({k_: (None if v is None else host(v)) for k_, v in lw.items()})
-        lw["w_gate_up"] = molt.pack_weights(lw["w_gate_up"])
-        lw["w_down"] = molt.pack_weights(lw["w_down"])
+        for key in molt.Model.PACKED:
+            lw[key] = molt.pack_weights(lw[key])
         layers.append(lw)
         kc, vc = workloads.make_kv_cache(w, layout, seed, l, device=dev)
         kcs.append(kc)
@@ -91,12 +91,14 @@ def build(w, seed, molt, keep_host=0):
             log(f"[bench] layer {l + 1}/{w.n_layers} generated, "
                 f"{torch.cuda.memory_allocated() / 2**30:.1f} GiB resident")
     head = workloads.make_head_weights(w, seed, device=dev)
+    host_head = {k_: host(v) for k_, v in head.items()}
+    head["lm_head"] = molt.pack_weights(head["lm_head"])
     model = molt.Model(layers, head, n_q_heads=w.n_q_heads, n_kv_heads=w.n_kv_heads,
                        head_dim=w.head_dim, top_k=w.top_k, rms_eps=w.rms_eps, rope_theta=w.rope_theta,
                        packed=True)
     kv = molt.KVCache(kcs, vcs, torch.from_numpy(layout.block_tables).to(dev),
                       torch.from_numpy(layout.context_lens).to(dev))
-    return layout, host_layers, head, model, kv
+    return layout, host_layers, host_head, model, kv
 
 
 def make_drafts(w, seed, molt, model, kv, ws):
@@ -154,7 +156,7 @@ def cpu_baseline(w, layout, host_layers, head, kv, tokens, q, u, n_seq=CPU_SAMPL
         vc = omodel.widen_cache(host(kv.v_caches[l][idx]), w.dtype)
         caches.append((kc, vc))
     ctx = layout.context_lens[:n_seq]
-    hh = {k_: host(v) for k_, v in head.items()}
+    hh = head
     toks = host(tokens)[:n_seq]
     t0 = time.perf_counter()
     x = omodel.embed(toks, hh, cfg)

@@ -122,7 +122,7 @@ int molt_spec_accept(const float* logits, const float* draft_probs, const int32_
  * by s_row * s_channel.
  *
  *   x            [T, d]        act_dtype (F32 or BF16)
- *   w_router     [E, d]        act_dtype
+ *   w_router     [E, d]        act_dtype, tiled (molt_pack_weights)
  *   router_bias  [E]           f32, or NULL (added to the logits before top-K)
  *   w_gate_up    [E, 2F, d]    w_dtype: rows 0..F-1 gate, F..2F-1 up; TILED layout
  *                              (molt_pack_weights with rows = E*2F, row_bytes = d*size)
@@ -149,17 +149,21 @@ int molt_moe_layer(const void* x, const void* w_router, const float* router_bias
                    molt_stream_t stream);
 
 /* ------------------------------------------------------------------------------
- * molt_pack_weights -- the expert-weight storage layout of this library (a layout
- * choice of the implementation; the paper fixes none). A row-major byte matrix of
- * `rows` rows and `row_bytes` bytes per row is cut into 32-row x 128-byte tiles; tile
- * (rb, kb) takes the 4096 bytes at ((rb * row_bytes / 128) + kb) * 4096, and byte j of
- * row r of the matrix (rb = r / 32, kb = j / 128) sits inside it at
+ * molt_pack_weights -- the GEMM operand layout of this library (a layout choice of the
+ * implementation; the paper fixes none). A row-major byte matrix of `rows` rows and
+ * `row_bytes` bytes per row, rows padded with zero rows to R = 32 * ceil(rows / 32), is
+ * cut into 32-row x 128-byte tiles; tile (rb, kb) takes the 4096 bytes at
+ * ((rb * row_bytes / 128) + kb) * 4096, and byte j of row r of the matrix (rb = r / 32,
+ * kb = j / 128) sits inside it at
  *     ((j % 64) / 16) * 1024 + (((j % 128) / 64) * 32 + r % 32) * 16 + j % 16.
- * Expert weights are packed once at load: w_gate_up as rows = E*2F, row_bytes =
- * d * sizeof(w_dtype); w_down as rows = E*d, row_bytes = F * sizeof(w_dtype). fp8 scales
- * stay row-major. dst receives rows*row_bytes bytes and must not overlap src.
- * Errors: INVALID_ARG for NULL or equal pointers, rows < 1 or rows % 32 != 0,
- * row_bytes < 128 or row_bytes % 128 != 0.
+ * Every weight matrix a GEMM of this library reads ([out, in], K = in contiguous) is in
+ * this layout, packed once at load: w_qkv, w_o, w_router, lm_head with rows = out
+ * features, row_bytes = in * sizeof(dtype); w_gate_up as rows = E*2F, row_bytes =
+ * d * sizeof(w_dtype); w_down as rows = E*d, row_bytes = F * sizeof(w_dtype). Embeddings,
+ * norms and fp8 scales stay row-major. dst receives R * row_bytes bytes and must not
+ * overlap src.
+ * Errors: INVALID_ARG for NULL or equal pointers, rows < 1, row_bytes < 128 or
+ * row_bytes % 128 != 0.
  * ---------------------------------------------------------------------------- */
 int molt_pack_weights(const void* src, void* dst, long long rows, long long row_bytes,
                       molt_stream_t stream);
@@ -188,13 +192,17 @@ int molt_paged_attention(const void* q, const void* k_cache, const void* v_cache
 
 /* ------------------------------------------------------------------------------
  * molt_dense_gemm -- the dense projection of the verify step's decoder (QKV, O, router,
- * LM head): C[M, N] (f32) = A[M, K] * B[N, K]^T, or C += A * B^T with accumulate != 0
- * (the O projection adds into the residual stream). A and B row-major in `dtype` (F32 or
- * BF16), K contiguous, f32 accumulation. Supported: M, N, K >= 1; BF16 needs K % 64 == 0.
- * No workspace.
+ * LM head): C[M, N] (f32, row-major) = A[M, K] * B[N, K]^T, or C += A * B^T with
+ * accumulate != 0 (the O projection adds into the residual stream). A and B in `dtype`
+ * (F32 or BF16) and in the tiled layout of molt_pack_weights (rows = M resp. N, row_bytes =
+ * K * sizeof(dtype); padding rows are read, their products dropped); f32 accumulation.
+ * Supported: M, N, K >= 1, K * sizeof(dtype) % 128 == 0. The workspace holds split-K
+ * partial sums for small grids (size from molt_dense_gemm_workspace_size, may be 0);
+ * splits are added in a fixed order, so results are deterministic.
  * ---------------------------------------------------------------------------- */
+size_t molt_dense_gemm_workspace_size(int M, int N, int K, molt_dtype dtype);
 int molt_dense_gemm(const void* A, const void* B, float* C, int M, int N, int K, molt_dtype dtype,
-                    int accumulate, molt_stream_t stream);
+                    int accumulate, void* workspace, size_t workspace_bytes, molt_stream_t stream);
 
 /* ------------------------------------------------------------------------------
  * Model description: a HOST struct holding device pointers; read only during a
@@ -213,12 +221,12 @@ typedef struct molt_model {
   molt_dtype expert_dtype; /* expert weights                                              */
   const void* embed;       /* [V, d] dtype (needed by molt_verify_step)                   */
   const float* final_norm; /* [d]                                                         */
-  const void* lm_head;     /* [V, d] dtype                                                */
+  const void* lm_head;     /* [V, d] dtype, tiled (molt_pack_weights)                     */
   const float* const* attn_norm;   /* [L] -> [d]                                          */
-  const void* const* w_qkv;        /* [L] -> [(Hq + 2 Hkv) D, d]: q heads, k heads, v heads */
-  const void* const* w_o;          /* [L] -> [d, Hq D]                                    */
+  const void* const* w_qkv;        /* [L] -> [(Hq + 2 Hkv) D, d]: q, k, v heads; tiled   */
+  const void* const* w_o;          /* [L] -> [d, Hq D], tiled                             */
   const float* const* moe_norm;    /* [L] -> [d]                                          */
-  const void* const* w_router;     /* [L] -> [E, d]                                       */
+  const void* const* w_router;     /* [L] -> [E, d], tiled                                */
   const float* const* router_bias; /* NULL, or [L] -> [E] f32 (entries may be NULL)       */
   const void* const* w_gate_up;    /* [L] -> [E, 2F, d], tiled (molt_pack_weights)        */
   const void* const* w_down;       /* [L] -> [E, d, F], tiled (molt_pack_weights)         */

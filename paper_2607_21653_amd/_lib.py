@@ -49,7 +49,8 @@ _SIGS = {
                                c_int, c_int, c_int, c_int, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp,
                                c_vp, c_vp, c_size, c_vp]),
     "molt_pack_weights": (c_int, [c_vp, c_vp, ctypes.c_longlong, ctypes.c_longlong, c_vp]),
-    "molt_dense_gemm": (c_int, [c_vp, c_vp, c_vp, c_int, c_int, c_int, c_int, c_int, c_vp]),
+    "molt_dense_gemm_workspace_size": (c_size, [c_int, c_int, c_int, c_int]),
+    "molt_dense_gemm": (c_int, [c_vp, c_vp, c_vp, c_int, c_int, c_int, c_int, c_int, c_vp, c_size, c_vp]),
     "molt_paged_attention_workspace_size": (c_size, [c_int] * 6),
     "molt_paged_attention": (c_int, [c_vp, c_vp, c_vp, c_vp, c_vp, c_int, c_int, c_int, c_int,
                                      c_int, c_int, c_int, c_vp, c_vp, c_size, c_vp]),
@@ -156,34 +157,45 @@ def spec_accept(logits, draft_tokens, uniforms, draft_probs=None, out=None, work
 # ------------------------------------------------------------------ weight layout
 
 def pack_weights(w):
-    """Returns a tensor of w's shape and dtype holding w (row-major, last dim contiguous) in
-    the library's tiled expert-weight layout (molt_pack_weights)."""
+    """w (row-major, last dim contiguous) in the library's tiled GEMM operand layout
+    (molt_pack_weights). Same dtype; shape [R, last] with the rows padded to a multiple
+    of 32, except that a matrix whose row count is already such a multiple keeps its shape."""
     lib = load()
     _dev(w, None, name="w")
     rows = w.numel() // w.shape[-1]
-    out = torch.empty_like(w)
+    padded = (rows + 31) // 32 * 32
+    shape = tuple(w.shape) if padded == rows else (padded, w.shape[-1])
+    out = torch.empty(shape, dtype=w.dtype, device=w.device)
     _check(lib.molt_pack_weights(_ptr(w), _ptr(out), rows, w.shape[-1] * w.element_size(), _stream()),
            "molt_pack_weights")
     return out
 
 
+def _rows(t):
+    return t.numel() // t.shape[-1]
+
+
 # ------------------------------------------------------------------ MoE layer
 
 def moe_layer(x, w_router, w_gate_up, w_down, top_k, router_bias=None, s_gate_up=None,
-              s_down=None, replay_ids=None, want_routing=False, workspace=None, packed=False):
-    """x [T, d] (f32|bf16); weights as in molt.h (fp8 experts as uint8 codes), expert weights
-    row-major (packed here, per call) or already tiled with packed=True.
+              s_down=None, replay_ids=None, want_routing=False, workspace=None, packed=False,
+              n_experts=None):
+    """x [T, d] (f32|bf16); weights as in molt.h (fp8 experts as uint8 codes): router and
+    expert weights row-major (packed here, per call), or already tiled with packed=True
+    (then give n_experts when the router's row count is not a multiple of 32).
     Returns out [T, d] f32, or (out, ids, weights, counts, offsets, perm) with want_routing."""
     lib = load()
-    if not packed:
-        w_gate_up, w_down = pack_weights(w_gate_up), pack_weights(w_down)
     T, d = x.shape
-    E = w_router.shape[0]
+    E = n_experts if n_experts is not None else w_router.shape[0]
+    if not packed:
+        _dev(w_router, x.dtype, (E, d), "w_router")
+        w_router = pack_weights(w_router)
+        w_gate_up, w_down = pack_weights(w_gate_up), pack_weights(w_down)
     F = w_gate_up.shape[1] // 2
     act = DTYPE_CODE[x.dtype]
     wdt = DTYPE_CODE[w_gate_up.dtype]
     _dev(x, None, name="x")
-    _dev(w_router, x.dtype, (E, d), "w_router")
+    _dev(w_router, x.dtype, ((E + 31) // 32 * 32 if E % 32 else E, d), "w_router")
     _dev(w_gate_up, None, (E, 2 * F, d), "w_gate_up")
     _dev(w_down, w_gate_up.dtype, (E, d, F), "w_down")
     _dev(router_bias, torch.float32, (E,), "router_bias")
@@ -212,8 +224,9 @@ def moe_layer(x, w_router, w_gate_up, w_down, top_k, router_bias=None, s_gate_up
 
 # ------------------------------------------------------------------ dense GEMM
 
-def dense_gemm(A, B, C=None, accumulate=False):
-    """C [M, N] f32 = A [M, K] @ B [N, K]^T (+ C when accumulate); A, B f32 or bf16."""
+def dense_gemm(A, B, C=None, accumulate=False, workspace=None):
+    """C [M, N] f32 = A [M, K] @ B [N, K]^T (+ C when accumulate); A, B f32 or bf16,
+    row-major (packed into the tiled operand layout here)."""
     lib = load()
     M, K = A.shape
     N = B.shape[0]
@@ -222,8 +235,11 @@ def dense_gemm(A, B, C=None, accumulate=False):
     if C is None:
         C = torch.zeros(M, N, dtype=torch.float32, device=A.device)
     _dev(C, torch.float32, (M, N), "C")
-    _check(lib.molt_dense_gemm(_ptr(A), _ptr(B), _ptr(C), M, N, K, DTYPE_CODE[A.dtype],
-                               1 if accumulate else 0, _stream()), "molt_dense_gemm")
+    At, Bt = pack_weights(A), pack_weights(B)
+    dt = DTYPE_CODE[A.dtype]
+    ws, nb = _workspace(lib.molt_dense_gemm_workspace_size(M, N, K, dt), A.device, workspace)
+    _check(lib.molt_dense_gemm(_ptr(At), _ptr(Bt), _ptr(C), M, N, K, dt, 1 if accumulate else 0,
+                               _ptr(ws), nb, _stream()), "molt_dense_gemm")
     return C
 
 
@@ -257,16 +273,21 @@ def paged_attention(q, k_cache, v_cache, block_tables, context_lens, k, workspac
 class Model:
     """Holds the device weights of a decoder and the molt_model struct that points at them.
     layers: list of dicts with attn_norm, w_qkv, w_o, moe_norm, w_router, w_gate_up, w_down,
-    optional router_bias, s_gate_up, s_down (expert weights row-major, packed here; or tiled
-    already with packed=True). head: dict with embed, final_norm, lm_head
-    (optional for the decoder-only entry point)."""
+    optional router_bias, s_gate_up, s_down. head: dict with embed, final_norm, lm_head
+    (optional for the decoder-only entry point). GEMM weights (w_qkv, w_o, w_router,
+    w_gate_up, w_down, lm_head) row-major, packed here into tiled copies; or already tiled
+    with packed=True (then pass vocab when the head has no embedding)."""
+
+    PACKED = ("w_qkv", "w_o", "w_router", "w_gate_up", "w_down")
 
     def __init__(self, layers, head=None, n_q_heads=None, n_kv_heads=None, head_dim=None,
-                 top_k=None, rms_eps=1e-6, rope_theta=1e6, packed=False):
-        if not packed:   # keep tiled copies of the expert weights (the caller keeps its own)
-            layers = [dict(lw, w_gate_up=pack_weights(lw["w_gate_up"]), w_down=pack_weights(lw["w_down"]))
-                      for lw in layers]
-        self.layers, self.head = layers, head or {}
+                 top_k=None, rms_eps=1e-6, rope_theta=1e6, packed=False, vocab=None):
+        head = dict(head or {})
+        if not packed:   # keep tiled copies of the GEMM weights (the caller keeps its own)
+            layers = [dict(lw, **{k_: pack_weights(lw[k_]) for k_ in self.PACKED}) for lw in layers]
+            if "lm_head" in head:
+                head["lm_head"] = pack_weights(head["lm_head"])
+        self.layers, self.head = layers, head
         l0 = layers[0]
         E, twoF, d = l0["w_gate_up"].shape
         self.dtype = l0["w_qkv"].dtype
@@ -274,7 +295,7 @@ class Model:
         m.n_layers = len(layers)
         m.d_model, m.n_q_heads, m.n_kv_heads, m.head_dim = d, n_q_heads, n_kv_heads, head_dim
         m.n_experts, m.top_k, m.d_ff = E, top_k, twoF // 2
-        m.vocab = self.head["lm_head"].shape[0] if "lm_head" in self.head else 0
+        m.vocab = vocab if vocab is not None else (self.head["embed"].shape[0] if "embed" in self.head else 0)
         m.rms_eps, m.rope_theta = rms_eps, rope_theta
         m.dtype = DTYPE_CODE[self.dtype]
         m.expert_dtype = DTYPE_CODE[l0["w_gate_up"].dtype]

@@ -166,17 +166,28 @@ static bool pair_ok(molt_dtype act, molt_dtype w) {
 
 namespace {
 
+long pad32(long n) { return (n + 31) / 32 * 32; }
+
+// floats of split-K partial sums a dense GEMM of this shape would use (0: no split)
+long gemm_part_elems(int M, int N, int K, molt_dtype dt) {
+  if (dt != MOLT_BF16) return 0;
+  const molt::GemmPlan g = molt::gemm_plan(M, N, K, 1L << 62);
+  return g.splits > 1 ? long(g.splits) * M * N : 0;
+}
+
 struct MoeWs {
   float* g; int32_t* ids; float* w; int32_t* counts; int32_t* offsets; int32_t* perm;
   int32_t* inv; int32_t* pperm; int32_t* n_padded; int32_t* tiles; int32_t* n_tiles;
   uint8_t* xq; float* xs; void* xt; void* h; uint8_t* hq; float* hs; float* o;
+  float* part; long part_elems;   // split-K partial sums of the router GEMM
   long max_rows; int max_tiles; int tile_m;
 };
 
 // Intermediates of the grouped GEMMs live in padded expert order (each expert's rows start
-// at a multiple of 32): the gathered activations xt and the SwiGLU product h (tiled layout
-// for bf16/fp8 experts, row-major for f32), and its fp8 codes hq/hs. The per-pair expert
-// outputs o are in pair order (token * K + slot).
+// at a multiple of 32), tiled: the gathered activations xt (expert dtype), the SwiGLU
+// product h (act dtype) and its fp8 codes hq/hs. xq/xs: fp8 codes of the input when the
+// caller has none. The per-pair expert outputs o are row-major in pair order (token * K +
+// slot).
 MoeWs carve_moe(molt::Carver& c, int T, int d, int E, int K, int F, molt_dtype act, molt_dtype w) {
   MoeWs m{};
   const long P = long(T) * K;
@@ -197,14 +208,16 @@ MoeWs carve_moe(molt::Carver& c, int T, int d, int E, int K, int F, molt_dtype a
   m.tiles = c.take<int32_t>(long(m.max_tiles) * 4);
   m.n_tiles = c.take<int32_t>(1);
   if (w == MOLT_FP8_E4M3) {
-    m.xq = c.take<uint8_t>(long(T) * d);
-    m.xs = c.take<float>(T);
+    m.xq = c.take<uint8_t>(pad32(T) * d);
+    m.xs = c.take<float>(pad32(T));
     m.hq = c.take<uint8_t>(R * F);
     m.hs = c.take<float>(R);
   }
-  if (w != MOLT_F32) m.xt = c.take<uint8_t>(R * d * dt_size(w));
+  m.xt = c.take<uint8_t>(R * d * dt_size(w));
   m.h = c.take<uint8_t>(R * F * dt_size(act));
   m.o = c.take<float>(P * d);
+  m.part_elems = gemm_part_elems(T, E, d, act);
+  m.part = c.take<float>(m.part_elems);
   return m;
 }
 
@@ -220,9 +233,9 @@ int moe_shape_ok(int T, int d, int E, int K, int F, molt_dtype act, molt_dtype w
   return MOLT_OK;
 }
 
-// Enqueues the MoE layer on normalised input x (act dtype; xq/xs = its fp8 codes when the
-// caller already quantised them). Expert weights are in the tiled layout. out = sum
-// (accumulate: out += sum).
+// Enqueues the MoE layer on normalised input x (act dtype, tiled, rows padded to 32; xq/xs =
+// its tiled fp8 codes when the caller already quantised them). Router and expert weights
+// tiled. out = sum (accumulate: out += sum).
 hipError_t run_moe(const MoeWs& m, const void* x, const uint8_t* xq, const float* xs,
                    const void* w_router, const float* bias, const void* w_gu, const void* w_d,
                    const float* s_gu, const float* s_d, int T, int d, int E, int K, int F,
@@ -231,7 +244,9 @@ hipError_t run_moe(const MoeWs& m, const void* x, const uint8_t* xq, const float
   hipError_t e;
   {
     ProfScope ps(MOLT_PROF_PROJECTIONS, s);
-    if ((e = molt::launch_gemm(x, w_router, m.g, T, E, d, act, false, s)) != hipSuccess) return e;
+    if ((e = molt::launch_gemm(x, w_router, m.g, T, E, d, act, false, m.part, m.part_elems, s)) !=
+        hipSuccess)
+      return e;
   }
   if ((e = molt::launch_route(m.g, bias, replay, T, E, K, m.ids, m.w, m.counts, m.offsets, m.perm,
                               m.inv, m.pperm, m.n_padded, m.tile_m, m.tiles, m.max_tiles,
@@ -239,23 +254,19 @@ hipError_t run_moe(const MoeWs& m, const void* x, const uint8_t* xq, const float
     return e;
   const bool fp8 = wdt == MOLT_FP8_E4M3;
   if (fp8 && xq == nullptr) {
-    if ((e = molt::launch_quant_rows_bf16(static_cast<const uint16_t*>(x), T, d, m.xq, m.xs, s)) !=
-        hipSuccess)
+    if ((e = molt::launch_quant_rows_tiled(static_cast<const uint16_t*>(x), nullptr, nullptr, T, d,
+                                           m.xq, m.xs, s)) != hipSuccess)
       return e;
     xq = m.xq;
     xs = m.xs;
   }
-  const void* a = x;
-  if (wdt != MOLT_F32) {
-    const void* src = fp8 ? static_cast<const void*>(xq) : x;
-    if ((e = molt::launch_gather_tiled(src, m.pperm, K, m.n_padded, m.max_rows,
-                                       long(d) * dt_size(wdt), m.xt, s)) != hipSuccess)
-      return e;
-    a = m.xt;
-  }
+  const void* src = fp8 ? static_cast<const void*>(xq) : x;
+  if ((e = molt::launch_gather_tiled(src, m.pperm, K, m.n_padded, m.max_rows,
+                                     long(d) * dt_size(wdt), m.xt, s)) != hipSuccess)
+    return e;
   {
     ProfScope ps(MOLT_PROF_EXPERT_GEMM, s);
-    if ((e = molt::launch_moe_gate_up(a, xs, m.pperm, K, w_gu, s_gu, d, F, wdt, m.tiles,
+    if ((e = molt::launch_moe_gate_up(m.xt, xs, m.pperm, K, w_gu, s_gu, d, F, wdt, m.tiles,
                                       m.n_tiles, m.max_tiles, m.tile_m, m.h, s)) != hipSuccess)
       return e;
   }
@@ -288,6 +299,7 @@ size_t molt_moe_layer_workspace_size(int T, int d, int E, int K, int F, molt_dty
                                      molt_dtype w) {
   if (T < 1 || E < 1 || K < 1 || d < 1 || F < 1 || !pair_ok(act, w)) return 0;
   molt::Carver c(nullptr, 0);
+  c.take<uint8_t>(pad32(T) * d * dt_size(act));   // tiled copy of x
   carve_moe(c, T, d, E, K, F, act, w);
   return c.used + 256;
 }
@@ -307,10 +319,12 @@ int molt_moe_layer(const void* x, const void* w_router, const float* router_bias
     return r;
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   molt::Carver c(workspace, workspace_bytes);
+  void* xt = c.take<uint8_t>(pad32(T) * d * dt_size(act_dtype));
   MoeWs m = carve_moe(c, T, d, E, K, F, act_dtype, w_dtype);
-  hipError_t e = run_moe(m, x, nullptr, nullptr, w_router, router_bias, w_gate_up, w_down,
-                         s_gate_up, s_down, T, d, E, K, F, act_dtype, w_dtype, replay_ids, out,
-                         false, s);
+  hipError_t e = molt::launch_pack_tiled(x, xt, T, long(d) * dt_size(act_dtype), s);
+  if (e == hipSuccess)
+    e = run_moe(m, xt, nullptr, nullptr, w_router, router_bias, w_gate_up, w_down, s_gate_up,
+                s_down, T, d, E, K, F, act_dtype, w_dtype, replay_ids, out, false, s);
   const size_t P = size_t(T) * K;
   if (e == hipSuccess) e = copy_out(out_ids, m.ids, P * 4, s);
   if (e == hipSuccess) e = copy_out(out_weights, m.w, P * 4, s);
@@ -326,7 +340,7 @@ int molt_pack_weights(const void* src, void* dst, long long rows, long long row_
                       molt_stream_t stream) {
   REQUIRE(src && dst, "a required pointer is NULL");
   REQUIRE(src != dst, "packing in place is not supported");
-  REQUIRE(rows >= 1 && rows % 32 == 0, "rows = %lld must be a positive multiple of 32", rows);
+  REQUIRE(rows >= 1, "rows = %lld must be >= 1", rows);
   REQUIRE(row_bytes >= 128 && row_bytes % 128 == 0,
           "row_bytes = %lld must be a positive multiple of 128", row_bytes);
   return hip_status(molt::launch_pack_tiled(src, dst, rows, row_bytes,
@@ -336,17 +350,25 @@ int molt_pack_weights(const void* src, void* dst, long long rows, long long row_
 
 // ------------------------------------------------------------------ dense GEMM
 
+size_t molt_dense_gemm_workspace_size(int M, int N, int K, molt_dtype dtype) {
+  if (M < 1 || N < 1 || K < 1 || !act_ok(dtype)) return 0;
+  const long e = gemm_part_elems(M, N, K, dtype);
+  return e ? size_t(e) * 4 + 256 : 0;
+}
+
 int molt_dense_gemm(const void* A, const void* B, float* C, int M, int N, int K, molt_dtype dtype,
-                    int accumulate, molt_stream_t stream) {
+                    int accumulate, void* workspace, size_t workspace_bytes, molt_stream_t stream) {
   REQUIRE(A && B && C, "a required pointer is NULL");
   REQUIRE(M >= 1 && N >= 1 && K >= 1, "M, N, K must be >= 1 (got %d, %d, %d)", M, N, K);
   REQUIRE(act_ok(dtype), "dtype must be F32 or BF16");
-  REQUIRE(dtype == MOLT_F32 || K % 64 == 0, "bf16 needs K %% 64 == 0 (K = %d)", K);
+  REQUIRE(long(K) * dt_size(dtype) % 128 == 0, "K * sizeof(dtype) must be a multiple of 128 (K = %d)", K);
+  if (int r = check_ws(workspace, workspace_bytes, molt_dense_gemm_workspace_size(M, N, K, dtype)))
+    return r;
   hipError_t e;
   {
     ProfScope ps(MOLT_PROF_PROJECTIONS, reinterpret_cast<hipStream_t>(stream));
-    e = molt::launch_gemm(A, B, C, M, N, K, dtype, accumulate != 0,
-                          reinterpret_cast<hipStream_t>(stream));
+    e = molt::launch_gemm(A, B, C, M, N, K, dtype, accumulate != 0, static_cast<float*>(workspace),
+                          long(workspace_bytes / 4), reinterpret_cast<hipStream_t>(stream));
   }
   return hip_status(e, "molt_dense_gemm");
 }
@@ -382,7 +404,7 @@ int molt_paged_attention(const void* q, const void* k_cache, const void* v_cache
   {
     ProfScope ps(MOLT_PROF_ATTENTION, reinterpret_cast<hipStream_t>(stream));
     e = molt::launch_paged_attention(q, k_cache, v_cache, block_tables, context_lens, B, k, Hq, Hkv,
-                                     D, max_blocks, dtype, out, workspace,
+                                     D, max_blocks, dtype, out, false, workspace,
                                      reinterpret_cast<hipStream_t>(stream));
   }
   return hip_status(e, "molt_paged_attention");
@@ -428,6 +450,7 @@ int model_ok(const molt_model* m, const molt_kv* kv, int B, int k, bool need_hea
 
 struct DecWs {
   void* y; uint8_t* yq; float* ys; float* qkv; void* q; void* attn; void* attn_ws; MoeWs moe;
+  float* part; long part_elems;   // split-K partial sums of the QKV and O projections
 };
 
 DecWs carve_dec(molt::Carver& c, const molt_model* m, int B, int k, int max_blocks) {
@@ -435,17 +458,22 @@ DecWs carve_dec(molt::Carver& c, const molt_model* m, int B, int k, int max_bloc
   const long T = long(B) * (k + 1);
   const int d = m->d_model, D = m->head_dim, Hq = m->n_q_heads, Hkv = m->n_kv_heads;
   const size_t es = dt_size(m->dtype);
-  w.y = c.take<uint8_t>(T * d * es);
+  const long Tp = pad32(T);                 // GEMM operands: tiled, rows padded to 32
+  w.y = c.take<uint8_t>(Tp * d * es);
   if (m->expert_dtype == MOLT_FP8_E4M3) {
-    w.yq = c.take<uint8_t>(T * d);
-    w.ys = c.take<float>(T);
+    w.yq = c.take<uint8_t>(Tp * d);
+    w.ys = c.take<float>(Tp);
   }
   w.qkv = c.take<float>(T * (Hq + 2 * Hkv) * D);
   w.q = c.take<uint8_t>(T * Hq * D * es);
-  w.attn = c.take<uint8_t>(T * Hq * D * es);
+  w.attn = c.take<uint8_t>(Tp * Hq * D * es);
   const size_t aws = m->dtype == MOLT_F32 ? 0 : molt::attention_ws_bytes(B, k, Hq, Hkv, D, max_blocks);
   w.attn_ws = c.take<uint8_t>(aws);
   w.moe = carve_moe(c, int(T), d, m->n_experts, m->top_k, m->d_ff, m->dtype, m->expert_dtype);
+  const long pq = gemm_part_elems(int(T), (Hq + 2 * Hkv) * D, d, m->dtype);
+  const long po = gemm_part_elems(int(T), d, Hq * D, m->dtype);
+  w.part_elems = pq > po ? pq : po;
+  w.part = c.take<float>(w.part_elems);
   return w;
 }
 
@@ -460,7 +488,8 @@ hipError_t run_decoder(const DecWs& w, const molt_model* m, const molt_kv* kv, i
     RUN(molt::launch_rmsnorm(x, m->attn_norm[l], T, d, m->rms_eps, m->dtype, w.y, nullptr, nullptr, s));
     {
       ProfScope ps(MOLT_PROF_PROJECTIONS, s);
-      RUN(molt::launch_gemm(w.y, m->w_qkv[l], w.qkv, T, (Hq + 2 * Hkv) * D, d, m->dtype, false, s));
+      RUN(molt::launch_gemm(w.y, m->w_qkv[l], w.qkv, T, (Hq + 2 * Hkv) * D, d, m->dtype, false,
+                            w.part, w.part_elems, s));
     }
     RUN(molt::launch_rope_kv_write(w.qkv, B, k, Hq, Hkv, D, m->rope_theta, kv->context_lens,
                                    kv->block_tables, kv->max_blocks_per_seq, kv->num_blocks,
@@ -469,11 +498,12 @@ hipError_t run_decoder(const DecWs& w, const molt_model* m, const molt_kv* kv, i
       ProfScope ps(MOLT_PROF_ATTENTION, s);
       RUN(molt::launch_paged_attention(w.q, kv->k_cache[l], kv->v_cache[l], kv->block_tables,
                                        kv->context_lens, B, k, Hq, Hkv, D, kv->max_blocks_per_seq,
-                                       m->dtype, w.attn, w.attn_ws, s));
+                                       m->dtype, w.attn, true, w.attn_ws, s));
     }
     {
       ProfScope ps(MOLT_PROF_PROJECTIONS, s);
-      RUN(molt::launch_gemm(w.attn, m->w_o[l], x, T, d, Hq * D, m->dtype, true, s));
+      RUN(molt::launch_gemm(w.attn, m->w_o[l], x, T, d, Hq * D, m->dtype, true, w.part,
+                            w.part_elems, s));
     }
     const bool fp8 = m->expert_dtype == MOLT_FP8_E4M3;
     RUN(molt::launch_rmsnorm(x, m->moe_norm[l], T, d, m->rms_eps, m->dtype, w.y,
@@ -517,7 +547,7 @@ StepWs carve_step(molt::Carver& c, const molt_model* m, int B, int k, int max_bl
   StepWs w{};
   const long T = long(B) * (k + 1);
   w.x = c.take<float>(T * m->d_model);
-  w.yf = c.take<uint8_t>(T * m->d_model * dt_size(m->dtype));
+  w.yf = c.take<uint8_t>(pad32(T) * m->d_model * dt_size(m->dtype));
   w.logits = own_logits ? c.take<float>(T * long(m->vocab)) : nullptr;
   w.samp = c.take<uint8_t>(molt::sampler_ws_bytes(B, k, m->vocab));
   w.dec = carve_dec(c, m, B, k, max_blocks);
@@ -556,7 +586,8 @@ int molt_verify_step(const molt_model* m, const molt_kv* kv, int B, int k, const
                              nullptr, nullptr, s);
   if (e == hipSuccess) {
     ProfScope ps(MOLT_PROF_LM_HEAD, s);
-    e = molt::launch_gemm(w.yf, m->lm_head, logits, T, m->vocab, m->d_model, m->dtype, false, s);
+    e = molt::launch_gemm(w.yf, m->lm_head, logits, T, m->vocab, m->d_model, m->dtype, false,
+                          nullptr, 0, s);
   }
   // drafts are tokens[:, 1:]: the sampler reads them with row stride k+1
   if (e == hipSuccess) {

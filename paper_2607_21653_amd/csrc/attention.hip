@@ -42,12 +42,18 @@ struct AttnParams {
   const uint16_t* vc;      // [nb, Hkv, D, 16]
   const int32_t* bt;       // [B, max_blocks]
   const int32_t* ctx;      // [B]
-  uint16_t* out;           // [T, Hq * D]
+  uint16_t* out;           // [T, Hq * D], row-major or tiled (out_tiled)
   float* part_o;           // [B, Hkv, S, R, D]
   float* part_ml;          // [B, Hkv, S, R, 2]
   int k, Hq, Hkv, max_blocks, splits, blocks_per_split;
   float scale_log2;        // log2(e) / sqrt(D)
+  int out_tiled;           // output in the GEMM operand layout (input of the O projection)
 };
+
+// element index of output (token t, column c) of `cols` columns
+MOLT_DEV long out_index(const AttnParams& p, long t, long c, long cols, int esize) {
+  return p.out_tiled ? tiled_index(t, c, cols, esize) : t * cols + c;
+}
 
 // K and V^T fragments of one 32-key block pair for one wavefront
 template <int D>
@@ -268,7 +274,7 @@ __global__ __launch_bounds__(kThreads) void attn_mfma_kernel(AttnParams p) {
     const int j = r / G, gi = r % G;
     if (p.splits == 1) {
       const float v = Lsum > 0.f ? s_o[idx] / Lsum : 0.f;
-      p.out[((long(b) * kp1 + j) * p.Hq + h * G + gi) * D + dd] = f32_to_bf16(v);
+      p.out[out_index(p, long(b) * kp1 + j, (h * G + gi) * D + dd, long(p.Hq) * D, 2)] = f32_to_bf16(v);
     } else {
       const long pr = (long(bh) * p.splits + split) * R + r;
       p.part_o[pr * D + dd] = s_o[idx];
@@ -303,9 +309,9 @@ __global__ __launch_bounds__(D) void attn_merge_kernel(AttnParams p, int out_f32
   }
   const int j = r / G, gi = r % G;
   const float v = L > 0.f ? acc / L : 0.f;
-  const long oi = ((long(b) * kp1 + j) * p.Hq + h * G + gi) * D + threadIdx.x;
-  if (out_f32) reinterpret_cast<float*>(p.out)[oi] = v;
-  else p.out[oi] = f32_to_bf16(v);
+  const long t = long(b) * kp1 + j, c = (h * G + gi) * D + threadIdx.x;
+  if (out_f32) reinterpret_cast<float*>(p.out)[out_index(p, t, c, long(p.Hq) * D, 4)] = v;
+  else p.out[out_index(p, t, c, long(p.Hq) * D, 2)] = f32_to_bf16(v);
 }
 
 // ---------------------------------------------------------------- f32 VALU path
@@ -354,10 +360,10 @@ __global__ __launch_bounds__(kWave) void attn_f32_kernel(const float* __restrict
     }
     m = mn;
   }
-  float* out = reinterpret_cast<float*>(p.out) + (long(t) * p.Hq + hq) * D;
+  float* out = reinterpret_cast<float*>(p.out);
   for (int c = 0; c < 4; ++c) {
     const int dd = lane + kWave * c;
-    if (dd < D) out[dd] = acc[c] / l;
+    if (dd < D) out[out_index(p, t, long(hq) * D + dd, long(p.Hq) * D, 4)] = acc[c] / l;
   }
 }
 
@@ -412,9 +418,10 @@ size_t attention_ws_bytes(int B, int k, int Hq, int Hkv, int D, int max_blocks) 
 
 hipError_t launch_paged_attention(const void* q, const void* kc, const void* vc, const int32_t* bt,
                                   const int32_t* ctx, int B, int k, int Hq, int Hkv, int D,
-                                  int max_blocks, molt_dtype dt, void* out, void* ws,
-                                  hipStream_t s) {
+                                  int max_blocks, molt_dtype dt, void* out, bool out_tiled,
+                                  void* ws, hipStream_t s) {
   AttnParams p{};
+  p.out_tiled = out_tiled;
   p.q = static_cast<const uint16_t*>(q);
   p.kc = static_cast<const uint16_t*>(kc);
   p.vc = static_cast<const uint16_t*>(vc);

@@ -71,6 +71,12 @@ MOLT_DEV uint32_t f32_to_fp8e4m3(float f) {
   return sign | code;
 }
 
+// Workgroup barrier for LDS exchange only: waits for this wavefront's LDS operations, not
+// for its outstanding global loads (__syncthreads() fences all memory, draining the
+// prefetches a software pipeline keeps in flight). The memory clobber keeps the compiler
+// from moving memory accesses across it.
+MOLT_DEV void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
 // ---------------------------------------------------------------- reductions
 
 MOLT_DEV float wave_max(float v) {
@@ -135,4 +141,8 @@ MOLT_DEV float silu(float x) { return x / (1.0f + expf(-x)); }
 MOLT_DEV long tiled_offset(long row, long j, long row_bytes) {
   return ((row >> 5) * (row_bytes >> 7) + (j >> 7)) * 4096 + ((j & 63) >> 4) * 1024 +
          ((((j & 127) >> 6) << 5) + (row & 31)) * 16 + (j & 15);
+}
+// element index of (row, col) of a tiled matrix of `cols` elements of `esize` bytes per row
+MOLT_DEV long tiled_index(long row, long col, long cols, int esize) {
+  return tiled_offset(row, col * esize, cols * esize) / esize;
 }

@@ -1,6 +1,6 @@
 // Row-wise kernels of the verify step: token embedding, RMSNorm (+ per-row fp8
-// quantisation), RoPE with the paged-KV write of the 1+k new positions, and the
-// weighted expert combine. All are HBM-bound with a few bytes per element; one
+// quantisation), fp8 quantisation of tiled rows, RoPE with the paged-KV write of the 1+k
+// new positions, and the weighted expert combine. All are HBM-bound with a few bytes per element; one
 // workgroup per token row.
 #include "device_common.h"
 #include "internal.h"
@@ -32,7 +32,7 @@ __global__ __launch_bounds__(kThreads) void embed_kernel(const void* __restrict_
 }
 
 // y = x / sqrt(mean(x^2) + eps) * g rounded to dt; with yq, also the per-row fp8 code
-// of y (s = amax|y| / 448, code = e4m3(y / s)).
+// of y (s = amax|y| / 448, code = e4m3(y / s)). y and yq are GEMM operands: tiled layout.
 __global__ __launch_bounds__(kThreads) void rmsnorm_kernel(const float* __restrict__ x,
                                                            const float* __restrict__ g, int d,
                                                            float eps, molt_dtype dt,
@@ -47,48 +47,36 @@ __global__ __launch_bounds__(kThreads) void rmsnorm_kernel(const float* __restri
   ss = block_sum<kThreads / kWave, float>(ss, red);
   const float r = 1.0f / sqrtf(ss / float(d) + eps);
   float amax = 0.f;
+  const int es = dt == MOLT_BF16 ? 2 : 4;
   for (int i = threadIdx.x; i < d; i += kThreads) {
     float v = xr[i] * r * g[i];
     if (dt == MOLT_BF16) v = round_to_bf16(v);
-    store_act(y, long(t) * d + i, v, dt);
+    store_act(y, tiled_index(t, i, d, es), v, dt);
     amax = fmaxf(amax, fabsf(v));
   }
   if (yq == nullptr) return;
   amax = block_max<kThreads / kWave>(amax, red);
   const float s = amax / 448.0f;
   for (int i = threadIdx.x; i < d; i += kThreads) {
-    const float v = load_act(y, long(t) * d + i, dt);
-    yq[long(t) * d + i] = s > 0.f ? uint8_t(f32_to_fp8e4m3(v / s)) : uint8_t(0);
+    const float v = load_act(y, tiled_index(t, i, d, es), dt);
+    yq[tiled_offset(t, i, d)] = s > 0.f ? uint8_t(f32_to_fp8e4m3(v / s)) : uint8_t(0);
   }
   if (threadIdx.x == 0) ys[t] = s;
 }
 
-// per-row fp8 quantisation of bf16 rows
-__global__ __launch_bounds__(kThreads) void quant_rows_kernel(const uint16_t* __restrict__ x,
-                                                              int cols, uint8_t* __restrict__ q,
-                                                              float* __restrict__ scale) {
-  __shared__ float red[kThreads / kWave];
-  const long r = blockIdx.x;
-  float amax = 0.f;
-  for (int i = threadIdx.x; i < cols; i += kThreads) amax = fmaxf(amax, fabsf(bf16_to_f32(x[r * cols + i])));
-  amax = block_max<kThreads / kWave>(amax, red);
-  const float s = amax / 448.0f;
-  for (int i = threadIdx.x; i < cols; i += kThreads)
-    q[r * cols + i] = s > 0.f ? uint8_t(f32_to_fp8e4m3(bf16_to_f32(x[r * cols + i]) / s)) : uint8_t(0);
-  if (threadIdx.x == 0) scale[r] = s;
-}
-
-// The same quantisation for the SwiGLU product of the grouped GEMMs: rows in padded
-// expert order, bf16 in and e4m3 codes out in the tiled layout; one wavefront per row,
-// 8 values per lane step. Padding rows (pair -1) get zero codes and scale 0.
+// Per-row fp8 quantisation of tiled bf16 rows into tiled e4m3 codes (s = amax / 448,
+// code = e4m3(v / s), zero row -> s = 0): the SwiGLU product of the grouped GEMMs (rows in
+// padded expert order, count on the device, padding rows with pair -1 get zero codes and
+// scale 0) or an input activation (all `rows` rows). One wavefront per row, 8 values per
+// lane step.
 __global__ __launch_bounds__(kThreads) void quant_rows_tiled_kernel(
     const uint16_t* __restrict__ h, const int32_t* __restrict__ pperm,
-    const int32_t* __restrict__ n_rows, int cols, uint8_t* __restrict__ q,
+    const int32_t* __restrict__ n_rows, long rows, int cols, uint8_t* __restrict__ q,
     float* __restrict__ scale) {
   const long r = long(blockIdx.x) * (kThreads / kWave) + threadIdx.x / kWave;
   const int lane = threadIdx.x % kWave;
-  if (r >= *n_rows) return;
-  const bool pad = pperm[r] < 0;
+  if (r >= (n_rows ? long(*n_rows) : rows)) return;
+  const bool pad = pperm && pperm[r] < 0;
   const long rb_in = 2L * cols, rb_out = cols;
   float amax = 0.f;
   for (int c = lane * 8; c < cols; c += kWave * 8) {
@@ -203,13 +191,6 @@ hipError_t launch_rmsnorm(const float* x, const float* g, int T, int d, float ep
   return hipGetLastError();
 }
 
-hipError_t launch_quant_rows_bf16(const uint16_t* x, int rows, int cols, uint8_t* q, float* scale,
-                                  hipStream_t s) {
-  if (rows == 0) return hipSuccess;
-  quant_rows_kernel<<<rows, kThreads, 0, s>>>(x, cols, q, scale);
-  return hipGetLastError();
-}
-
 hipError_t launch_rope_kv_write(const float* qkv, int B, int k, int Hq, int Hkv, int D,
                                 float theta, const int32_t* ctx, const int32_t* bt, int max_blocks,
                                 int num_blocks, molt_dtype dt, void* q_out, void* k_cache,
@@ -225,7 +206,7 @@ hipError_t launch_quant_rows_tiled(const uint16_t* h, const int32_t* pperm, cons
   constexpr int rows_per_block = kThreads / kWave;
   const long grid = (max_rows + rows_per_block - 1) / rows_per_block;
   if (grid == 0) return hipSuccess;
-  quant_rows_tiled_kernel<<<grid, kThreads, 0, s>>>(h, pperm, n_rows, cols, q, scale);
+  quant_rows_tiled_kernel<<<grid, kThreads, 0, s>>>(h, pperm, n_rows, max_rows, cols, q, scale);
   return hipGetLastError();
 }
 

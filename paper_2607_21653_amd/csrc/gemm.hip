@@ -3,16 +3,13 @@
 // epilogue, down), in bf16 (v_mfma_f32_32x32x16_bf16) or fp8 e4m3 with f32 per-row x
 // per-channel scales (v_mfma_f32_32x32x64_f8f6f4), f32 accumulation.
 //
-// One kernel template: a workgroup of 4 wavefronts computes a BM x 128 output tile,
-// staging 128-byte K-slices of A (BM rows) and B (128 weight rows) through LDS with
-// double buffering (rows padded to 144 B so the 16-lane phases of ds_read_b128 hit 16
-// distinct bank groups). A rows are gathered: dense rows, token rows via the expert
-// permutation (gate_up), or the expert's contiguous rows (down). Grouped launches run
-// over a device-side tile table (expert, first row, end row) built by the permutation
-// kernel, so the host never reads expert counts; unused table slots exit at once.
-// All matrices are row-major with K contiguous (weights [out, in]).
+// Every operand is in the tiled layout of device_common.h (weights packed once at load;
+// activations written tiled by their producers, rows padded to a multiple of 32). One
+// kernel template streams the weights per wavefront (see below). Grouped launches run over
+// a device-side tile table (expert, first row, end row) in padded expert order built by
+// the permutation kernel, so the host never reads expert counts.
 //
-// The f32 model (tiny test model) takes a plain VALU path with the same epilogues.
+// The f32 model (tiny test model) takes a plain VALU path over the same layouts.
 #include "device_common.h"
 #include "internal.h"
 
@@ -21,33 +18,26 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kBN = 128;         // output columns per tile (gate_up: 64 gate + 64 up)
-constexpr int kRowBytes = 128;   // K-slice per stage, bytes
-constexpr int kLdsStride = 144;  // padded LDS row
+constexpr int kRowBytes = 128;   // K-slice, bytes
 
 enum Mode { kDense = 0, kGateUp = 1, kDown = 2 };
 
 struct GemmParams {
-  const void* A;           // dense: [M, K]; gate_up: tokens [T, K] (x or fp8 codes); down: h [P, K]
-  const void* B;           // dense: [N, K]; gate_up: [E, 2F, K]; down: [E, N, K]
-  void* C;                 // dense/down: f32 [.., ldc]; gate_up: h [P, F] (act dtype)
+  const void* A;           // tiled. dense: [M, K]; gate_up: gathered rows [R, K]; down: h [R, K]
+  const void* B;           // tiled. dense: [N, K]; gate_up: [E, 2F, K]; down: [E, N, K]
+  void* C;                 // dense: f32 [M, ldc]; gate_up: h tiled [R, F]; down: f32 [P, ldc]
   int M, N, K;             // N: output columns (gate_up: F)
   int ldc;
   const int4* tiles;       // grouped: {expert, row0, row1, -}
   const int32_t* n_tiles_live;   // grouped (device): entries of `tiles` in use
   int n_mtiles, n_ntiles;
-  const int32_t* perm;     // gate_up: permuted pair -> token * ktop + slot
+  const int32_t* perm;     // grouped: padded row -> pair (token * ktop + slot), -1 = padding
   int ktop;
-  const float* a_scale;    // fp8: per A row (token for gate_up, permuted row for down)
+  const float* a_scale;    // fp8: per A row (token for gate_up, padded row for down)
   const float* b_scale;    // fp8: [E, b_scale_ld]
   int b_scale_ld;
   int accumulate;          // dense: C += result
-  int xcd_remap;
 };
-
-// MFMA operand fragment types
-template <bool FP8> struct Frag;
-template <> struct Frag<false> { typedef bf16x8_t T; };
-template <> struct Frag<true> { typedef int32x8_t T; };
 
 MOLT_DEV floatx16_t mfma(const bf16x8_t& a, const bf16x8_t& b, const floatx16_t& c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
@@ -57,222 +47,11 @@ MOLT_DEV floatx16_t mfma(const int32x8_t& a, const int32x8_t& b, const floatx16_
   return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, c, 0, 0, 0, 0, 0, 0);
 }
 
-template <int BM>
-struct WaveLayout {
-  static constexpr int WM = BM >= 128 ? 2 : 1;   // wavefronts along M
-  static constexpr int WN = 4 / WM;              // wavefronts along N
-  static constexpr int TM = BM / WM / 32;        // 32x32 MFMA tiles per wave along M
-  static constexpr int TN = kBN / WN / 32;       // ... along N
-};
-
-template <int BM, bool FP8, int MODE>
-__global__ __launch_bounds__(kThreads) void mfma_gemm_kernel(GemmParams p) {
-  typedef WaveLayout<BM> L;
-  constexpr int kElem = FP8 ? 1 : 2;
-  constexpr int kBK = kRowBytes / kElem;              // K elements per stage
-  constexpr int kARows = BM / 32, kBRows = kBN / 32;  // 16-byte loads per thread
-  constexpr int kStage = (BM + kBN) * kLdsStride;
-  __shared__ __attribute__((aligned(16))) uint8_t lds[2 * kStage];
-
-  // ---- which tile
-  int id = blockIdx.x;
-  const int G = gridDim.x;
-  if (p.xcd_remap && (G % 8) == 0) id = (id % 8) * (G / 8) + id / 8;  // same XCD: neighbours
-  const int mt = id % p.n_mtiles;
-  const int nt = id / p.n_mtiles;
-  int expert = 0, row0, row1;
-  if (MODE == kDense) {
-    row0 = mt * BM;
-    row1 = min(row0 + BM, p.M);
-  } else {
-    const int4 tinfo = p.tiles[mt];
-    if (tinfo.x < 0) return;
-    expert = tinfo.x;
-    row0 = tinfo.y;
-    row1 = tinfo.z;
-  }
-  const int n0 = (MODE == kGateUp) ? nt * (kBN / 2) : nt * kBN;
-  const long K = p.K;
-
-  // ---- per-thread global row pointers (16-byte chunk c of rows r = tid/8 + 32 i)
-  const int chunk = threadIdx.x % 8;
-  const uint8_t* a_src[kARows];
-  const uint8_t* b_src[kBRows];
-#pragma unroll
-  for (int i = 0; i < kARows; ++i) {
-    const int r = threadIdx.x / 8 + 32 * i;
-    const int grow = row0 + r;
-    a_src[i] = nullptr;
-    if (grow < row1) {
-      long arow = grow;
-      if (MODE == kGateUp) arow = p.perm[grow] / p.ktop;
-      a_src[i] = static_cast<const uint8_t*>(p.A) + (arow * K) * kElem + chunk * 16;
-    }
-  }
-#pragma unroll
-  for (int i = 0; i < kBRows; ++i) {
-    const int r = threadIdx.x / 8 + 32 * i;
-    long brow;
-    bool ok = true;
-    if (MODE == kGateUp) {
-      brow = long(expert) * 2 * p.N + (r < kBN / 2 ? n0 + r : p.N + n0 + r - kBN / 2);
-    } else if (MODE == kDown) {
-      brow = long(expert) * p.N + n0 + r;
-    } else {
-      brow = n0 + r;
-      ok = n0 + r < p.N;
-    }
-    b_src[i] = ok ? static_cast<const uint8_t*>(p.B) + (brow * K) * kElem + chunk * 16 : nullptr;
-  }
-
-  int4 ra[kARows], rb[kBRows];
-  auto gload = [&](int kb) {
-    const long off = long(kb) * kRowBytes;
-#pragma unroll
-    for (int i = 0; i < kARows; ++i)
-      ra[i] = a_src[i] ? *reinterpret_cast<const int4*>(a_src[i] + off) : make_int4(0, 0, 0, 0);
-#pragma unroll
-    for (int i = 0; i < kBRows; ++i)
-      rb[i] = b_src[i] ? *reinterpret_cast<const int4*>(b_src[i] + off) : make_int4(0, 0, 0, 0);
-  };
-  auto sstore = [&](int buf) {
-    uint8_t* base = lds + buf * kStage;
-#pragma unroll
-    for (int i = 0; i < kARows; ++i)
-      *reinterpret_cast<int4*>(base + (threadIdx.x / 8 + 32 * i) * kLdsStride + chunk * 16) = ra[i];
-#pragma unroll
-    for (int i = 0; i < kBRows; ++i)
-      *reinterpret_cast<int4*>(base + (BM + threadIdx.x / 8 + 32 * i) * kLdsStride + chunk * 16) = rb[i];
-  };
-
-  const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
-  const int wm = wave / L::WN, wn = wave % L::WN;
-  const int wrow = wm * (BM / L::WM), wcol = wn * (kBN / L::WN);
-  floatx16_t acc[L::TM][L::TN];
-#pragma unroll
-  for (int i = 0; i < L::TM; ++i)
-#pragma unroll
-    for (int j = 0; j < L::TN; ++j)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
-
-  const int nk = int(K / kBK);
-  gload(0);
-  sstore(0);
-  __syncthreads();
-  for (int kb = 0; kb < nk; ++kb) {
-    if (kb + 1 < nk) gload(kb + 1);
-    const uint8_t* base = lds + (kb & 1) * kStage;
-    const int lrow = lane % 32, lhalf = lane / 32;
-    if (!FP8) {
-#pragma unroll
-      for (int s = 0; s < 4; ++s) {  // 4 k-steps of 16
-        bf16x8_t af[L::TM], bfr[L::TN];
-#pragma unroll
-        for (int i = 0; i < L::TM; ++i)
-          af[i] = *reinterpret_cast<const bf16x8_t*>(base + (wrow + i * 32 + lrow) * kLdsStride + s * 32 + lhalf * 16);
-#pragma unroll
-        for (int j = 0; j < L::TN; ++j)
-          bfr[j] = *reinterpret_cast<const bf16x8_t*>(base + (BM + wcol + j * 32 + lrow) * kLdsStride + s * 32 + lhalf * 16);
-#pragma unroll
-        for (int i = 0; i < L::TM; ++i)
-#pragma unroll
-          for (int j = 0; j < L::TN; ++j) acc[i][j] = mfma(af[i], bfr[j], acc[i][j]);
-      }
-    } else {
-#pragma unroll
-      for (int s = 0; s < 2; ++s) {  // 2 k-steps of 64
-        int32x8_t af[L::TM], bfr[L::TN];
-#pragma unroll
-        for (int i = 0; i < L::TM; ++i) {
-          const uint8_t* q = base + (wrow + i * 32 + lrow) * kLdsStride + s * 64 + lhalf * 32;
-          int32x4_t lo = *reinterpret_cast<const int32x4_t*>(q);
-          int32x4_t hi = *reinterpret_cast<const int32x4_t*>(q + 16);
-          af[i] = int32x8_t{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-        }
-#pragma unroll
-        for (int j = 0; j < L::TN; ++j) {
-          const uint8_t* q = base + (BM + wcol + j * 32 + lrow) * kLdsStride + s * 64 + lhalf * 32;
-          int32x4_t lo = *reinterpret_cast<const int32x4_t*>(q);
-          int32x4_t hi = *reinterpret_cast<const int32x4_t*>(q + 16);
-          bfr[j] = int32x8_t{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-        }
-#pragma unroll
-        for (int i = 0; i < L::TM; ++i)
-#pragma unroll
-          for (int j = 0; j < L::TN; ++j) acc[i][j] = mfma(af[i], bfr[j], acc[i][j]);
-      }
-    }
-    if (kb + 1 < nk) sstore((kb + 1) & 1);
-    __syncthreads();
-  }
-
-  // ---- epilogue. acc[i][j][e] holds row wrow+32i+8(e/4)+4(lane/32)+e%4, col wcol+32j+lane%32
-  const int lcol = lane % 32, lgrp = lane / 32;
-  if (MODE == kGateUp) {
-    // waves holding "up" columns (tile cols 64..127) park them in LDS; the "gate" waves
-    // finish h = silu(gate) * up for their columns
-    float* upbuf = reinterpret_cast<float*>(lds);   // [BM][64]
-    const bool is_up = wcol >= kBN / 2;
-    if (is_up) {
-#pragma unroll
-      for (int i = 0; i < L::TM; ++i)
-#pragma unroll
-        for (int j = 0; j < L::TN; ++j)
-#pragma unroll
-          for (int e = 0; e < 16; ++e) {
-            const int r = wrow + 32 * i + 8 * (e / 4) + 4 * lgrp + (e % 4);
-            const int c = wcol - kBN / 2 + 32 * j + lcol;
-            upbuf[r * 64 + c] = acc[i][j][e];
-          }
-    }
-    __syncthreads();
-    if (!is_up) {
-#pragma unroll
-      for (int i = 0; i < L::TM; ++i)
-#pragma unroll
-        for (int j = 0; j < L::TN; ++j)
-#pragma unroll
-          for (int e = 0; e < 16; ++e) {
-            const int r = wrow + 32 * i + 8 * (e / 4) + 4 * lgrp + (e % 4);
-            const int c = wcol + 32 * j + lcol;
-            const int grow = row0 + r;
-            if (grow >= row1) continue;
-            float g = acc[i][j][e], u = upbuf[r * 64 + c];
-            if (FP8) {
-              const float sx = p.a_scale[p.perm[grow] / p.ktop];
-              const float* sw = p.b_scale + long(expert) * p.b_scale_ld;
-              g = g * sx * sw[n0 + c];
-              u = u * sx * sw[p.N + n0 + c];
-            }
-            const float h = silu(g) * u;
-            static_cast<uint16_t*>(p.C)[long(grow) * p.ldc + n0 + c] = f32_to_bf16(h);
-          }
-    }
-  } else {
-#pragma unroll
-    for (int i = 0; i < L::TM; ++i)
-#pragma unroll
-      for (int j = 0; j < L::TN; ++j)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const int r = wrow + 32 * i + 8 * (e / 4) + 4 * lgrp + (e % 4);
-          const int c = n0 + wcol + 32 * j + lcol;
-          const int grow = row0 + r;
-          if (grow >= row1 || c >= p.N) continue;
-          float v = acc[i][j][e];
-          if (FP8) v = v * p.a_scale[grow] * p.b_scale[long(expert) * p.b_scale_ld + c];
-          float* dst = static_cast<float*>(p.C) + long(grow) * p.ldc + c;
-          if (MODE == kDense && p.accumulate) v += *dst;
-          *dst = v;
-        }
-  }
-}
-
-// ---------------------------------------------------------------- weight-streaming grouped GEMM
+// ---------------------------------------------------------------- weight-streaming GEMM
 // Expert GEMMs are HBM-bound at the verify step's row counts (tens of rows per expert),
-// so the weights must stream at full bandwidth and be read once. Workgroup = BM rows of
-// one expert x 128 output columns; each of the 4 wavefronts owns 32 output columns (32
+// and the dense projections nearly so at a few hundred rows: the weights must stream at
+// full bandwidth and be read once. Workgroup = BM rows (of
+// one expert) x 128 output columns; each of the 4 wavefronts owns 32 output columns (32
 // weight rows) and loads its weight fragments straight from global memory into MFMA
 // operand registers, kPD 128-byte K slices ahead; a weight element is used by exactly one
 // wavefront, so no LDS and no barrier is needed in the main loop. The activation rows
@@ -284,8 +63,7 @@ __global__ __launch_bounds__(kThreads) void mfma_gemm_kernel(GemmParams p) {
 struct Slice16 { int4 c[4]; };   // one lane's 64 bytes of a 32-row x 128-byte tile
 
 template <int BM, bool FP8, int MODE>
-__global__ __launch_bounds__(kThreads) void moe_stream_kernel(GemmParams p) {
-  static_assert(MODE == kGateUp || MODE == kDown, "grouped modes only");
+__global__ __launch_bounds__(kThreads) void stream_gemm_kernel(GemmParams p) {
   constexpr int MS = BM / 32;                        // 32-row MFMA tiles per wavefront
   constexpr int kPD = 4;                             // weight slices in flight
   constexpr int kPA = 2;                             // activation slices in flight
@@ -293,17 +71,27 @@ __global__ __launch_bounds__(kThreads) void moe_stream_kernel(GemmParams p) {
   __shared__ __attribute__((aligned(16))) float upbuf[MODE == kGateUp ? BM * 64 : 1];
 
   // Workgroup b runs on XCD b % 8. Each XCD takes one contiguous eighth of the live
-  // (m-tile, n-tile) pairs, m-tile major: the n-tiles of one row tile run back to back on
-  // one XCD, so its activation tile is read from HBM once and then hits that XCD's L2.
-  const int total = *p.n_tiles_live * p.n_ntiles;
+  // (m-tile, n-tile) pairs. Grouped: m-tile major, so the n-tiles of one row tile run back
+  // to back on one XCD and its activation tile is read from HBM once, then hits that XCD's
+  // L2. Dense: n-tile major, so each XCD reads its own eighth of the weights, and the row
+  // tiles sharing a weight tile run together.
+  const int total = (MODE == kDense ? p.n_mtiles : *p.n_tiles_live) * p.n_ntiles;
   const int chunk = (total + 7) / 8;
   const int k8 = blockIdx.x / 8;
   const int id = (blockIdx.x % 8) * chunk + k8;
   if (k8 >= chunk || id >= total) return;
-  const int mt = id / p.n_ntiles;
-  const int nt = id % p.n_ntiles;
-  const int4 t = p.tiles[mt];
-  const int expert = t.x, row0 = t.y, row1 = t.z;     // row0 % 32 == 0
+  int mt, nt, expert = 0, row0, row1;
+  if (MODE == kDense) {
+    nt = id / p.n_mtiles;
+    mt = id % p.n_mtiles;
+    row0 = mt * BM;
+    row1 = min(row0 + BM, p.M);
+  } else {
+    mt = id / p.n_ntiles;
+    nt = id % p.n_ntiles;
+    const int4 t = p.tiles[mt];
+    expert = t.x; row0 = t.y; row1 = t.z;             // row0 % 32 == 0
+  }
   const long RB = long(p.K) * kElem;                  // bytes per operand row
   const int nk = int(RB / kRowBytes);                 // 128-byte K slices
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
@@ -318,6 +106,9 @@ __global__ __launch_bounds__(kThreads) void moe_stream_kernel(GemmParams p) {
     n0 = nt * kBN;
     wrow = long(expert) * p.N + n0 + 32 * wave;
   }
+  // dense: B's rows are padded to a multiple of 32; a wavefront past the last column block
+  // re-reads the last one and stores nothing
+  if (MODE == kDense && n0 + 32 * wave >= p.N) wrow = (p.N - 1) & ~31;
   const uint8_t* bsrc = static_cast<const uint8_t*>(p.B) + wrow * RB + lane * 16;
   const uint8_t* asrc[MS];
   const int last_block = (row1 - 1) & ~31;            // 32-row blocks past the tile end
@@ -410,6 +201,18 @@ __global__ __launch_bounds__(kThreads) void moe_stream_kernel(GemmParams p) {
                                        tiled_offset(grow, 2L * (n0 + c), hrb)) = f32_to_bf16(silu(g) * u);
         }
     }
+  } else if (MODE == kDense) {
+    const int c = n0 + 32 * wave + lcol;
+    if (c >= p.N) return;
+#pragma unroll
+    for (int i = 0; i < MS; ++i)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int grow = row0 + 32 * i + 8 * (e / 4) + 4 * lgrp + (e % 4);
+        if (grow >= row1) continue;
+        float* dst = static_cast<float*>(p.C) + long(grow) * p.ldc + c;
+        *dst = p.accumulate ? *dst + acc[i][e] : acc[i][e];
+      }
   } else {
     // per-pair expert output, f32, row = pair index (token * K + slot)
     const int c = n0 + 32 * wave + lcol;
@@ -431,27 +234,162 @@ template <bool FP8, int MODE>
 hipError_t run_stream(GemmParams p, int tile_m, hipStream_t s) {
   int grid = p.n_mtiles * p.n_ntiles;
   grid = (grid + 7) / 8 * 8;
-  if (tile_m == 32) moe_stream_kernel<32, FP8, MODE><<<grid, kThreads, 0, s>>>(p);
-  else if (tile_m == 64) moe_stream_kernel<64, FP8, MODE><<<grid, kThreads, 0, s>>>(p);
-  else moe_stream_kernel<128, FP8, MODE><<<grid, kThreads, 0, s>>>(p);
+  if (tile_m == 32) stream_gemm_kernel<32, FP8, MODE><<<grid, kThreads, 0, s>>>(p);
+  else if (tile_m == 64) stream_gemm_kernel<64, FP8, MODE><<<grid, kThreads, 0, s>>>(p);
+  else stream_gemm_kernel<128, FP8, MODE><<<grid, kThreads, 0, s>>>(p);
   return hipGetLastError();
 }
 
+// ---------------------------------------------------------------- LDS-tiled dense GEMM
+// Dense projections and the LM head have a few hundred rows: every weight tile feeds
+// several row tiles and every activation tile many column tiles, so both operands are
+// shared through LDS. Workgroup = BM x 128 outputs, 4 wavefronts in a 2 x 2 grid. Per
+// 128-byte K slice the workgroup copies (BM/32 + 4) tiled 4 KB blocks (one 16-byte chunk
+// per thread per block: coalesced 4 KB loads from one page) into a double-buffered LDS
+// ring, loaded two slices ahead into registers; the tiled layout makes each wavefront's
+// MFMA fragment a contiguous 1 KB LDS read (conflict-free, no padding). One barrier per
+// slice. Split-K: split s covers slices [s * nk / S, (s + 1) * nk / S) and writes its
+// partial sums to `part[s]`; a fixed-order reduction adds them (deterministic).
+template <int BM>
+__global__ __launch_bounds__(kThreads) void lds_gemm_kernel(GemmParams p, float* part, int splits) {
+  constexpr int AB = BM / 32;                 // activation row blocks
+  constexpr int NB = AB + 4;                  // 4 KB blocks per slice (A then B)
+  constexpr int TM = BM / 64 > 0 ? BM / 64 : 1;   // 32-row MFMA tiles per wavefront
+  constexpr int WROWS = 32 * TM;              // rows per wavefront (2 x 2 wavefronts)
+  static_assert(BM == 64 || BM == 128, "BM");
+  __shared__ __attribute__((aligned(16))) uint8_t lds[2][NB * 4096];
+
+  const int total = p.n_mtiles * p.n_ntiles * splits;
+  const int chunk = (total + 7) / 8;
+  const int k8 = blockIdx.x / 8;
+  const int id = (blockIdx.x % 8) * chunk + k8;   // XCD-contiguous; split, n-tile, m-tile
+  if (k8 >= chunk || id >= total) return;
+  const int mt = id % p.n_mtiles;
+  const int nt = (id / p.n_mtiles) % p.n_ntiles;
+  const int split = id / (p.n_mtiles * p.n_ntiles);
+  const int row0 = mt * BM, n0 = nt * kBN;
+  const long RB = long(p.K) * 2;
+  const int nk = int(RB / kRowBytes);
+  const int kb0 = int(long(nk) * split / splits), kb1 = int(long(nk) * (split + 1) / splits);
+
+  // global source of block b (clamped into the padded operands) for this thread's chunk
+  const uint8_t* src[NB];
+  const int last_a = (p.M - 1) & ~31, last_b = (p.N - 1) & ~31;
+#pragma unroll
+  for (int b = 0; b < NB; ++b) {
+    const long r = b < AB ? min(row0 + 32 * b, last_a) : min(n0 + 32 * (b - AB), last_b);
+    src[b] = static_cast<const uint8_t*>(b < AB ? p.A : p.B) + r * RB + threadIdx.x * 16;
+  }
+  // register slots of two slices in flight (native vector type: HIP's int4 struct copied
+  // into LDS made the compiler keep these arrays in scratch memory)
+  int32x4_t st0[NB], st1[NB];
+#define MOLT_GLOAD(ST, KB)                                                            \
+  {                                                                                   \
+    const long off_ = long(min((KB), kb1 - 1)) * 4096;                                \
+    _Pragma("unroll") for (int b_ = 0; b_ < NB; ++b_)                                 \
+        ST[b_] = *reinterpret_cast<const int32x4_t*>(src[b_] + off_);                 \
+  }
+#define MOLT_SSTORE(ST, BUF)                                                          \
+  {                                                                                   \
+    _Pragma("unroll") for (int b_ = 0; b_ < NB; ++b_)                                 \
+        *reinterpret_cast<int32x4_t*>(&lds[BUF][b_ * 4096 + threadIdx.x * 16]) = ST[b_]; \
+  }
+  const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+  const int wm = wave / 2, wn = wave % 2;       // wavefront rows wm*WROWS.., cols wn*64..
+  floatx16_t acc[TM][2];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+
+  MOLT_GLOAD(st0, kb0);
+  MOLT_GLOAD(st1, kb0 + 1);
+  MOLT_SSTORE(st0, 0);
+  MOLT_GLOAD(st0, kb0 + 2);
+  lds_barrier();
+  // Step over slice k from LDS buffer u: at its start buffer u holds slice k, register slot
+  // 1 - u slice k + 1 and slot u slice k + 2. It computes, stores slice k + 1 into buffer
+  // 1 - u (last read before the previous barrier), refills slot 1 - u with slice k + 3.
+#define MOLT_STEP(U, ST_NEXT, K)                                                                  \
+  {                                                                                                \
+    const uint8_t* base_ = lds[U];                                                                 \
+    _Pragma("unroll") for (int c = 0; c < 4; ++c) {                                                \
+      bf16x8_t af[TM], bfr[2];                                                                     \
+      _Pragma("unroll") for (int i = 0; i < TM; ++i) af[i] = *reinterpret_cast<const bf16x8_t*>(   \
+          base_ + ((wm * WROWS) / 32 + i) * 4096 + c * 1024 + lane * 16);                          \
+      _Pragma("unroll") for (int j = 0; j < 2; ++j) bfr[j] = *reinterpret_cast<const bf16x8_t*>(   \
+          base_ + (AB + wn * 2 + j) * 4096 + c * 1024 + lane * 16);                                \
+      _Pragma("unroll") for (int i = 0; i < TM; ++i)                                               \
+          _Pragma("unroll") for (int j = 0; j < 2; ++j) acc[i][j] = mfma(af[i], bfr[j], acc[i][j]); \
+    }                                                                                              \
+    MOLT_SSTORE(ST_NEXT, 1 - (U));                                                                 \
+    MOLT_GLOAD(ST_NEXT, (K) + 3);                                                                  \
+    lds_barrier();                                                                                 \
+  }
+  // Step over slice k from LDS buffer u: at its start buffer u holds slice k, register slot
+  // 1 - u slice k + 1 and slot u slice k + 2. It computes, stores slice k + 1 into buffer
+  // 1 - u (last read before the previous barrier), refills slot 1 - u with slice k + 3.
+  int kb = kb0;
+  for (; kb + 1 < kb1; kb += 2) {   // loads are clamped, never behind a branch
+    MOLT_STEP(0, st1, kb);
+    MOLT_STEP(1, st0, kb + 1);
+  }
+  if (kb < kb1) MOLT_STEP(0, st1, kb);   // odd slice count: the last slice sits in buffer 0
+#undef MOLT_STEP
+#undef MOLT_SSTORE
+#undef MOLT_GLOAD
+
+  // acc[i][j][e]: row wm*WROWS + 32 i + 8 (e / 4) + 4 (lane / 32) + e % 4, col wn*64 + 32 j + lane % 32
+  const int lcol = lane % 32, lgrp = lane / 32;
+  float* out = splits > 1 ? part + long(split) * p.M * p.ldc : static_cast<float*>(p.C);
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    const int c = n0 + wn * 64 + 32 * j + lcol;
+    if (c >= p.N) continue;
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int grow = row0 + wm * WROWS + 32 * i + 8 * (e / 4) + 4 * lgrp + (e % 4);
+        if (grow >= p.M) continue;
+        float* dst = out + long(grow) * p.ldc + c;
+        *dst = (splits == 1 && p.accumulate) ? *dst + acc[i][j][e] : acc[i][j][e];
+      }
+  }
+}
+
+// C (+)= sum over s of part[s], in split order
+__global__ __launch_bounds__(kThreads) void splitk_reduce_kernel(const float* __restrict__ part,
+                                                                 int splits, long n, float* __restrict__ C,
+                                                                 int accumulate) {
+  const long i = long(blockIdx.x) * kThreads + threadIdx.x;
+  if (i >= n) return;
+  float v = accumulate ? C[i] : 0.f;
+  for (int s = 0; s < splits; ++s) v += part[s * n + i];
+  C[i] = v;
+}
+
 // ---------------------------------------------------------------- tiled-layout kernels
-// pack: row-major [rows, RB bytes] -> tiled; one thread per 16-byte chunk (reads coalesced)
+// pack: row-major [rows, RB bytes] -> tiled with rows padded to a multiple of 32 (padding
+// rows zero); one thread per 16-byte chunk of the destination
 __global__ __launch_bounds__(kThreads) void pack_tiled_kernel(const uint8_t* __restrict__ src,
                                                               uint8_t* __restrict__ dst, long rows,
                                                               long RB) {
   const long q = long(blockIdx.x) * kThreads + threadIdx.x;
   const long per_row = RB / 16;
-  if (q >= rows * per_row) return;
+  const long padded = (rows + 31) / 32 * 32;
+  if (q >= padded * per_row) return;
   const long r = q / per_row, j = (q % per_row) * 16;
-  *reinterpret_cast<int4*>(dst + tiled_offset(r, j, RB)) =
-      *reinterpret_cast<const int4*>(src + r * RB + j);
+  int4 v = make_int4(0, 0, 0, 0);
+  if (r < rows) v = *reinterpret_cast<const int4*>(src + r * RB + j);
+  *reinterpret_cast<int4*>(dst + tiled_offset(r, j, RB)) = v;
 }
 
-// gather: tiled activation rows in padded expert order, row = src[pperm[row] / ktop]
-// (zeros for padding rows); one workgroup per 4 KB tile, thread = 16-byte chunk of it
+// gather: tiled activation rows in padded expert order from tiled token rows,
+// row = src[pperm[row] / ktop] (zeros for padding rows); one workgroup per 4 KB tile of
+// the destination, thread = 16-byte chunk of it
 __global__ __launch_bounds__(kThreads) void gather_tiled_kernel(
     const uint8_t* __restrict__ src, const int32_t* __restrict__ pperm, int ktop,
     const int32_t* __restrict__ n_rows, long RB, uint8_t* __restrict__ dst) {
@@ -464,15 +402,13 @@ __global__ __launch_bounds__(kThreads) void gather_tiled_kernel(
   const long j = kb * 128 + (l / 32) * 64 + quarter * 16;
   const int pair = pperm[row];
   int4 v = make_int4(0, 0, 0, 0);
-  if (pair >= 0) v = *reinterpret_cast<const int4*>(src + long(pair / ktop) * RB + j);
+  if (pair >= 0) v = *reinterpret_cast<const int4*>(src + tiled_offset(pair / ktop, j, RB));
   *reinterpret_cast<int4*>(dst + tile * 4096 + threadIdx.x * 16) = v;
 }
 
 // ---------------------------------------------------------------- f32 VALU path
 // One workgroup per (row tile of 16, column tile of 64); each thread owns 4 outputs.
-// Dense: row-major operands. Grouped: weights tiled (f32 element k of row n at byte 4k),
-// activations row-major, rows in padded expert order (gate_up reads token rows through
-// the padded permutation; down writes pair rows).
+// Operands tiled as in the MFMA path (f32 element k of row n at byte 4k).
 template <int MODE>
 __global__ __launch_bounds__(kThreads) void f32_gemm_kernel(GemmParams p) {
   const int id = blockIdx.x;
@@ -489,46 +425,32 @@ __global__ __launch_bounds__(kThreads) void f32_gemm_kernel(GemmParams p) {
     row1 = t.z;
   }
   const int K = p.K;
-  const long RB = 4L * K;
   const float* A = static_cast<const float*>(p.A);
-  const uint8_t* B = static_cast<const uint8_t*>(p.B);
-  auto w = [&](long n, int kk) { return *reinterpret_cast<const float*>(B + tiled_offset(n, 4L * kk, RB)); };
+  const float* B = static_cast<const float*>(p.B);
   for (int o = threadIdx.x; o < 16 * 64; o += kThreads) {
     const int r = o / 64, c = o % 64;
     const int grow = row0 + r;
     const int col = nt * 64 + c;
     if (grow >= row1 || col >= p.N) continue;
-    if (MODE == kDense) {
-      const float* a = A + long(grow) * K;
-      const float* b = static_cast<const float*>(p.B) + long(col) * K;
-      float s = 0.f;
-      for (int kk = 0; kk < K; ++kk) s += a[kk] * b[kk];
-      float* dst = static_cast<float*>(p.C) + long(grow) * p.ldc + col;
-      if (p.accumulate) s += *dst;
-      *dst = s;
-    } else if (MODE == kGateUp) {
-      const float* a = A + long(p.perm[grow] / p.ktop) * K;
+    auto a = [&](int kk) { return A[tiled_index(grow, kk, K, 4)]; };
+    if (MODE == kGateUp) {
       const long ng = long(expert) * 2 * p.N + col, nu = ng + p.N;
       float g = 0.f, u = 0.f;
       for (int kk = 0; kk < K; ++kk) {
-        g += a[kk] * w(ng, kk);
-        u += a[kk] * w(nu, kk);
+        g += a(kk) * B[tiled_index(ng, kk, K, 4)];
+        u += a(kk) * B[tiled_index(nu, kk, K, 4)];
       }
-      static_cast<float*>(p.C)[long(grow) * p.ldc + col] = silu(g) * u;
+      static_cast<float*>(p.C)[tiled_index(grow, col, p.N, 4)] = silu(g) * u;
     } else {
-      const float* a = A + long(grow) * K;
-      const long n = long(expert) * p.N + col;
+      const long n = (MODE == kDown ? long(expert) * p.N : 0) + col;
       float s = 0.f;
-      for (int kk = 0; kk < K; ++kk) s += a[kk] * w(n, kk);
-      static_cast<float*>(p.C)[long(p.perm[grow]) * p.ldc + col] = s;
+      for (int kk = 0; kk < K; ++kk) s += a(kk) * B[tiled_index(n, kk, K, 4)];
+      const long crow = MODE == kDown ? long(p.perm[grow]) : long(grow);
+      float* dst = static_cast<float*>(p.C) + crow * p.ldc + col;
+      if (MODE == kDense && p.accumulate) s += *dst;
+      *dst = s;
     }
   }
-}
-
-template <int BM, bool FP8, int MODE>
-hipError_t run_mfma(GemmParams p, int grid, hipStream_t s) {
-  mfma_gemm_kernel<BM, FP8, MODE><<<grid, kThreads, 0, s>>>(p);
-  return hipGetLastError();
 }
 
 }  // namespace
@@ -541,8 +463,22 @@ int moe_tile_m(molt_dtype wdt, int T, int K, int E) {
   return avg <= 24 ? 32 : avg <= 56 ? 64 : 128;
 }
 
+// Tile height and split-K count of a dense bf16 GEMM: 128-row tiles when there are plenty
+// of them, else 64; then the K range is halved while the grid is under one workgroup per
+// CU, each split keeps >= 4 slices and the partial sums fit `part_elems` floats.
+GemmPlan gemm_plan(int M, int N, int K, long part_elems) {
+  GemmPlan g{128, 1};
+  const long nt = (N + kBN - 1) / kBN;
+  if ((M + 127) / 128 * nt < 512) g.bm = 64;
+  const long wg = (M + g.bm - 1) / g.bm * nt;
+  const int nk = int(2L * K / kRowBytes);
+  while (wg * g.splits < 256 && nk / (2 * g.splits) >= 4 && 2L * g.splits * M * N <= part_elems)
+    g.splits *= 2;
+  return g;
+}
+
 hipError_t launch_gemm(const void* A, const void* Bw, float* C, int M, int N, int K, molt_dtype dt,
-                       bool accumulate, hipStream_t s) {
+                       bool accumulate, float* part, long part_elems, hipStream_t s) {
   GemmParams p{};
   p.A = A; p.B = Bw; p.C = C; p.M = M; p.N = N; p.K = K; p.ldc = N;
   p.accumulate = accumulate;
@@ -552,14 +488,18 @@ hipError_t launch_gemm(const void* A, const void* Bw, float* C, int M, int N, in
     f32_gemm_kernel<kDense><<<p.n_mtiles * p.n_ntiles, kThreads, 0, s>>>(p);
     return hipGetLastError();
   }
+  const GemmPlan g = gemm_plan(M, N, K, part_elems);
+  p.n_mtiles = (M + g.bm - 1) / g.bm;
   p.n_ntiles = (N + kBN - 1) / kBN;
-  p.xcd_remap = 1;
-  if (M > 64) {
-    p.n_mtiles = (M + 127) / 128;
-    return run_mfma<128, false, kDense>(p, p.n_mtiles * p.n_ntiles, s);
+  const int grid = (p.n_mtiles * p.n_ntiles * g.splits + 7) / 8 * 8;
+  if (g.bm == 64) lds_gemm_kernel<64><<<grid, kThreads, 0, s>>>(p, part, g.splits);
+  else lds_gemm_kernel<128><<<grid, kThreads, 0, s>>>(p, part, g.splits);
+  if (g.splits > 1) {
+    const long n = long(M) * N;
+    splitk_reduce_kernel<<<(n + kThreads - 1) / kThreads, kThreads, 0, s>>>(part, g.splits, n, C,
+                                                                             accumulate);
   }
-  p.n_mtiles = (M + 31) / 32;
-  return run_mfma<32, false, kDense>(p, p.n_mtiles * p.n_ntiles, s);
+  return hipGetLastError();
 }
 
 hipError_t launch_moe_gate_up(const void* a, const float* a_scale, const int32_t* pperm, int K_top,
@@ -605,7 +545,7 @@ hipError_t launch_moe_down(const void* a, const float* a_scale, const int32_t* p
 }
 
 hipError_t launch_pack_tiled(const void* src, void* dst, long rows, long row_bytes, hipStream_t s) {
-  const long chunks = rows * (row_bytes / 16);
+  const long chunks = (rows + 31) / 32 * 32 * (row_bytes / 16);
   if (chunks == 0) return hipSuccess;
   pack_tiled_kernel<<<(chunks + kThreads - 1) / kThreads, kThreads, 0, s>>>(
       static_cast<const uint8_t*>(src), static_cast<uint8_t*>(dst), rows, row_bytes);

@@ -34,16 +34,16 @@ hipError_t launch_spec_accept(const float* logits, const float* q, const int32_t
 // ------------------------------------------------------------- elementwise
 hipError_t launch_embed(const void* table, const int32_t* tokens, int T, int d, int V,
                         molt_dtype dt, float* x, hipStream_t s);
-// y = rmsnorm(x) * g in act dtype; optional fp8 row quantisation of y
+// y = rmsnorm(x) * g in act dtype, tiled layout (rows padded to 32 by the caller's
+// allocation); optional fp8 row quantisation of y (tiled codes, per-row scales)
 hipError_t launch_rmsnorm(const float* x, const float* g, int T, int d, float eps, molt_dtype dt,
                           void* y, uint8_t* yq, float* yq_scale, hipStream_t s);
-hipError_t launch_quant_rows_bf16(const uint16_t* x, int rows, int cols, uint8_t* q, float* scale,
-                                  hipStream_t s);
 hipError_t launch_rope_kv_write(const float* qkv, int B, int k, int Hq, int Hkv, int D,
                                 float theta, const int32_t* ctx, const int32_t* bt, int max_blocks,
                                 int num_blocks, molt_dtype dt, void* q_out, void* k_cache,
                                 void* v_cache, hipStream_t s);
-// fp8 rows of the tiled SwiGLU product (padded expert order; n_rows on the device)
+// fp8 rows of a tiled bf16 matrix: rows = *n_rows when n_rows is given (padded expert
+// order, pperm marks padding rows), else max_rows
 hipError_t launch_quant_rows_tiled(const uint16_t* h, const int32_t* pperm, const int32_t* n_rows,
                                    long max_rows, int cols, uint8_t* q, float* scale,
                                    hipStream_t s);
@@ -63,10 +63,13 @@ int max_expert_tiles(int T, int E, int K, int tile_m);
 long max_padded_rows(int T, int E, int K);
 
 // ------------------------------------------------------------- GEMMs
-// C[M, N] (f32) = A[M, K] * B[N, K]^T, A/B in dt (F32 or BF16); epilogue adds into C when
-// accumulate. Row-major, K contiguous.
+// C[M, N] (f32, row-major) = A[M, K] * B[N, K]^T, A/B in dt (F32 or BF16), both tiled (rows
+// padded to 32); epilogue adds into C when accumulate. bf16 may split K when `part` holds
+// enough floats for the partial sums (gemm_plan).
+struct GemmPlan { int bm, splits; };
+GemmPlan gemm_plan(int M, int N, int K, long part_elems);
 hipError_t launch_gemm(const void* A, const void* Bw, float* C, int M, int N, int K, molt_dtype dt,
-                       bool accumulate, hipStream_t s);
+                       bool accumulate, float* part, long part_elems, hipStream_t s);
 // Grouped expert GEMMs over the tile table built by launch_route. bf16/fp8: A and the
 // weights in the tiled layout, gate_up writes h tiled; f32: row-major A and h, tiled
 // weights. Rows are padded-order; down writes o[pair].
@@ -78,9 +81,11 @@ hipError_t launch_moe_down(const void* a, const float* a_scale, const int32_t* p
                            const void* w_d, const float* s_d, int d, int F, molt_dtype wdt,
                            const int32_t* tiles, const int32_t* n_tiles, int max_tiles,
                            int tile_m, float* o, hipStream_t s);
-// row-major [rows, row_bytes] -> tiled layout (rows % 32 == 0, row_bytes % 128 == 0)
+// row-major [rows, row_bytes] -> tiled layout (row_bytes % 128 == 0), rows padded to a
+// multiple of 32 with zeros
 hipError_t launch_pack_tiled(const void* src, void* dst, long rows, long row_bytes, hipStream_t s);
-// tiled rows in padded expert order: row = src[pperm[row] / K_top], zeros for padding
+// tiled rows in padded expert order from tiled token rows: row = src[pperm[row] / K_top],
+// zeros for padding
 hipError_t launch_gather_tiled(const void* src, const int32_t* pperm, int K_top,
                                const int32_t* n_rows, long max_rows, long row_bytes, void* dst,
                                hipStream_t s);
@@ -88,9 +93,10 @@ int moe_tile_m(molt_dtype wdt, int T, int K, int E);
 
 // ------------------------------------------------------------- attention
 size_t attention_ws_bytes(int B, int k, int Hq, int Hkv, int D, int max_blocks);
+// out [T, Hq*D] row-major, or tiled (rows padded to 32 by the caller) with out_tiled
 hipError_t launch_paged_attention(const void* q, const void* kc, const void* vc, const int32_t* bt,
                                   const int32_t* ctx, int B, int k, int Hq, int Hkv, int D,
-                                  int max_blocks, molt_dtype dt, void* out, void* ws,
-                                  hipStream_t s);
+                                  int max_blocks, molt_dtype dt, void* out, bool out_tiled,
+                                  void* ws, hipStream_t s);
 
 }  // namespace molt

@@ -42,8 +42,12 @@ def max_abs(a, b):
 def tiled_layout(mat_bytes):
     """The library's tiled expert-weight layout, from its definition in include/molt.h
     (molt_pack_weights), written with numpy index arithmetic: mat_bytes [rows, row_bytes]
-    uint8 -> flat uint8 of the same size."""
+    uint8 -> flat uint8 of the size with rows padded (zeros) to a multiple of 32."""
     rows, rb = mat_bytes.shape
+    pad = (-rows) % 32
+    if pad:   # zero rows up to a multiple of 32
+        mat_bytes = np.concatenate([mat_bytes, np.zeros((pad, rb), np.uint8)])
+        rows += pad
     r = np.arange(rows)[:, None]
     j = np.arange(rb)[None, :]
     off = ((r // 32) * (rb // 128) + j // 128) * 4096 + ((j % 64) // 16) * 1024 \

@@ -103,7 +103,7 @@ def test_pack_validation(L):
     p, q = ctypes.c_void_p(0x1000), ctypes.c_void_p(0x2000)
     assert L.molt_pack_weights(None, q, 32, 128, None) == INVALID
     assert L.molt_pack_weights(p, p, 32, 128, None) == INVALID      # in place
-    assert L.molt_pack_weights(p, q, 48, 128, None) == INVALID      # rows % 32
+    assert L.molt_pack_weights(p, q, 32, 0, None) == INVALID        # row_bytes < 128
     assert L.molt_pack_weights(p, q, 32, 192, None) == INVALID      # row_bytes % 128
     assert L.molt_pack_weights(p, q, 0, 128, None) == INVALID
 

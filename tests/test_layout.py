@@ -30,7 +30,8 @@ def test_layout_is_a_tile_preserving_permutation():
 
 @pytest.mark.gpu
 @pytest.mark.parametrize("dtype,shape", [(torch.uint8, (2, 96, 256)), (torch.bfloat16, (4, 64, 320)),
-                                         (torch.float32, (1, 32, 96))])
+                                         (torch.float32, (1, 32, 96)), (torch.bfloat16, (40, 192)),
+                                         (torch.float32, (7, 64))])
 def test_pack_weights_matches_definition(lib, dtype, shape):
     g = torch.Generator().manual_seed(7)
     raw = torch.randint(0, 256, (int(np.prod(shape)) * torch.tensor([], dtype=dtype).element_size(),),
@@ -38,7 +39,9 @@ def test_pack_weights_matches_definition(lib, dtype, shape):
     w = raw.view(dtype).reshape(shape)
     packed = lib.pack_weights(w.cuda())
     torch.cuda.synchronize()
-    assert packed.shape == w.shape and packed.dtype == w.dtype
+    rows = int(np.prod(shape[:-1]))
+    want_shape = shape if rows % 32 == 0 else ((rows + 31) // 32 * 32, shape[-1])
+    assert tuple(packed.shape) == tuple(want_shape) and packed.dtype == w.dtype
     rb = shape[-1] * w.element_size()
     want = tiled_layout(raw.numpy().reshape(-1, rb))
     got = packed.cpu().contiguous().view(torch.uint8).numpy().ravel()
