@@ -47,51 +47,42 @@ MOLT_DEV floatx16_t mfma(const int32x8_t& a, const int32x8_t& b, const floatx16_
   return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, c, 0, 0, 0, 0, 0, 0);
 }
 
-// ---------------------------------------------------------------- weight-streaming GEMM
-// Expert GEMMs are HBM-bound at the verify step's row counts (tens of rows per expert),
-// and the dense projections nearly so at a few hundred rows: the weights must stream at
-// full bandwidth and be read once. Workgroup = BM rows (of
-// one expert) x 128 output columns; each of the 4 wavefronts owns 32 output columns (32
-// weight rows) and loads its weight fragments straight from global memory into MFMA
-// operand registers, kPD 128-byte K slices ahead; a weight element is used by exactly one
-// wavefront, so no LDS and no barrier is needed in the main loop. The activation rows
-// (shared by the 4 wavefronts, served from L2) are loaded per wavefront kPA slices ahead.
-// Both operands are in the tiled layout, so every load instruction reads 1 KB of one page:
-// with row-major operands each instruction touched 32 rows, and the address translation
-// requests, not HBM, set the pace. Tiles start at multiples of 32 rows (padded expert
-// order), so each 32-row block of A is one tile column of the tiled activation buffer.
+// ---------------------------------------------------------------- grouped expert GEMM
+// Expert GEMMs are HBM-bound at the verify step's row counts (tens of rows per expert):
+// the weights must stream at full bandwidth and be read once. Workgroup = BM rows of one
+// expert x 128 output columns; each of the 4 wavefronts owns 32 output columns (32 weight
+// rows) and loads its weight fragments straight from global memory into MFMA operand
+// registers, 4 K slices (128 bytes each) ahead; a weight element is used by exactly one
+// wavefront, so weights never touch LDS. The BM activation rows, shared by the 4
+// wavefronts, go through a double-buffered LDS ring: per slice each thread copies one
+// 16-byte chunk of each 4 KB activation block, loaded two slices ahead into registers; one
+// LDS-only barrier per slice (it does not wait for the weight loads in flight).
+// Both operands are in the tiled layout, so every global load instruction reads 1 KB of
+// one page (with row-major operands each instruction touched 32 rows, and the address
+// translation requests, not HBM, set the pace) and every LDS fragment read is a
+// contiguous 1 KB. Tiles start at multiples of 32 rows (padded expert order), so each
+// 32-row block of A is one tile column of the tiled activation buffer.
 struct Slice16 { int4 c[4]; };   // one lane's 64 bytes of a 32-row x 128-byte tile
 
 template <int BM, bool FP8, int MODE>
 __global__ __launch_bounds__(kThreads) void stream_gemm_kernel(GemmParams p) {
+  static_assert(MODE == kGateUp || MODE == kDown, "grouped modes");
   constexpr int MS = BM / 32;                        // 32-row MFMA tiles per wavefront
-  constexpr int kPD = 4;                             // weight slices in flight
-  constexpr int kPA = 2;                             // activation slices in flight
   constexpr int kElem = FP8 ? 1 : 2;
   __shared__ __attribute__((aligned(16))) float upbuf[MODE == kGateUp ? BM * 64 : 1];
 
   // Workgroup b runs on XCD b % 8. Each XCD takes one contiguous eighth of the live
-  // (m-tile, n-tile) pairs. Grouped: m-tile major, so the n-tiles of one row tile run back
-  // to back on one XCD and its activation tile is read from HBM once, then hits that XCD's
-  // L2. Dense: n-tile major, so each XCD reads its own eighth of the weights, and the row
-  // tiles sharing a weight tile run together.
-  const int total = (MODE == kDense ? p.n_mtiles : *p.n_tiles_live) * p.n_ntiles;
+  // (m-tile, n-tile) pairs, m-tile major: the n-tiles of one row tile run back to back on
+  // one XCD, so its activation tile is read from HBM once and then hits that XCD's L2.
+  const int total = *p.n_tiles_live * p.n_ntiles;
   const int chunk = (total + 7) / 8;
   const int k8 = blockIdx.x / 8;
   const int id = (blockIdx.x % 8) * chunk + k8;
   if (k8 >= chunk || id >= total) return;
-  int mt, nt, expert = 0, row0, row1;
-  if (MODE == kDense) {
-    nt = id / p.n_mtiles;
-    mt = id % p.n_mtiles;
-    row0 = mt * BM;
-    row1 = min(row0 + BM, p.M);
-  } else {
-    mt = id / p.n_ntiles;
-    nt = id % p.n_ntiles;
-    const int4 t = p.tiles[mt];
-    expert = t.x; row0 = t.y; row1 = t.z;             // row0 % 32 == 0
-  }
+  const int mt = id / p.n_ntiles;
+  const int nt = id % p.n_ntiles;
+  const int4 t = p.tiles[mt];
+  const int expert = t.x, row0 = t.y, row1 = t.z;     // row0 % 32 == 0
   const long RB = long(p.K) * kElem;                  // bytes per operand row
   const int nk = int(RB / kRowBytes);                 // 128-byte K slices
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
@@ -106,66 +97,85 @@ __global__ __launch_bounds__(kThreads) void stream_gemm_kernel(GemmParams p) {
     n0 = nt * kBN;
     wrow = long(expert) * p.N + n0 + 32 * wave;
   }
-  // dense: B's rows are padded to a multiple of 32; a wavefront past the last column block
-  // re-reads the last one and stores nothing
-  if (MODE == kDense && n0 + 32 * wave >= p.N) wrow = (p.N - 1) & ~31;
   const uint8_t* bsrc = static_cast<const uint8_t*>(p.B) + wrow * RB + lane * 16;
+  const int last_block = (row1 - 1) & ~31;
   const uint8_t* asrc[MS];
-  const int last_block = (row1 - 1) & ~31;            // 32-row blocks past the tile end
-#pragma unroll                                        // re-read its last one
+#pragma unroll
   for (int i = 0; i < MS; ++i)
-    asrc[i] = static_cast<const uint8_t*>(p.A) + long(min(row0 + 32 * i, last_block)) * RB + lane * 16;
-  auto ld = [](Slice16& f, const uint8_t* src) {
+    asrc[i] = static_cast<const uint8_t*>(p.A) + long(min(row0 + 32 * i, last_block)) * RB + threadIdx.x * 16;
+  __shared__ __attribute__((aligned(16))) uint8_t alds[2][MS * 4096];
+  int32x4_t st0[MS], st1[MS];
+  Slice16 wb[4];
+  auto wld = [&](Slice16& f, int kb) __attribute__((always_inline)) {
+    const uint8_t* src = bsrc + long(min(kb, nk - 1)) * 4096;
 #pragma unroll
     for (int c = 0; c < 4; ++c) f.c[c] = *reinterpret_cast<const int4*>(src + 1024 * c);
   };
-  Slice16 wb[kPD];
-  Slice16 ab[kPA][MS];
-#pragma unroll
-  for (int s = 0; s < kPD; ++s) if (s < nk) ld(wb[s], bsrc + long(s) * 4096);
-#pragma unroll
-  for (int s = 0; s < kPA; ++s) if (s < nk)
-#pragma unroll
-    for (int i = 0; i < MS; ++i) ld(ab[s][i], asrc[i] + long(s) * 4096);
+#define MOLT_GLOAD(ST, KB)                                                            \
+  {                                                                                   \
+    const long off_ = long(min((KB), nk - 1)) * 4096;                                 \
+    _Pragma("unroll") for (int b_ = 0; b_ < MS; ++b_)                                 \
+        ST[b_] = *reinterpret_cast<const int32x4_t*>(asrc[b_] + off_);                \
+  }
+#define MOLT_SSTORE(ST, BUF)                                                          \
+  {                                                                                   \
+    _Pragma("unroll") for (int b_ = 0; b_ < MS; ++b_)                                 \
+        *reinterpret_cast<int32x4_t*>(&alds[BUF][b_ * 4096 + threadIdx.x * 16]) = ST[b_]; \
+  }
   floatx16_t acc[MS];
 #pragma unroll
   for (int i = 0; i < MS; ++i)
 #pragma unroll
     for (int e = 0; e < 16; ++e) acc[i][e] = 0.f;
-  auto slice = [&](const Slice16& w, const Slice16 (&a)[MS]) {
-    if (!FP8) {
+  MOLT_GLOAD(st0, 0);
+  MOLT_GLOAD(st1, 1);
 #pragma unroll
-      for (int s = 0; s < 4; ++s) {
-        const bf16x8_t bv = *reinterpret_cast<const bf16x8_t*>(&w.c[s]);
-#pragma unroll
-        for (int i = 0; i < MS; ++i) acc[i] = mfma(*reinterpret_cast<const bf16x8_t*>(&a[i].c[s]), bv, acc[i]);
-      }
-    } else {
-#pragma unroll
-      for (int s = 0; s < 2; ++s) {
-        const int4 w0 = w.c[2 * s], w1 = w.c[2 * s + 1];
-        const int32x8_t bv = int32x8_t{w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};
-#pragma unroll
-        for (int i = 0; i < MS; ++i) {
-          const int4 lo = a[i].c[2 * s], hi = a[i].c[2 * s + 1];
-          acc[i] = mfma(int32x8_t{lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w}, bv, acc[i]);
-        }
-      }
-    }
-  };
-  for (int kb0 = 0; kb0 < nk; kb0 += kPD) {
-#pragma unroll
-    for (int s = 0; s < kPD; ++s) {
-      const int kb = kb0 + s;
-      if (kb < nk) {
-        slice(wb[s], ab[s % kPA]);
-        if (kb + kPD < nk) ld(wb[s], bsrc + long(kb + kPD) * 4096);
-        if (kb + kPA < nk)
-#pragma unroll
-          for (int i = 0; i < MS; ++i) ld(ab[s % kPA][i], asrc[i] + long(kb + kPA) * 4096);
-      }
-    }
+  for (int s = 0; s < 4; ++s) wld(wb[s], s);
+  MOLT_SSTORE(st0, 0);
+  MOLT_GLOAD(st0, 2);
+  lds_barrier();
+  // Step over slice k: LDS buffer U holds its activations, weight slot W its weights,
+  // register slot ST_NEXT slice k + 1 (the other slot k + 2). It computes, refills W with
+  // slice k + 4, stores slice k + 1 into buffer 1 - U (last read before the previous
+  // barrier) and refills ST_NEXT with slice k + 3. Loads past the end re-read the last slice.
+#define MOLT_STEP(U, ST_NEXT, W, K)                                                                 \
+  {                                                                                                  \
+    const uint8_t* base_ = alds[U] + lane * 16;                                                      \
+    if (!FP8) {                                                                                      \
+      _Pragma("unroll") for (int c = 0; c < 4; ++c) {                                                \
+        const bf16x8_t bv = *reinterpret_cast<const bf16x8_t*>(&wb[W].c[c]);                         \
+        _Pragma("unroll") for (int i = 0; i < MS; ++i) acc[i] =                                      \
+            mfma(*reinterpret_cast<const bf16x8_t*>(base_ + i * 4096 + c * 1024), bv, acc[i]);       \
+      }                                                                                              \
+    } else {                                                                                         \
+      _Pragma("unroll") for (int c = 0; c < 2; ++c) {                                                \
+        const int4 w0 = wb[W].c[2 * c], w1 = wb[W].c[2 * c + 1];                                     \
+        const int32x8_t bv = int32x8_t{w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};             \
+        _Pragma("unroll") for (int i = 0; i < MS; ++i) {                                             \
+          const int32x4_t lo = *reinterpret_cast<const int32x4_t*>(base_ + i * 4096 + 2 * c * 1024); \
+          const int32x4_t hi = *reinterpret_cast<const int32x4_t*>(base_ + i * 4096 + (2 * c + 1) * 1024); \
+          acc[i] = mfma(int32x8_t{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]}, bv, acc[i]); \
+        }                                                                                            \
+      }                                                                                              \
+    }                                                                                                \
+    wld(wb[W], (K) + 4);                                                                             \
+    MOLT_SSTORE(ST_NEXT, 1 - (U));                                                                   \
+    MOLT_GLOAD(ST_NEXT, (K) + 3);                                                                    \
+    lds_barrier();                                                                                   \
   }
+  int kb = 0;
+  for (; kb + 3 < nk; kb += 4) {
+    MOLT_STEP(0, st1, 0, kb);
+    MOLT_STEP(1, st0, 1, kb + 1);
+    MOLT_STEP(0, st1, 2, kb + 2);
+    MOLT_STEP(1, st0, 3, kb + 3);
+  }
+  if (kb < nk) MOLT_STEP(0, st1, 0, kb);
+  if (kb + 1 < nk) MOLT_STEP(1, st0, 1, kb + 1);
+  if (kb + 2 < nk) MOLT_STEP(0, st1, 2, kb + 2);
+#undef MOLT_STEP
+#undef MOLT_SSTORE
+#undef MOLT_GLOAD
   // accumulator element e of lane (lcol, lgrp) in tile i: row 32 i + 8 (e / 4) + 4 lgrp + e % 4
   const int lcol = lane % 32, lgrp = lane / 32;
   if (MODE == kGateUp) {
@@ -201,18 +211,6 @@ __global__ __launch_bounds__(kThreads) void stream_gemm_kernel(GemmParams p) {
                                        tiled_offset(grow, 2L * (n0 + c), hrb)) = f32_to_bf16(silu(g) * u);
         }
     }
-  } else if (MODE == kDense) {
-    const int c = n0 + 32 * wave + lcol;
-    if (c >= p.N) return;
-#pragma unroll
-    for (int i = 0; i < MS; ++i)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const int grow = row0 + 32 * i + 8 * (e / 4) + 4 * lgrp + (e % 4);
-        if (grow >= row1) continue;
-        float* dst = static_cast<float*>(p.C) + long(grow) * p.ldc + c;
-        *dst = p.accumulate ? *dst + acc[i][e] : acc[i][e];
-      }
   } else {
     // per-pair expert output, f32, row = pair index (token * K + slot)
     const int c = n0 + 32 * wave + lcol;

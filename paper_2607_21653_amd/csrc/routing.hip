@@ -9,8 +9,8 @@
 // max-reduction select the experts in descending order.
 //
 // permute_kernel: one 1024-thread workgroup. Pass 1 counts pairs per expert (LDS
-// integer atomics: the totals are order-free), a serial scan gives offsets and the
-// grouped-GEMM tile table. Pass 2 walks the T*K pairs in (token, slot) order, 1024 at
+// integer atomics: the totals are order-free); wavefront prefix sums over the experts give
+// offsets and the grouped-GEMM tile table. Pass 2 walks the T*K pairs in (token, slot) order, 1024 at
 // a time: inside a wavefront, lanes holding the same expert find each other with 8
 // ballots over the expert id bits; the rank of a lane among them is a popcount of the
 // lower lanes; across the 16 wavefronts an exclusive LDS prefix per expert adds the
@@ -106,6 +106,8 @@ __global__ __launch_bounds__(kPermThreads) void permute_kernel(
   __shared__ int poff[kMaxE + 1];
   __shared__ int run[kMaxE];
   __shared__ int wc[kPermWaves][kMaxE];
+  __shared__ int wsum[3][kMaxE / kWave];
+  __shared__ int wtmp[3][kMaxE];
   __shared__ int s_nt;
   const int tid = threadIdx.x;
   const int wave = tid / kWave, lane = tid % kWave;
@@ -113,21 +115,49 @@ __global__ __launch_bounds__(kPermThreads) void permute_kernel(
   __syncthreads();
   for (int p = tid; p < P; p += kPermThreads) atomicAdd(&cnt[ids[p]], 1);
   __syncthreads();
-  if (tid == 0) {
-    off[0] = 0;
-    poff[0] = 0;
-    int nt = 0;
-    for (int e = 0; e < E; ++e) {
-      off[e + 1] = off[e] + cnt[e];
-      poff[e + 1] = poff[e] + (cnt[e] + 31) / 32 * 32;
-      for (int m0 = 0; m0 < cnt[e] && nt < max_tiles; m0 += tile_m)
-        tiles[nt++] = make_int4(e, poff[e] + m0, poff[e] + min(m0 + tile_m, cnt[e]), 0);
+  // exclusive prefix sums over experts (threads 0..255, one expert each) of the count, the
+  // padded count and the tile count: offsets, padded offsets, first tile of each expert
+  int tile0 = 0;
+  if (tid < kMaxE) {
+    const int c = tid < E ? cnt[tid] : 0;
+    int v[3] = {c, (c + 31) / 32 * 32, (c + tile_m - 1) / tile_m};
+#pragma unroll
+    for (int q = 0; q < 3; ++q) {
+#pragma unroll
+      for (int o = 1; o < kWave; o <<= 1) {
+        const int u = __shfl_up(v[q], o, kWave);
+        if (lane >= o) v[q] += u;
+      }
+      if (lane == kWave - 1) wsum[q][wave] = v[q];
     }
-    s_nt = nt;
-    *n_tiles = nt;
-    *n_padded = poff[E];
+    wtmp[0][tid] = v[0];
+    wtmp[1][tid] = v[1];
+    wtmp[2][tid] = v[2];
   }
   __syncthreads();
+  if (tid < kMaxE) {
+    int add[3] = {0, 0, 0};
+    for (int w2 = 0; w2 < wave; ++w2)
+#pragma unroll
+      for (int q = 0; q < 3; ++q) add[q] += wsum[q][w2];
+    const int c = tid < E ? cnt[tid] : 0;
+    const int tn = (c + tile_m - 1) / tile_m;
+    off[tid + 1] = wtmp[0][tid] + add[0];
+    poff[tid + 1] = wtmp[1][tid] + add[1];
+    tile0 = wtmp[2][tid] + add[2] - tn;
+    if (tid == 0) { off[0] = 0; poff[0] = 0; }
+    if (tid == E - 1) {
+      s_nt = min(tile0 + tn, max_tiles);
+      *n_tiles = s_nt;
+      *n_padded = poff[E];
+    }
+  }
+  __syncthreads();
+  if (tid < E) {                                       // this expert's tiles
+    const int c = cnt[tid];
+    for (int m0 = 0, i = tile0; m0 < c && i < max_tiles; m0 += tile_m, ++i)
+      tiles[i] = make_int4(tid, poff[tid] + m0, poff[tid] + min(m0 + tile_m, c), 0);
+  }
   for (int i = tid; i < E * 32; i += kPermThreads) {   // padding slots of each expert
     const int e = i / 32, r = cnt[e] + i % 32;
     if (r < poff[e + 1] - poff[e]) pperm[poff[e] + r] = -1;
