@@ -62,7 +62,7 @@ MOLT_DEV floatx16_t mfma(const int32x8_t& a, const int32x8_t& b, const floatx16_
 // translation requests, not HBM, set the pace) and every LDS fragment read is a
 // contiguous 1 KB. Tiles start at multiples of 32 rows (padded expert order), so each
 // 32-row block of A is one tile column of the tiled activation buffer.
-struct Slice16 { int4 c[4]; };   // one lane's 64 bytes of a 32-row x 128-byte tile
+struct Slice16 { int32x4_t c[4]; };   // one lane's 64 bytes of a 32-row x 128-byte tile
 
 template <int BM, bool FP8, int MODE>
 __global__ __launch_bounds__(kThreads) void stream_gemm_kernel(GemmParams p) {
@@ -106,10 +106,11 @@ __global__ __launch_bounds__(kThreads) void stream_gemm_kernel(GemmParams p) {
   __shared__ __attribute__((aligned(16))) uint8_t alds[2][MS * 4096];
   int32x4_t st0[MS], st1[MS];
   Slice16 wb[4];
+  // weights are read once per step: nontemporal loads
   auto wld = [&](Slice16& f, int kb) __attribute__((always_inline)) {
     const uint8_t* src = bsrc + long(min(kb, nk - 1)) * 4096;
 #pragma unroll
-    for (int c = 0; c < 4; ++c) f.c[c] = *reinterpret_cast<const int4*>(src + 1024 * c);
+    for (int c = 0; c < 4; ++c) f.c[c] = __builtin_nontemporal_load(reinterpret_cast<const int32x4_t*>(src + 1024 * c));
   };
 #define MOLT_GLOAD(ST, KB)                                                            \
   {                                                                                   \
@@ -149,8 +150,8 @@ __global__ __launch_bounds__(kThreads) void stream_gemm_kernel(GemmParams p) {
       }                                                                                              \
     } else {                                                                                         \
       _Pragma("unroll") for (int c = 0; c < 2; ++c) {                                                \
-        const int4 w0 = wb[W].c[2 * c], w1 = wb[W].c[2 * c + 1];                                     \
-        const int32x8_t bv = int32x8_t{w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};             \
+        const int32x4_t w0 = wb[W].c[2 * c], w1 = wb[W].c[2 * c + 1];                                \
+        const int32x8_t bv = int32x8_t{w0[0], w0[1], w0[2], w0[3], w1[0], w1[1], w1[2], w1[3]};     \
         _Pragma("unroll") for (int i = 0; i < MS; ++i) {                                             \
           const int32x4_t lo = *reinterpret_cast<const int32x4_t*>(base_ + i * 4096 + 2 * c * 1024); \
           const int32x4_t hi = *reinterpret_cast<const int32x4_t*>(base_ + i * 4096 + (2 * c + 1) * 1024); \
