@@ -235,22 +235,24 @@ int moe_shape_ok(int T, int d, int E, int K, int F, molt_dtype act, molt_dtype w
 
 // Enqueues the MoE layer on normalised input x (act dtype, tiled, rows padded to 32; xq/xs =
 // its tiled fp8 codes when the caller already quantised them). Router and expert weights
-// tiled. out = sum (accumulate: out += sum).
+// tiled. With out: out = sum (accumulate: out += sum); without, the per-pair expert outputs
+// m.o and route weights m.w are left for the caller to combine.
 hipError_t run_moe(const MoeWs& m, const void* x, const uint8_t* xq, const float* xs,
                    const void* w_router, const float* bias, const void* w_gu, const void* w_d,
                    const float* s_gu, const float* s_d, int T, int d, int E, int K, int F,
                    molt_dtype act, molt_dtype wdt, const int32_t* replay, float* out,
                    bool accumulate, hipStream_t s) {
   hipError_t e;
+  int nparts = 1;
   {
     ProfScope ps(MOLT_PROF_PROJECTIONS, s);
-    if ((e = molt::launch_gemm(x, w_router, m.g, T, E, d, act, false, m.part, m.part_elems, s)) !=
-        hipSuccess)
+    if ((e = molt::launch_gemm(x, w_router, m.g, T, E, d, act, false, m.part, m.part_elems, s,
+                               &nparts)) != hipSuccess)
       return e;
   }
-  if ((e = molt::launch_route(m.g, bias, replay, T, E, K, m.ids, m.w, m.counts, m.offsets, m.perm,
-                              m.inv, m.pperm, m.n_padded, m.tile_m, m.tiles, m.max_tiles,
-                              m.n_tiles, s)) != hipSuccess)
+  if ((e = molt::launch_route(nparts > 1 ? m.part : m.g, nparts, bias, replay, T, E, K, m.ids, m.w,
+                              m.counts, m.offsets, m.perm, m.inv, m.pperm, m.n_padded, m.tile_m,
+                              m.tiles, m.max_tiles, m.n_tiles, s)) != hipSuccess)
     return e;
   const bool fp8 = wdt == MOLT_FP8_E4M3;
   if (fp8 && xq == nullptr) {
@@ -283,6 +285,7 @@ hipError_t run_moe(const MoeWs& m, const void* x, const uint8_t* xq, const float
         hipSuccess)
       return e;
   }
+  if (out == nullptr) return hipSuccess;
   return molt::launch_combine(m.o, m.w, T, K, d, out, accumulate, s);
 }
 
@@ -451,6 +454,7 @@ int model_ok(const molt_model* m, const molt_kv* kv, int B, int k, bool need_hea
 struct DecWs {
   void* y; uint8_t* yq; float* ys; float* qkv; void* q; void* attn; void* attn_ws; MoeWs moe;
   float* part; long part_elems;   // split-K partial sums of the QKV and O projections
+  void* rope;                     // RoPE cos/sin of the step's positions, [T, D/2] f64 pairs
 };
 
 DecWs carve_dec(molt::Carver& c, const molt_model* m, int B, int k, int max_blocks) {
@@ -474,24 +478,31 @@ DecWs carve_dec(molt::Carver& c, const molt_model* m, int B, int k, int max_bloc
   const long po = gemm_part_elems(int(T), d, Hq * D, m->dtype);
   w.part_elems = pq > po ? pq : po;
   w.part = c.take<float>(w.part_elems);
+  w.rope = c.take<double>(T * D);
   return w;
 }
 
+// All layers on the residual stream x. With final_g, the last layer's MoE combine is fused
+// with the final RMSNorm, whose tiled output goes to final_y.
 hipError_t run_decoder(const DecWs& w, const molt_model* m, const molt_kv* kv, int B, int k,
-                       float* x, int32_t* routes, hipStream_t s) {
+                       float* x, int32_t* routes, const float* final_g, void* final_y,
+                       hipStream_t s) {
   const int T = B * (k + 1);
   const int d = m->d_model, D = m->head_dim, Hq = m->n_q_heads, Hkv = m->n_kv_heads;
-  const int K = m->top_k;
+  const int K = m->top_k, L = m->n_layers;
+  const bool fp8 = m->expert_dtype == MOLT_FP8_E4M3;
   hipError_t e = hipSuccess;
 #define RUN(call) do { if ((e = (call)) != hipSuccess) return e; } while (0)
-  for (int l = 0; l < m->n_layers; ++l) {
-    RUN(molt::launch_rmsnorm(x, m->attn_norm[l], T, d, m->rms_eps, m->dtype, w.y, nullptr, nullptr, s));
+  RUN(molt::launch_rope_table(kv->context_lens, B, k, D, m->rope_theta, w.rope, s));
+  RUN(molt::launch_residual_norm(x, nullptr, 0, nullptr, nullptr, 0, m->attn_norm[0], T, d,
+                                 m->rms_eps, m->dtype, w.y, nullptr, nullptr, s));
+  for (int l = 0; l < L; ++l) {
     {
       ProfScope ps(MOLT_PROF_PROJECTIONS, s);
       RUN(molt::launch_gemm(w.y, m->w_qkv[l], w.qkv, T, (Hq + 2 * Hkv) * D, d, m->dtype, false,
                             w.part, w.part_elems, s));
     }
-    RUN(molt::launch_rope_kv_write(w.qkv, B, k, Hq, Hkv, D, m->rope_theta, kv->context_lens,
+    RUN(molt::launch_rope_kv_write(w.qkv, B, k, Hq, Hkv, D, w.rope, kv->context_lens,
                                    kv->block_tables, kv->max_blocks_per_seq, kv->num_blocks,
                                    m->dtype, w.q, kv->k_cache[l], kv->v_cache[l], s));
     {
@@ -500,19 +511,26 @@ hipError_t run_decoder(const DecWs& w, const molt_model* m, const molt_kv* kv, i
                                        kv->context_lens, B, k, Hq, Hkv, D, kv->max_blocks_per_seq,
                                        m->dtype, w.attn, true, w.attn_ws, s));
     }
+    int np = 1;   // O projection: accumulate into x, or leave split-K partials
     {
       ProfScope ps(MOLT_PROF_PROJECTIONS, s);
       RUN(molt::launch_gemm(w.attn, m->w_o[l], x, T, d, Hq * D, m->dtype, true, w.part,
-                            w.part_elems, s));
+                            w.part_elems, s, &np));
     }
-    const bool fp8 = m->expert_dtype == MOLT_FP8_E4M3;
-    RUN(molt::launch_rmsnorm(x, m->moe_norm[l], T, d, m->rms_eps, m->dtype, w.y,
-                             fp8 ? w.yq : nullptr, fp8 ? w.ys : nullptr, s));
+    // x += O partials; y = RMSNorm(x) * moe_norm (+ fp8 codes)
+    RUN(molt::launch_residual_norm(x, np > 1 ? w.part : nullptr, np > 1 ? np : 0, nullptr, nullptr,
+                                   0, m->moe_norm[l], T, d, m->rms_eps, m->dtype, w.y,
+                                   fp8 ? w.yq : nullptr, fp8 ? w.ys : nullptr, s));
     RUN(run_moe(w.moe, w.y, fp8 ? w.yq : nullptr, fp8 ? w.ys : nullptr, m->w_router[l],
                 m->router_bias ? m->router_bias[l] : nullptr, m->w_gate_up[l], m->w_down[l],
                 fp8 ? m->s_gate_up[l] : nullptr, fp8 ? m->s_down[l] : nullptr, T, d,
-                m->n_experts, K, m->d_ff, m->dtype, m->expert_dtype, nullptr, x, true, s));
+                m->n_experts, K, m->d_ff, m->dtype, m->expert_dtype, nullptr, nullptr, false, s));
     if (routes) RUN(copy_out(routes + size_t(l) * T * K, w.moe.ids, size_t(T) * K * 4, s));
+    // x += MoE combine; then the next layer's attention norm (or the final norm)
+    const bool last = l + 1 == L;
+    RUN(molt::launch_residual_norm(x, nullptr, 0, w.moe.o, w.moe.w, K,
+                                   last ? final_g : m->attn_norm[l + 1], T, d, m->rms_eps,
+                                   m->dtype, last ? final_y : w.y, nullptr, nullptr, s));
   }
 #undef RUN
   return e;
@@ -537,7 +555,8 @@ int molt_decoder_forward(const molt_model* m, const molt_kv* kv, int B, int k, f
     return r;
   molt::Carver c(workspace, workspace_bytes);
   DecWs w = carve_dec(c, m, B, k, kv->max_blocks_per_seq);
-  return hip_status(run_decoder(w, m, kv, B, k, x, out_routes, reinterpret_cast<hipStream_t>(stream)),
+  return hip_status(run_decoder(w, m, kv, B, k, x, out_routes, nullptr, nullptr,
+                                reinterpret_cast<hipStream_t>(stream)),
                     "molt_decoder_forward");
 }
 
@@ -580,10 +599,7 @@ int molt_verify_step(const molt_model* m, const molt_kv* kv, int B, int k, const
   float* logits = out_logits ? out_logits : w.logits;
   const int T = B * (k + 1);
   hipError_t e = molt::launch_embed(m->embed, tokens, T, m->d_model, m->vocab, m->dtype, w.x, s);
-  if (e == hipSuccess) e = run_decoder(w.dec, m, kv, B, k, w.x, out_routes, s);
-  if (e == hipSuccess)
-    e = molt::launch_rmsnorm(w.x, m->final_norm, T, m->d_model, m->rms_eps, m->dtype, w.yf,
-                             nullptr, nullptr, s);
+  if (e == hipSuccess) e = run_decoder(w.dec, m, kv, B, k, w.x, out_routes, m->final_norm, w.yf, s);
   if (e == hipSuccess) {
     ProfScope ps(MOLT_PROF_LM_HEAD, s);
     e = molt::launch_gemm(w.yf, m->lm_head, logits, T, m->vocab, m->d_model, m->dtype, false,

@@ -31,19 +31,46 @@ __global__ __launch_bounds__(kThreads) void embed_kernel(const void* __restrict_
     x[long(t) * d + i] = ok ? load_act(table, long(tok) * d + i, dt) : 0.f;
 }
 
-// y = x / sqrt(mean(x^2) + eps) * g rounded to dt; with yq, also the per-row fp8 code
-// of y (s = amax|y| / 448, code = e4m3(y / s)). y and yq are GEMM operands: tiled layout.
-__global__ __launch_bounds__(kThreads) void rmsnorm_kernel(const float* __restrict__ x,
-                                                           const float* __restrict__ g, int d,
-                                                           float eps, molt_dtype dt,
-                                                           void* __restrict__ y,
-                                                           uint8_t* __restrict__ yq,
-                                                           float* __restrict__ ys) {
+// Residual update and RMSNorm of token row t, fused:
+//   x[t] += part[0][t] + part[1][t] + ...   (split-K partial sums of the O projection, in
+//                                            split order; nparts = 0: none)
+//   x[t] += sum_j w[t, j] * o[t * K + j]     (MoE combine, slot order; o = NULL: none)
+//   y = x[t] / sqrt(mean(x[t]^2) + eps) * g  rounded to dt, tiled (g = NULL: no norm)
+// With yq, also the per-row fp8 code of y (s = amax|y| / 448, code = e4m3(y / s)).
+__global__ __launch_bounds__(kThreads) void residual_norm_kernel(
+    float* __restrict__ x, const float* __restrict__ part, int nparts, long part_stride,
+    const float* __restrict__ o, const float* __restrict__ w, int K, const float* __restrict__ g,
+    int d, float eps, molt_dtype dt, void* __restrict__ y, uint8_t* __restrict__ yq,
+    float* __restrict__ ys) {
   __shared__ float red[kThreads / kWave];
   const int t = blockIdx.x;
-  const float* xr = x + long(t) * d;
+  float* xr = x + long(t) * d;
   float ss = 0.f;
-  for (int i = threadIdx.x; i < d; i += kThreads) ss += xr[i] * xr[i];
+  // 4 consecutive elements per thread step (d % 4 == 0); the loops over splits and slots
+  // are unrolled so that their loads issue together
+  for (int i = threadIdx.x * 4; i < d; i += kThreads * 4) {
+    float4 v = *reinterpret_cast<const float4*>(xr + i);
+    if (nparts > 0 || o) {
+#pragma unroll 4
+      for (int s = 0; s < nparts; ++s) {
+        const float4 q = *reinterpret_cast<const float4*>(part + s * part_stride + long(t) * d + i);
+        v.x += q.x; v.y += q.y; v.z += q.z; v.w += q.w;
+      }
+      if (o) {
+        float4 a = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll 8
+        for (int j = 0; j < K; ++j) {
+          const float wj = w[long(t) * K + j];
+          const float4 q = *reinterpret_cast<const float4*>(o + (long(t) * K + j) * d + i);
+          a.x += wj * q.x; a.y += wj * q.y; a.z += wj * q.z; a.w += wj * q.w;
+        }
+        v.x += a.x; v.y += a.y; v.z += a.z; v.w += a.w;
+      }
+      *reinterpret_cast<float4*>(xr + i) = v;
+    }
+    ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+  }
+  if (g == nullptr) return;
   ss = block_sum<kThreads / kWave, float>(ss, red);
   const float r = 1.0f / sqrtf(ss / float(d) + eps);
   float amax = 0.f;
@@ -107,25 +134,32 @@ __global__ __launch_bounds__(kThreads) void quant_rows_tiled_kernel(
   if (lane == 0) scale[r] = s;
 }
 
-// RoPE on q and k of token t = b*(1+k)+j at position ctx[b]+j (rotate-half pairs
-// (i, i+D/2), inverse frequency theta^(-2i/D), angle and rotation in f64), then
+// RoPE angle table of the step: token t = b*(1+k)+j sits at position ctx[b]+j; pair i
+// (i, i+D/2) turns by position * theta^(-2i/D); cos and sin evaluated in f64, once per step
+// for all layers. table[t][i] = {cos, sin}.
+__global__ __launch_bounds__(kThreads) void rope_table_kernel(const int32_t* __restrict__ ctx, int k,
+                                                              int D, float theta,
+                                                              double2* __restrict__ table) {
+  const int t = blockIdx.x;
+  const long pos = long(ctx[t / (k + 1)]) + t % (k + 1);
+  for (int i = threadIdx.x; i < D / 2; i += kThreads) {
+    const double inv_freq = pow(double(theta), -2.0 * double(i) / double(D));
+    const double ang = double(pos) * inv_freq;
+    table[long(t) * (D / 2) + i] = make_double2(cos(ang), sin(ang));
+  }
+}
+
+// RoPE on q and k of token t (rotation in f64 with the step's table), then
 // q -> q_out[t, Hq, D]; k -> K cache slot; v -> V cache slot (transposed layout).
 __global__ __launch_bounds__(kThreads) void rope_kv_kernel(
-    const float* __restrict__ qkv, int k, int Hq, int Hkv, int D, float theta,
+    const float* __restrict__ qkv, int k, int Hq, int Hkv, int D, const double2* __restrict__ table,
     const int32_t* __restrict__ ctx, const int32_t* __restrict__ bt, int max_blocks, int num_blocks,
     molt_dtype dt, void* __restrict__ q_out, void* __restrict__ kc, void* __restrict__ vc) {
-  __shared__ double cs[2][128 / 2 * 2];  // cos, sin per pair (D <= 256)
   const int t = blockIdx.x;
   const int b = t / (k + 1), j = t % (k + 1);
   const long pos = long(ctx[b]) + j;
   const int half = D / 2;
-  for (int i = threadIdx.x; i < half; i += kThreads) {
-    const double inv_freq = pow(double(theta), -2.0 * double(i) / double(D));
-    const double ang = double(pos) * inv_freq;
-    cs[0][i] = cos(ang);
-    cs[1][i] = sin(ang);
-  }
-  __syncthreads();
+  const double2* cs = table + long(t) * half;
   const int width = (Hq + 2 * Hkv) * D;
   const float* row = qkv + long(t) * width;
   const int blk = bt[long(b) * max_blocks + pos / 16];
@@ -135,8 +169,9 @@ __global__ __launch_bounds__(kThreads) void rope_kv_kernel(
   for (int w = threadIdx.x; w < (Hq + Hkv) * half; w += kThreads) {
     const int h = w / half, i = w % half;
     const double a = row[h * D + i], c = row[h * D + i + half];
-    const float lo = float(a * cs[0][i] - c * cs[1][i]);
-    const float hi = float(c * cs[0][i] + a * cs[1][i]);
+    const double2 r = cs[i];
+    const float lo = float(a * r.x - c * r.y);
+    const float hi = float(c * r.x + a * r.y);
     if (h < Hq) {
       store_act(q_out, (long(t) * Hq + h) * D + i, lo, dt);
       store_act(q_out, (long(t) * Hq + h) * D + i + half, hi, dt);
@@ -185,18 +220,28 @@ hipError_t launch_embed(const void* table, const int32_t* tokens, int T, int d, 
   return hipGetLastError();
 }
 
-hipError_t launch_rmsnorm(const float* x, const float* g, int T, int d, float eps, molt_dtype dt,
-                          void* y, uint8_t* yq, float* ys, hipStream_t s) {
-  rmsnorm_kernel<<<T, kThreads, 0, s>>>(x, g, d, eps, dt, y, yq, ys);
+hipError_t launch_residual_norm(float* x, const float* part, int nparts, const float* o,
+                                const float* w, int K, const float* g, int T, int d, float eps,
+                                molt_dtype dt, void* y, uint8_t* yq, float* ys, hipStream_t s) {
+  residual_norm_kernel<<<T, kThreads, 0, s>>>(x, part, nparts, long(T) * d, o, w, K, g, d, eps, dt,
+                                              y, yq, ys);
+  return hipGetLastError();
+}
+
+hipError_t launch_rope_table(const int32_t* ctx, int B, int k, int D, float theta, void* table,
+                             hipStream_t s) {
+  rope_table_kernel<<<B * (k + 1), kThreads, 0, s>>>(ctx, k, D, theta, static_cast<double2*>(table));
   return hipGetLastError();
 }
 
 hipError_t launch_rope_kv_write(const float* qkv, int B, int k, int Hq, int Hkv, int D,
-                                float theta, const int32_t* ctx, const int32_t* bt, int max_blocks,
-                                int num_blocks, molt_dtype dt, void* q_out, void* k_cache,
-                                void* v_cache, hipStream_t s) {
-  rope_kv_kernel<<<B * (k + 1), kThreads, 0, s>>>(qkv, k, Hq, Hkv, D, theta, ctx, bt, max_blocks,
-                                                   num_blocks, dt, q_out, k_cache, v_cache);
+                                const void* table, const int32_t* ctx, const int32_t* bt,
+                                int max_blocks, int num_blocks, molt_dtype dt, void* q_out,
+                                void* k_cache, void* v_cache, hipStream_t s) {
+  rope_kv_kernel<<<B * (k + 1), kThreads, 0, s>>>(qkv, k, Hq, Hkv, D,
+                                                   static_cast<const double2*>(table), ctx, bt,
+                                                   max_blocks, num_blocks, dt, q_out, k_cache,
+                                                   v_cache);
   return hipGetLastError();
 }
 

@@ -477,7 +477,9 @@ GemmPlan gemm_plan(int M, int N, int K, long part_elems) {
 }
 
 hipError_t launch_gemm(const void* A, const void* Bw, float* C, int M, int N, int K, molt_dtype dt,
-                       bool accumulate, float* part, long part_elems, hipStream_t s) {
+                       bool accumulate, float* part, long part_elems, hipStream_t s,
+                       int* splits_out) {
+  if (splits_out) *splits_out = 1;
   GemmParams p{};
   p.A = A; p.B = Bw; p.C = C; p.M = M; p.N = N; p.K = K; p.ldc = N;
   p.accumulate = accumulate;
@@ -493,7 +495,9 @@ hipError_t launch_gemm(const void* A, const void* Bw, float* C, int M, int N, in
   const int grid = (p.n_mtiles * p.n_ntiles * g.splits + 7) / 8 * 8;
   if (g.bm == 64) lds_gemm_kernel<64><<<grid, kThreads, 0, s>>>(p, part, g.splits);
   else lds_gemm_kernel<128><<<grid, kThreads, 0, s>>>(p, part, g.splits);
-  if (g.splits > 1) {
+  if (g.splits > 1 && splits_out) {
+    *splits_out = g.splits;         // the caller adds part[0 .. splits) (in order) into C
+  } else if (g.splits > 1) {
     const long n = long(M) * N;
     splitk_reduce_kernel<<<(n + kThreads - 1) / kThreads, kThreads, 0, s>>>(part, g.splits, n, C,
                                                                              accumulate);

@@ -34,14 +34,20 @@ hipError_t launch_spec_accept(const float* logits, const float* q, const int32_t
 // ------------------------------------------------------------- elementwise
 hipError_t launch_embed(const void* table, const int32_t* tokens, int T, int d, int V,
                         molt_dtype dt, float* x, hipStream_t s);
-// y = rmsnorm(x) * g in act dtype, tiled layout (rows padded to 32 by the caller's
-// allocation); optional fp8 row quantisation of y (tiled codes, per-row scales)
-hipError_t launch_rmsnorm(const float* x, const float* g, int T, int d, float eps, molt_dtype dt,
-                          void* y, uint8_t* yq, float* yq_scale, hipStream_t s);
+// x[t] += sum of nparts split-K partials (part[s * T * d ..], split order) and, with o, the
+// MoE combine sum_j w[t, j] o[t * K + j]; then with g: y = rmsnorm(x) * g in act dtype,
+// tiled layout (rows padded to 32 by the caller's allocation), optionally with its fp8
+// row codes (tiled) and scales
+hipError_t launch_residual_norm(float* x, const float* part, int nparts, const float* o,
+                                const float* w, int K, const float* g, int T, int d, float eps,
+                                molt_dtype dt, void* y, uint8_t* yq, float* ys, hipStream_t s);
+// RoPE cos/sin of the step's B*(1+k) positions (f64 pairs, [T, D/2]), shared by all layers
+hipError_t launch_rope_table(const int32_t* ctx, int B, int k, int D, float theta, void* table,
+                             hipStream_t s);
 hipError_t launch_rope_kv_write(const float* qkv, int B, int k, int Hq, int Hkv, int D,
-                                float theta, const int32_t* ctx, const int32_t* bt, int max_blocks,
-                                int num_blocks, molt_dtype dt, void* q_out, void* k_cache,
-                                void* v_cache, hipStream_t s);
+                                const void* table, const int32_t* ctx, const int32_t* bt,
+                                int max_blocks, int num_blocks, molt_dtype dt, void* q_out,
+                                void* k_cache, void* v_cache, hipStream_t s);
 // fp8 rows of a tiled bf16 matrix: rows = *n_rows when n_rows is given (padded expert
 // order, pperm marks padding rows), else max_rows
 hipError_t launch_quant_rows_tiled(const uint16_t* h, const int32_t* pperm, const int32_t* n_rows,
@@ -52,24 +58,28 @@ hipError_t launch_combine(const float* o, const float* w, int T, int K, int d, f
                           bool accumulate, hipStream_t s);
 
 // ------------------------------------------------------------- routing
-// top-K + softmax of router logits (or replay ids); stable permutation (perm/inv) and its
-// padded copy (pperm: padded row -> pair or -1, n_padded rows); tile table in padded rows
-hipError_t launch_route(const float* logits, const float* bias, const int32_t* replay, int T,
-                        int E, int K, int32_t* ids, float* w, int32_t* counts, int32_t* offsets,
-                        int32_t* perm, int32_t* inv, int32_t* pperm, int32_t* n_padded,
-                        int tile_m, int32_t* tiles, int max_tiles, int32_t* n_tiles,
-                        hipStream_t s);
+// top-K + softmax of router logits (the sum, in order, of nparts split-K partials
+// logits[s * T * E ..]; or replay ids); stable permutation (perm/inv) and its padded copy
+// (pperm: padded row -> pair or -1, n_padded rows); tile table in padded rows
+hipError_t launch_route(const float* logits, int nparts, const float* bias, const int32_t* replay,
+                        int T, int E, int K, int32_t* ids, float* w, int32_t* counts,
+                        int32_t* offsets, int32_t* perm, int32_t* inv, int32_t* pperm,
+                        int32_t* n_padded, int tile_m, int32_t* tiles, int max_tiles,
+                        int32_t* n_tiles, hipStream_t s);
 int max_expert_tiles(int T, int E, int K, int tile_m);
 long max_padded_rows(int T, int E, int K);
 
 // ------------------------------------------------------------- GEMMs
 // C[M, N] (f32, row-major) = A[M, K] * B[N, K]^T, A/B in dt (F32 or BF16), both tiled (rows
 // padded to 32); epilogue adds into C when accumulate. bf16 may split K when `part` holds
-// enough floats for the partial sums (gemm_plan).
+// enough floats for the partial sums (gemm_plan). With splits_out the fixed-order sum of
+// the partials is left to the caller: *splits_out = S > 1 means C was not touched and
+// part[s * M * N ..] holds split s; S = 1 means C was written as usual.
 struct GemmPlan { int bm, splits; };
 GemmPlan gemm_plan(int M, int N, int K, long part_elems);
 hipError_t launch_gemm(const void* A, const void* Bw, float* C, int M, int N, int K, molt_dtype dt,
-                       bool accumulate, float* part, long part_elems, hipStream_t s);
+                       bool accumulate, float* part, long part_elems, hipStream_t s,
+                       int* splits_out = nullptr);
 // Grouped expert GEMMs over the tile table built by launch_route. bf16/fp8: A and the
 // weights in the tiled layout, gate_up writes h tiled; f32: row-major A and h, tiled
 // weights. Rows are padded-order; down writes o[pair].

@@ -46,7 +46,7 @@ MOLT_DEV unsigned long long wave_max_u64(unsigned long long v) {
   return v;
 }
 
-__global__ __launch_bounds__(256) void topk_kernel(const float* __restrict__ logits,
+__global__ __launch_bounds__(256) void topk_kernel(const float* __restrict__ logits, int nparts,
                                                    const float* __restrict__ bias,
                                                    const int32_t* __restrict__ replay, int T, int E,
                                                    int K, int32_t* __restrict__ ids,
@@ -54,7 +54,15 @@ __global__ __launch_bounds__(256) void topk_kernel(const float* __restrict__ log
   const int t = blockIdx.x * 4 + threadIdx.x / kWave;
   const int lane = threadIdx.x % kWave;
   if (t >= T) return;
-  const float* g = logits + long(t) * E;
+  // router logit: the split-K partial sums of the router GEMM added in split order
+  const float* gt = logits + long(t) * E;
+  const long stride = long(T) * E;
+  auto gval = [&](int e) {
+    float v = gt[e];
+#pragma unroll 8
+    for (int s = 1; s < nparts; ++s) v += gt[s * stride + e];
+    return v;
+  };
   float sel_v = -INFINITY;
   int sel_e = 0;
   if (replay) {
@@ -62,14 +70,14 @@ __global__ __launch_bounds__(256) void topk_kernel(const float* __restrict__ log
       int e = replay[long(t) * K + lane];
       if (e < 0 || e >= E) e = 0;              // out-of-range replay id: expert 0
       sel_e = e;
-      sel_v = g[e] + (bias ? bias[e] : 0.f);
+      sel_v = gval(e) + (bias ? bias[e] : 0.f);
     }
   } else {
     unsigned long long key[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int e = lane + kWave * i;
-      key[i] = e < E ? route_key(g[e] + (bias ? bias[e] : 0.f), e) : 0ull;
+      key[i] = e < E ? route_key(gval(e) + (bias ? bias[e] : 0.f), e) : 0ull;
     }
     for (int j = 0; j < K; ++j) {
       unsigned long long mine = key[0];
@@ -82,7 +90,7 @@ __global__ __launch_bounds__(256) void topk_kernel(const float* __restrict__ log
       const int e = int(0xFFFFFFFFu - uint32_t(best & 0xFFFFFFFFull));
       if (lane == j) {
         sel_e = e;
-        sel_v = g[e] + (bias ? bias[e] : 0.f);
+        sel_v = gval(e) + (bias ? bias[e] : 0.f);
       }
     }
   }
@@ -217,12 +225,12 @@ long max_padded_rows(int T, int E, int K) {
   return (worst + 31) / 32 * 32;
 }
 
-hipError_t launch_route(const float* logits, const float* bias, const int32_t* replay, int T,
-                        int E, int K, int32_t* ids, float* w, int32_t* counts, int32_t* offsets,
-                        int32_t* perm, int32_t* inv, int32_t* pperm, int32_t* n_padded,
-                        int tile_m, int32_t* tiles, int max_tiles, int32_t* n_tiles,
-                        hipStream_t s) {
-  topk_kernel<<<(T + 3) / 4, 256, 0, s>>>(logits, bias, replay, T, E, K, ids, w);
+hipError_t launch_route(const float* logits, int nparts, const float* bias, const int32_t* replay,
+                        int T, int E, int K, int32_t* ids, float* w, int32_t* counts,
+                        int32_t* offsets, int32_t* perm, int32_t* inv, int32_t* pperm,
+                        int32_t* n_padded, int tile_m, int32_t* tiles, int max_tiles,
+                        int32_t* n_tiles, hipStream_t s) {
+  topk_kernel<<<(T + 3) / 4, 256, 0, s>>>(logits, nparts, bias, replay, T, E, K, ids, w);
   permute_kernel<<<1, kPermThreads, 0, s>>>(ids, T * K, E, tile_m, counts, offsets, perm, inv,
                                             pperm, n_padded, reinterpret_cast<int4*>(tiles),
                                             max_tiles, n_tiles);
