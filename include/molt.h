@@ -274,9 +274,10 @@ int molt_verify_step(const molt_model* m, const molt_kv* kv, int B, int k, const
                      molt_stream_t stream);
 
 /* ------------------------------------------------------------------------------
- * Kernel-group timing (a measurement aid, not part of the method). While enabled,
- * every launch of a group is bracketed by two HIP events recorded on the call's
- * stream; molt_profile_read synchronises on the recorded events and returns the
+ * Kernel-group timing (a measurement aid, not part of the method). While a group is
+ * enabled, every launch of it is bracketed by two HIP events recorded on the call's
+ * stream (each pair costs a few microseconds of stream time: enable only the groups
+ * being measured); molt_profile_read synchronises on the recorded events and returns the
  * summed elapsed time and the number of bracketed launches of one group. Events come
  * from a pool of 4096 pairs created on the first enable (no device memory);
  * launches beyond the pool are not timed. Process-wide state: enable, run and read
@@ -291,7 +292,8 @@ typedef enum {
   MOLT_PROF_SAMPLER = 3,
   MOLT_PROF_PROJECTIONS = 4
 } molt_prof_group;
-int molt_profile_enable(int enable); /* 1: start (and clear), 0: stop recording */
+/* group_mask: bit g times group g (-1: all); nonzero starts and clears, 0 stops */
+int molt_profile_enable(int group_mask);
 int molt_profile_read(int group, double* total_ms, int* launches);
 
 #ifdef __cplusplus

@@ -395,7 +395,16 @@ PROF_GROUPS = {"attention": 0, "expert_gemm": 1, "lm_head": 2, "sampler": 3, "pr
 
 
 def profile_enable(on=True):
-    _check(load().molt_profile_enable(1 if on else 0), "molt_profile_enable")
+    """on: True (all groups), False (stop), or an iterable of group names to time."""
+    if on is True:
+        mask = -1
+    elif not on:
+        mask = 0
+    else:
+        mask = 0
+        for g in on:
+            mask |= 1 << PROF_GROUPS[g]
+    _check(load().molt_profile_enable(mask), "molt_profile_enable")
 
 
 def profile_read(group):

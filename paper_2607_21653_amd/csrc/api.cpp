@@ -37,7 +37,7 @@ int hip_status(hipError_t e, const char* where) {
 // ---- kernel-group timing with HIP events (opt-in, process-wide)
 struct Profiler {
   static constexpr int kPairs = 4096;
-  bool on = false;
+  int mask = 0;                 // bit g: group g is timed
   bool ready = false;
   hipEvent_t ev[2 * kPairs];
   int used = 0;
@@ -49,7 +49,7 @@ struct ProfScope {
   int slot = -1;
   hipStream_t s;
   ProfScope(int grp, hipStream_t st) : s(st) {
-    if (!g_prof.on || g_prof.used >= Profiler::kPairs) return;
+    if (!((g_prof.mask >> grp) & 1) || g_prof.used >= Profiler::kPairs) return;
     slot = g_prof.used++;
     g_prof.group[slot] = grp;
     hipEventRecord(g_prof.ev[2 * slot], s);
@@ -81,7 +81,8 @@ int molt_version(void) { return 101; }
 
 // ------------------------------------------------------------------ profiling
 
-int molt_profile_enable(int enable) {
+int molt_profile_enable(int group_mask) {
+  const bool enable = group_mask != 0;
   if (enable && !g_prof.ready) {
     for (int i = 0; i < 2 * Profiler::kPairs; ++i) {
       hipError_t e = hipEventCreate(&g_prof.ev[i]);
@@ -90,7 +91,7 @@ int molt_profile_enable(int enable) {
     g_prof.ready = true;
   }
   if (enable) g_prof.used = 0;
-  g_prof.on = enable != 0;
+  g_prof.mask = group_mask;
   return ok();
 }
 
