@@ -107,14 +107,22 @@ __global__ __launch_bounds__(kThreads) void stream_gemm_kernel(GemmParams p) {
   int32x4_t st0[MS], st1[MS];
   Slice16 wb[4];
   // weights are read once per step: nontemporal loads
+  // K slices are visited in an order rotated by the column tile, so the workgroups of one
+  // row tile (running side by side on one XCD) read different activation blocks at any
+  // moment instead of all hitting the same L2 lines
+  const int rot = int((long(nt) * nk) / p.n_ntiles);
+  auto rs = [&](int kb) __attribute__((always_inline)) {
+    const int k = min(kb, nk - 1) + rot;
+    return long(k >= nk ? k - nk : k) * 4096;
+  };
   auto wld = [&](Slice16& f, int kb) __attribute__((always_inline)) {
-    const uint8_t* src = bsrc + long(min(kb, nk - 1)) * 4096;
+    const uint8_t* src = bsrc + rs(kb);
 #pragma unroll
     for (int c = 0; c < 4; ++c) f.c[c] = __builtin_nontemporal_load(reinterpret_cast<const int32x4_t*>(src + 1024 * c));
   };
 #define MOLT_GLOAD(ST, KB)                                                            \
   {                                                                                   \
-    const long off_ = long(min((KB), nk - 1)) * 4096;                                 \
+    const long off_ = rs(KB);                                                         \
     _Pragma("unroll") for (int b_ = 0; b_ < MS; ++b_)                                 \
         ST[b_] = *reinterpret_cast<const int32x4_t*>(asrc[b_] + off_);                \
   }
