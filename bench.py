@@ -275,7 +275,7 @@ def main():
                    "heads": f"{w.n_q_heads}q/{w.n_kv_heads}kv x {w.head_dim}",
                    "experts": f"{w.n_experts} top-{w.top_k}, ffn {w.d_ff}", "block": 16,
                    "drafts": f"q = softmax(target + N(0, {w.draft_sigma}^2))" if w.draft == "perturbed" else "uniform"},
-        "roofline": {"kernel": "paged attention (attn_mfma_kernel + split merge), per layer launch",
+        "roofline": {"kernel": "paged attention (attn_lds_kernel + split merge), per layer launch",
                      "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": attention_traffic(),
                      "algorithmic_bytes_per_launch": abytes, "avg_launch_ms": round(attn_avg, 4)},

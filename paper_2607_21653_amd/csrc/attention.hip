@@ -5,23 +5,19 @@
 //
 // Work split: workgroup = (b, h, split of the key range), 4 wavefronts; the number of
 // splits is chosen so the grid holds ~512 workgroups (at B*Hkv >= 512 there is no split and
-// no merge pass). Each wavefront takes block pairs (32 keys) round-robin and keeps its own
-// online softmax; the next pair's fragments are loaded into a second register set while
-// the current pair computes (software pipelining through registers). Per pair, on
-// v_mfma_f32_16x16x32_bf16:
-//   S^T[32 keys x R] = K Q^T   (A = K rows straight from the cache: [16 keys x 32 dims]
-//                               per operand, 16 B per lane; B = Q^T held in registers)
-//   O^T[D x R]      += V^T P^T (A = V^T: the V cache stores a block as [D][16 tokens], so
-//                               a lane's 4 consecutive keys of one dim are 8 contiguous
-//                               bytes; B = P^T is exactly the S^T accumulator layout
-//                               rounded to bf16: no cross-lane shuffles)
-// The MFMA k-index is a free permutation as long as A and B agree: slot s of lane group g
-// is key 4g+s of the first block (s < 4) or of the second block (s >= 4).
+// no merge pass) and no split exceeds 2048 blocks. The wavefronts split the R query rows and
+// share every 32-key block pair through a double-buffered LDS ring (details at the kernel).
+// Per pair, on v_mfma_f32_16x16x32_bf16:
+//   S^T[32 keys x 16 rows] = K Q^T   (A = K rows from LDS, B = Q^T held in registers)
+//   O^T[D x 16 rows]      += V^T P^T (A = V^T: the V cache stores a block as [D][16 tokens],
+//                                    so 8 consecutive keys of one dim are 16 contiguous
+//                                    bytes; B = P^T is the S^T accumulator layout rounded to
+//                                    bf16: no cross-lane shuffles)
 // Causality: row r = j*G + g (position j) sees keys <= ctx_b + j; only pairs reaching past
 // ctx_b need masks. Softmax in f32 with exp2 of log2(e)-scaled scores; the output is
 // rescaled lazily, only when a row maximum grows by more than 8 (in log2 units) over the
-// reference it was accumulated with. The four wavefronts merge through LDS in a fixed order;
-// splits are merged by a log-sum-exp pass (a single split writes the output directly).
+// reference it was accumulated with. Splits are merged by a log-sum-exp pass (a single
+// split writes the output directly). Deterministic.
 #include "device_common.h"
 #include "internal.h"
 
@@ -33,8 +29,8 @@ constexpr int kWaves = 4;
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kNegBig = -1.0e30f;   // finite "minus infinity" for running maxima
 constexpr float kRescaleSlack = 8.0f; // probabilities may grow to 2^8 before O is rescaled
+constexpr int kMaxSplitBlocks = 2048; // KV blocks of one split (its block table sits in LDS)
 
-typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
 
 struct AttnParams {
   const uint16_t* q;       // [T, Hq, D]
@@ -55,21 +51,35 @@ MOLT_DEV long out_index(const AttnParams& p, long t, long c, long cols, int esiz
   return p.out_tiled ? tiled_index(t, c, cols, esize) : t * cols + c;
 }
 
-// K and V^T fragments of one 32-key block pair for one wavefront
+// ---------------------------------------------------------------- MFMA kernel
+// Workgroup = (b, h, split), 4 wavefronts that split the R query rows (wavefront w owns
+// row tiles w and w + 4) and share every 32-key block pair through LDS: per pair the 256
+// threads copy its K and V blocks (4 x 16 D bytes) with coalesced 16-byte loads, kept
+// kDepth pairs ahead in registers, into a double-buffered ring; one LDS-only barrier per
+// pair. Each wavefront keeps only its own rows' Q fragments and O accumulator, so a
+// workgroup needs few registers and two fit per CU; no cross-wavefront merge at the end.
+// Key order inside a pair for the MFMA k-index: lane group g (of 4) holds keys
+// 8 (g % 2) .. +7 of block g / 2. S^T MFMA t (t = 0, 1) computes rows m = 4 g + i for keys
+// 8 (g % 2) + 4 t + i of block g / 2, so the 8 scores of a lane are those 8 contiguous keys
+// and the V^T operand is one 16-byte read of the [D][16] V block.
+// LDS swizzles keep every ds_read_b128 conflict-free: K row k (key) of block j stores its
+// 16-byte chunk c at chunk c ^ f(k, j); V row d (dim) stores chunk c at c ^ v(d).
 template <int D>
-struct PairFrags {
-  bf16x8_t k[2][D / 32];
-  bf16x8_t v[D / 16];
-};
+MOLT_DEV int kswz(int key, int blk) {
+  const int f = (key & 3) | ((key >> 1) & 4);
+  return D == 128 ? (f | (blk << 3)) : f;
+}
+MOLT_DEV int vswz(int dim) { return ((dim >> 2) ^ (dim >> 3)) & 1; }
 
-template <int D, int RT>
-__global__ __launch_bounds__(kThreads) void attn_mfma_kernel(AttnParams p) {
-  constexpr int DS = D / 32;      // 32-dim k-steps for S
-  constexpr int DT = D / 16;      // 16-dim tiles of O^T
-  constexpr int RP = RT * 16;     // padded rows
-  __shared__ float s_m[kWaves][RP];
-  __shared__ float s_l[kWaves][RP];
-  __shared__ float s_o[RP * D];
+template <int D, int RTW>
+__global__ __launch_bounds__(kThreads) void attn_lds_kernel(AttnParams p) {
+  constexpr int DS = D / 32;            // 32-dim k-steps for S
+  constexpr int DT = D / 16;            // 16-dim tiles of O^T
+  constexpr int KB = 16 * D * 2;        // bytes of one K (or V) block
+  constexpr int PAIR = 4 * KB;          // K0, K1, V0, V1
+  constexpr int CPT = PAIR / 16 / kThreads;   // 16-byte chunks per thread per pair
+  constexpr int kDepth = 6;             // pairs loaded ahead into registers
+  __shared__ __attribute__((aligned(16))) uint8_t lds[2][PAIR];
 
   const int split = blockIdx.x % p.splits;
   const int bh = blockIdx.x / p.splits;
@@ -82,207 +92,241 @@ __global__ __launch_bounds__(kThreads) void attn_mfma_kernel(AttnParams p) {
   const int nblk = (nkeys + 15) / 16;
   const int blk0 = split * p.blocks_per_split;
   const int blk1 = min(blk0 + p.blocks_per_split, nblk);
-  // wave-uniform in a scalar register, so block-table reads become scalar loads that do not
-  // share the vector memory counter with the K/V prefetch
+  const int npairs = (blk1 - blk0 + 1) / 2;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
   const int lane = threadIdx.x % kWave;
   const int l16 = lane % 16, g4 = lane / 16;
   const float c = p.scale_log2;
 
-  // Q^T fragments: row r = l16 + 16 * rt; dims [32 s + 8 g4, +8)
-  bf16x8_t qf[RT][DS];
-  int lim[RT];   // last visible key position of the lane's row (-1: padding row)
+  // Q^T fragments of the wavefront's rows r = 16 (wave + 4 i) + l16, dims [32 s + 8 g4, +8)
+  bf16x8_t qf[RTW][DS];
+  int lim[RTW];
 #pragma unroll
-  for (int rt = 0; rt < RT; ++rt) {
-    const int r = rt * 16 + l16;
+  for (int i = 0; i < RTW; ++i) {
+    const int r = 16 * (wave + 4 * i) + l16;
     const int j = r / G, gi = r % G;
-    lim[rt] = r < R ? ctx + j : -1;
+    lim[i] = r < R ? ctx + j : -1;
 #pragma unroll
     for (int s = 0; s < DS; ++s) {
       if (r < R) {
-        const uint16_t* src = p.q + ((long(b) * kp1 + j) * p.Hq + h * G + gi) * D + s * 32 + g4 * 8;
-        qf[rt][s] = *reinterpret_cast<const bf16x8_t*>(src);
+        qf[i][s] = *reinterpret_cast<const bf16x8_t*>(
+            p.q + ((long(b) * kp1 + j) * p.Hq + h * G + gi) * D + s * 32 + g4 * 8);
       } else {
 #pragma unroll
-        for (int e = 0; e < 8; ++e) qf[rt][s][e] = __bf16(0.f);
+        for (int e = 0; e < 8; ++e) qf[i][s][e] = __bf16(0.f);
       }
     }
   }
-
-  floatx4_t o[DT][RT];
+  floatx4_t o[DT][RTW];
 #pragma unroll
   for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
-    for (int rt = 0; rt < RT; ++rt) o[dt][rt] = floatx4_t{0.f, 0.f, 0.f, 0.f};
-  float m_run[RT], l_run[RT];
+    for (int i = 0; i < RTW; ++i) o[dt][i] = floatx4_t{0.f, 0.f, 0.f, 0.f};
+  float m_run[RTW], l_run[RTW];
 #pragma unroll
-  for (int rt = 0; rt < RT; ++rt) { m_run[rt] = kNegBig; l_run[rt] = 0.f; }
+  for (int i = 0; i < RTW; ++i) { m_run[i] = kNegBig; l_run[i] = 0.f; }
+  const bool active = 16 * wave < R;    // wavefronts without rows only help with the loads
 
+  __shared__ int s_bt[kMaxSplitBlocks];
   const int* btab = p.bt + long(b) * p.max_blocks;
-  const long kv_blk_stride = long(p.Hkv) * 16 * D;
-  const uint16_t* kbase = p.kc + long(h) * 16 * D + l16 * D + g4 * 8;
-  const uint16_t* vbase = p.vc + long(h) * D * 16 + l16 * 16 + g4 * 4;
-
-  // K/V are read once per step: nontemporal loads (they stream at ~7.1 TB/s on MI355X
-  // against ~6.3 TB/s for ordinary loads)
-  auto load_pair = [&](PairFrags<D>& f, int pb) {
-    const long phys0 = btab[pb];
-    const long phys1 = (pb + 1 < blk1) ? btab[pb + 1] : phys0;
+  for (int i = threadIdx.x; i < blk1 - blk0; i += kThreads) s_bt[i] = btab[blk0 + i];
+  __syncthreads();
+  const long kv_blk_stride = long(p.Hkv) * 16 * D;    // elements per physical block
+  // staging: thread t copies 16-byte chunk t (and t + 256 for D = 64) of each of the 4
+  // blocks K0, K1, V0, V1; the K (V) chunks of the two blocks sit at the same offsets
+  static_assert(KB / 16 == kThreads || KB / 16 == kThreads / 2, "chunks per block");
+  constexpr int CPB = CPT / 4 > 0 ? CPT / 4 : 1;      // chunks per thread per block (D=128: 1)
+  int k_src[CPB], v_src[CPB], k_dst[CPB], v_dst[CPB];
+  bool has[CPB];
 #pragma unroll
-    for (int s = 0; s < DS; ++s) {
-      f.k[0][s] = __builtin_nontemporal_load(reinterpret_cast<const bf16x8_t*>(kbase + phys0 * kv_blk_stride + s * 32));
-      f.k[1][s] = __builtin_nontemporal_load(reinterpret_cast<const bf16x8_t*>(kbase + phys1 * kv_blk_stride + s * 32));
+  for (int u = 0; u < CPB; ++u) {
+    const int chu = threadIdx.x + kThreads * u;
+    has[u] = chu < KB / 16;
+    const int ch = chu % (KB / 16);                    // chunk inside a block (threads past the
+                                                       // block's chunks re-load one, store none)
+    const int key = ch / (D / 8), kc = ch % (D / 8);
+    k_src[u] = (h * 16 + key) * D + kc * 8;
+    k_dst[u] = key * (2 * D) + ((kc ^ kswz<D>(key, 0)) * 16);
+    const int dim = ch / 2, vc = ch % 2;
+    v_src[u] = (h * D + dim) * 16 + vc * 8;
+    v_dst[u] = dim * 32 + ((vc ^ vswz(dim)) * 16);
+  }
+  // kswz depends on the block for D = 128 (bit 3): K1's chunk index is XORed with 8
+  int32x4_t st[kDepth][4 * CPB];
+  // The split's block-table entries are read from LDS: a global load of them, issued behind
+  // the K/V prefetches, would have its wait drain every load in flight (the vector memory
+  // counter retires in order).
+  auto gload = [&](int32x4_t (&dst)[4 * CPB], int pi) __attribute__((always_inline)) {
+    const int rel = 2 * min(pi, npairs - 1);
+    const long phys0 = s_bt[rel];
+    const long phys1r = s_bt[min(rel + 1, blk1 - blk0 - 1)];
+    const long phys1 = blk0 + rel + 1 < blk1 ? phys1r : phys0;
+#pragma unroll
+    for (int u = 0; u < CPB; ++u) {
+      dst[4 * u + 0] = __builtin_nontemporal_load(reinterpret_cast<const int32x4_t*>(p.kc + phys0 * kv_blk_stride + k_src[u]));
+      dst[4 * u + 1] = __builtin_nontemporal_load(reinterpret_cast<const int32x4_t*>(p.kc + phys1 * kv_blk_stride + k_src[u]));
+      dst[4 * u + 2] = __builtin_nontemporal_load(reinterpret_cast<const int32x4_t*>(p.vc + phys0 * kv_blk_stride + v_src[u]));
+      dst[4 * u + 3] = __builtin_nontemporal_load(reinterpret_cast<const int32x4_t*>(p.vc + phys1 * kv_blk_stride + v_src[u]));
     }
+  };
+  auto sstore = [&](const int32x4_t (&src)[4 * CPB], int buf) __attribute__((always_inline)) {
 #pragma unroll
-    for (int dt = 0; dt < DT; ++dt) {
-      const bf16x4_t a = __builtin_nontemporal_load(reinterpret_cast<const bf16x4_t*>(vbase + phys0 * kv_blk_stride + dt * 256));
-      const bf16x4_t e = __builtin_nontemporal_load(reinterpret_cast<const bf16x4_t*>(vbase + phys1 * kv_blk_stride + dt * 256));
-      f.v[dt] = bf16x8_t{a[0], a[1], a[2], a[3], e[0], e[1], e[2], e[3]};
+    for (int u = 0; u < CPB; ++u) {
+      if (!has[u]) continue;
+      uint8_t* base = lds[buf];
+      *reinterpret_cast<int32x4_t*>(base + k_dst[u]) = src[4 * u + 0];
+      *reinterpret_cast<int32x4_t*>(base + KB + (D == 128 ? (k_dst[u] ^ 128) : k_dst[u])) = src[4 * u + 1];
+      *reinterpret_cast<int32x4_t*>(base + 2 * KB + v_dst[u]) = src[4 * u + 2];
+      *reinterpret_cast<int32x4_t*>(base + 3 * KB + v_dst[u]) = src[4 * u + 3];
     }
   };
 
-  auto compute_pair = [&](const PairFrags<D>& f, int pb) {
-    // S^T tiles: lane holds keys 4 g4 + e of block pb (t = 0) and pb + 1 (t = 1)
-    floatx4_t st[2][RT];
+  // K fragment: block j = l16 / 8, key 8 ((l16 / 4) % 2) + 4 t + l16 % 4 (the swizzle is the
+  // same for t = 0 and 1, so t only adds 4 rows), chunk 4 s + g4 (dims 32 s + 8 g4).
+  // V fragment: block g4 / 2, dim 16 dt + l16 (the swizzle does not change with dt), chunk g4 % 2
+  int koff[DS];
+  {
+    const int j = l16 / 8, key = 8 * ((l16 / 4) % 2) + l16 % 4;
 #pragma unroll
-    for (int t = 0; t < 2; ++t)
+    for (int s = 0; s < DS; ++s) koff[s] = j * KB + key * (2 * D) + (((4 * s + g4) ^ kswz<D>(key, j)) * 16);
+  }
+  const int voff = (2 + g4 / 2) * KB + l16 * 32 + (((g4 % 2) ^ vswz(l16)) * 16);
+
+  auto compute = [&](int buf, int pi) __attribute__((always_inline)) {
+    if (!active) return;
+    const int pb = blk0 + 2 * pi;
+    const uint8_t* base = lds[buf];
+    floatx4_t sv[2][RTW];
 #pragma unroll
-      for (int rt = 0; rt < RT; ++rt) {
+    for (int t = 0; t < 2; ++t) {
+      bf16x8_t kf[DS];
+#pragma unroll
+      for (int s = 0; s < DS; ++s) kf[s] = *reinterpret_cast<const bf16x8_t*>(base + koff[s] + t * 4 * (2 * D));
+#pragma unroll
+      for (int i = 0; i < RTW; ++i) {
         floatx4_t acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int s = 0; s < DS; ++s)
-          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(f.k[t][s], qf[rt][s], acc, 0, 0, 0);
-        st[t][rt] = acc;
+        for (int s = 0; s < DS; ++s) acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[s], qf[i][s], acc, 0, 0, 0);
+        sv[t][i] = acc;
       }
-    // keys at or past pb*16 + 31 <= ctx are visible to every row: no mask needed
-    const bool full = pb * 16 + 31 <= ctx;
-    if (!full) {
-      const bool has2 = pb + 1 < blk1;
+    }
+    // lane's 8 keys: block pb + g4 / 2, keys 8 (g4 % 2) + 4 t + e
+    if (!(pb * 16 + 31 <= ctx)) {
+      const bool blk_ok = (g4 / 2 == 0) || (pb + 1 < blk1);
 #pragma unroll
-      for (int rt = 0; rt < RT; ++rt)
+      for (int i = 0; i < RTW; ++i)
 #pragma unroll
         for (int t = 0; t < 2; ++t)
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
-            const int kpos = (pb + t) * 16 + g4 * 4 + e;
-            if (!((t == 0 || has2) && kpos <= lim[rt])) st[t][rt][e] = -INFINITY;
+            const int kpos = (pb + g4 / 2) * 16 + 8 * (g4 % 2) + 4 * t + e;
+            if (!(blk_ok && kpos <= lim[i])) sv[t][i][e] = -INFINITY;
           }
     }
-    // row maxima (raw scores; the scale is positive) across the lane's 8 keys and 4 groups
-    float mx[RT];
+    float mx[RTW];
     bool grow = false;
 #pragma unroll
-    for (int rt = 0; rt < RT; ++rt) {
-      float v = fmaxf(fmaxf(fmaxf(st[0][rt][0], st[0][rt][1]), fmaxf(st[0][rt][2], st[0][rt][3])),
-                      fmaxf(fmaxf(st[1][rt][0], st[1][rt][1]), fmaxf(st[1][rt][2], st[1][rt][3])));
+    for (int i = 0; i < RTW; ++i) {
+      float v = fmaxf(fmaxf(fmaxf(sv[0][i][0], sv[0][i][1]), fmaxf(sv[0][i][2], sv[0][i][3])),
+                      fmaxf(fmaxf(sv[1][i][0], sv[1][i][1]), fmaxf(sv[1][i][2], sv[1][i][3])));
       v = fmaxf(v, __shfl_xor(v, 16, kWave));
       v = fmaxf(v, __shfl_xor(v, 32, kWave));
-      mx[rt] = v * c;
-      grow |= mx[rt] > m_run[rt] + kRescaleSlack;
+      mx[i] = v * c;
+      grow |= mx[i] > m_run[i] + kRescaleSlack;
     }
-    // lazy rescale, uniform over the wavefront: only when some row's maximum has grown by
-    // more than the slack (the result is the same softmax for any reference maximum)
     if (__builtin_amdgcn_read_exec() & __ballot(grow)) {
 #pragma unroll
-      for (int rt = 0; rt < RT; ++rt) {
-        const float m_new = fmaxf(m_run[rt], mx[rt]);
-        const float alpha = exp2f(m_run[rt] - m_new);
-        l_run[rt] *= alpha;
-        m_run[rt] = m_new;
+      for (int i = 0; i < RTW; ++i) {
+        const float m_new = fmaxf(m_run[i], mx[i]);
+        const float alpha = exp2f(m_run[i] - m_new);
+        l_run[i] *= alpha;
+        m_run[i] = m_new;
 #pragma unroll
-        for (int dt = 0; dt < DT; ++dt) o[dt][rt] *= alpha;
+        for (int dt = 0; dt < DT; ++dt) o[dt][i] *= alpha;
       }
     }
+    bf16x8_t pf[RTW];
 #pragma unroll
-    for (int rt = 0; rt < RT; ++rt) {
-      const float nm = -m_run[rt];
+    for (int i = 0; i < RTW; ++i) {
+      const float nm = -m_run[i];
       float ps = 0.f;
-      bf16x8_t pf;
 #pragma unroll
       for (int t = 0; t < 2; ++t)
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          const __bf16 pb16 = __bf16(exp2f(fmaf(st[t][rt][e], c, nm)));
-          pf[t * 4 + e] = pb16;
-          ps += float(pb16);   // the normaliser sums the same rounded weights the MFMA uses
+          const __bf16 w = __bf16(exp2f(fmaf(sv[t][i][e], c, nm)));
+          pf[i][t * 4 + e] = w;
+          ps += float(w);   // the normaliser sums the same rounded weights the MFMA uses
         }
-      l_run[rt] += ps;
+      l_run[i] += ps;
+    }
 #pragma unroll
-      for (int dt = 0; dt < DT; ++dt)
-        o[dt][rt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(f.v[dt], pf, o[dt][rt], 0, 0, 0);
+    for (int dt = 0; dt < DT; ++dt) {
+      const bf16x8_t vf = *reinterpret_cast<const bf16x8_t*>(base + voff + dt * 16 * 32);
+#pragma unroll
+      for (int i = 0; i < RTW; ++i) o[dt][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[i], o[dt][i], 0, 0, 0);
     }
   };
 
-  // software pipeline: the next block pair's fragments load while the current one computes
-  int pb = blk0 + 2 * wave;
-  if (pb < blk1) {
-    PairFrags<D> fa, fb;
-    load_pair(fa, pb);
-    while (true) {
-      if (pb + 2 * kWaves < blk1) load_pair(fb, pb + 2 * kWaves);
-      compute_pair(fa, pb);
-      pb += 2 * kWaves;
-      if (pb >= blk1) break;
-      if (pb + 2 * kWaves < blk1) load_pair(fa, pb + 2 * kWaves);
-      compute_pair(fb, pb);
-      pb += 2 * kWaves;
-      if (pb >= blk1) break;
+  // pipeline: pair pi sits in LDS buffer pi % 2; register slot (pi + 1) % kDepth holds pair
+  // pi + 1 (slots hold pi + 1 .. pi + kDepth). Step pi first stores pair pi + 1 into the
+  // other buffer (last read before the previous barrier) and refills its slot with pair
+  // pi + 1 + kDepth, so the new loads are in flight during the compute; then it computes
+  // pair pi. Loads past the last pair re-read it.
+  if (npairs > 0) {
+    gload(st[0], 0);
+    sstore(st[0], 0);
+#pragma unroll
+    for (int u = 1; u <= kDepth; ++u) gload(st[u % kDepth], u);
+    lds_barrier();
+    int pi = 0;
+    for (; pi + kDepth - 1 < npairs; pi += kDepth) {
+#pragma unroll
+      for (int u = 0; u < kDepth; ++u) {
+        sstore(st[(u + 1) % kDepth], 1 - u % 2);
+        gload(st[(u + 1) % kDepth], pi + u + 1 + kDepth);
+        compute(u % 2, pi + u);
+        lds_barrier();
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < kDepth - 1; ++u) {
+      if (pi + u < npairs) {
+        sstore(st[(u + 1) % kDepth], 1 - u % 2);
+        compute(u % 2, pi + u);
+        lds_barrier();
+      }
     }
   }
+  if (!active) return;
 
-  // ---- merge the four wavefronts (fixed order), then write
+  // row totals across the 4 lane groups, then the output (or this split's partials)
 #pragma unroll
-  for (int rt = 0; rt < RT; ++rt) {
-    float lt = l_run[rt];
+  for (int i = 0; i < RTW; ++i) {
+    float lt = l_run[i];
     lt += __shfl_xor(lt, 16, kWave);
     lt += __shfl_xor(lt, 32, kWave);
-    if (g4 == 0) {
-      s_m[wave][rt * 16 + l16] = m_run[rt];
-      s_l[wave][rt * 16 + l16] = lt;
-    }
-  }
-  __syncthreads();
-  float fac[RT];
-#pragma unroll
-  for (int rt = 0; rt < RT; ++rt) {
-    const int r = rt * 16 + l16;
-    float M = kNegBig;
-    for (int w = 0; w < kWaves; ++w) M = fmaxf(M, s_m[w][r]);
-    fac[rt] = exp2f(s_m[wave][r] - M);
-  }
-  // O^T accumulator element e of lane: dim 16 dt + 4 g4 + e, row 16 rt + l16
-  for (int w = 0; w < kWaves; ++w) {
-    if (wave == w) {
+    const int r = 16 * (wave + 4 * i) + l16;
+    if (r >= R) continue;
+    const int j = r / G, gi = r % G;
+    // O^T element e of tile dt: dim 16 dt + 4 g4 + e
+    if (p.splits == 1) {
+      const float inv = lt > 0.f ? 1.f / lt : 0.f;
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
-        for (int rt = 0; rt < RT; ++rt)
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const int idx = (rt * 16 + l16) * D + dt * 16 + g4 * 4 + e;
-            const float v = o[dt][rt][e] * fac[rt];
-            s_o[idx] = (w == 0) ? v : s_o[idx] + v;
-          }
-    }
-    __syncthreads();
-  }
-  // final row statistics and output
-  for (int idx = threadIdx.x; idx < R * D; idx += kThreads) {
-    const int r = idx / D, dd = idx % D;
-    float M = kNegBig;
-    for (int w = 0; w < kWaves; ++w) M = fmaxf(M, s_m[w][r]);
-    float Lsum = 0.f;
-    for (int w = 0; w < kWaves; ++w) Lsum += s_l[w][r] * exp2f(s_m[w][r] - M);
-    const int j = r / G, gi = r % G;
-    if (p.splits == 1) {
-      const float v = Lsum > 0.f ? s_o[idx] / Lsum : 0.f;
-      p.out[out_index(p, long(b) * kp1 + j, (h * G + gi) * D + dd, long(p.Hq) * D, 2)] = f32_to_bf16(v);
+        for (int e = 0; e < 4; ++e)
+          p.out[out_index(p, long(b) * kp1 + j, (h * G + gi) * D + 16 * dt + 4 * g4 + e, long(p.Hq) * D, 2)] =
+              f32_to_bf16(o[dt][i][e] * inv);
     } else {
       const long pr = (long(bh) * p.splits + split) * R + r;
-      p.part_o[pr * D + dd] = s_o[idx];
-      if (dd == 0) {
-        p.part_ml[pr * 2 + 0] = M;
-        p.part_ml[pr * 2 + 1] = Lsum;
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) p.part_o[pr * D + 16 * dt + 4 * g4 + e] = o[dt][i][e];
+      if (g4 == 0) {
+        p.part_ml[pr * 2 + 0] = m_run[i];
+        p.part_ml[pr * 2 + 1] = lt;
       }
     }
   }
@@ -377,30 +421,17 @@ void split_plan(int B, int Hkv, int max_blocks, int& splits, int& bps) {
   const int cap = (max_blocks + 31) / 32;
   if (s > cap) s = cap;
   if (s < 1) s = 1;
+  if (s < (max_blocks + kMaxSplitBlocks - 1) / kMaxSplitBlocks)
+    s = (max_blocks + kMaxSplitBlocks - 1) / kMaxSplitBlocks;
   bps = (max_blocks + s - 1) / s;
   bps = (bps + 7) / 8 * 8;
   splits = (max_blocks + bps - 1) / bps;
 }
 
-template <int D, int RT>
-void launch_mfma(const AttnParams& p, int B, hipStream_t s) {
-  attn_mfma_kernel<D, RT><<<B * p.Hkv * p.splits, kThreads, 0, s>>>(p);
-}
-
 template <int D>
 hipError_t launch_d(const AttnParams& p, int B, int R, hipStream_t s) {
-  const int rt = (R + 15) / 16;
-  switch (rt) {
-    case 1: launch_mfma<D, 1>(p, B, s); break;
-    case 2: launch_mfma<D, 2>(p, B, s); break;
-    case 3: launch_mfma<D, 3>(p, B, s); break;
-    case 4: launch_mfma<D, 4>(p, B, s); break;
-    case 5: launch_mfma<D, 5>(p, B, s); break;
-    case 6: launch_mfma<D, 6>(p, B, s); break;
-    case 7: launch_mfma<D, 7>(p, B, s); break;
-    case 8: launch_mfma<D, 8>(p, B, s); break;
-    default: return hipErrorInvalidValue;
-  }
+  if (R <= 64) attn_lds_kernel<D, 1><<<B * p.Hkv * p.splits, kThreads, 0, s>>>(p);
+  else attn_lds_kernel<D, 2><<<B * p.Hkv * p.splits, kThreads, 0, s>>>(p);
   if (p.splits > 1) attn_merge_kernel<D><<<B * p.Hkv * R, D, 0, s>>>(p, 0);
   return hipGetLastError();
 }
