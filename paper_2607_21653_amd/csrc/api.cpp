@@ -456,6 +456,7 @@ struct DecWs {
   void* y; uint8_t* yq; float* ys; float* qkv; void* q; void* attn; void* attn_ws; MoeWs moe;
   float* part; long part_elems;   // split-K partial sums of the QKV and O projections
   void* rope;                     // RoPE cos/sin of the step's positions, [T, D/2] f64 pairs
+  int32_t* kv_slot;               // KV-cache slot of each token of the step (or -1)
 };
 
 DecWs carve_dec(molt::Carver& c, const molt_model* m, int B, int k, int max_blocks) {
@@ -469,7 +470,8 @@ DecWs carve_dec(molt::Carver& c, const molt_model* m, int B, int k, int max_bloc
     w.yq = c.take<uint8_t>(Tp * d);
     w.ys = c.take<float>(Tp);
   }
-  w.qkv = c.take<float>(T * (Hq + 2 * Hkv) * D);
+  if (!(m->dtype == MOLT_BF16 && D == 128))   // else RoPE is fused into the QKV epilogue
+    w.qkv = c.take<float>(T * (Hq + 2 * Hkv) * D);
   w.q = c.take<uint8_t>(T * Hq * D * es);
   w.attn = c.take<uint8_t>(Tp * Hq * D * es);
   const size_t aws = m->dtype == MOLT_F32 ? 0 : molt::attention_ws_bytes(B, k, Hq, Hkv, D, max_blocks);
@@ -480,6 +482,7 @@ DecWs carve_dec(molt::Carver& c, const molt_model* m, int B, int k, int max_bloc
   w.part_elems = pq > po ? pq : po;
   w.part = c.take<float>(w.part_elems);
   w.rope = c.take<double>(T * D);
+  w.kv_slot = c.take<int32_t>(T);
   return w;
 }
 
@@ -494,18 +497,26 @@ hipError_t run_decoder(const DecWs& w, const molt_model* m, const molt_kv* kv, i
   const bool fp8 = m->expert_dtype == MOLT_FP8_E4M3;
   hipError_t e = hipSuccess;
 #define RUN(call) do { if ((e = (call)) != hipSuccess) return e; } while (0)
-  RUN(molt::launch_rope_table(kv->context_lens, B, k, D, m->rope_theta, w.rope, s));
+  RUN(molt::launch_rope_table(kv->context_lens, B, k, D, m->rope_theta, w.rope, kv->block_tables,
+                              kv->max_blocks_per_seq, kv->num_blocks, w.kv_slot, s));
   RUN(molt::launch_residual_norm(x, nullptr, 0, nullptr, nullptr, 0, m->attn_norm[0], T, d,
                                  m->rms_eps, m->dtype, w.y, nullptr, nullptr, s));
   for (int l = 0; l < L; ++l) {
-    {
+    if (m->dtype == MOLT_BF16 && D == 128) {
+      // one 128-column tile per head: RoPE and the KV-cache write in the GEMM epilogue
       ProfScope ps(MOLT_PROF_PROJECTIONS, s);
-      RUN(molt::launch_gemm(w.y, m->w_qkv[l], w.qkv, T, (Hq + 2 * Hkv) * D, d, m->dtype, false,
-                            w.part, w.part_elems, s));
+      RUN(molt::launch_qkv_rope(w.y, m->w_qkv[l], T, d, Hq, Hkv, w.rope, w.kv_slot, w.q,
+                                kv->k_cache[l], kv->v_cache[l], s));
+    } else {
+      {
+        ProfScope ps(MOLT_PROF_PROJECTIONS, s);
+        RUN(molt::launch_gemm(w.y, m->w_qkv[l], w.qkv, T, (Hq + 2 * Hkv) * D, d, m->dtype, false,
+                              w.part, w.part_elems, s));
+      }
+      RUN(molt::launch_rope_kv_write(w.qkv, B, k, Hq, Hkv, D, w.rope, kv->context_lens,
+                                     kv->block_tables, kv->max_blocks_per_seq, kv->num_blocks,
+                                     m->dtype, w.q, kv->k_cache[l], kv->v_cache[l], s));
     }
-    RUN(molt::launch_rope_kv_write(w.qkv, B, k, Hq, Hkv, D, w.rope, kv->context_lens,
-                                   kv->block_tables, kv->max_blocks_per_seq, kv->num_blocks,
-                                   m->dtype, w.q, kv->k_cache[l], kv->v_cache[l], s));
     {
       ProfScope ps(MOLT_PROF_ATTENTION, s);
       RUN(molt::launch_paged_attention(w.q, kv->k_cache[l], kv->v_cache[l], kv->block_tables,

@@ -137,11 +137,16 @@ __global__ __launch_bounds__(kThreads) void quant_rows_tiled_kernel(
 // RoPE angle table of the step: token t = b*(1+k)+j sits at position ctx[b]+j; pair i
 // (i, i+D/2) turns by position * theta^(-2i/D); cos and sin evaluated in f64, once per step
 // for all layers. table[t][i] = {cos, sin}.
-__global__ __launch_bounds__(kThreads) void rope_table_kernel(const int32_t* __restrict__ ctx, int k,
-                                                              int D, float theta,
-                                                              double2* __restrict__ table) {
+__global__ __launch_bounds__(kThreads) void rope_table_kernel(
+    const int32_t* __restrict__ ctx, int k, int D, float theta, double2* __restrict__ table,
+    const int32_t* __restrict__ bt, int max_blocks, int num_blocks, int32_t* __restrict__ kv_slot) {
   const int t = blockIdx.x;
-  const long pos = long(ctx[t / (k + 1)]) + t % (k + 1);
+  const int b = t / (k + 1);
+  const long pos = long(ctx[b]) + t % (k + 1);
+  if (kv_slot && threadIdx.x == 0) {
+    const int blk = bt[long(b) * max_blocks + pos / 16];
+    kv_slot[t] = blk >= 0 && blk < num_blocks ? blk * 16 + int(pos % 16) : -1;
+  }
   for (int i = threadIdx.x; i < D / 2; i += kThreads) {
     const double inv_freq = pow(double(theta), -2.0 * double(i) / double(D));
     const double ang = double(pos) * inv_freq;
@@ -229,8 +234,10 @@ hipError_t launch_residual_norm(float* x, const float* part, int nparts, const f
 }
 
 hipError_t launch_rope_table(const int32_t* ctx, int B, int k, int D, float theta, void* table,
+                             const int32_t* bt, int max_blocks, int num_blocks, int32_t* kv_slot,
                              hipStream_t s) {
-  rope_table_kernel<<<B * (k + 1), kThreads, 0, s>>>(ctx, k, D, theta, static_cast<double2*>(table));
+  rope_table_kernel<<<B * (k + 1), kThreads, 0, s>>>(ctx, k, D, theta, static_cast<double2*>(table),
+                                                     bt, max_blocks, num_blocks, kv_slot);
   return hipGetLastError();
 }
 

@@ -257,8 +257,20 @@ hipError_t run_stream(GemmParams p, int tile_m, hipStream_t s) {
 // MFMA fragment a contiguous 1 KB LDS read (conflict-free, no padding). One barrier per
 // slice. Split-K: split s covers slices [s * nk / S, (s + 1) * nk / S) and writes its
 // partial sums to `part[s]`; a fixed-order reduction adds them (deterministic).
-template <int BM>
-__global__ __launch_bounds__(kThreads) void lds_gemm_kernel(GemmParams p, float* part, int splits) {
+// Epilogue of the QKV projection with RoPE and the paged-KV write fused in (head_dim 128:
+// output column tile nt is head nt; q heads, then k heads, then v heads).
+struct RopeKv {
+  const double2* table;     // [T][64] {cos, sin} of each token's position
+  const int32_t* slot;      // [T] KV-cache slot of token t: block * 16 + position % 16, or -1
+  int Hq, Hkv;
+  uint16_t* q;              // [T, Hq, 128] bf16
+  uint16_t* kc;             // [num_blocks, Hkv, 16, 128]
+  uint16_t* vc;             // [num_blocks, Hkv, 128, 16]
+};
+
+template <int BM, bool ROPE>
+__global__ __launch_bounds__(kThreads) void lds_gemm_kernel(GemmParams p, float* part, int splits,
+                                                            RopeKv rk) {
   constexpr int AB = BM / 32;                 // activation row blocks
   constexpr int NB = AB + 4;                  // 4 KB blocks per slice (A then B)
   constexpr int TM = BM / 64 > 0 ? BM / 64 : 1;   // 32-row MFMA tiles per wavefront
@@ -350,6 +362,67 @@ __global__ __launch_bounds__(kThreads) void lds_gemm_kernel(GemmParams p, float*
 
   // acc[i][j][e]: row wm*WROWS + 32 i + 8 (e / 4) + 4 (lane / 32) + e % 4, col wn*64 + 32 j + lane % 32
   const int lcol = lane % 32, lgrp = lane / 32;
+  if constexpr (ROPE) {
+    // The f32 tile goes through the (now idle) LDS ring so that each rotation pair (i, i + 64)
+    // meets in one thread; the rotation is done in f64 with the step's cos/sin table. The
+    // table entries and cache slots are fetched first, so their latency overlaps the exchange.
+    // thread (pr, pi) rotates pair pi of rows pr + 4 n, n < BM / 4, in groups of 16 rows
+    constexpr int NG = BM / 64;
+    const int h = nt, pi = threadIdx.x % 64, pr = threadIdx.x / 64;
+    const bool rotate = h < rk.Hq + rk.Hkv;
+    double2 cs[16];
+    auto fetch = [&](int g) __attribute__((always_inline)) {
+#pragma unroll
+      for (int n = 0; n < 16; ++n)
+        cs[n] = rk.table[long(min(row0 + pr + 4 * (16 * g + n), p.M - 1)) * 64 + pi];
+    };
+    if (rotate) fetch(0);
+    __shared__ int s_slot[BM];
+    if (threadIdx.x < BM) s_slot[threadIdx.x] = row0 + int(threadIdx.x) < p.M ? rk.slot[row0 + threadIdx.x] : -1;
+    __syncthreads();
+    float* ob = reinterpret_cast<float*>(&lds[0][0]);     // [BM][128]
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int e = 0; e < 16; ++e)
+          ob[(wm * WROWS + 32 * i + 8 * (e / 4) + 4 * lgrp + (e % 4)) * 128 + wn * 64 + 32 * j + lcol] =
+              acc[i][j][e];
+    __syncthreads();
+    if (rotate) {
+#pragma unroll
+      for (int g = 0; g < NG; ++g) {
+        if (g > 0) fetch(g);
+#pragma unroll
+        for (int n = 0; n < 16; ++n) {
+          const int r = pr + 4 * (16 * g + n), t = row0 + r;
+          if (t >= p.M) break;
+          const double a = ob[r * 128 + pi], c = ob[r * 128 + pi + 64];
+          const uint16_t lo = f32_to_bf16(float(a * cs[n].x - c * cs[n].y));
+          const uint16_t hi = f32_to_bf16(float(c * cs[n].x + a * cs[n].y));
+          uint16_t* dst;
+          if (h < rk.Hq) {
+            dst = rk.q + (long(t) * rk.Hq + h) * 128;
+          } else {
+            const int sl = s_slot[r];
+            if (sl < 0) continue;
+            dst = rk.kc + ((long(sl >> 4) * rk.Hkv + (h - rk.Hq)) * 16 + (sl & 15)) * 128;
+          }
+          dst[pi] = lo;
+          dst[pi + 64] = hi;
+        }
+      }
+    } else {
+      const int hk = h - rk.Hq - rk.Hkv;
+      for (int w = threadIdx.x; w < BM * 128; w += kThreads) {
+        const int r = w % BM, i = w / BM, sl = s_slot[r];
+        if (sl < 0) continue;
+        rk.vc[((long(sl >> 4) * rk.Hkv + hk) * 128 + i) * 16 + (sl & 15)] = f32_to_bf16(ob[r * 128 + i]);
+      }
+    }
+    return;
+  }
   float* out = splits > 1 ? part + long(split) * p.M * p.ldc : static_cast<float*>(p.C);
 #pragma unroll
   for (int j = 0; j < 2; ++j) {
@@ -501,8 +574,8 @@ hipError_t launch_gemm(const void* A, const void* Bw, float* C, int M, int N, in
   p.n_mtiles = (M + g.bm - 1) / g.bm;
   p.n_ntiles = (N + kBN - 1) / kBN;
   const int grid = (p.n_mtiles * p.n_ntiles * g.splits + 7) / 8 * 8;
-  if (g.bm == 64) lds_gemm_kernel<64><<<grid, kThreads, 0, s>>>(p, part, g.splits);
-  else lds_gemm_kernel<128><<<grid, kThreads, 0, s>>>(p, part, g.splits);
+  if (g.bm == 64) lds_gemm_kernel<64, false><<<grid, kThreads, 0, s>>>(p, part, g.splits, RopeKv{});
+  else lds_gemm_kernel<128, false><<<grid, kThreads, 0, s>>>(p, part, g.splits, RopeKv{});
   if (g.splits > 1 && splits_out) {
     *splits_out = g.splits;         // the caller adds part[0 .. splits) (in order) into C
   } else if (g.splits > 1) {
@@ -510,6 +583,22 @@ hipError_t launch_gemm(const void* A, const void* Bw, float* C, int M, int N, in
     splitk_reduce_kernel<<<(n + kThreads - 1) / kThreads, kThreads, 0, s>>>(part, g.splits, n, C,
                                                                              accumulate);
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_qkv_rope(const void* A, const void* Bw, int M, int K_in, int Hq, int Hkv,
+                           const void* table, const int32_t* kv_slot, void* q_out, void* k_cache,
+                           void* v_cache, hipStream_t s) {
+  GemmParams p{};
+  p.A = A; p.B = Bw; p.M = M; p.N = (Hq + 2 * Hkv) * 128; p.K = K_in; p.ldc = p.N;
+  RopeKv rk{static_cast<const double2*>(table), kv_slot, Hq, Hkv, static_cast<uint16_t*>(q_out),
+            static_cast<uint16_t*>(k_cache), static_cast<uint16_t*>(v_cache)};
+  const GemmPlan g = gemm_plan(M, p.N, K_in, 0);     // no split: the epilogue needs whole sums
+  p.n_mtiles = (M + g.bm - 1) / g.bm;
+  p.n_ntiles = Hq + 2 * Hkv;
+  const int grid = (p.n_mtiles * p.n_ntiles + 7) / 8 * 8;
+  if (g.bm == 64) lds_gemm_kernel<64, true><<<grid, kThreads, 0, s>>>(p, nullptr, 1, rk);
+  else lds_gemm_kernel<128, true><<<grid, kThreads, 0, s>>>(p, nullptr, 1, rk);
   return hipGetLastError();
 }
 

@@ -41,8 +41,11 @@ hipError_t launch_embed(const void* table, const int32_t* tokens, int T, int d, 
 hipError_t launch_residual_norm(float* x, const float* part, int nparts, const float* o,
                                 const float* w, int K, const float* g, int T, int d, float eps,
                                 molt_dtype dt, void* y, uint8_t* yq, float* ys, hipStream_t s);
-// RoPE cos/sin of the step's B*(1+k) positions (f64 pairs, [T, D/2]), shared by all layers
+// RoPE cos/sin of the step's B*(1+k) positions (f64 pairs, [T, D/2]), shared by all layers;
+// with kv_slot also each token's KV-cache slot (block * 16 + position % 16, -1 when the block
+// table entry is out of range)
 hipError_t launch_rope_table(const int32_t* ctx, int B, int k, int D, float theta, void* table,
+                             const int32_t* bt, int max_blocks, int num_blocks, int32_t* kv_slot,
                              hipStream_t s);
 hipError_t launch_rope_kv_write(const float* qkv, int B, int k, int Hq, int Hkv, int D,
                                 const void* table, const int32_t* ctx, const int32_t* bt,
@@ -80,6 +83,12 @@ GemmPlan gemm_plan(int M, int N, int K, long part_elems);
 hipError_t launch_gemm(const void* A, const void* Bw, float* C, int M, int N, int K, molt_dtype dt,
                        bool accumulate, float* part, long part_elems, hipStream_t s,
                        int* splits_out = nullptr);
+// bf16 QKV projection (A tiled [M, K_in], weights tiled [(Hq + 2 Hkv) * 128, K_in]) with the
+// RoPE of launch_rope_kv_write and its q / paged K / paged V writes fused into the epilogue;
+// head_dim 128, same arithmetic (f32 sums rotated in f64 with the step's table)
+hipError_t launch_qkv_rope(const void* A, const void* Bw, int M, int K_in, int Hq, int Hkv,
+                           const void* table, const int32_t* kv_slot, void* q_out, void* k_cache,
+                           void* v_cache, hipStream_t s);
 // Grouped expert GEMMs over the tile table built by launch_route. bf16/fp8: A and the
 // weights in the tiled layout, gate_up writes h tiled; f32: row-major A and h, tiled
 // weights. Rows are padded-order; down writes o[pair].
