@@ -37,6 +37,19 @@ __global__ __launch_bounds__(kThreads) void embed_kernel(const void* __restrict_
 //   x[t] += sum_j w[t, j] * o[t * K + j]     (MoE combine, slot order; o = NULL: none)
 //   y = x[t] / sqrt(mean(x[t]^2) + eps) * g  rounded to dt, tiled (g = NULL: no norm)
 // With yq, also the per-row fp8 code of y (s = amax|y| / 448, code = e4m3(y / s)).
+// Each thread owns runs of 8 consecutive elements (d % 8 == 0, d <= 8 * 256 * kNormRuns),
+// kept in registers from the residual update to the stores: one 16-byte store of y per run
+// (8 bf16 are contiguous in the tiled layout).
+constexpr int kNormRuns = 8;
+
+template <typename T>
+MOLT_DEV void add8(float (&v)[8], const T* src, float wgt) {
+  const float4 a = *reinterpret_cast<const float4*>(src);
+  const float4 b = *reinterpret_cast<const float4*>(src + 4);
+  v[0] += wgt * a.x; v[1] += wgt * a.y; v[2] += wgt * a.z; v[3] += wgt * a.w;
+  v[4] += wgt * b.x; v[5] += wgt * b.y; v[6] += wgt * b.z; v[7] += wgt * b.w;
+}
+
 __global__ __launch_bounds__(kThreads) void residual_norm_kernel(
     float* __restrict__ x, const float* __restrict__ part, int nparts, long part_stride,
     const float* __restrict__ o, const float* __restrict__ w, int K, const float* __restrict__ g,
@@ -45,50 +58,81 @@ __global__ __launch_bounds__(kThreads) void residual_norm_kernel(
   __shared__ float red[kThreads / kWave];
   const int t = blockIdx.x;
   float* xr = x + long(t) * d;
+  float v[kNormRuns][8];
   float ss = 0.f;
-  // 4 consecutive elements per thread step (d % 4 == 0); the loops over splits and slots
-  // are unrolled so that their loads issue together
-  for (int i = threadIdx.x * 4; i < d; i += kThreads * 4) {
-    float4 v = *reinterpret_cast<const float4*>(xr + i);
+#pragma unroll
+  for (int r = 0; r < kNormRuns; ++r) {
+    const int i = (threadIdx.x + r * kThreads) * 8;
+    if (i >= d) break;
+    const float4 a = *reinterpret_cast<const float4*>(xr + i);
+    const float4 b = *reinterpret_cast<const float4*>(xr + i + 4);
+    v[r][0] = a.x; v[r][1] = a.y; v[r][2] = a.z; v[r][3] = a.w;
+    v[r][4] = b.x; v[r][5] = b.y; v[r][6] = b.z; v[r][7] = b.w;
     if (nparts > 0 || o) {
+      // each addend is summed exactly as v += p (splits) and v += (sum_j w_j o_j) (slots)
 #pragma unroll 4
-      for (int s = 0; s < nparts; ++s) {
-        const float4 q = *reinterpret_cast<const float4*>(part + s * part_stride + long(t) * d + i);
-        v.x += q.x; v.y += q.y; v.z += q.z; v.w += q.w;
-      }
+      for (int s = 0; s < nparts; ++s) add8(v[r], part + s * part_stride + long(t) * d + i, 1.0f);
       if (o) {
-        float4 a = make_float4(0.f, 0.f, 0.f, 0.f);
+        float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
 #pragma unroll 8
-        for (int j = 0; j < K; ++j) {
-          const float wj = w[long(t) * K + j];
-          const float4 q = *reinterpret_cast<const float4*>(o + (long(t) * K + j) * d + i);
-          a.x += wj * q.x; a.y += wj * q.y; a.z += wj * q.z; a.w += wj * q.w;
-        }
-        v.x += a.x; v.y += a.y; v.z += a.z; v.w += a.w;
+        for (int j = 0; j < K; ++j) add8(acc, o + (long(t) * K + j) * d + i, w[long(t) * K + j]);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[r][e] += acc[e];
       }
-      *reinterpret_cast<float4*>(xr + i) = v;
+      *reinterpret_cast<float4*>(xr + i) = make_float4(v[r][0], v[r][1], v[r][2], v[r][3]);
+      *reinterpret_cast<float4*>(xr + i + 4) = make_float4(v[r][4], v[r][5], v[r][6], v[r][7]);
     }
-    ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) ss += v[r][e] * v[r][e];
   }
   if (g == nullptr) return;
   ss = block_sum<kThreads / kWave, float>(ss, red);
-  const float r = 1.0f / sqrtf(ss / float(d) + eps);
+  const float rs = 1.0f / sqrtf(ss / float(d) + eps);
   float amax = 0.f;
-  const int es = dt == MOLT_BF16 ? 2 : 4;
-  for (int i = threadIdx.x; i < d; i += kThreads) {
-    float v = xr[i] * r * g[i];
-    if (dt == MOLT_BF16) v = round_to_bf16(v);
-    store_act(y, tiled_index(t, i, d, es), v, dt);
-    amax = fmaxf(amax, fabsf(v));
+#pragma unroll
+  for (int r = 0; r < kNormRuns; ++r) {
+    const int i = (threadIdx.x + r * kThreads) * 8;
+    if (i >= d) break;
+    const float4 ga = *reinterpret_cast<const float4*>(g + i);
+    const float4 gb = *reinterpret_cast<const float4*>(g + i + 4);
+    const float gv[8] = {ga.x, ga.y, ga.z, ga.w, gb.x, gb.y, gb.z, gb.w};
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      float u = v[r][e] * rs * gv[e];
+      if (dt == MOLT_BF16) u = round_to_bf16(u);
+      v[r][e] = u;
+      amax = fmaxf(amax, fabsf(u));
+    }
+    if (dt == MOLT_BF16) {
+      uint32_t pk[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        pk[e] = uint32_t(f32_to_bf16(v[r][2 * e])) | (uint32_t(f32_to_bf16(v[r][2 * e + 1])) << 16);
+      *reinterpret_cast<uint4*>(static_cast<uint8_t*>(y) + tiled_offset(t, 2L * i, 2L * d)) =
+          make_uint4(pk[0], pk[1], pk[2], pk[3]);
+    } else {
+      uint8_t* yb = static_cast<uint8_t*>(y);
+      *reinterpret_cast<float4*>(yb + tiled_offset(t, 4L * i, 4L * d)) =
+          make_float4(v[r][0], v[r][1], v[r][2], v[r][3]);
+      *reinterpret_cast<float4*>(yb + tiled_offset(t, 4L * (i + 4), 4L * d)) =
+          make_float4(v[r][4], v[r][5], v[r][6], v[r][7]);
+    }
   }
   if (yq == nullptr) return;
   amax = block_max<kThreads / kWave>(amax, red);
-  const float s = amax / 448.0f;
-  for (int i = threadIdx.x; i < d; i += kThreads) {
-    const float v = load_act(y, tiled_index(t, i, d, es), dt);
-    yq[tiled_offset(t, i, d)] = s > 0.f ? uint8_t(f32_to_fp8e4m3(v / s)) : uint8_t(0);
+  const float sc = amax / 448.0f;
+#pragma unroll
+  for (int r = 0; r < kNormRuns; ++r) {
+    const int i = (threadIdx.x + r * kThreads) * 8;
+    if (i >= d) break;
+    uint32_t c[2] = {0u, 0u};
+    if (sc > 0.f) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) c[e / 4] |= f32_to_fp8e4m3(v[r][e] / sc) << (8 * (e % 4));
+    }
+    *reinterpret_cast<uint2*>(yq + tiled_offset(t, i, d)) = make_uint2(c[0], c[1]);
   }
-  if (threadIdx.x == 0) ys[t] = s;
+  if (threadIdx.x == 0) ys[t] = sc;
 }
 
 // Per-row fp8 quantisation of tiled bf16 rows into tiled e4m3 codes (s = amax / 448,

@@ -8,14 +8,14 @@
 // largest logit with ties resolved to the lower expert id. K rounds of a wavefront
 // max-reduction select the experts in descending order.
 //
-// permute_kernel: one 1024-thread workgroup. Pass 1 counts pairs per expert (LDS
-// integer atomics: the totals are order-free); wavefront prefix sums over the experts give
-// offsets and the grouped-GEMM tile table. Pass 2 walks the T*K pairs in (token, slot) order, 1024 at
-// a time: inside a wavefront, lanes holding the same expert find each other with 8
-// ballots over the expert id bits; the rank of a lane among them is a popcount of the
-// lower lanes; across the 16 wavefronts an exclusive LDS prefix per expert adds the
-// earlier wavefronts' counts. Position = offset[e] + earlier chunks + earlier
-// wavefronts + rank: the stable (expert, token, slot) order, bit-exact.
+// permute_kernel: one 1024-thread workgroup, one pass over the ids. Wavefront w owns a
+// contiguous range of the T*K pairs (in (token, slot) order) and visits it 64 pairs at a
+// time: lanes holding the same expert find each other with 8 ballots over the expert id
+// bits, a popcount of the lower lanes gives the rank inside the step, and a running LDS
+// count per (wavefront, expert) adds the earlier steps. An exclusive prefix of those counts
+// over the wavefronts, and wavefront prefix sums over the experts (offsets, padded offsets,
+// grouped-GEMM tile table), then give position = offset[e] + earlier wavefronts + rank:
+// the stable (expert, token, slot) order, bit-exact, with no atomics.
 // The grouped GEMMs work on a padded copy of that order: every expert's rows start at a
 // multiple of 32 (padded offset poff[e] = sum of the earlier counts rounded up to 32), so
 // each 32-row block of a GEMM tile belongs to one expert; padded slots hold pair -1. The
@@ -35,6 +35,12 @@ MOLT_DEV unsigned long long route_key(float v, int e) {
   const uint32_t u = __float_as_uint(c);
   const uint32_t ord = (u >> 31) ? ~u : (u | 0x80000000u);
   return (static_cast<unsigned long long>(ord) << 32) | (0xFFFFFFFFu - uint32_t(e));
+}
+
+// inverse of route_key's high word (-0.0 comes back as +0.0, equal for the softmax)
+MOLT_DEV float key_value(unsigned long long key) {
+  const uint32_t ord = uint32_t(key >> 32);
+  return __uint_as_float((ord >> 31) ? (ord & 0x7fffffffu) : ~ord);
 }
 
 MOLT_DEV unsigned long long wave_max_u64(unsigned long long v) {
@@ -87,10 +93,10 @@ __global__ __launch_bounds__(256) void topk_kernel(const float* __restrict__ log
         if (key[i] > mine) { mine = key[i]; which = i; }
       const unsigned long long best = wave_max_u64(mine);
       if (mine == best && best != 0ull) key[which] = 0ull;   // the unique owner drops it
-      const int e = int(0xFFFFFFFFu - uint32_t(best & 0xFFFFFFFFull));
       if (lane == j) {
-        sel_e = e;
-        sel_v = gval(e) + (bias ? bias[e] : 0.f);
+        // the key holds the logit's order-preserving bits: decode instead of re-reading
+        sel_e = int(0xFFFFFFFFu - uint32_t(best & 0xFFFFFFFFull));
+        sel_v = key_value(best);
       }
     }
   }
@@ -109,25 +115,71 @@ __global__ __launch_bounds__(kPermThreads) void permute_kernel(
     int32_t* __restrict__ offsets_out, int32_t* __restrict__ perm, int32_t* __restrict__ inv,
     int32_t* __restrict__ pperm, int32_t* __restrict__ n_padded, int4* __restrict__ tiles,
     int max_tiles, int32_t* __restrict__ n_tiles) {
+  __shared__ int wc[kPermWaves][kMaxE];    // pass 1: count per (wavefront, expert); then its
+                                           // exclusive prefix over the wavefronts
   __shared__ int cnt[kMaxE];
   __shared__ int off[kMaxE + 1];
   __shared__ int poff[kMaxE + 1];
-  __shared__ int run[kMaxE];
-  __shared__ int wc[kPermWaves][kMaxE];
   __shared__ int wsum[3][kMaxE / kWave];
   __shared__ int wtmp[3][kMaxE];
   __shared__ int s_nt;
   const int tid = threadIdx.x;
   const int wave = tid / kWave, lane = tid % kWave;
-  for (int e = tid; e < kMaxE; e += kPermThreads) { cnt[e] = 0; run[e] = 0; }
+  // Wavefront w owns the contiguous pair range [w * per, (w + 1) * per), visited 64 at a
+  // time, so pair order = (wavefront, step, lane) order.
+  const int steps = (P + kPermThreads - 1) / kPermThreads;
+  const int per = steps * kWave;
+  const int p0 = wave * per;
+  for (int e = lane; e < kMaxE; e += kWave) wc[wave][e] = 0;   // own row only: no barrier
+  const unsigned long long lt = (1ull << lane) - 1ull;
+  // pass 1: the rank of each pair among the earlier pairs of its expert in this wavefront
+  // (earlier steps: the running count in wc; this step: popcount of the lower lanes with the
+  // same expert, found with 8 ballots over the id bits). The rank is parked in inv[p] (each
+  // thread reads back only what it wrote).
+  constexpr int kBatch = 8;                // loads of a batch issue together
+  for (int s0 = 0; s0 < steps; s0 += kBatch) {
+    int ev[kBatch];
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) {
+      const int p = p0 + (s0 + u) * kWave + lane;
+      ev[u] = (s0 + u < steps && p < P) ? ids[p] : -1;
+    }
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) {
+      if (s0 + u >= steps) break;
+      const int e = ev[u];
+      const bool valid = e >= 0;
+      unsigned long long mask = __ballot(valid);
+#pragma unroll
+      for (int bit = 0; bit < 8; ++bit) {
+        const bool on = (e >> bit) & 1;
+        const unsigned long long b = __ballot(valid && on);
+        mask &= on ? b : ~b;
+      }
+      const int below = __popcll(mask & lt);
+      int before = 0;
+      if (valid) before = wc[wave][e];
+      if (valid && below == 0) wc[wave][e] = before + __popcll(mask);
+      if (valid) inv[p0 + (s0 + u) * kWave + lane] = before + below;
+    }
+  }
   __syncthreads();
-  for (int p = tid; p < P; p += kPermThreads) atomicAdd(&cnt[ids[p]], 1);
+  // per expert: exclusive prefix of the wavefront counts, and the total
+  if (tid < kMaxE) {
+    int run = 0;
+    for (int w2 = 0; w2 < kPermWaves; ++w2) {
+      const int c = wc[w2][tid];
+      wc[w2][tid] = run;
+      run += c;
+    }
+    cnt[tid] = tid < E ? run : 0;
+  }
   __syncthreads();
   // exclusive prefix sums over experts (threads 0..255, one expert each) of the count, the
   // padded count and the tile count: offsets, padded offsets, first tile of each expert
   int tile0 = 0;
   if (tid < kMaxE) {
-    const int c = tid < E ? cnt[tid] : 0;
+    const int c = cnt[tid];
     int v[3] = {c, (c + 31) / 32 * 32, (c + tile_m - 1) / tile_m};
 #pragma unroll
     for (int q = 0; q < 3; ++q) {
@@ -148,7 +200,7 @@ __global__ __launch_bounds__(kPermThreads) void permute_kernel(
     for (int w2 = 0; w2 < wave; ++w2)
 #pragma unroll
       for (int q = 0; q < 3; ++q) add[q] += wsum[q][w2];
-    const int c = tid < E ? cnt[tid] : 0;
+    const int c = cnt[tid];
     const int tn = (c + tile_m - 1) / tile_m;
     off[tid + 1] = wtmp[0][tid] + add[0];
     poff[tid + 1] = wtmp[1][tid] + add[1];
@@ -176,40 +228,26 @@ __global__ __launch_bounds__(kPermThreads) void permute_kernel(
     offsets_out[e] = off[e];
   }
   if (tid == 0) offsets_out[E] = off[E];
-  const unsigned long long lt = (1ull << lane) - 1ull;
-  for (int base = 0; base < P; base += kPermThreads) {
-    for (int e = lane; e < kMaxE; e += kWave) wc[wave][e] = 0;
-    const int p = base + tid;
-    const bool valid = p < P;
-    const int e = valid ? ids[p] : 0;
-    unsigned long long mask = __ballot(valid);
+  // pass 2: position = offset of the expert + earlier wavefronts' pairs of it + rank
+  for (int s0 = 0; s0 < steps; s0 += kBatch) {
+    int ev[kBatch], rk[kBatch];
 #pragma unroll
-    for (int bit = 0; bit < 8; ++bit) {
-      const bool on = (e >> bit) & 1;
-      const unsigned long long b = __ballot(valid && on);
-      mask &= on ? b : ~b;
+    for (int u = 0; u < kBatch; ++u) {
+      const int p = p0 + (s0 + u) * kWave + lane;
+      const bool ok = s0 + u < steps && p < P;
+      ev[u] = ok ? ids[p] : -1;
+      rk[u] = ok ? inv[p] : 0;
     }
-    const int rank = __popcll(mask & lt);
-    __syncthreads();
-    if (valid && rank == 0) wc[wave][e] = __popcll(mask);
-    __syncthreads();
-    if (tid < E) {
-      int s = run[tid];
-      for (int w2 = 0; w2 < kPermWaves; ++w2) {
-        const int c = wc[w2][tid];
-        wc[w2][tid] = s;
-        s += c;
-      }
-      run[tid] = s;
-    }
-    __syncthreads();
-    if (valid) {
-      const int pos = off[e] + wc[wave][e] + rank;
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) {
+      const int e = ev[u];
+      if (e < 0) continue;
+      const int p = p0 + (s0 + u) * kWave + lane;
+      const int pos = off[e] + wc[wave][e] + rk[u];
       perm[pos] = p;
       inv[p] = pos;
       pperm[pos - off[e] + poff[e]] = p;
     }
-    __syncthreads();
   }
 }
 

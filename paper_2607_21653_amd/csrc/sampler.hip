@@ -3,26 +3,29 @@
 // temperature 1 and no truncation; paper Sec. 4.1 control table, Sec. 4.2, Sec. 5.3/5.4;
 // rule of Leviathan et al. 2023 / Chen et al. 2023).
 //
-// Four launches, all HBM-streaming and deterministic (fixed reduction orders, integer
-// prefix sums, no atomics):
+// Three launches, all deterministic (fixed reduction orders, integer prefix sums, no
+// atomics):
 //   1. chunk_stats  grid = rows * chunks: per 8192-logit chunk its max and
 //                   sum exp(l - chunk max) (f32 exp of the exactly compensated
-//                   difference, f64 accumulation across threads).
-//   2. accept       one thread per sequence: combines the chunk statistics of the rows
-//                   it needs into (m, S), runs the k accept tests u*q*S < exp(l_x - m)
-//                   in f64, writes accepted drafts and their log-probs, and the
-//                   descriptor of the final draw (row, residual mode).
-//   3. draw_mass    grid = B * chunks: per chunk, the integer mass sum floor(r_t 2^62)
-//                   of the residual max(0, p - q) (or p for a bonus draw), p_t from an
-//                   f64 exp so that the only rounding left in the draw is that of S.
-//   4. draw_pick    one workgroup per sequence: Tot, target = (Tot * floor(u 2^32)) >> 32,
-//                   the chunk holding the target, then an in-chunk integer scan.
-// Bytes: pass 1 reads B(1+k)V logits once; passes 3-4 read one row (+ one q row on a
-// rejection) per sequence, plus one chunk again.
+//                   difference, f64 accumulation).
+//   2. accept_mass  grid = B * chunks. Every workgroup of sequence b first takes the
+//                   sequence's accept decisions (identically in all of them: row moments
+//                   (m, S) from the chunk statistics, the k tests u*q*S < exp(l_x - m) in
+//                   f64); chunk 0's workgroup writes the accepted drafts, their log-probs,
+//                   n and the descriptor of the final draw. Then each workgroup computes the
+//                   integer mass floor(r_t 2^62) of its chunk of the final draw's row
+//                   (residual max(0, p - q), or p for a bonus draw; p_t from an f64 exp so
+//                   that the only rounding left in the draw is that of S), summed per
+//                   256-logit sub-block and per chunk.
+//   3. draw_pick    one wavefront per sequence: Tot, target = (Tot * floor(u 2^32)) >> 32,
+//                   then three integer prefix searches (chunk, sub-block, 4 logits per lane)
+//                   that recompute only the one sub-block's masses.
+// Bytes: pass 1 reads the B(1+k)V logits once; pass 2 reads one row (+ one q row on a
+// rejection) per sequence; pass 3 reads 1 KB (+ 1 KB) per sequence.
 #include "device_common.h"
 #include "internal.h"
 
-// The draw recomputes each grid mass in two kernels; both must round identically, so no
+// The draw recomputes masses in two kernels; both must round identically, so no
 // floating-point contraction in this file.
 #pragma clang fp contract(off)
 
@@ -32,6 +35,9 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kPerThread = 32;
 constexpr int kChunk = kThreads * kPerThread;  // 8192 logits per chunk
+constexpr int kSub = 4 * kWave;                // 256 logits per draw sub-block
+constexpr int kSubs = kChunk / kSub;           // 32 sub-blocks per chunk
+constexpr int kRowsPerBatch = 16;              // accept rows examined per batch (4 per wave)
 
 struct FinalDraw {
   double m;      // row max
@@ -96,73 +102,19 @@ __global__ __launch_bounds__(kThreads) void chunk_stats_kernel(const float* __re
   }
 }
 
-__device__ void row_moments(const float* cmax, const double* csum, long row, int nch, double& m,
-                            double& S) {
-  float mx = -INFINITY;
-  for (int c = 0; c < nch; ++c) mx = fmaxf(mx, cmax[row * nch + c]);
-  double acc = 0.0;
-  for (int c = 0; c < nch; ++c) {
-    float cm = cmax[row * nch + c];
-    if (cm != -INFINITY) acc += csum[row * nch + c] * exp(double(cm) - double(mx));
+// inclusive prefix sum over the wavefront (integers: exact)
+MOLT_DEV unsigned long long wave_incl_scan(unsigned long long v, int lane) {
+#pragma unroll
+  for (int o = 1; o < kWave; o <<= 1) {
+    const unsigned long long u = __shfl_up(v, o, kWave);
+    if (lane >= o) v += u;
   }
-  m = double(mx);
-  S = acc;
-}
-
-// ---- pass 2 ---------------------------------------------------------------------------
-__global__ __launch_bounds__(kThreads) void accept_kernel(
-    const float* __restrict__ logits, const float* __restrict__ q, const int32_t* __restrict__ drafts,
-    const float* __restrict__ u, int B, int k, int V, int nch, const float* __restrict__ cmax,
-    const double* __restrict__ csum, int32_t* __restrict__ out_tokens, int32_t* __restrict__ out_n,
-    float* __restrict__ out_lp, FinalDraw* __restrict__ fin, int dstride, int doff) {
-  const int b = blockIdx.x * kThreads + threadIdx.x;
-  if (b >= B) return;
-  const long r0 = long(b) * (k + 1);
-  int n = k;
-  int mode = 0, rej_draft = 0;
-  double m = 0.0, S = 1.0;
-  for (int i = 1; i <= k; ++i) {
-    const int row = i - 1;
-    row_moments(cmax, csum, r0 + row, nch, m, S);
-    const int x = drafts[long(b) * dstride + doff + row];
-    bool accept = false;
-    double lx = 0.0;
-    if (x >= 0 && x < V) {
-      lx = double(logits[(r0 + row) * V + x]);
-      const double ex = exp(lx - m);
-      const double qx = q ? double(q[(long(b) * k + row) * V + x]) : 1.0;
-      const double lhs = double(u[r0 + row]) * qx * S;
-      accept = lhs < ex;
-    }
-    if (accept) {
-      out_tokens[r0 + row] = x;
-      if (out_lp) out_lp[r0 + row] = float((lx - m) - log(S));
-    } else {
-      n = row;
-      mode = q ? 1 : 2;
-      rej_draft = x;
-      break;
-    }
-  }
-  if (mode == 0) row_moments(cmax, csum, r0 + k, nch, m, S);  // bonus row k (also k == 0)
-  for (int j = n + 1; j <= k; ++j) {
-    out_tokens[r0 + j] = -1;
-    if (out_lp) out_lp[r0 + j] = __builtin_nanf("");
-  }
-  out_n[b] = n;
-  FinalDraw f;
-  f.m = m;
-  f.S = S;
-  f.row = n;
-  f.mode = mode;
-  f.draft = rej_draft;
-  f.pad = 0;
-  fin[b] = f;
+  return v;
 }
 
 // residual mass of one logit on the 2^62 grid
-__device__ __forceinline__ unsigned long long grid_mass(float l, double m, double invS, int mode,
-                                                        float qv, bool is_draft) {
+MOLT_DEV unsigned long long grid_mass(float l, double m, double invS, int mode, float qv,
+                                      bool is_draft) {
   const double p = exp(double(l) - m) * invS;   // f64: only the rounding of S remains
   double r = p;
   if (mode == 1) r = p - double(qv);
@@ -171,130 +123,303 @@ __device__ __forceinline__ unsigned long long grid_mass(float l, double m, doubl
   return (unsigned long long)(r * 4611686018427387904.0);  // 2^62; truncation == floor
 }
 
-// ---- pass 3 ---------------------------------------------------------------------------
-__global__ __launch_bounds__(kThreads) void draw_mass_kernel(
-    const float* __restrict__ logits, const float* __restrict__ q, int k, int V, int nch,
-    const FinalDraw* __restrict__ fin, unsigned long long* __restrict__ chunk_tot) {
-  __shared__ unsigned long long red[kThreads / kWave];
-  const long id = blockIdx.x;
-  const int b = int(id / nch);
-  const int c = int(id % nch);
-  const FinalDraw f = fin[b];
-  const float* lrow = logits + (long(b) * (k + 1) + f.row) * V;
-  const float* qrow = (f.mode == 1) ? q + (long(b) * k + f.row) * V : nullptr;
-    const double invS = 1.0 / f.S;
-  const int base = c * kChunk;
-  const int n = min(kChunk, V - base);
-  unsigned long long acc = 0;
-  for (int i = threadIdx.x; i < n; i += kThreads) {
-    const int t = base + i;
-    acc += grid_mass(lrow[t], f.m, invS, f.mode, qrow ? qrow[t] : 0.f, t == f.draft);
-  }
-  acc = block_sum<kThreads / kWave, unsigned long long>(acc, red);
-  if (threadIdx.x == 0) chunk_tot[id] = acc;
-}
-
-// ---- pass 4 ---------------------------------------------------------------------------
-__global__ __launch_bounds__(kThreads) void draw_pick_kernel(
-    const float* __restrict__ logits, const float* __restrict__ q, const float* __restrict__ u,
-    int k, int V, int nch, const FinalDraw* __restrict__ fin,
-    unsigned long long* __restrict__ chunk_tot, int32_t* __restrict__ out_tokens,
-    float* __restrict__ out_lp) {
-  __shared__ unsigned long long scan[kThreads];
-  __shared__ unsigned long long s_target;
-  __shared__ int s_chunk, s_mode, s_token;
-  __shared__ unsigned long long red[kThreads / kWave];
-  const int b = blockIdx.x;
-  FinalDraw f = fin[b];
-  const float* lrow = logits + (long(b) * (k + 1) + f.row) * V;
-  const float* qrow = (f.mode == 1) ? q + (long(b) * k + f.row) * V : nullptr;
-    const double invS = 1.0 / f.S;
-  const unsigned long long* tots = chunk_tot + long(b) * nch;
-
-  if (threadIdx.x == 0) {
-    unsigned long long tot = 0;
-    for (int c = 0; c < nch; ++c) tot += tots[c];
-    s_mode = (tot == 0) ? 0 : f.mode;       // vanished residual: fall back to p
-    scan[0] = tot;
-  }
-  __syncthreads();
-  const int mode = s_mode;
-  if (mode != f.mode) {
-    // recompute the per-chunk masses of p (rare degenerate path)
-    for (int c = 0; c < nch; ++c) {
-      unsigned long long acc = 0;
-      const int base = c * kChunk, n = min(kChunk, V - base);
-      for (int i = threadIdx.x; i < n; i += kThreads)
-        acc += grid_mass(lrow[base + i], f.m, invS, 0, 0.f, false);
-      acc = block_sum<kThreads / kWave, unsigned long long>(acc, red);
-      if (threadIdx.x == 0) chunk_tot[long(b) * nch + c] = acc;
-      __syncthreads();
+// Masses of the 4 consecutive logits [t0, t0 + 4) of a draw row (0 past V), summed.
+template <bool kVec>
+MOLT_DEV unsigned long long quad_mass(const float* lrow, const float* qrow, int t0, int V,
+                                      const FinalDraw& f, double invS, int mode,
+                                      unsigned long long (&g)[4]) {
+  float l[4] = {0.f, 0.f, 0.f, 0.f}, qv[4] = {0.f, 0.f, 0.f, 0.f};
+  if (kVec) {
+    if (t0 < V) {       // V % 4 == 0: the quad is all in or all out
+      const float4 a = *reinterpret_cast<const float4*>(lrow + t0);
+      l[0] = a.x; l[1] = a.y; l[2] = a.z; l[3] = a.w;
+      if (mode == 1) {
+        const float4 b = *reinterpret_cast<const float4*>(qrow + t0);
+        qv[0] = b.x; qv[1] = b.y; qv[2] = b.z; qv[3] = b.w;
+      }
     }
-  }
-  if (threadIdx.x == 0) {
-    unsigned long long tot = 0;
-    for (int c = 0; c < nch; ++c) tot += tots[c];
-    const float ub = u[long(b) * (k + 1) + k];
-    const unsigned long long u32 = (unsigned long long)(double(ub) * 4294967296.0);
-    const unsigned long long target = (tot >> 32) * u32 + (((tot & 0xffffffffull) * u32) >> 32);
-    unsigned long long pre = 0;
-    int c = 0;
-    for (; c < nch - 1; ++c) {
-      if (pre + tots[c] > target) break;
-      pre += tots[c];
-    }
-    s_chunk = c;
-    s_target = target - pre;  // offset inside chunk c
-    s_token = -1;
-  }
-  __syncthreads();
-  const int c = s_chunk;
-  const unsigned long long tgt = s_target;
-  // each thread owns kPerThread consecutive logits of the chunk
-  const int base = c * kChunk;
-  const int n = min(kChunk, V - base);
-  const int e0 = threadIdx.x * kPerThread;
-  unsigned long long mass[kPerThread];
-  unsigned long long local = 0;
+  } else {
 #pragma unroll
-  for (int i = 0; i < kPerThread; ++i) {
-    const int e = e0 + i;
-    unsigned long long g = 0;
-    if (e < n) {
-      const int t = base + e;
-      g = grid_mass(lrow[t], f.m, invS, mode, qrow ? qrow[t] : 0.f, t == f.draft);
-    }
-    mass[i] = g;
-    local += g;
-  }
-  // inclusive block scan of the per-thread totals (Hillis-Steele, integers: exact)
-  scan[threadIdx.x] = local;
-  __syncthreads();
-  for (int off = 1; off < kThreads; off <<= 1) {
-    unsigned long long add = threadIdx.x >= off ? scan[threadIdx.x - off] : 0ull;
-    __syncthreads();
-    scan[threadIdx.x] += add;
-    __syncthreads();
-  }
-  const unsigned long long incl = scan[threadIdx.x];
-  const unsigned long long excl = incl - local;
-  if (local > 0 && excl <= tgt && tgt < incl) {
-    unsigned long long run = excl;
-    for (int i = 0; i < kPerThread; ++i) {
-      run += mass[i];
-      if (run > tgt) {
-        s_token = base + e0 + i;
-        break;
+    for (int e = 0; e < 4; ++e) {
+      if (t0 + e < V) {
+        l[e] = lrow[t0 + e];
+        if (mode == 1) qv[e] = qrow[t0 + e];
       }
     }
   }
+  unsigned long long sum = 0;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    g[e] = t0 + e < V ? grid_mass(l[e], f.m, invS, mode, qv[e], t0 + e == f.draft) : 0ull;
+    sum += g[e];
+  }
+  return sum;
+}
+
+// ---- pass 2 ---------------------------------------------------------------------------
+// Logit t of chunk c sits at c*8192 + 2048 w + 256 i + 4 l + e for wavefront w, step i < 8,
+// lane l, e < 4; sub-block 8 w + i is [256 (8 w + i), +256) of the chunk.
+template <bool kVec>
+__global__ __launch_bounds__(kThreads) void accept_mass_kernel(
+    const float* __restrict__ logits, const float* __restrict__ q, const int32_t* __restrict__ drafts,
+    const float* __restrict__ u, int k, int V, int nch, const float* __restrict__ cmax,
+    const double* __restrict__ csum, int dstride, int doff, int32_t* __restrict__ out_tokens,
+    int32_t* __restrict__ out_n, float* __restrict__ out_lp, FinalDraw* __restrict__ fin,
+    unsigned long long* __restrict__ chunk_tot, unsigned long long* __restrict__ sub_tot) {
+  __shared__ double s_m[kRowsPerBatch], s_S[kRowsPerBatch], s_lx[kRowsPerBatch];
+  __shared__ int s_ok[kRowsPerBatch], s_x[kRowsPerBatch];
+  __shared__ int s_n;
+  __shared__ FinalDraw s_fin;
+  __shared__ unsigned long long s_sub[kSubs];
+  const int b = blockIdx.x / nch;
+  const int c = blockIdx.x % nch;
+  const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+  const long r0 = long(b) * (k + 1);
+  const bool writer = c == 0;
+  if (threadIdx.x == 0) s_n = -1;
+  // ---- the sequence's decisions, batches of 16 rows (row r on wavefront r % 4)
+  for (int base = 0; base <= k; base += kRowsPerBatch) {
+    constexpr int kPer = kRowsPerBatch / 4;
+    float cm[kPer];
+    double cs[kPer];
+    int xv[kPer];
+    // issue every load of the batch first: chunk statistics (lane = chunk) and, on lane 0,
+    // the draft id
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {
+      const int r = base + wave + 4 * j;
+      cm[j] = -INFINITY;
+      cs[j] = 0.0;
+      xv[j] = -1;
+      if (r <= k && lane < nch) {
+        cm[j] = cmax[(r0 + r) * nch + lane];
+        cs[j] = csum[(r0 + r) * nch + lane];
+      }
+      if (r < k && lane == 0) xv[j] = drafts[long(b) * dstride + doff + r];
+    }
+    float lxv[kPer];
+    float qxv[kPer];
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {
+      const int r = base + wave + 4 * j;
+      lxv[j] = 0.f;
+      qxv[j] = 1.f;
+      const int x = xv[j];
+      if (r < k && lane == 0 && x >= 0 && x < V) {
+        lxv[j] = logits[(r0 + r) * V + x];
+        if (q) qxv[j] = q[(long(b) * k + r) * V + x];
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {
+      const int r = base + wave + 4 * j;
+      if (r > k) break;
+      // row moments: m = max of the chunk maxima, S = sum csum * exp(cmax - m) (f64)
+      float mx = -INFINITY;
+      for (int cc = lane; cc < nch; cc += kWave) {
+        const float v = cc == lane ? cm[j] : cmax[(r0 + r) * nch + cc];
+        mx = fmaxf(mx, v);
+      }
+      mx = wave_max(mx);
+      double acc = 0.0;
+      for (int cc = lane; cc < nch; cc += kWave) {
+        const float v = cc == lane ? cm[j] : cmax[(r0 + r) * nch + cc];
+        const double sv = cc == lane ? cs[j] : csum[(r0 + r) * nch + cc];
+        if (v != -INFINITY) acc += sv * exp(double(v) - double(mx));
+      }
+      acc = wave_sum(acc);
+      if (lane == 0) {
+        const int i = r - base;
+        const double m = double(mx);
+        s_m[i] = m;
+        s_S[i] = acc;
+        s_x[i] = xv[j];
+        s_ok[i] = 0;
+        if (r < k) {
+          const int x = xv[j];
+          bool accept = false;
+          double lx = 0.0;
+          if (x >= 0 && x < V) {
+            lx = double(lxv[j]);
+            const double ex = exp(lx - m);
+            const double qx = q ? double(qxv[j]) : 1.0;
+            accept = double(u[r0 + r]) * qx * acc < ex;
+          }
+          s_ok[i] = accept;
+          s_lx[i] = lx;
+        }
+      }
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      // first rejection in this batch decides n; accepted rows before it are emitted
+      const int last = min(k, base + kRowsPerBatch - 1);
+      for (int r = base; r <= last; ++r) {
+        const int i = r - base;
+        if (r == k || !s_ok[i]) {
+          s_n = r;
+          FinalDraw f;
+          f.m = s_m[i];
+          f.S = s_S[i];
+          f.row = r;
+          f.mode = r == k ? 0 : (q ? 1 : 2);
+          f.draft = r == k ? -1 : s_x[i];
+          f.pad = 0;
+          s_fin = f;
+          break;
+        }
+        if (writer) {
+          out_tokens[r0 + r] = s_x[i];
+          if (out_lp) out_lp[r0 + r] = float((s_lx[i] - s_m[i]) - log(s_S[i]));
+        }
+      }
+    }
+    __syncthreads();
+    if (s_n >= 0) break;
+  }
+  const FinalDraw f = s_fin;
+  const int n = s_n;
+  if (writer) {
+    for (int j = n + 1 + int(threadIdx.x); j <= k; j += kThreads) {
+      out_tokens[r0 + j] = -1;
+      if (out_lp) out_lp[r0 + j] = __builtin_nanf("");
+    }
+    if (threadIdx.x == 0) {
+      out_n[b] = n;
+      fin[b] = f;
+    }
+  }
+  // ---- integer mass of this chunk of the final draw's row
+  const float* lrow = logits + (r0 + f.row) * V;
+  const float* qrow = f.mode == 1 ? q + (long(b) * k + f.row) * V : nullptr;
+  const double invS = 1.0 / f.S;
+  const int t_base = c * kChunk + 2048 * wave + 4 * lane;
+  unsigned long long part[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    unsigned long long g[4];
+    part[i] = quad_mass<kVec>(lrow, qrow, t_base + kSub * i, V, f, invS, f.mode, g);
+  }
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const unsigned long long sb = wave_sum(part[i]);
+    if (lane == 0) s_sub[8 * wave + i] = sb;
+  }
   __syncthreads();
+  if (threadIdx.x < kSubs) sub_tot[(long(b) * nch + c) * kSubs + threadIdx.x] = s_sub[threadIdx.x];
   if (threadIdx.x == 0) {
-    const int tok = s_token;
-    out_tokens[long(b) * (k + 1) + f.row] = tok;
+    unsigned long long tot = 0;
+    for (int j = 0; j < kSubs; ++j) tot += s_sub[j];
+    chunk_tot[long(b) * nch + c] = tot;
+  }
+}
+
+// ---- pass 3 ---------------------------------------------------------------------------
+// One wavefront per sequence. Zero residual mass (p <= q everywhere after rounding) falls
+// back to p: the chunk and sub-block masses of p are then recomputed here (rare path).
+template <bool kVec>
+__global__ __launch_bounds__(kWave) void draw_pick_kernel(
+    const float* __restrict__ logits, const float* __restrict__ q, const float* __restrict__ u,
+    int k, int V, int nch, const FinalDraw* __restrict__ fin,
+    const unsigned long long* __restrict__ chunk_tot, const unsigned long long* __restrict__ sub_tot,
+    int32_t* __restrict__ out_tokens, float* __restrict__ out_lp) {
+  const int b = blockIdx.x;
+  const int lane = threadIdx.x;
+  const FinalDraw f = fin[b];
+  const float* lrow = logits + (long(b) * (k + 1) + f.row) * V;
+  const float* qrow = f.mode == 1 ? q + (long(b) * k + f.row) * V : nullptr;
+  const double invS = 1.0 / f.S;
+  const unsigned long long* tots = chunk_tot + long(b) * nch;
+  const float ub = u[long(b) * (k + 1) + k];
+  unsigned long long tot = 0;
+  for (int c = lane; c < nch; c += kWave) tot += tots[c];
+  tot = wave_sum(tot);
+  int mode = f.mode;
+  // sum of the masses of sub-block j of chunk c under `mode`, recomputed by the wavefront
+  auto sub_mass = [&](int c, int j, int md) {
+    unsigned long long g[4];
+    const int t0 = c * kChunk + kSub * j + 4 * lane;
+    return wave_sum(quad_mass<kVec>(lrow, qrow, t0, V, f, invS, md, g));
+  };
+  if (tot == 0 && mode != 0) {
+    mode = 0;
+    tot = 0;
+    for (int c = 0; c < nch; ++c)
+      for (int j = 0; j < kSubs; ++j) tot += sub_mass(c, j, 0);
+  }
+  const unsigned long long u32 = (unsigned long long)(double(ub) * 4294967296.0);
+  // target = (tot * u32) >> 32 without a 128-bit type
+  const unsigned long long target = (tot >> 32) * u32 + (((tot & 0xffffffffull) * u32) >> 32);
+  // 1. the chunk holding the target
+  unsigned long long pre = 0;   // mass before the current window
+  int chunk = -1;
+  for (int c0 = 0; c0 < nch && chunk < 0; c0 += kWave) {
+    const int c = c0 + lane;
+    unsigned long long v = 0;
+    if (mode == f.mode) {
+      if (c < nch) v = tots[c];
+    } else {
+      // fallback: chunk masses of p, one chunk at a time (wavefront-wide sums)
+      for (int cc = c0; cc < min(nch, c0 + kWave); ++cc) {
+        unsigned long long sm = 0;
+        for (int j = 0; j < kSubs; ++j) sm += sub_mass(cc, j, 0);
+        if (lane == cc - c0) v = sm;
+      }
+    }
+    const unsigned long long incl = wave_incl_scan(v, lane);
+    const unsigned long long hit = __ballot(c < nch && pre + incl > target);
+    if (hit) {
+      const int l = __builtin_ctzll(hit);
+      chunk = c0 + l;
+      pre += __shfl(incl - v, l, kWave);
+    } else {
+      pre += __shfl(incl, kWave - 1, kWave);
+    }
+  }
+  int token = -1;
+  if (chunk >= 0) {
+    // 2. the sub-block inside the chunk (lanes 0..31 hold the 32 sub-block masses)
+    unsigned long long v = 0;
+    if (mode == f.mode) {
+      if (lane < kSubs) v = sub_tot[(long(b) * nch + chunk) * kSubs + lane];
+    } else {
+      for (int j = 0; j < kSubs; ++j) {
+        const unsigned long long s = sub_mass(chunk, j, 0);
+        if (lane == j) v = s;
+      }
+    }
+    unsigned long long incl = wave_incl_scan(v, lane);
+    unsigned long long hit = __ballot(lane < kSubs && pre + incl > target);
+    if (hit) {
+      const int j = __builtin_ctzll(hit);
+      pre += __shfl(incl - v, j, kWave);
+      // 3. four logits per lane inside the sub-block
+      unsigned long long g[4];
+      const int t0 = chunk * kChunk + kSub * j + 4 * lane;
+      const unsigned long long mine = quad_mass<kVec>(lrow, qrow, t0, V, f, invS, mode, g);
+      incl = wave_incl_scan(mine, lane);
+      hit = __ballot(pre + incl > target);
+      if (hit) {
+        const int l = __builtin_ctzll(hit);
+        if (lane == l) {
+          unsigned long long run = pre + incl - mine;
+          for (int e = 0; e < 4; ++e) {
+            run += g[e];
+            if (run > target) {
+              token = t0 + e;
+              break;
+            }
+          }
+        }
+        token = __shfl(token, l, kWave);
+      }
+    }
+  }
+  if (lane == 0) {
+    out_tokens[long(b) * (k + 1) + f.row] = token;
     if (out_lp)
       out_lp[long(b) * (k + 1) + f.row] =
-          tok >= 0 ? float((double(lrow[tok]) - f.m) - log(f.S)) : __builtin_nanf("");
+          token >= 0 ? float((double(lrow[token]) - f.m) - log(f.S)) : __builtin_nanf("");
   }
 }
 
@@ -310,6 +435,7 @@ size_t sampler_ws_bytes(int B, int k, int V) {
   c.take<double>(rows * nch);
   c.take<FinalDraw>(B);
   c.take<unsigned long long>(long(B) * nch);
+  c.take<unsigned long long>(long(B) * nch * kSubs);
   return c.used + 256;
 }
 
@@ -324,20 +450,26 @@ hipError_t launch_spec_accept(const float* logits, const float* q, const int32_t
   double* csum = c.take<double>(rows * nch);
   FinalDraw* fin = c.take<FinalDraw>(B);
   unsigned long long* ctot = c.take<unsigned long long>(long(B) * nch);
-  const bool vec = (V % 4 == 0) && ((reinterpret_cast<uintptr_t>(logits) & 15) == 0);
-  if (vec)
-    chunk_stats_kernel<true><<<dim3(unsigned(rows * nch)), kThreads, 0, s>>>(logits, rows, V, nch,
-                                                                              cmax, csum);
-  else
-    chunk_stats_kernel<false><<<dim3(unsigned(rows * nch)), kThreads, 0, s>>>(logits, rows, V, nch,
-                                                                               cmax, csum);
-  accept_kernel<<<dim3((B + kThreads - 1) / kThreads), kThreads, 0, s>>>(
-      logits, q, drafts, u, B, k, V, nch, cmax, csum, out_tokens, out_n, out_lp, fin,
-      draft_stride < 0 ? k : draft_stride, draft_offset);
-  draw_mass_kernel<<<dim3(unsigned(long(B) * nch)), kThreads, 0, s>>>(logits, q, k, V, nch, fin,
-                                                                       ctot);
-  draw_pick_kernel<<<dim3(B), kThreads, 0, s>>>(logits, q, u, k, V, nch, fin, ctot, out_tokens,
-                                                out_lp);
+  unsigned long long* stot = c.take<unsigned long long>(long(B) * nch * kSubs);
+  const bool vec = (V % 4 == 0) && ((reinterpret_cast<uintptr_t>(logits) & 15) == 0) &&
+                   (q == nullptr || (reinterpret_cast<uintptr_t>(q) & 15) == 0);
+  const int ds = draft_stride < 0 ? k : draft_stride;
+  const dim3 g1{unsigned(rows * nch)}, g2{unsigned(long(B) * nch)}, g3{unsigned(B)};
+  if (vec) {
+    chunk_stats_kernel<true><<<g1, kThreads, 0, s>>>(logits, rows, V, nch, cmax, csum);
+    accept_mass_kernel<true><<<g2, kThreads, 0, s>>>(logits, q, drafts, u, k, V, nch, cmax, csum,
+                                                     ds, draft_offset, out_tokens, out_n, out_lp,
+                                                     fin, ctot, stot);
+    draw_pick_kernel<true><<<g3, kWave, 0, s>>>(logits, q, u, k, V, nch, fin, ctot, stot,
+                                                out_tokens, out_lp);
+  } else {
+    chunk_stats_kernel<false><<<g1, kThreads, 0, s>>>(logits, rows, V, nch, cmax, csum);
+    accept_mass_kernel<false><<<g2, kThreads, 0, s>>>(logits, q, drafts, u, k, V, nch, cmax, csum,
+                                                      ds, draft_offset, out_tokens, out_n, out_lp,
+                                                      fin, ctot, stot);
+    draw_pick_kernel<false><<<g3, kWave, 0, s>>>(logits, q, u, k, V, nch, fin, ctot, stot,
+                                                 out_tokens, out_lp);
+  }
   return hipGetLastError();
 }
 
