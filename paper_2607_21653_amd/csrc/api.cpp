@@ -425,6 +425,7 @@ int model_ok(const molt_model* m, const molt_kv* kv, int B, int k, bool need_hea
   if (int r = moe_shape_ok(B * (k + 1), m->d_model, m->n_experts, m->top_k, m->d_ff, m->dtype,
                            m->expert_dtype))
     return r;
+  REQUIRE(m->d_model <= 16384, "d_model = %d must be <= 16384", m->d_model);
   REQUIRE(m->rms_eps >= 0.f, "rms_eps must be >= 0");
   REQUIRE(m->rope_theta > 0.f, "rope_theta must be > 0");
   REQUIRE(m->attn_norm && m->w_qkv && m->w_o && m->moe_norm && m->w_router && m->w_gate_up &&

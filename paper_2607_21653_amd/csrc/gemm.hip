@@ -105,7 +105,10 @@ __global__ __launch_bounds__(kThreads) void stream_gemm_kernel(GemmParams p) {
     asrc[i] = static_cast<const uint8_t*>(p.A) + long(min(row0 + 32 * i, last_block)) * RB + threadIdx.x * 16;
   __shared__ __attribute__((aligned(16))) uint8_t alds[2][MS * 4096];
   int32x4_t st0[MS], st1[MS];
-  Slice16 wb[4];
+  // weight slices in flight per wavefront (each 4 KB slice of a wavefront's 32 weight rows
+  // is 16 registers; 8 in flight measured slower than 4)
+  constexpr int WD = 4;
+  Slice16 wb[WD];
   // weights are read once per step: nontemporal loads
   // K slices are visited in an order rotated by the column tile, so the workgroups of one
   // row tile (running side by side on one XCD) read different activation blocks at any
@@ -139,13 +142,13 @@ __global__ __launch_bounds__(kThreads) void stream_gemm_kernel(GemmParams p) {
   MOLT_GLOAD(st0, 0);
   MOLT_GLOAD(st1, 1);
 #pragma unroll
-  for (int s = 0; s < 4; ++s) wld(wb[s], s);
+  for (int s = 0; s < WD; ++s) wld(wb[s], s);
   MOLT_SSTORE(st0, 0);
   MOLT_GLOAD(st0, 2);
   lds_barrier();
   // Step over slice k: LDS buffer U holds its activations, weight slot W its weights,
   // register slot ST_NEXT slice k + 1 (the other slot k + 2). It computes, refills W with
-  // slice k + 4, stores slice k + 1 into buffer 1 - U (last read before the previous
+  // slice k + WD, stores slice k + 1 into buffer 1 - U (last read before the previous
   // barrier) and refills ST_NEXT with slice k + 3. Loads past the end re-read the last slice.
 #define MOLT_STEP(U, ST_NEXT, W, K)                                                                 \
   {                                                                                                  \
@@ -167,7 +170,7 @@ __global__ __launch_bounds__(kThreads) void stream_gemm_kernel(GemmParams p) {
         }                                                                                            \
       }                                                                                              \
     }                                                                                                \
-    wld(wb[W], (K) + 4);                                                                             \
+    wld(wb[W], (K) + WD);                                                                            \
     MOLT_SSTORE(ST_NEXT, 1 - (U));                                                                   \
     MOLT_GLOAD(ST_NEXT, (K) + 3);                                                                    \
     lds_barrier();                                                                                   \

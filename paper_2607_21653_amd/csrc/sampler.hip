@@ -14,8 +14,9 @@
 //                   f64); chunk 0's workgroup writes the accepted drafts, their log-probs,
 //                   n and the descriptor of the final draw. Then each workgroup computes the
 //                   integer mass floor(r_t 2^62) of its chunk of the final draw's row
-//                   (residual max(0, p - q), or p for a bonus draw; p_t from an f64 exp so
-//                   that the only rounding left in the draw is that of S), summed per
+//                   (residual max(0, p - q), or p for a bonus draw; p_t from an f64 exp,
+//                   table-driven, so that the only rounding left in the draw is that of S
+//                   and of the exp's last bit), summed per
 //                   256-logit sub-block and per chunk.
 //   3. draw_pick    one wavefront per sequence: Tot, target = (Tot * floor(u 2^32)) >> 32,
 //                   then three integer prefix searches (chunk, sub-block, 4 logits per lane)
@@ -112,10 +113,36 @@ MOLT_DEV unsigned long long wave_incl_scan(unsigned long long v, int lane) {
   return v;
 }
 
+// f64 exp(x) for x <= 0 by the table-driven method of P. T. P. Tang (ACM TOMS 15(2),
+// 1989): x = (256 m + j) ln2/256 + r with |r| <= ln2/512, exp(x) = 2^m * 2^(j/256) *
+// exp(r), exp(r) - 1 by its degree-5 Taylor polynomial (truncation < 1e-20). tab[j] =
+// 2^(j/256) (f64, built in LDS by exp_table_init). About 1 ulp, like a library exp, at
+// half the instructions: the draw evaluates it for every logit of B rows.
+constexpr double kExpInvL = 0x1.71547652b82fep+8;   // 256 / ln2
+constexpr double kExpLhi = 0x1.62e42fef80000p-9;    // ln2 / 256, 34 significant bits
+constexpr double kExpLlo = 0x1.1cf79abc9e3b4p-44;   // ln2 / 256 - kExpLhi
+
+MOLT_DEV double exp_nonpos(double x, const double* tab) {
+  if (!(x > -746.0)) return 0.0;                     // underflow, -inf (and NaN)
+  const double n = rint(x * kExpInvL);
+  const int N = int(n);
+  double r = fma(-n, kExpLhi, x);                    // exact: n * kExpLhi has <= 53 bits
+  r = fma(-n, kExpLlo, r);
+  const double pr =
+      r * fma(r, fma(r, fma(r, fma(r, 1.0 / 120.0, 1.0 / 24.0), 1.0 / 6.0), 0.5), 1.0);
+  const double t = tab[N & 255];
+  return ldexp(fma(t, pr, t), N >> 8);               // N >> 8 == floor(N / 256)
+}
+
+// tab[j] = 2^(j / 256), j < 256, by nthreads threads; the caller synchronises
+MOLT_DEV void exp_table_init(double* tab, int tid, int nthreads) {
+  for (int j = tid; j < 256; j += nthreads) tab[j] = exp2(double(j) / 256.0);
+}
+
 // residual mass of one logit on the 2^62 grid
 MOLT_DEV unsigned long long grid_mass(float l, double m, double invS, int mode, float qv,
-                                      bool is_draft) {
-  const double p = exp(double(l) - m) * invS;   // f64: only the rounding of S remains
+                                      bool is_draft, const double* tab) {
+  const double p = exp_nonpos(double(l) - m, tab) * invS;   // f64: only S's rounding remains
   double r = p;
   if (mode == 1) r = p - double(qv);
   else if (mode == 2 && is_draft) r = p - 1.0;
@@ -123,34 +150,42 @@ MOLT_DEV unsigned long long grid_mass(float l, double m, double invS, int mode, 
   return (unsigned long long)(r * 4611686018427387904.0);  // 2^62; truncation == floor
 }
 
-// Masses of the 4 consecutive logits [t0, t0 + 4) of a draw row (0 past V), summed.
+// The 4 consecutive logits [t0, t0 + 4) of a draw row and, for a residual draw against a
+// q row, their q values (0 past V). Loads are issued separately from the arithmetic so that
+// a thread's loads are all in flight before the first exp waits on one.
+struct Quad {
+  float l[4], q[4];
+};
+
 template <bool kVec>
-MOLT_DEV unsigned long long quad_mass(const float* lrow, const float* qrow, int t0, int V,
-                                      const FinalDraw& f, double invS, int mode,
-                                      unsigned long long (&g)[4]) {
-  float l[4] = {0.f, 0.f, 0.f, 0.f}, qv[4] = {0.f, 0.f, 0.f, 0.f};
+MOLT_DEV void quad_load(const float* lrow, const float* qrow, int t0, int V, int mode, Quad& d) {
+  // Unconditional loads from clamped addresses (values past V are masked by quad_mass; a
+  // non-residual draw reads its logits row again in place of q): no branch separates a
+  // load from the next one, so none waits for an earlier one to return.
+  const float* qsrc = mode == 1 ? qrow : lrow;
   if (kVec) {
-    if (t0 < V) {       // V % 4 == 0: the quad is all in or all out
-      const float4 a = *reinterpret_cast<const float4*>(lrow + t0);
-      l[0] = a.x; l[1] = a.y; l[2] = a.z; l[3] = a.w;
-      if (mode == 1) {
-        const float4 b = *reinterpret_cast<const float4*>(qrow + t0);
-        qv[0] = b.x; qv[1] = b.y; qv[2] = b.z; qv[3] = b.w;
-      }
-    }
+    const int a = min(t0, V - 4);       // V % 4 == 0, V >= 4: the quad is all in or all out
+    const float4 x = *reinterpret_cast<const float4*>(lrow + a);
+    const float4 y = *reinterpret_cast<const float4*>(qsrc + a);
+    d.l[0] = x.x; d.l[1] = x.y; d.l[2] = x.z; d.l[3] = x.w;
+    d.q[0] = y.x; d.q[1] = y.y; d.q[2] = y.z; d.q[3] = y.w;
   } else {
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      if (t0 + e < V) {
-        l[e] = lrow[t0 + e];
-        if (mode == 1) qv[e] = qrow[t0 + e];
-      }
+      const int a = min(t0 + e, V - 1);
+      d.l[e] = lrow[a];
+      d.q[e] = qsrc[a];
     }
   }
+}
+
+// masses of a loaded quad (0 past V), and their sum
+MOLT_DEV unsigned long long quad_mass(const Quad& d, int t0, int V, const FinalDraw& f, double invS,
+                                      int mode, const double* tab, unsigned long long (&g)[4]) {
   unsigned long long sum = 0;
 #pragma unroll
   for (int e = 0; e < 4; ++e) {
-    g[e] = t0 + e < V ? grid_mass(l[e], f.m, invS, mode, qv[e], t0 + e == f.draft) : 0ull;
+    g[e] = t0 + e < V ? grid_mass(d.l[e], f.m, invS, mode, d.q[e], t0 + e == f.draft, tab) : 0ull;
     sum += g[e];
   }
   return sum;
@@ -171,6 +206,8 @@ __global__ __launch_bounds__(kThreads) void accept_mass_kernel(
   __shared__ int s_n;
   __shared__ FinalDraw s_fin;
   __shared__ unsigned long long s_sub[kSubs];
+  __shared__ double s_tab[256];
+  exp_table_init(s_tab, threadIdx.x, kThreads);   // the batch loop's barriers publish it
   const int b = blockIdx.x / nch;
   const int c = blockIdx.x % nch;
   const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
@@ -294,11 +331,14 @@ __global__ __launch_bounds__(kThreads) void accept_mass_kernel(
   const float* qrow = f.mode == 1 ? q + (long(b) * k + f.row) * V : nullptr;
   const double invS = 1.0 / f.S;
   const int t_base = c * kChunk + 2048 * wave + 4 * lane;
+  Quad qd[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) quad_load<kVec>(lrow, qrow, t_base + kSub * i, V, f.mode, qd[i]);
   unsigned long long part[8];
 #pragma unroll
   for (int i = 0; i < 8; ++i) {
     unsigned long long g[4];
-    part[i] = quad_mass<kVec>(lrow, qrow, t_base + kSub * i, V, f, invS, f.mode, g);
+    part[i] = quad_mass(qd[i], t_base + kSub * i, V, f, invS, f.mode, s_tab, g);
   }
 #pragma unroll
   for (int i = 0; i < 8; ++i) {
@@ -323,8 +363,11 @@ __global__ __launch_bounds__(kWave) void draw_pick_kernel(
     int k, int V, int nch, const FinalDraw* __restrict__ fin,
     const unsigned long long* __restrict__ chunk_tot, const unsigned long long* __restrict__ sub_tot,
     int32_t* __restrict__ out_tokens, float* __restrict__ out_lp) {
+  __shared__ double s_tab[256];
   const int b = blockIdx.x;
   const int lane = threadIdx.x;
+  exp_table_init(s_tab, lane, kWave);
+  __syncthreads();
   const FinalDraw f = fin[b];
   const float* lrow = logits + (long(b) * (k + 1) + f.row) * V;
   const float* qrow = f.mode == 1 ? q + (long(b) * k + f.row) * V : nullptr;
@@ -339,7 +382,9 @@ __global__ __launch_bounds__(kWave) void draw_pick_kernel(
   auto sub_mass = [&](int c, int j, int md) {
     unsigned long long g[4];
     const int t0 = c * kChunk + kSub * j + 4 * lane;
-    return wave_sum(quad_mass<kVec>(lrow, qrow, t0, V, f, invS, md, g));
+    Quad d;
+    quad_load<kVec>(lrow, qrow, t0, V, md, d);
+    return wave_sum(quad_mass(d, t0, V, f, invS, md, s_tab, g));
   };
   if (tot == 0 && mode != 0) {
     mode = 0;
@@ -396,7 +441,9 @@ __global__ __launch_bounds__(kWave) void draw_pick_kernel(
       // 3. four logits per lane inside the sub-block
       unsigned long long g[4];
       const int t0 = chunk * kChunk + kSub * j + 4 * lane;
-      const unsigned long long mine = quad_mass<kVec>(lrow, qrow, t0, V, f, invS, mode, g);
+      Quad d;
+      quad_load<kVec>(lrow, qrow, t0, V, mode, d);
+      const unsigned long long mine = quad_mass(d, t0, V, f, invS, mode, s_tab, g);
       incl = wave_incl_scan(mine, lane);
       hit = __ballot(pre + incl > target);
       if (hit) {
