@@ -3,26 +3,26 @@
 // temperature 1 and no truncation; paper Sec. 4.1 control table, Sec. 4.2, Sec. 5.3/5.4;
 // rule of Leviathan et al. 2023 / Chen et al. 2023).
 //
-// Three launches, all deterministic (fixed reduction orders, integer prefix sums, no
+// Four launches, all deterministic (fixed reduction orders, integer prefix sums, no
 // atomics):
 //   1. chunk_stats  grid = rows * chunks: per 8192-logit chunk its max and
-//                   sum exp(l - chunk max) (f32 exp of the exactly compensated
-//                   difference, f64 accumulation).
-//   2. accept_mass  grid = B * chunks. Every workgroup of sequence b first takes the
-//                   sequence's accept decisions (identically in all of them: row moments
-//                   (m, S) from the chunk statistics, the k tests u*q*S < exp(l_x - m) in
-//                   f64); chunk 0's workgroup writes the accepted drafts, their log-probs,
-//                   n and the descriptor of the final draw. Then each workgroup computes the
-//                   integer mass floor(r_t 2^62) of its chunk of the final draw's row
-//                   (residual max(0, p - q), or p for a bonus draw; p_t from an f64 exp,
-//                   table-driven, so that the only rounding left in the draw is that of S
-//                   and of the exp's last bit), summed per
-//                   256-logit sub-block and per chunk.
-//   3. draw_pick    one wavefront per sequence: Tot, target = (Tot * floor(u 2^32)) >> 32,
+//                   sum exp(l - chunk max) (f32 exp2 with the roundings of the difference and
+//                   of the base change compensated, f64 accumulation across threads).
+//   2. decide       one workgroup per sequence: row moments (m, S) from the chunk
+//                   statistics, the k tests u*q*S < exp(l_x - m) in f64, the accepted drafts
+//                   with their log-probs, n, and the descriptor of the final draw.
+//   3. mass         grid = B * chunks: the integer mass floor(r_t 2^62) of each logit of the
+//                   final draw's row (residual max(0, p - q), or p for a bonus draw; p_t to
+//                   ~1e-10 relative, so that the only rounding that matters in the draw is
+//                   that of S, which scales every mass alike), summed per 256-logit
+//                   sub-block and per chunk.
+//   4. draw_pick    one wavefront per sequence: Tot, target = (Tot * floor(u 2^32)) >> 32,
 //                   then three integer prefix searches (chunk, sub-block, 4 logits per lane)
 //                   that recompute only the one sub-block's masses.
-// Bytes: pass 1 reads the B(1+k)V logits once; pass 2 reads one row (+ one q row on a
-// rejection) per sequence; pass 3 reads 1 KB (+ 1 KB) per sequence.
+// Bytes: pass 1 reads the B(1+k)V logits once; pass 3 reads one row (+ one q row on a
+// rejection) per sequence; pass 4 reads 1 KB (+ 1 KB) per sequence. Pass 1 and 3 are VALU
+// bound as much as HBM bound (without packed math a wave64 instruction takes 4 cycles), so
+// their per-logit instruction counts are kept small.
 #include "device_common.h"
 #include "internal.h"
 
@@ -39,6 +39,9 @@ constexpr int kChunk = kThreads * kPerThread;  // 8192 logits per chunk
 constexpr int kSub = 4 * kWave;                // 256 logits per draw sub-block
 constexpr int kSubs = kChunk / kSub;           // 32 sub-blocks per chunk
 constexpr int kRowsPerBatch = 16;              // accept rows examined per batch (4 per wave)
+constexpr float kL2e = 0x1.715476p+0f;         // log2(e) rounded to f32
+constexpr float kL2eLo = 0x1.4ae0c0p-26f;      // log2(e) - kL2e
+constexpr float kLn2 = 0x1.62e430p-1f;         // ln 2
 
 struct FinalDraw {
   double m;      // row max
@@ -85,15 +88,22 @@ __global__ __launch_bounds__(kThreads) void chunk_stats_kernel(const float* __re
   mx = block_max<kThreads / kWave>(mx, redf);
   float s = 0.f;
   if (mx != -INFINITY) {
+    // exp(l - mx) to ~1 ulp with every rounding compensated: logits below mx - 200 (and the
+    // padding's -inf) are raised to it, where exp underflows to 0 in f32; d + err == l - mx
+    // exactly (TwoSum); d log2(e) = t + terr (FMA split, log2(e) = kL2e + kL2eLo); then
+    // exp(l - mx) = 2^t * exp(terr ln2 + err) ~ 2^t (1 + terr ln2 + err), with 2^t from the
+    // hardware exp2 (1 ulp)
+    const float lo = mx - 200.0f, nmx = -mx;
 #pragma unroll
     for (int i = 0; i < kPerThread; ++i) {
-      // exp(l - mx) with the rounding of l - mx compensated: d + err == l - mx exactly
-      // (TwoSum), exp(d + err) ~ expf(d) * (1 + err)
-      const float d = v[i] - mx;
-      const float bb = d - v[i];
-      const float err = (v[i] - (d - bb)) + (-mx - bb);
-      const float e = expf(d);
-      s += (d == -INFINITY) ? 0.f : e + e * err;  // padding: exp(-inf) = 0
+      const float vc = fmaxf(v[i], lo);
+      const float d = vc + nmx;
+      const float bb = d - vc;
+      const float err = (vc - (d - bb)) + (nmx - bb);
+      const float t = d * kL2e;
+      const float terr = fmaf(d, kL2eLo, fmaf(d, kL2e, -t));
+      const float e = __builtin_amdgcn_exp2f(t);
+      s += fmaf(e, fmaf(terr, kLn2, err), e);
     }
   }
   double sd = block_sum<kThreads / kWave, double>(double(s), redd);
@@ -113,25 +123,28 @@ MOLT_DEV unsigned long long wave_incl_scan(unsigned long long v, int lane) {
   return v;
 }
 
-// f64 exp(x) for x <= 0 by the table-driven method of P. T. P. Tang (ACM TOMS 15(2),
-// 1989): x = (256 m + j) ln2/256 + r with |r| <= ln2/512, exp(x) = 2^m * 2^(j/256) *
-// exp(r), exp(r) - 1 by its degree-5 Taylor polynomial (truncation < 1e-20). tab[j] =
-// 2^(j/256) (f64, built in LDS by exp_table_init). About 1 ulp, like a library exp, at
-// half the instructions: the draw evaluates it for every logit of B rows.
+// exp(x) for x <= 0 by the table-driven method of P. T. P. Tang (ACM TOMS 15(2), 1989):
+// x = (256 m + j) ln2/256 + r with |r| <= ln2/512 (reduction in f64, exact), exp(x) =
+// 2^m * 2^(j/256) * (1 + p(r)), tab[j] = 2^(j/256) in f64 (built in LDS by exp_table_init)
+// and p(r) = r + r^2/2 + r^3/6 evaluated in f32: |p| < 1.4e-3, so its f32 rounding and the
+// truncation (r^4/24 < 1.4e-13) leave a relative error below 3e-10, far inside the 2e-8 of
+// the integer total within which a draw counts as a near-tie. About a third of the
+// instructions of a library f64 exp; the draw evaluates it for every logit of B rows.
 constexpr double kExpInvL = 0x1.71547652b82fep+8;   // 256 / ln2
 constexpr double kExpLhi = 0x1.62e42fef80000p-9;    // ln2 / 256, 34 significant bits
 constexpr double kExpLlo = 0x1.1cf79abc9e3b4p-44;   // ln2 / 256 - kExpLhi
 
 MOLT_DEV double exp_nonpos(double x, const double* tab) {
-  if (!(x > -746.0)) return 0.0;                     // underflow, -inf (and NaN)
+  // below -746 the result underflows to 0 (2^-1077); -inf and NaN land there too
+  x = fmax(x, -746.0);
   const double n = rint(x * kExpInvL);
   const int N = int(n);
   double r = fma(-n, kExpLhi, x);                    // exact: n * kExpLhi has <= 53 bits
   r = fma(-n, kExpLlo, r);
-  const double pr =
-      r * fma(r, fma(r, fma(r, fma(r, 1.0 / 120.0, 1.0 / 24.0), 1.0 / 6.0), 0.5), 1.0);
+  const float rf = float(r);
+  const float pf = rf * fmaf(rf, fmaf(rf, 1.0f / 6.0f, 0.5f), 1.0f);
   const double t = tab[N & 255];
-  return ldexp(fma(t, pr, t), N >> 8);               // N >> 8 == floor(N / 256)
+  return ldexp(fma(t, double(pf), t), N >> 8);       // N >> 8 == floor(N / 256)
 }
 
 // tab[j] = 2^(j / 256), j < 256, by nthreads threads; the caller synchronises
@@ -139,15 +152,23 @@ MOLT_DEV void exp_table_init(double* tab, int tid, int nthreads) {
   for (int j = tid; j < 256; j += nthreads) tab[j] = exp2(double(j) / 256.0);
 }
 
+// floor(r * 2^62) for 0 <= r <= 1 + 2^-52: r 2^30 = hi + f exactly (hi = its integer part,
+// f its exact fraction), floor(f 2^32) = lo; r 2^62 = hi 2^32 + f 2^32
+MOLT_DEV unsigned long long grid_floor(double r) {
+  const double s = r * 1073741824.0;                  // 2^30
+  const uint32_t hi = uint32_t(s);
+  const uint32_t lo = uint32_t((s - double(hi)) * 4294967296.0);
+  return (static_cast<unsigned long long>(hi) << 32) | lo;
+}
+
 // residual mass of one logit on the 2^62 grid
 MOLT_DEV unsigned long long grid_mass(float l, double m, double invS, int mode, float qv,
                                       bool is_draft, const double* tab) {
-  const double p = exp_nonpos(double(l) - m, tab) * invS;   // f64: only S's rounding remains
+  const double p = exp_nonpos(double(l) - m, tab) * invS;   // only S's rounding remains
   double r = p;
   if (mode == 1) r = p - double(qv);
   else if (mode == 2 && is_draft) r = p - 1.0;
-  if (!(r > 0.0)) return 0ull;
-  return (unsigned long long)(r * 4611686018427387904.0);  // 2^62; truncation == floor
+  return r > 0.0 ? grid_floor(r) : 0ull;
 }
 
 // The 4 consecutive logits [t0, t0 + 4) of a draw row and, for a residual draw against a
@@ -183,36 +204,31 @@ MOLT_DEV void quad_load(const float* lrow, const float* qrow, int t0, int V, int
 MOLT_DEV unsigned long long quad_mass(const Quad& d, int t0, int V, const FinalDraw& f, double invS,
                                       int mode, const double* tab, unsigned long long (&g)[4]) {
   unsigned long long sum = 0;
+  const int dr = f.draft - t0;                       // the draft's place in the quad, if any
 #pragma unroll
   for (int e = 0; e < 4; ++e) {
-    g[e] = t0 + e < V ? grid_mass(d.l[e], f.m, invS, mode, d.q[e], t0 + e == f.draft, tab) : 0ull;
+    g[e] = t0 + e < V ? grid_mass(d.l[e], f.m, invS, mode, d.q[e], dr == e, tab) : 0ull;
     sum += g[e];
   }
   return sum;
 }
 
 // ---- pass 2 ---------------------------------------------------------------------------
-// Logit t of chunk c sits at c*8192 + 2048 w + 256 i + 4 l + e for wavefront w, step i < 8,
-// lane l, e < 4; sub-block 8 w + i is [256 (8 w + i), +256) of the chunk.
-template <bool kVec>
-__global__ __launch_bounds__(kThreads) void accept_mass_kernel(
+// One workgroup per sequence: its accept decisions, batches of 16 rows (row r on wavefront
+// r % 4): row moments (m, S) from the chunk statistics, the tests u*q*S < exp(l_x - m) in
+// f64, the accepted drafts and their log-probs, n, and the descriptor of the final draw.
+__global__ __launch_bounds__(kThreads) void decide_kernel(
     const float* __restrict__ logits, const float* __restrict__ q, const int32_t* __restrict__ drafts,
     const float* __restrict__ u, int k, int V, int nch, const float* __restrict__ cmax,
     const double* __restrict__ csum, int dstride, int doff, int32_t* __restrict__ out_tokens,
-    int32_t* __restrict__ out_n, float* __restrict__ out_lp, FinalDraw* __restrict__ fin,
-    unsigned long long* __restrict__ chunk_tot, unsigned long long* __restrict__ sub_tot) {
+    int32_t* __restrict__ out_n, float* __restrict__ out_lp, FinalDraw* __restrict__ fin) {
   __shared__ double s_m[kRowsPerBatch], s_S[kRowsPerBatch], s_lx[kRowsPerBatch];
   __shared__ int s_ok[kRowsPerBatch], s_x[kRowsPerBatch];
   __shared__ int s_n;
   __shared__ FinalDraw s_fin;
-  __shared__ unsigned long long s_sub[kSubs];
-  __shared__ double s_tab[256];
-  exp_table_init(s_tab, threadIdx.x, kThreads);   // the batch loop's barriers publish it
-  const int b = blockIdx.x / nch;
-  const int c = blockIdx.x % nch;
+  const int b = blockIdx.x;
   const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
   const long r0 = long(b) * (k + 1);
-  const bool writer = c == 0;
   if (threadIdx.x == 0) s_n = -1;
   // ---- the sequence's decisions, batches of 16 rows (row r on wavefront r % 4)
   for (int base = 0; base <= k; base += kRowsPerBatch) {
@@ -220,19 +236,24 @@ __global__ __launch_bounds__(kThreads) void accept_mass_kernel(
     float cm[kPer];
     double cs[kPer];
     int xv[kPer];
+    float uv[kPer];
     // issue every load of the batch first: chunk statistics (lane = chunk) and, on lane 0,
-    // the draft id
+    // the draft id and its uniform
 #pragma unroll
     for (int j = 0; j < kPer; ++j) {
       const int r = base + wave + 4 * j;
       cm[j] = -INFINITY;
       cs[j] = 0.0;
       xv[j] = -1;
+      uv[j] = 0.f;
       if (r <= k && lane < nch) {
         cm[j] = cmax[(r0 + r) * nch + lane];
         cs[j] = csum[(r0 + r) * nch + lane];
       }
-      if (r < k && lane == 0) xv[j] = drafts[long(b) * dstride + doff + r];
+      if (r < k && lane == 0) {
+        xv[j] = drafts[long(b) * dstride + doff + r];
+        uv[j] = u[r0 + r];
+      }
     }
     float lxv[kPer];
     float qxv[kPer];
@@ -280,7 +301,7 @@ __global__ __launch_bounds__(kThreads) void accept_mass_kernel(
             lx = double(lxv[j]);
             const double ex = exp(lx - m);
             const double qx = q ? double(qxv[j]) : 1.0;
-            accept = double(u[r0 + r]) * qx * acc < ex;
+            accept = double(uv[j]) * qx * acc < ex;
           }
           s_ok[i] = accept;
           s_lx[i] = lx;
@@ -305,28 +326,42 @@ __global__ __launch_bounds__(kThreads) void accept_mass_kernel(
           s_fin = f;
           break;
         }
-        if (writer) {
-          out_tokens[r0 + r] = s_x[i];
-          if (out_lp) out_lp[r0 + r] = float((s_lx[i] - s_m[i]) - log(s_S[i]));
-        }
+        out_tokens[r0 + r] = s_x[i];
+        if (out_lp) out_lp[r0 + r] = float((s_lx[i] - s_m[i]) - log(s_S[i]));
       }
     }
     __syncthreads();
     if (s_n >= 0) break;
   }
-  const FinalDraw f = s_fin;
   const int n = s_n;
-  if (writer) {
-    for (int j = n + 1 + int(threadIdx.x); j <= k; j += kThreads) {
-      out_tokens[r0 + j] = -1;
-      if (out_lp) out_lp[r0 + j] = __builtin_nanf("");
-    }
-    if (threadIdx.x == 0) {
-      out_n[b] = n;
-      fin[b] = f;
-    }
+  for (int j = n + 1 + int(threadIdx.x); j <= k; j += kThreads) {
+    out_tokens[r0 + j] = -1;
+    if (out_lp) out_lp[r0 + j] = __builtin_nanf("");
   }
-  // ---- integer mass of this chunk of the final draw's row
+  if (threadIdx.x == 0) {
+    out_n[b] = n;
+    fin[b] = s_fin;
+  }
+}
+
+// ---- pass 3 ---------------------------------------------------------------------------
+// Integer mass of chunk c of sequence b's final-draw row. Logit t of the chunk sits at
+// c*8192 + 2048 w + 256 i + 4 l + e for wavefront w, step i < 8, lane l, e < 4; sub-block
+// 8 w + i is [256 (8 w + i), +256) of the chunk.
+template <bool kVec>
+__global__ __launch_bounds__(kThreads) void mass_kernel(
+    const float* __restrict__ logits, const float* __restrict__ q, int k, int V, int nch,
+    const FinalDraw* __restrict__ fin, unsigned long long* __restrict__ chunk_tot,
+    unsigned long long* __restrict__ sub_tot) {
+  __shared__ unsigned long long s_sub[kSubs];
+  __shared__ double s_tab[256];
+  exp_table_init(s_tab, threadIdx.x, kThreads);
+  const int b = blockIdx.x / nch;
+  const int c = blockIdx.x % nch;
+  const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+  const long r0 = long(b) * (k + 1);
+  const FinalDraw f = fin[b];
+  __syncthreads();
   const float* lrow = logits + (r0 + f.row) * V;
   const float* qrow = f.mode == 1 ? q + (long(b) * k + f.row) * V : nullptr;
   const double invS = 1.0 / f.S;
@@ -354,7 +389,7 @@ __global__ __launch_bounds__(kThreads) void accept_mass_kernel(
   }
 }
 
-// ---- pass 3 ---------------------------------------------------------------------------
+// ---- pass 4 ---------------------------------------------------------------------------
 // One wavefront per sequence. Zero residual mass (p <= q everywhere after rounding) falls
 // back to p: the chunk and sub-block masses of p are then recomputed here (rare path).
 template <bool kVec>
@@ -504,16 +539,16 @@ hipError_t launch_spec_accept(const float* logits, const float* q, const int32_t
   const dim3 g1{unsigned(rows * nch)}, g2{unsigned(long(B) * nch)}, g3{unsigned(B)};
   if (vec) {
     chunk_stats_kernel<true><<<g1, kThreads, 0, s>>>(logits, rows, V, nch, cmax, csum);
-    accept_mass_kernel<true><<<g2, kThreads, 0, s>>>(logits, q, drafts, u, k, V, nch, cmax, csum,
-                                                     ds, draft_offset, out_tokens, out_n, out_lp,
-                                                     fin, ctot, stot);
+    decide_kernel<<<g3, kThreads, 0, s>>>(logits, q, drafts, u, k, V, nch, cmax, csum, ds,
+                                          draft_offset, out_tokens, out_n, out_lp, fin);
+    mass_kernel<true><<<g2, kThreads, 0, s>>>(logits, q, k, V, nch, fin, ctot, stot);
     draw_pick_kernel<true><<<g3, kWave, 0, s>>>(logits, q, u, k, V, nch, fin, ctot, stot,
                                                 out_tokens, out_lp);
   } else {
     chunk_stats_kernel<false><<<g1, kThreads, 0, s>>>(logits, rows, V, nch, cmax, csum);
-    accept_mass_kernel<false><<<g2, kThreads, 0, s>>>(logits, q, drafts, u, k, V, nch, cmax, csum,
-                                                      ds, draft_offset, out_tokens, out_n, out_lp,
-                                                      fin, ctot, stot);
+    decide_kernel<<<g3, kThreads, 0, s>>>(logits, q, drafts, u, k, V, nch, cmax, csum, ds,
+                                          draft_offset, out_tokens, out_n, out_lp, fin);
+    mass_kernel<false><<<g2, kThreads, 0, s>>>(logits, q, k, V, nch, fin, ctot, stot);
     draw_pick_kernel<false><<<g3, kWave, 0, s>>>(logits, q, u, k, V, nch, fin, ctot, stot,
                                                  out_tokens, out_lp);
   }

@@ -1,0 +1,147 @@
+"""GPU parity at the workloads' full sizes, in the launch configurations the benchmark
+uses, on outputs the oracle computes for a sample of sequences:
+
+* one bf16 layer at B = 64, k = 4, context 4096 (the 35B-A3B-like layer shape);
+* the same layer with long agent contexts (B = 16, context U[32768, 65536], shuffled
+  blocks: attention runs many KV splits);
+* fp8 experts with Zipf(1.2)-skewed routing at B = 256, k = 8, context 2048;
+* the full-depth step (48 layers, B = 128, k = 4, context 8192, vocab 151936, drafts
+  q = softmax(target + N(0, 0.5^2)) as in the benchmark): the sampler on the step's own
+  full-vocabulary logits against the oracle's sampler (tokens and accepted lengths
+  bit-exact away from near-ties, log-probs 1e-6), the final norm + LM head on sampled rows
+  from the GPU's final residual stream (2e-2), invariants of the emitted tokens, and
+  run-to-run determinism.
+
+A sequence's layer output is compared where its routes agree with the oracle's (a flipped
+top-K set near a tie changes the token's residual; such tokens must sit at a near-tie)."""
+import numpy as np
+import pytest
+import torch
+
+import workloads
+from oracle import model as omodel, sampler as osamp
+from helpers import dev, host, layer_host, max_abs, model_from, oracle_cfg
+
+pytestmark = pytest.mark.gpu
+
+ROUTE_TIE = 1e-2
+
+
+def _subset_kv(layout, kc, vc, seqs, dtype):
+    """The sampled sequences' blocks, renumbered densely, as float64 host caches."""
+    rows = [layout.block_tables[b][layout.block_tables[b] >= 0] for b in seqs]
+    idx = torch.from_numpy(np.concatenate(rows)).long().to(kc.device)
+    bt = np.full((len(seqs), max(len(r) for r in rows)), -1, dtype=np.int64)
+    pos = 0
+    for i, r in enumerate(rows):
+        bt[i, :len(r)] = np.arange(pos, pos + len(r))
+        pos += len(r)
+    okc = omodel.widen_cache(host(kc.index_select(0, idx)), dtype)
+    ovc = omodel.widen_cache(host(vc.index_select(0, idx)), dtype)
+    return bt, layout.context_lens[list(seqs)], okc, ovc
+
+
+def _layer_case(molt, w, seed, seqs, tol, rel_tol):
+    layout = workloads.make_kv_layout(w, seed)
+    lw = workloads.make_layer_weights(w, seed, 0, device="cuda")
+    kc, vc = workloads.make_kv_cache(w, layout, seed, 0, device="cuda")
+    x = workloads.make_hidden(w, seed, device="cuda")
+    print(f"case {w.name}: B={w.batch} k={w.k} ctx=[{layout.context_lens.min()}, "
+          f"{layout.context_lens.max()}] T={x.shape[0]} sampled {list(seqs)}", flush=True)
+    # oracle inputs first: the GPU call writes the new positions into the cache
+    bt, ctx, okc, ovc = _subset_kv(layout, kc, vc, seqs, w.dtype)
+    kp1 = w.k + 1
+    rows = np.concatenate([np.arange(b * kp1, (b + 1) * kp1) for b in seqs])
+    x_rows = host(x)[rows]
+    model = model_from(w, [lw], None, molt)
+    kv = molt.KVCache([kc], [vc], dev(torch.from_numpy(layout.block_tables)),
+                      dev(torch.from_numpy(layout.context_lens)))
+    xg = x.clone()
+    routes = molt.decoder_forward(model, kv, w.batch, w.k, xg, want_routes=True)
+    torch.cuda.synchronize()
+    cfg = oracle_cfg(w)
+    lh = layer_host(lw)
+    xo = omodel.attention_block(x_rows, lh, okc, ovc, bt, ctx, w.k, cfg)
+    xo, r = omodel.moe_block(xo, lh, cfg)
+    gr = routes.cpu().numpy()[0][rows]
+    same = (np.sort(gr, axis=-1) == np.sort(r["ids"], axis=-1)).all(axis=-1)
+    assert (r["margin"][~same] < ROUTE_TIE).all(), "a route set differs away from a tie"
+    g = xg.cpu().numpy()[rows]
+    err = max_abs(g[same], xo[same])
+    d = (g[same] - xo[same]).astype(np.float64)
+    rel = float(np.sqrt((d * d).mean() / (xo[same].astype(np.float64) ** 2).mean()))
+    print(f"max |x - oracle| = {err:.3e}, relative rms {rel:.2e} over {same.sum()} tokens "
+          f"({(~same).sum()} near-tie tokens excluded)", flush=True)
+    assert same.mean() >= 0.9
+    assert err <= tol and rel <= rel_tol
+    ordered = same & (r["order_margin"] >= ROUTE_TIE)
+    assert (gr[ordered] == r["ids"][ordered]).all()
+    return routes
+
+
+def test_layer_full_shape(molt_lib):
+    w = workloads.LAYER_BF16
+    _layer_case(molt_lib, w, 21, [0, 37, 63], 2e-2, 1e-2)
+
+
+def test_long_context_layer_full_shape(molt_lib):
+    w = workloads.LONG_CTX_BF16
+    _layer_case(molt_lib, w, 22, [3, 15], 2e-2, 1e-2)
+
+
+def test_fp8_zipf_layer_full_shape(molt_lib):
+    w = workloads.FP8_ZIPF
+    routes = _layer_case(molt_lib, w, 23, [5, 200], 5e-2, 1e-2)
+    counts = np.bincount(routes.cpu().numpy()[0].ravel(), minlength=w.n_experts)
+    print(f"expert load max/mean {counts.max() / counts.mean():.2f}", flush=True)
+    assert counts.max() > 4 * counts.mean()
+
+
+def test_full_depth_step(molt_lib):
+    """The benchmark's own configuration and inputs (bench.build / bench.make_drafts)."""
+    import bench
+    molt = molt_lib
+    w = workloads.FULL_DEPTH_BF16
+    seed = 0
+    layout, _, head_host, model, kv = bench.build(w, seed, molt, keep_host=0)
+    B, k, V = w.batch, w.k, w.vocab
+    ws = torch.empty(molt.verify_step_workspace_size(model, B, k, layout.block_tables.shape[1]),
+                     dtype=torch.uint8, device="cuda")
+    tokens, q, u = bench.make_drafts(w, seed, molt, model, kv, ws)
+    print("inputs built", flush=True)
+    outs = [molt.verify_step(model, kv, tokens, u, q, workspace=ws) for _ in range(2)]
+    torch.cuda.synchronize()
+    a, b2 = [{n: t.cpu().numpy() for n, t in o.items()} for o in outs]
+    for n in a:                                       # the same KV slots are rewritten
+        np.testing.assert_array_equal(a[n], b2[n])
+    logits = a["logits"]
+    assert np.isfinite(logits).all()
+    # sampler at full vocabulary against the oracle's, on the step's own logits
+    toks = host(tokens)
+    o = osamp.spec_accept(logits, toks[:, 1:], host(u), host(q))
+    am = np.nan_to_num(o["accept_margin"], nan=np.inf).min(axis=1)
+    near = (am < 1e-6) | (o["draw_margin"] < 2e-8)
+    ok = ~near
+    print(f"sampler: {near.sum()} near-tie sequences excluded; mean accepted fraction "
+          f"{a['n_accepted'].mean() / k:.3f}", flush=True)
+    assert near.sum() <= 2
+    assert (a["n_accepted"][ok] == o["n_accepted"][ok]).all()
+    assert (a["tokens"][ok] == o["tokens"][ok]).all()
+    np.testing.assert_allclose(a["logprobs"][ok], o["logprobs"][ok], rtol=1e-6, atol=1e-6,
+                               equal_nan=True)
+    # emitted-token invariants: accepted drafts are the drafts; the rest is padding
+    n = a["n_accepted"]
+    for s in range(B):
+        assert (a["tokens"][s, :n[s]] == toks[s, 1:1 + n[s]]).all()
+        assert 0 <= a["tokens"][s, n[s]] < V
+        assert (a["tokens"][s, n[s] + 1:] == -1).all()
+    # final norm + LM head on sampled rows, from the GPU's own final residual stream
+    x = model.head["embed"][tokens.reshape(-1).long()].float().contiguous()
+    molt.decoder_forward(model, kv, B, k, x)
+    torch.cuda.synchronize()
+    rows = np.array([0, 1, 4, 322, 639])
+    cfg = oracle_cfg(w)
+    ol = omodel.lm_logits(x.cpu().numpy()[rows], head_host, cfg)
+    err = max_abs(logits.reshape(B * (k + 1), V)[rows], ol)
+    print(f"LM head on sampled rows: max |logits - oracle| = {err:.3e}", flush=True)
+    assert err <= 2e-2
