@@ -62,6 +62,69 @@ def attention_bytes(w, ctx):
     return kv + qo
 
 
+def sampler_roofline(w, molt, out, tokens, q, u, reps=20):
+    """The standalone sampler (molt_spec_accept) on the step's own logits, drafts, q and
+    uniforms, timed with HIP events on the library's stream after the timed region.
+    Algorithmic bytes: every logit read once (softmax statistics), then per sequence one
+    full row for the final draw and, when that draw is a residual against q (a rejection),
+    one q row."""
+    import torch
+    B, k, V = w.batch, w.k, w.vocab
+    logits = out["logits"]
+    drafts = tokens[:, 1:].contiguous()
+    ws = torch.empty(molt._lib.load().molt_spec_accept_workspace_size(B, k, V), dtype=torch.uint8,
+                     device=logits.device)
+    res = molt.spec_accept(logits, drafts, u, q, workspace=ws)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        molt.spec_accept(logits, drafts, u, q, workspace=ws, out=res)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    rejected = int((res[1] < k).sum().item())
+    nbytes = B * (k + 1) * V * 4 + B * V * 4 + rejected * V * 4
+    return {"avg_ms": ms, "bytes": nbytes, "rejected": rejected}
+
+
+def other_rooflines(w, groups, samp):
+    """Fractions of roofline of the other spec kernels: the sampler (HBM), the expert
+    GEMMs (HBM: every expert's weights read once per layer; also their raw MFMA rate) and the
+    LM head (MFMA, bf16 dense peak)."""
+    B, k, V, d = w.batch, w.k, w.vocab, w.d_model
+    T = B * (k + 1)
+    out = {}
+    a = samp["bytes"] / (samp["avg_ms"] / 1e3) / 1e9
+    out["sampler"] = {"bound": "hbm", "achieved": round(a, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                      "frac": round(a / HBM_PEAK_GBS, 4), "avg_launch_ms": round(samp["avg_ms"], 4),
+                      "algorithmic_bytes_per_launch": samp["bytes"],
+                      "note": f"molt_spec_accept on the step's logits; {samp['rejected']} of {B} draws residual against q"}
+    t, n = groups["expert_gemm"]
+    if n:
+        pair_ms = 2 * t / n                       # gate_up + down per layer
+        eb = 1 if w.expert_dtype == "fp8" else 2
+        wbytes = w.n_experts * 3 * w.d_ff * d * eb
+        flops = 2.0 * T * w.top_k * 3 * w.d_ff * d
+        a = wbytes / (pair_ms / 1e3) / 1e9
+        mf = flops / (pair_ms / 1e3) / 1e12
+        peak_tf = 5000.0 if eb == 1 else BF16_PEAK_TFLOPS
+        out["expert_gemm"] = {"bound": "hbm", "achieved": round(a, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                              "frac": round(a / HBM_PEAK_GBS, 4), "avg_layer_ms": round(pair_ms, 4),
+                              "algorithmic_bytes_per_layer": wbytes,
+                              "mfma_tflops": round(mf, 1), "mfma_frac": round(mf / peak_tf, 4),
+                              "note": "all experts' weights once per layer (gate_up + down); the MFMA "
+                                      "fraction is capped by arithmetic intensity at this batch"}
+    t, n = groups["lm_head"]
+    if n:
+        ms = t / n
+        tf = 2.0 * T * V * d / (ms / 1e3) / 1e12
+        out["lm_head"] = {"bound": "mfma", "achieved": round(tf, 1), "peak": BF16_PEAK_TFLOPS,
+                          "unit": "TFLOP/s", "frac": round(tf / BF16_PEAK_TFLOPS, 4),
+                          "avg_launch_ms": round(ms, 4)}
+    return out
+
+
 CPU_SAMPLE_SEQS, CPU_SAMPLE_LAYERS = 8, 12
 
 
@@ -245,6 +308,7 @@ def main():
     molt.profile_enable(False)
     groups = {g: molt.profile_read(g) for g in molt._lib.PROF_GROUPS}
     n_break = min(a.steps, 3)
+    samp = sampler_roofline(w, molt, out, tokens, q, u)
     n_acc = out["n_accepted"].cpu().numpy()
     positions = B * (k + 1)
     value = positions / (ms / 1e3)
@@ -284,6 +348,7 @@ def main():
         "kernel_groups": per_group,
         "kernel_groups_note": f"HIP-event times of each group over {n_break} untimed steps after the timed region",
         "lm_head_tflops": round(lm_flops / (lm_ms / max(lm_n, 1) / 1e3) / 1e12, 1) if lm_n else None,
+        "other_rooflines": other_rooflines(w, groups, samp),
     }
     if not a.no_cpu_baseline:
         log("[bench] timing the CPU oracle on a bounded sample")

@@ -65,7 +65,8 @@ MOLT_DEV floatx16_t mfma(const int32x8_t& a, const int32x8_t& b, const floatx16_
 struct Slice16 { int32x4_t c[4]; };   // one lane's 64 bytes of a 32-row x 128-byte tile
 
 template <int BM, bool FP8, int MODE>
-__global__ __launch_bounds__(kThreads) void stream_gemm_kernel(GemmParams p) {
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(BM <= 64 ? 3 : 2)))
+void stream_gemm_kernel(GemmParams p) {
   static_assert(MODE == kGateUp || MODE == kDown, "grouped modes");
   constexpr int MS = BM / 32;                        // 32-row MFMA tiles per wavefront
   constexpr int kElem = FP8 ? 1 : 2;

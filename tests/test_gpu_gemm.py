@@ -1,6 +1,7 @@
 """GPU parity of molt_dense_gemm (the decoder's dense projections and LM head) against a
 float64 product of the same bf16/f32 operands: |C - ref| <= 1e-4 * sqrt(K) * max|a||b|
-(f32 accumulation), at the verify step's shapes and ragged row/column counts."""
+(f32 accumulation), at the verify step's shapes and ragged row/column counts, with and
+without split-K."""
 import numpy as np
 import pytest
 import torch
@@ -14,6 +15,8 @@ pytestmark = pytest.mark.gpu
     (77, 128, 2048, torch.bfloat16, False),     # router, 64-row tiles
     (25, 256, 2048, torch.bfloat16, False),     # 32-row tiles
     (640, 151936, 2048, torch.bfloat16, False), # LM head
+    (200, 131195, 512, torch.bfloat16, True),   # many columns: ragged rows and columns, accumulate
+    (130, 131104, 192, torch.bfloat16, False),  # odd slice count
     (33, 200, 128, torch.bfloat16, False),      # N not a multiple of 128
     (16, 768, 256, torch.float32, True),        # f32 model
 ])
