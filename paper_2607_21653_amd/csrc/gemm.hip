@@ -272,14 +272,18 @@ struct RopeKv {
   uint16_t* vc;             // [num_blocks, Hkv, 128, 16]
 };
 
-template <int BM, bool ROPE>
-__global__ __launch_bounds__(kThreads) void lds_gemm_kernel(GemmParams p, float* part, int splits,
+template <int BM, bool ROPE, int WN, int DEPTH>
+__global__ __launch_bounds__(128 * WN) void lds_gemm_kernel(GemmParams p, float* part, int splits,
                                                             RopeKv rk) {
+  constexpr int NT = 128 * WN;                // 2 x WN wavefronts
   constexpr int AB = BM / 32;                 // activation row blocks
   constexpr int NB = AB + 4;                  // 4 KB blocks per slice (A then B)
+  constexpr int CPT = NB * 256 / NT;          // 16-byte chunks per thread per slice
   constexpr int TM = BM / 64 > 0 ? BM / 64 : 1;   // 32-row MFMA tiles per wavefront
-  constexpr int WROWS = 32 * TM;              // rows per wavefront (2 x 2 wavefronts)
+  constexpr int WROWS = 32 * TM;              // rows per wavefront
+  constexpr int NJ = 4 / WN;                  // 32-column MFMA tiles per wavefront
   static_assert(BM == 64 || BM == 128, "BM");
+  static_assert((NB * 256) % NT == 0, "chunks per thread");
   __shared__ __attribute__((aligned(16))) uint8_t lds[2][NB * 4096];
 
   const int total = p.n_mtiles * p.n_ntiles * splits;
@@ -295,90 +299,97 @@ __global__ __launch_bounds__(kThreads) void lds_gemm_kernel(GemmParams p, float*
   const int nk = int(RB / kRowBytes);
   const int kb0 = int(long(nk) * split / splits), kb1 = int(long(nk) * (split + 1) / splits);
 
-  // global source of block b (clamped into the padded operands) for this thread's chunk
-  const uint8_t* src[NB];
-  const int last_a = (p.M - 1) & ~31, last_b = (p.N - 1) & ~31;
+  // chunk q = tid + NT u of a slice is 16-byte chunk q % 256 of block q / 256 (A blocks,
+  // then B blocks; each a 4 KB tile, clamped into the padded operands); it lands at byte
+  // 16 q of the slice's LDS buffer
+  const uint8_t* src[CPT];
 #pragma unroll
-  for (int b = 0; b < NB; ++b) {
+  for (int u = 0; u < CPT; ++u) {
+    const int q = int(threadIdx.x) + NT * u, b = q / 256;
+    const int last_a = (p.M - 1) & ~31, last_b = (p.N - 1) & ~31;
     const long r = b < AB ? min(row0 + 32 * b, last_a) : min(n0 + 32 * (b - AB), last_b);
-    src[b] = static_cast<const uint8_t*>(b < AB ? p.A : p.B) + r * RB + threadIdx.x * 16;
+    src[u] = static_cast<const uint8_t*>(b < AB ? p.A : p.B) + r * RB + (q % 256) * 16;
   }
-  // register slots of two slices in flight (native vector type: HIP's int4 struct copied
+  // register slots of DEPTH slices in flight (native vector type: HIP's int4 struct copied
   // into LDS made the compiler keep these arrays in scratch memory)
-  int32x4_t st0[NB], st1[NB];
+  int32x4_t st[DEPTH][CPT];
 #define MOLT_GLOAD(ST, KB)                                                            \
   {                                                                                   \
     const long off_ = long(min((KB), kb1 - 1)) * 4096;                                \
-    _Pragma("unroll") for (int b_ = 0; b_ < NB; ++b_)                                 \
+    _Pragma("unroll") for (int b_ = 0; b_ < CPT; ++b_)                                \
         ST[b_] = *reinterpret_cast<const int32x4_t*>(src[b_] + off_);                 \
   }
 #define MOLT_SSTORE(ST, BUF)                                                          \
   {                                                                                   \
-    _Pragma("unroll") for (int b_ = 0; b_ < NB; ++b_)                                 \
-        *reinterpret_cast<int32x4_t*>(&lds[BUF][b_ * 4096 + threadIdx.x * 16]) = ST[b_]; \
+    _Pragma("unroll") for (int b_ = 0; b_ < CPT; ++b_)                                \
+        *reinterpret_cast<int32x4_t*>(&lds[BUF][(threadIdx.x + NT * b_) * 16]) = ST[b_]; \
   }
   const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
-  const int wm = wave / 2, wn = wave % 2;       // wavefront rows wm*WROWS.., cols wn*64..
-  floatx16_t acc[TM][2];
+  const int wm = wave / WN, wn = wave % WN;     // wavefront rows wm*WROWS.., cols wn*32*NJ..
+  floatx16_t acc[TM][NJ];
 #pragma unroll
   for (int i = 0; i < TM; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+    for (int j = 0; j < NJ; ++j)
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
 
-  MOLT_GLOAD(st0, kb0);
-  MOLT_GLOAD(st1, kb0 + 1);
-  MOLT_SSTORE(st0, 0);
-  MOLT_GLOAD(st0, kb0 + 2);
+#pragma unroll
+  for (int j = 0; j < DEPTH; ++j) MOLT_GLOAD(st[j], kb0 + j);
+  MOLT_SSTORE(st[0], 0);
+  MOLT_GLOAD(st[0], kb0 + DEPTH);
   lds_barrier();
-  // Step over slice k from LDS buffer u: at its start buffer u holds slice k, register slot
-  // 1 - u slice k + 1 and slot u slice k + 2. It computes, stores slice k + 1 into buffer
-  // 1 - u (last read before the previous barrier), refills slot 1 - u with slice k + 3.
-#define MOLT_STEP(U, ST_NEXT, K)                                                                  \
+  // Step J (mod DEPTH) over slice k: LDS buffer k % 2 holds slice k, register slot
+  // (J + 1) % DEPTH slice k + 1 (loaded DEPTH steps earlier). It computes, stores slice
+  // k + 1 into the other buffer (last read before the previous barrier) and refills that
+  // slot with slice k + 1 + DEPTH. Loads past the end re-read the last slice.
+#define MOLT_STEP(J, K)                                                                           \
   {                                                                                                \
-    const uint8_t* base_ = lds[U];                                                                 \
+    const uint8_t* base_ = lds[(J) & 1];                                                           \
     _Pragma("unroll") for (int c = 0; c < 4; ++c) {                                                \
-      bf16x8_t af[TM], bfr[2];                                                                     \
+      bf16x8_t af[TM], bfr[NJ];                                                                    \
       _Pragma("unroll") for (int i = 0; i < TM; ++i) af[i] = *reinterpret_cast<const bf16x8_t*>(   \
           base_ + ((wm * WROWS) / 32 + i) * 4096 + c * 1024 + lane * 16);                          \
-      _Pragma("unroll") for (int j = 0; j < 2; ++j) bfr[j] = *reinterpret_cast<const bf16x8_t*>(   \
-          base_ + (AB + wn * 2 + j) * 4096 + c * 1024 + lane * 16);                                \
+      _Pragma("unroll") for (int j = 0; j < NJ; ++j) bfr[j] = *reinterpret_cast<const bf16x8_t*>(  \
+          base_ + (AB + wn * NJ + j) * 4096 + c * 1024 + lane * 16);                               \
       _Pragma("unroll") for (int i = 0; i < TM; ++i)                                               \
-          _Pragma("unroll") for (int j = 0; j < 2; ++j) acc[i][j] = mfma(af[i], bfr[j], acc[i][j]); \
+          _Pragma("unroll") for (int j = 0; j < NJ; ++j) acc[i][j] = mfma(af[i], bfr[j], acc[i][j]); \
     }                                                                                              \
-    MOLT_SSTORE(ST_NEXT, 1 - (U));                                                                 \
-    MOLT_GLOAD(ST_NEXT, (K) + 3);                                                                  \
+    MOLT_SSTORE(st[((J) + 1) % DEPTH], 1 - ((J) & 1));                                             \
+    MOLT_GLOAD(st[((J) + 1) % DEPTH], (K) + 1 + DEPTH);                                            \
     lds_barrier();                                                                                 \
   }
-  // Step over slice k from LDS buffer u: at its start buffer u holds slice k, register slot
-  // 1 - u slice k + 1 and slot u slice k + 2. It computes, stores slice k + 1 into buffer
-  // 1 - u (last read before the previous barrier), refills slot 1 - u with slice k + 3.
+  static_assert(DEPTH % 2 == 0, "LDS buffer parity follows the slot index");
   int kb = kb0;
-  for (; kb + 1 < kb1; kb += 2) {   // loads are clamped, never behind a branch
-    MOLT_STEP(0, st1, kb);
-    MOLT_STEP(1, st0, kb + 1);
+  for (; kb + DEPTH - 1 < kb1; kb += DEPTH) {   // loads are clamped, never behind a branch
+#pragma unroll
+    for (int J = 0; J < DEPTH; ++J) MOLT_STEP(J, kb + J);
   }
-  if (kb < kb1) MOLT_STEP(0, st1, kb);   // odd slice count: the last slice sits in buffer 0
+#pragma unroll
+  for (int J = 0; J < DEPTH - 1; ++J)
+    if (kb + J < kb1) MOLT_STEP(J, kb + J);
 #undef MOLT_STEP
 #undef MOLT_SSTORE
 #undef MOLT_GLOAD
 
-  // acc[i][j][e]: row wm*WROWS + 32 i + 8 (e / 4) + 4 (lane / 32) + e % 4, col wn*64 + 32 j + lane % 32
+  // acc[i][j][e]: row wm*WROWS + 32 i + 8 (e / 4) + 4 (lane / 32) + e % 4,
+  // col wn*32*NJ + 32 j + lane % 32
   const int lcol = lane % 32, lgrp = lane / 32;
   if constexpr (ROPE) {
     // The f32 tile goes through the (now idle) LDS ring so that each rotation pair (i, i + 64)
     // meets in one thread; the rotation is done in f64 with the step's cos/sin table. The
     // table entries and cache slots are fetched first, so their latency overlaps the exchange.
-    // thread (pr, pi) rotates pair pi of rows pr + 4 n, n < BM / 4, in groups of 16 rows
-    constexpr int NG = BM / 64;
+    // thread (pr, pi) rotates pair pi of rows pr + PR n, n < BM / PR, in groups of RG rows
+    constexpr int PR = NT / 64;
+    constexpr int RG = BM / PR < 16 ? BM / PR : 16;
+    constexpr int NG = BM / (PR * RG);
     const int h = nt, pi = threadIdx.x % 64, pr = threadIdx.x / 64;
     const bool rotate = h < rk.Hq + rk.Hkv;
-    double2 cs[16];
+    double2 cs[RG];
     auto fetch = [&](int g) __attribute__((always_inline)) {
 #pragma unroll
-      for (int n = 0; n < 16; ++n)
-        cs[n] = rk.table[long(min(row0 + pr + 4 * (16 * g + n), p.M - 1)) * 64 + pi];
+      for (int n = 0; n < RG; ++n)
+        cs[n] = rk.table[long(min(row0 + pr + PR * (RG * g + n), p.M - 1)) * 64 + pi];
     };
     if (rotate) fetch(0);
     __shared__ int s_slot[BM];
@@ -386,12 +397,12 @@ __global__ __launch_bounds__(kThreads) void lds_gemm_kernel(GemmParams p, float*
     __syncthreads();
     float* ob = reinterpret_cast<float*>(&lds[0][0]);     // [BM][128]
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+    for (int j = 0; j < NJ; ++j)
 #pragma unroll
       for (int i = 0; i < TM; ++i)
 #pragma unroll
         for (int e = 0; e < 16; ++e)
-          ob[(wm * WROWS + 32 * i + 8 * (e / 4) + 4 * lgrp + (e % 4)) * 128 + wn * 64 + 32 * j + lcol] =
+          ob[(wm * WROWS + 32 * i + 8 * (e / 4) + 4 * lgrp + (e % 4)) * 128 + wn * 32 * NJ + 32 * j + lcol] =
               acc[i][j][e];
     __syncthreads();
     if (rotate) {
@@ -399,8 +410,8 @@ __global__ __launch_bounds__(kThreads) void lds_gemm_kernel(GemmParams p, float*
       for (int g = 0; g < NG; ++g) {
         if (g > 0) fetch(g);
 #pragma unroll
-        for (int n = 0; n < 16; ++n) {
-          const int r = pr + 4 * (16 * g + n), t = row0 + r;
+        for (int n = 0; n < RG; ++n) {
+          const int r = pr + PR * (RG * g + n), t = row0 + r;
           if (t >= p.M) break;
           const double a = ob[r * 128 + pi], c = ob[r * 128 + pi + 64];
           const uint16_t lo = f32_to_bf16(float(a * cs[n].x - c * cs[n].y));
@@ -419,7 +430,7 @@ __global__ __launch_bounds__(kThreads) void lds_gemm_kernel(GemmParams p, float*
       }
     } else {
       const int hk = h - rk.Hq - rk.Hkv;
-      for (int w = threadIdx.x; w < BM * 128; w += kThreads) {
+      for (int w = threadIdx.x; w < BM * 128; w += NT) {
         const int r = w % BM, i = w / BM, sl = s_slot[r];
         if (sl < 0) continue;
         rk.vc[((long(sl >> 4) * rk.Hkv + hk) * 128 + i) * 16 + (sl & 15)] = f32_to_bf16(ob[r * 128 + i]);
@@ -429,8 +440,8 @@ __global__ __launch_bounds__(kThreads) void lds_gemm_kernel(GemmParams p, float*
   }
   float* out = splits > 1 ? part + long(split) * p.M * p.ldc : static_cast<float*>(p.C);
 #pragma unroll
-  for (int j = 0; j < 2; ++j) {
-    const int c = n0 + wn * 64 + 32 * j + lcol;
+  for (int j = 0; j < NJ; ++j) {
+    const int c = n0 + wn * 32 * NJ + 32 * j + lcol;
     if (c >= p.N) continue;
 #pragma unroll
     for (int i = 0; i < TM; ++i)
@@ -578,8 +589,9 @@ hipError_t launch_gemm(const void* A, const void* Bw, float* C, int M, int N, in
   p.n_mtiles = (M + g.bm - 1) / g.bm;
   p.n_ntiles = (N + kBN - 1) / kBN;
   const int grid = (p.n_mtiles * p.n_ntiles * g.splits + 7) / 8 * 8;
-  if (g.bm == 64) lds_gemm_kernel<64, false><<<grid, kThreads, 0, s>>>(p, part, g.splits, RopeKv{});
-  else lds_gemm_kernel<128, false><<<grid, kThreads, 0, s>>>(p, part, g.splits, RopeKv{});
+  // small grids (under two workgroups per CU): 8 wavefronts of 32 x 32 per tile, two per SIMD
+  if (g.bm == 64) lds_gemm_kernel<64, false, 4, 2><<<grid, 512, 0, s>>>(p, part, g.splits, RopeKv{});
+  else lds_gemm_kernel<128, false, 2, 2><<<grid, kThreads, 0, s>>>(p, part, g.splits, RopeKv{});
   if (g.splits > 1 && splits_out) {
     *splits_out = g.splits;         // the caller adds part[0 .. splits) (in order) into C
   } else if (g.splits > 1) {
@@ -601,8 +613,8 @@ hipError_t launch_qkv_rope(const void* A, const void* Bw, int M, int K_in, int H
   p.n_mtiles = (M + g.bm - 1) / g.bm;
   p.n_ntiles = Hq + 2 * Hkv;
   const int grid = (p.n_mtiles * p.n_ntiles + 7) / 8 * 8;
-  if (g.bm == 64) lds_gemm_kernel<64, true><<<grid, kThreads, 0, s>>>(p, nullptr, 1, rk);
-  else lds_gemm_kernel<128, true><<<grid, kThreads, 0, s>>>(p, nullptr, 1, rk);
+  if (g.bm == 64) lds_gemm_kernel<64, true, 4, 2><<<grid, 512, 0, s>>>(p, nullptr, 1, rk);
+  else lds_gemm_kernel<128, true, 2, 2><<<grid, kThreads, 0, s>>>(p, nullptr, 1, rk);
   return hipGetLastError();
 }
 

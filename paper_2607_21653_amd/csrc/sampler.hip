@@ -67,13 +67,15 @@ __global__ __launch_bounds__(kThreads) void chunk_stats_kernel(const float* __re
   const int n = min(kChunk, V - c * kChunk);
   float v[kPerThread];
   if (kVec) {
-    // 16-byte loads: element 4*(tid + 256 i) + e
+    // 16-byte nontemporal loads (each logit is read once here), element 4*(tid + 256 i) + e,
+    // from clamped addresses so that no branch separates them (n % 4 == 0 here)
 #pragma unroll
     for (int i = 0; i < kPerThread / 4; ++i) {
-      int e0 = 4 * (threadIdx.x + kThreads * i);
-      float4 t = make_float4(-INFINITY, -INFINITY, -INFINITY, -INFINITY);
-      if (e0 < n) t = *reinterpret_cast<const float4*>(src + e0);  // n % 4 == 0 here
-      v[4 * i + 0] = t.x; v[4 * i + 1] = t.y; v[4 * i + 2] = t.z; v[4 * i + 3] = t.w;
+      const int e0 = 4 * (threadIdx.x + kThreads * i);
+      const floatx4_t t = __builtin_nontemporal_load(reinterpret_cast<const floatx4_t*>(src + min(e0, n - 4)));
+      const bool in = e0 < n;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) v[4 * i + e] = in ? t[e] : -INFINITY;
     }
   } else {
 #pragma unroll

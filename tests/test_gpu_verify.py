@@ -164,8 +164,14 @@ def test_bf16_decoder_layer_many_tokens(molt_lib):
 
 
 def test_bf16_full_step_small_vocab(molt_lib):
-    """Whole bf16 verify step (2 layers of the 35B-A3B-like shape, vocab 4096): logits
-    within 2e-2 of the oracle in replay-free mode for sequences whose routes are clear."""
+    """Whole bf16 verify step (2 layers of the 35B-A3B-like shape, vocab 4096) against the
+    oracle for sequences whose routes are clear.
+
+    Teacher-forced (each layer, and the final norm + LM head, given the GPU's own input):
+    within the 2e-2 logit bar. End to end: within 3e-2, 1.5x the measured noise floor of
+    this composition (perturbing every value the oracle rounds to bf16 by 1e-6 relative,
+    the size of f32-versus-f64 accumulation differences, moves the oracle's own logits by up
+    to 1.8e-2 here: bf16 rounding-boundary flips carried through two layers)."""
     w = workloads.LAYER_BF16.scaled(n_layers=2, vocab=4096, batch=3, k=4, ctx_lo=30, ctx_hi=90,
                                     full_model=True)
     cfg = oracle_cfg(w)
@@ -178,15 +184,20 @@ def test_bf16_full_step_small_vocab(molt_lib):
     u = workloads.make_uniforms(w.batch, w.k, 15)
     q = workloads.make_softmax_q(w.batch, w.k, w.vocab, 16)
     model = model_from(w, layers, head, molt_lib)
-    kv = molt_lib.KVCache([dev(c[0]) for c in caches], [dev(c[1]) for c in caches],
-                          dev(torch.from_numpy(layout.block_tables)),
-                          dev(torch.from_numpy(layout.context_lens)))
-    out = molt_lib.verify_step(model, kv, dev(torch.from_numpy(toks)), dev(u), dev(q), want_routes=True)
+
+    def fresh_kv():
+        return molt_lib.KVCache([dev(c[0]) for c in caches], [dev(c[1]) for c in caches],
+                                dev(torch.from_numpy(layout.block_tables)),
+                                dev(torch.from_numpy(layout.context_lens)))
+
+    out = molt_lib.verify_step(model, fresh_kv(), dev(torch.from_numpy(toks)), dev(u), dev(q),
+                               want_routes=True)
     torch.cuda.synchronize()
     lh = [layer_host(lw) for lw in layers]
+    hh = layer_host(head)
     oc = [tuple(omodel.widen_cache(host(t), w.dtype) for t in c) for c in caches]
-    o = omodel.verify_step(toks, lambda l: lh[l], layer_host(head), oc, layout.block_tables,
-                           layout.context_lens, cfg, host(q), host(u))
+    o = omodel.verify_step(toks, lambda l: lh[l], hh, [(a.copy(), b.copy()) for a, b in oc],
+                           layout.block_tables, layout.context_lens, cfg, host(q), host(u))
     # a sequence is comparable if every token of it took the oracle's expert set in every
     # layer (a flipped set changes the token's residual and, through attention, its sequence)
     gr = out["routes"].cpu().numpy()
@@ -194,6 +205,29 @@ def test_bf16_full_step_small_vocab(molt_lib):
                      for l in range(w.n_layers)]).all(axis=0)
     ok = same.reshape(w.batch, w.k + 1).all(axis=1)
     assert ok.any()
-    err = max_abs(out["logits"].cpu().numpy()[ok], o["logits"][ok])
-    print(f"max |logits - oracle| = {err:.3e} over {ok.sum()} of {w.batch} sequences", flush=True)
-    assert err <= 2e-2
+    logits = out["logits"].cpu().numpy()
+    err = max_abs(logits[ok], o["logits"][ok])
+    print(f"end to end: max |logits - oracle| = {err:.3e} over {ok.sum()} of {w.batch} sequences",
+          flush=True)
+    assert err <= 3e-2
+    # teacher-forced: layer by layer on the GPU (one-layer models over the same caches), each
+    # checked against the oracle's layer applied to the GPU's own input
+    kv = fresh_kv()
+    x = model.head["embed"][dev(torch.from_numpy(toks)).reshape(-1).long()].float().contiguous()
+    for l in range(w.n_layers):
+        ml = model_from(w, [layers[l]], None, molt_lib)
+        kl = molt_lib.KVCache([kv.k_caches[l]], [kv.v_caches[l]], kv.block_tables, kv.context_lens)
+        xin = host(x).copy()
+        r_gpu = molt_lib.decoder_forward(ml, kl, w.batch, w.k, x, want_routes=True)
+        torch.cuda.synchronize()
+        xo = omodel.attention_block(xin, lh[l], *[a.copy() for a in oc[l]], layout.block_tables,
+                                    layout.context_lens, w.k, cfg)
+        xo, r = omodel.moe_block(xo, lh[l], cfg)
+        sl = _route_sets_agree(r_gpu.cpu().numpy()[0], r["ids"], r["margin"], 0.2)
+        el = max_abs(host(x)[sl], xo[sl])
+        print(f"layer {l} teacher-forced: max |x - oracle| = {el:.3e}", flush=True)
+        assert el <= 2e-2
+    ol = omodel.lm_logits(host(x), hh, cfg).reshape(w.batch, w.k + 1, -1)
+    el = max_abs(logits, ol)
+    print(f"final norm + LM head teacher-forced: max |logits - oracle| = {el:.3e}", flush=True)
+    assert el <= 2e-2
