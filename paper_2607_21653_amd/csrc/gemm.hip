@@ -455,6 +455,165 @@ __global__ __launch_bounds__(128 * WN) void lds_gemm_kernel(GemmParams p, float*
   }
 }
 
+// ---------------------------------------------------------------- big-tile dense GEMM
+// The LM head (640 x 151936 x 2048) is bound by what the memory pipeline can hand the
+// MFMAs, so its tile is sized for flops per loaded byte: 160 rows x 256 columns per
+// workgroup, 101 flops per byte (the 128 x 128 LDS-tiled kernel reaches 64). Wavefront w
+// computes all 160 rows x columns 64 w .. 64 w + 63, so the activation tile is shared by the
+// four wavefronts and each weight column block belongs to one of them:
+// * the 5 activation blocks (tiled, 4 KB per K slice) go through a 4-stage LDS ring, copied
+//   by the LDS-DMA form of the buffer load three slices ahead (each wavefront a quarter of
+//   every block; it waits for its own copies and one barrier per slice publishes them);
+// * the wavefront's 2 weight blocks are loaded straight into MFMA operand registers (the
+//   tiled layout is the fragment layout) kBigDepth slices ahead: they never touch LDS.
+// Per 16-wide k step 5 LDS fragments and 2 register fragments feed 10 MFMAs. The barrier
+// sits before the last k step of a slice, so the next slice's first fragments are read
+// behind that step's MFMAs. The row tiles of one column tile are consecutive on one XCD, so
+// its weights come from HBM once.
+constexpr int kBigBM = 160, kBigBN = 256;
+constexpr int kBigAB = kBigBM / 32;            // activation blocks per K slice
+constexpr int kBigAStages = 4;
+constexpr int kBigAStage = kBigAB * 4096;
+constexpr int kBigDepth = 3;                   // weight slices in flight per wavefront
+constexpr int kBigBLoads = 8;                  // weight loads per wavefront per slice
+
+// Buffer resource word 3 for raw byte-addressed loads (32-bit data format, no swizzle).
+constexpr int kRawRsrcWord3 = 0x00020000;
+
+MOLT_DEV __amdgpu_buffer_rsrc_t raw_rsrc(const void* base, long bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, int(bytes), kRawRsrcWord3);
+}
+
+// Each lane copies the 16 bytes at voff + soff of the buffer into LDS at l + 16 * lane
+// (l wave-uniform). The buffer form is a plain vector-memory instruction for the compiler's
+// wait counting (the flat/global form makes it wait for every LDS read in flight).
+MOLT_DEV void lds_dma16(__amdgpu_buffer_rsrc_t r, int voff, int soff, uint8_t* l) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)l, 16, voff, soff, 0, 0);
+}
+
+__global__ __launch_bounds__(kThreads) void bigtile_gemm_kernel(GemmParams p) {
+  __shared__ __attribute__((aligned(16))) uint8_t ring[kBigAStages * kBigAStage];
+  const int total = p.n_mtiles * p.n_ntiles;
+  const int chunk = (total + 7) / 8;
+  const int k8 = blockIdx.x / 8;
+  const int id = (blockIdx.x % 8) * chunk + k8;
+  if (k8 >= chunk || id >= total) return;
+  const int mt = id % p.n_mtiles, nt = id / p.n_mtiles;
+  const int row0 = mt * kBigBM, n0 = nt * kBigBN;
+  const long RB = long(p.K) * 2;
+  const int nk = int(RB / kRowBytes);
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+  const int lane = threadIdx.x % kWave;
+  const int last_a = (p.M - 1) & ~31, last_b = (p.N - 1) & ~31;
+  // byte offsets relative to the activation matrix and to this tile's first weight row; row
+  // blocks past the end re-read the last one (their results are never stored)
+  const __amdgpu_buffer_rsrc_t ra = raw_rsrc(p.A, long(last_a + 32) * RB);
+  const __amdgpu_buffer_rsrc_t rb = raw_rsrc(static_cast<const uint8_t*>(p.B) + long(n0) * RB,
+                                             long(min(n0 + kBigBN, last_b + 32) - n0) * RB);
+  int avoff[kBigAB], bvoff[2];
+#pragma unroll
+  for (int j = 0; j < kBigAB; ++j) avoff[j] = int(min(row0 + 32 * j, last_a) * RB) + wave * 1024 + lane * 16;
+#pragma unroll
+  for (int j = 0; j < 2; ++j) bvoff[j] = int((min(n0 + 64 * wave + 32 * j, last_b) - n0) * RB) + lane * 16;
+  // slices past the end re-copy the last one
+  auto issue_a = [&](int kb) __attribute__((always_inline)) {
+    const int soff = min(kb, nk - 1) * 4096;
+    uint8_t* dst = ring + (kb % kBigAStages) * kBigAStage + wave * 1024;
+#pragma unroll
+    for (int j = 0; j < kBigAB; ++j) lds_dma16(ra, avoff[j], soff, dst + j * 4096);
+  };
+  typedef bf16x8_t BSlice[4][2];   // [k step][column block]
+  auto load_b = [&](int kb, BSlice& b) __attribute__((always_inline)) {
+    const int soff = min(kb, nk - 1) * 4096;
+#pragma unroll
+    for (int c = 0; c < 4; ++c)
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+        b[c][j] = __builtin_bit_cast(bf16x8_t, __builtin_amdgcn_raw_buffer_load_b128(rb, bvoff[j] + c * 1024, soff, 0));
+  };
+  floatx16_t acc[kBigAB][2];
+#pragma unroll
+  for (int i = 0; i < kBigAB; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+  // activation fragments of one k step, two register sets
+  bf16x8_t af[2][kBigAB];
+  auto frag = [&](const uint8_t* base, int c, int set) __attribute__((always_inline)) {
+#pragma unroll
+    for (int i = 0; i < kBigAB; ++i) af[set][i] = *reinterpret_cast<const bf16x8_t*>(base + i * 4096 + c * 1024);
+  };
+  auto step = [&](int set, const bf16x8_t (&b)[2]) __attribute__((always_inline)) {
+    // the scheduler would otherwise sink the next step's reads below these MFMAs
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int i = 0; i < kBigAB; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) acc[i][j] = mfma(af[set][i], b[j], acc[i][j]);
+    __builtin_amdgcn_sched_barrier(0);
+  };
+  BSlice bs[kBigDepth];
+  issue_a(0);
+  issue_a(1);
+  issue_a(2);
+#pragma unroll
+  for (int J = 0; J < kBigDepth; ++J) load_b(J, bs[J]);
+  // slice 0's activations are in (what follows them in the queue may be in flight)
+  asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"n"(2 * kBigAB + kBigBLoads * kBigDepth) : "memory");
+  frag(ring + lane * 16, 0, 0);
+  // Per slice kb the vector-memory queue gets: activations kb + 3 (after the barrier), then
+  // weights kb + depth (after the last MFMAs). The barrier of slice kb needs activations
+  // kb + 1, issued in slice kb - 2; what may still be in flight behind them is at least
+  // weights kb - 2 + depth, activations kb + 2 and weights kb - 1 + depth (exactly that from
+  // slice 2 on, more before), so waiting for that many leaves it complete.
+  constexpr int kAWait = 2 * kBigBLoads + kBigAB;
+  auto body = [&](int kb, BSlice& b) __attribute__((always_inline)) {
+    const uint8_t* base = ring + (kb % kBigAStages) * kBigAStage + lane * 16;
+    frag(base, 1, 1);
+    step(0, b[0]);
+    frag(base, 2, 0);
+    step(1, b[1]);
+    frag(base, 3, 1);
+    step(0, b[2]);
+    // this wavefront's copies of slice kb + 1 are done and all its reads of slice kb - 1's
+    // stage have returned: after the barrier slice kb + 1 is complete for everyone and that
+    // stage takes slice kb + 3
+    asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(kAWait) : "memory");
+    issue_a(kb + 3);
+    frag(ring + ((kb + 1) % kBigAStages) * kBigAStage + lane * 16, 0, 0);
+    step(1, b[3]);
+    load_b(kb + kBigDepth, b);
+  };
+  int kb = 0;
+  for (; kb + kBigDepth - 1 < nk; kb += kBigDepth) {   // register sets are indexed statically
+#pragma unroll
+    for (int J = 0; J < kBigDepth; ++J) body(kb + J, bs[J]);
+  }
+#pragma unroll
+  for (int J = 0; J < kBigDepth - 1; ++J)
+    if (kb + J < nk) body(kb + J, bs[J]);
+  // no copy may still be writing into LDS when the workgroup ends
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  // acc[i][j][e]: row 32 i + 8 (e / 4) + 4 lgrp + e % 4, column 64 wave + 32 j + lcol
+  const int lcol = lane % 32, lgrp = lane / 32;
+  float* C = static_cast<float*>(p.C);
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    const int col = n0 + 64 * wave + 32 * j + lcol;
+    if (col >= p.N) continue;
+#pragma unroll
+    for (int i = 0; i < kBigAB; ++i)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int grow = row0 + 32 * i + 8 * (e / 4) + 4 * lgrp + (e % 4);
+        if (grow >= p.M) continue;
+        float* dst = C + long(grow) * p.ldc + col;
+        *dst = p.accumulate ? *dst + acc[i][j][e] : acc[i][j][e];
+      }
+  }
+}
+
 // C (+)= sum over s of part[s], in split order
 __global__ __launch_bounds__(kThreads) void splitk_reduce_kernel(const float* __restrict__ part,
                                                                  int splits, long n, float* __restrict__ C,
@@ -583,6 +742,16 @@ hipError_t launch_gemm(const void* A, const void* Bw, float* C, int M, int N, in
     p.n_mtiles = (M + 15) / 16;
     p.n_ntiles = (N + 63) / 64;
     f32_gemm_kernel<kDense><<<p.n_mtiles * p.n_ntiles, kThreads, 0, s>>>(p);
+    return hipGetLastError();
+  }
+  if (N >= 8192 && long((M + kBigBM - 1) / kBigBM) * ((N + kBigBN - 1) / kBigBN) >= 512 &&
+      long(M + 31) * 2 * K < (1L << 31) && long(kBigBN) * 2 * K < (1L << 31)) {
+    // many more columns than rows (the LM head): big tiles fed by LDS-DMA (32-bit buffer
+    // offsets: the activations and one tile's weights under 2 GB)
+    p.n_mtiles = (M + kBigBM - 1) / kBigBM;
+    p.n_ntiles = (N + kBigBN - 1) / kBigBN;
+    const int grid = (p.n_mtiles * p.n_ntiles + 7) / 8 * 8;
+    bigtile_gemm_kernel<<<grid, kThreads, 0, s>>>(p);
     return hipGetLastError();
   }
   const GemmPlan g = gemm_plan(M, N, K, part_elems);
