@@ -64,22 +64,13 @@ MOLT_DEV floatx16_t mfma(const int32x8_t& a, const int32x8_t& b, const floatx16_
 // 32-row block of A is one tile column of the tiled activation buffer.
 struct Slice16 { int32x4_t c[4]; };   // one lane's 64 bytes of a 32-row x 128-byte tile
 
+// One (m-tile, n-tile) pair of a grouped launch.
 template <int BM, bool FP8, int MODE>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(BM <= 64 ? 3 : 2)))
-void stream_gemm_kernel(GemmParams p) {
+MOLT_DEV void stream_tile(const GemmParams& p, int id) {
   static_assert(MODE == kGateUp || MODE == kDown, "grouped modes");
   constexpr int MS = BM / 32;                        // 32-row MFMA tiles per wavefront
   constexpr int kElem = FP8 ? 1 : 2;
   __shared__ __attribute__((aligned(16))) float upbuf[MODE == kGateUp ? BM * 64 : 1];
-
-  // Workgroup b runs on XCD b % 8. Each XCD takes one contiguous eighth of the live
-  // (m-tile, n-tile) pairs, m-tile major: the n-tiles of one row tile run back to back on
-  // one XCD, so its activation tile is read from HBM once and then hits that XCD's L2.
-  const int total = *p.n_tiles_live * p.n_ntiles;
-  const int chunk = (total + 7) / 8;
-  const int k8 = blockIdx.x / 8;
-  const int id = (blockIdx.x % 8) * chunk + k8;
-  if (k8 >= chunk || id >= total) return;
   const int mt = id / p.n_ntiles;
   const int nt = id % p.n_ntiles;
   const int4 t = p.tiles[mt];
@@ -241,10 +232,46 @@ void stream_gemm_kernel(GemmParams p) {
   }
 }
 
+// Persistent grouped GEMM: the grid is what the chip holds at once (a multiple of 8, see
+// run_stream). Workgroup b runs on XCD b % 8 and walks that XCD's contiguous eighth of the
+// live (m-tile, n-tile) pairs, m-tile major, with the XCD's workgroup count as stride: the
+// n-tiles of one row tile run side by side on one XCD, so its activation tile is read from
+// HBM once and then hits that XCD's L2. Launching one workgroup per pair left the chip
+// at 50-80% of its resident workgroups on average (dispatch gaps between short tiles).
+template <int BM, bool FP8, int MODE>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(BM <= 64 ? 3 : 2)))
+void stream_gemm_kernel(GemmParams p) {
+  const int total = *p.n_tiles_live * p.n_ntiles;
+  const int chunk = (total + 7) / 8;
+  const int stride = gridDim.x / 8;
+  for (int k8 = blockIdx.x / 8; k8 < chunk; k8 += stride) {
+    const int id = (blockIdx.x % 8) * chunk + k8;
+    if (id >= total) break;
+    stream_tile<BM, FP8, MODE>(p, id);
+  }
+}
+
+// Workgroups of `kernel` (kThreads each) resident on the whole device at once, rounded
+// down to a multiple of 8 (>= 8).
+template <typename K>
+int resident_grid(K kernel) {
+  int dev = 0, cus = 0, per_cu = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, kThreads, 0) != hipSuccess)
+    return 8;
+  return (cus * per_cu) / 8 * 8 > 8 ? (cus * per_cu) / 8 * 8 : 8;
+}
+
 template <bool FP8, int MODE>
 hipError_t run_stream(GemmParams p, int tile_m, hipStream_t s) {
-  int grid = p.n_mtiles * p.n_ntiles;
-  grid = (grid + 7) / 8 * 8;
+  // resident workgroups per kernel, queried once per process (one device model)
+  static const int r32 = resident_grid(stream_gemm_kernel<32, FP8, MODE>);
+  static const int r64 = resident_grid(stream_gemm_kernel<64, FP8, MODE>);
+  static const int r128 = resident_grid(stream_gemm_kernel<128, FP8, MODE>);
+  const int pairs = (p.n_mtiles * p.n_ntiles + 7) / 8 * 8;   // upper bound of the live pairs
+  const int cap = tile_m == 32 ? r32 : tile_m == 64 ? r64 : r128;
+  const int grid = pairs < cap ? pairs : cap;
   if (tile_m == 32) stream_gemm_kernel<32, FP8, MODE><<<grid, kThreads, 0, s>>>(p);
   else if (tile_m == 64) stream_gemm_kernel<64, FP8, MODE><<<grid, kThreads, 0, s>>>(p);
   else stream_gemm_kernel<128, FP8, MODE><<<grid, kThreads, 0, s>>>(p);
