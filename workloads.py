@@ -135,13 +135,14 @@ class KVLayout:
     block_size: int
 
 
-def make_kv_layout(w: Workload, seed: int, spare_blocks: int = 0) -> KVLayout:
+def make_kv_layout(w: Workload, seed: int, spare_blocks: int = 0, extra_tokens: int = 0) -> KVLayout:
     """Context lengths uniform in [ctx_lo, ctx_hi] and a seeded permutation of physical
-    blocks; every sequence owns enough blocks for its context plus the 1+k new tokens."""
+    blocks; every sequence owns enough blocks for its context plus the 1+k new tokens (plus
+    extra_tokens: the draft head writes up to k - 1 positions past them)."""
     g = np.random.Generator(np.random.Philox(_seed(seed, w.name, "ctx")))
     B, bs = w.batch, w.block_size
     ctx = g.integers(w.ctx_lo, w.ctx_hi + 1, size=B).astype(np.int32)
-    need = (ctx.astype(np.int64) + w.k + 1 + bs - 1) // bs
+    need = (ctx.astype(np.int64) + w.k + 1 + extra_tokens + bs - 1) // bs
     max_blocks = int(need.max())
     total = int(need.sum()) + spare_blocks
     perm = g.permutation(total).astype(np.int32)
@@ -222,6 +223,23 @@ def make_head_weights(w: Workload, seed: int, device="cpu") -> dict:
         "embed": _normal((w.vocab, w.d_model), w.weight_std, rng(seed, w.name, "embed", device=device), device, dt),
         "lm_head": _normal((w.vocab, w.d_model), w.weight_std, rng(seed, w.name, "lmhead", device=device), device, dt),
         "final_norm": torch.ones(w.d_model, dtype=torch.float32, device=device),
+    }
+
+
+def make_mtp_weights(w: Workload, seed: int, device="cpu") -> dict:
+    """MTP draft head: norms of the embedding and hidden halves, eh_proj [d, 2d] (input
+    [RMSNorm(e); RMSNorm(h)]), one decoder layer of the target's shape (seeded as layer
+    n_layers) and the head's output norm. Norm gains are 1 + N(0, 0.1^2) so that the halves
+    and the output norm are told apart."""
+    d = w.d_model
+    g = rng(seed, w.name, "mtp_norms", device=device)
+    gains = 1.0 + 0.1 * torch.randn(3, d, generator=g, device=device, dtype=torch.float32)
+    return {
+        "enorm": gains[0].contiguous(), "hnorm": gains[1].contiguous(),
+        "final_norm": gains[2].contiguous(),
+        "eh_proj": _normal((d, 2 * d), w.weight_std, rng(seed, w.name, "mtp_eh", device=device),
+                           device, torch_dtype(w.dtype)),
+        "layer": make_layer_weights(w, seed, w.n_layers, device=device),
     }
 
 
