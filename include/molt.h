@@ -265,13 +265,69 @@ int molt_decoder_forward(const molt_model* m, const molt_kv* kv, int B, int k, f
  *                molt_spec_accept (drafts are tokens[:, 1:])
  *   out_logits   [B, 1+k, V] f32, or NULL (then kept in the workspace)
  *   out_routes   [n_layers, B*(1+k), top_k] i32, or NULL
+ *   out_hidden   [B*(1+k), d] f32 final residual stream (before the final norm), or
+ *                NULL: the input of molt_mtp_draft
  * ---------------------------------------------------------------------------- */
 size_t molt_verify_step_workspace_size(const molt_model* m, int B, int k, int max_blocks_per_seq);
 int molt_verify_step(const molt_model* m, const molt_kv* kv, int B, int k, const int32_t* tokens,
                      const float* draft_probs, const float* uniforms, float* out_logits,
                      int32_t* out_tokens, int32_t* out_num_accepted, float* out_logprobs,
-                     int32_t* out_routes, void* workspace, size_t workspace_bytes,
-                     molt_stream_t stream);
+                     int32_t* out_routes, float* out_hidden, void* workspace,
+                     size_t workspace_bytes, molt_stream_t stream);
+
+/* ------------------------------------------------------------------------------
+ * MTP draft head: the checkpoint's multi-token-prediction head that drafts the k
+ * tokens the next verify step checks (Sec. 4.1 control table: number of
+ * speculative tokens; Sec. 5.4: the MTP head shortens generation about five-fold).
+ * The paper does not print the head; it is the DeepSeek-V3 MTP module: one decoder
+ * layer of the target's structure with its own paged KV cache, sharing the target's
+ * embedding and LM head:
+ *   x = [RMSNorm(Emb(t); enorm) ; RMSNorm(h; hnorm)] eh_proj^T   (halves rounded to dtype)
+ *   x = layer(x);  logits = RMSNorm(x; layer->final_norm) lm_head^T;  q = softmax(logits)
+ * A row (h_p, token at p+1) sits at cache position p and predicts the token at p+2.
+ * ---------------------------------------------------------------------------- */
+typedef struct molt_mtp {
+  const float* enorm;       /* [d] gain of the embedding half                            */
+  const float* hnorm;       /* [d] gain of the hidden-state half                         */
+  const void* eh_proj;      /* [d, 2d] dtype, tiled (molt_pack_weights, row_bytes 2d*es) */
+  const molt_model* layer;  /* the head's decoder layer: n_layers = 1, the target's
+                               d_model/heads/experts/dtypes; layer->final_norm is the
+                               head's output norm; its embed/lm_head/vocab are not used  */
+} molt_mtp;
+
+/* ------------------------------------------------------------------------------
+ * molt_mtp_draft -- one draft step after a verify step of sequence b (context c_b,
+ * tokens x_0..x_k at positions c_b..c_b+k, n_b accepted drafts, emitted token y_b):
+ *  * catch-up: rows j = 0..k at positions c_b + j with h = hidden row b*(1+k)+j and
+ *    token x_{j+1} (j < n_b) or y_b (j >= n_b); row n_b yields draft 1 (rows past n_b
+ *    are computed and ignored; their cache slots are rewritten later);
+ *  * drafting: draft i+1 (i = 1..k-1) from one row at position c_b + n_b + i with h =
+ *    the head's previous output and token = draft i.
+ * Each draft is drawn from q with molt_spec_accept's integer inverse CDF and one
+ * uniform; with out_draft_probs == NULL the drafts are greedy (first argmax of the
+ * logits; verify them with draft_probs = NULL).
+ *   target        the target model (embed, lm_head, vocab, d_model, dtype are used)
+ *   mtp, mtp_kv   the head and its one-layer cache; mtp_kv's block tables and
+ *                 context_lens are the verify step's (c_b, before the caller advances)
+ *   k             >= 1
+ *   hidden        [B*(1+k), d] f32: molt_verify_step's out_hidden
+ *   tokens        [B, 1+k] i32: the verify step's tokens
+ *   n_accepted    [B] i32 in [0, k];  next_tokens [B] i32: out_tokens[b, n_accepted[b]]
+ *   uniforms      [B, k] f32 in [0, 1) (draft i+1 uses uniforms[b, i]); NULL if greedy
+ *   out_drafts    [B, k] i32: the next verify step's drafts
+ *   out_draft_probs [B, k, V] f32: q of each draft (the next verify step's draft_probs),
+ *                 or NULL for greedy drafts
+ * Writes the head's cache at positions c_b .. c_b + k and c_b + n_b + 1 .. c_b + n_b + k
+ * - 1; c_b + max(k, n_b + k - 1) < 16 * max_blocks_per_seq is the caller's duty
+ * (positions past the block table are computed and not written).
+ * ---------------------------------------------------------------------------- */
+size_t molt_mtp_draft_workspace_size(const molt_model* target, const molt_mtp* mtp, int B, int k,
+                                     int max_blocks_per_seq);
+int molt_mtp_draft(const molt_model* target, const molt_mtp* mtp, const molt_kv* mtp_kv, int B,
+                   int k, const float* hidden, const int32_t* tokens, const int32_t* n_accepted,
+                   const int32_t* next_tokens, const float* uniforms, int32_t* out_drafts,
+                   float* out_draft_probs, void* workspace, size_t workspace_bytes,
+                   molt_stream_t stream);
 
 /* ------------------------------------------------------------------------------
  * Kernel-group timing (a measurement aid, not part of the method). While a group is

@@ -38,6 +38,11 @@ class MoltKV(ctypes.Structure):
                 ("block_size", c_int)]
 
 
+class MoltMtp(ctypes.Structure):
+    _fields_ = [("enorm", c_vp), ("hnorm", c_vp), ("eh_proj", c_vp),
+                ("layer", ctypes.POINTER(MoltModel))]
+
+
 _SIGS = {
     "molt_last_error": (ctypes.c_char_p, []),
     "molt_version": (c_int, []),
@@ -61,8 +66,13 @@ _SIGS = {
     "molt_profile_read": (c_int, [c_int, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(c_int)]),
     "molt_verify_step_workspace_size": (c_size, [ctypes.POINTER(MoltModel), c_int, c_int, c_int]),
     "molt_verify_step": (c_int, [ctypes.POINTER(MoltModel), ctypes.POINTER(MoltKV), c_int, c_int,
-                                 c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_size,
-                                 c_vp]),
+                                 c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp,
+                                 c_size, c_vp]),
+    "molt_mtp_draft_workspace_size": (c_size, [ctypes.POINTER(MoltModel), ctypes.POINTER(MoltMtp),
+                                               c_int, c_int, c_int]),
+    "molt_mtp_draft": (c_int, [ctypes.POINTER(MoltModel), ctypes.POINTER(MoltMtp),
+                               ctypes.POINTER(MoltKV), c_int, c_int, c_vp, c_vp, c_vp, c_vp, c_vp,
+                               c_vp, c_vp, c_vp, c_size, c_vp]),
 }
 
 
@@ -361,8 +371,9 @@ def verify_step_workspace_size(model, B, k, max_blocks):
 
 
 def verify_step(model, kv, tokens, uniforms, draft_probs=None, want_logits=True, want_routes=False,
-                workspace=None, out=None):
-    """tokens [B, 1+k] i32. Returns dict(tokens, n_accepted, logprobs, logits?, routes?)."""
+                workspace=None, out=None, want_hidden=False):
+    """tokens [B, 1+k] i32. Returns dict(tokens, n_accepted, logprobs, logits?, routes?,
+    hidden?) (hidden: the final residual stream [B*(1+k), d] f32, the draft head's input)."""
     lib = load()
     B, kp1 = tokens.shape
     k = kp1 - 1
@@ -380,12 +391,67 @@ def verify_step(model, kv, tokens, uniforms, draft_probs=None, want_logits=True,
         if want_routes:
             out["routes"] = torch.empty(model.struct.n_layers, B * kp1, model.struct.top_k,
                                         dtype=torch.int32, device=dev)
+        if want_hidden:
+            out["hidden"] = torch.empty(B * kp1, model.struct.d_model, dtype=torch.float32, device=dev)
     ws, nb = _workspace(verify_step_workspace_size(model, B, k, kv.struct.max_blocks_per_seq), dev, workspace)
     st = lib.molt_verify_step(ctypes.byref(model.struct), ctypes.byref(kv.struct), B, k, _ptr(tokens),
                               _ptr(draft_probs), _ptr(uniforms), _ptr(out.get("logits")),
                               _ptr(out["tokens"]), _ptr(out["n_accepted"]), _ptr(out["logprobs"]),
-                              _ptr(out.get("routes")), _ptr(ws), nb, _stream())
+                              _ptr(out.get("routes")), _ptr(out.get("hidden")), _ptr(ws), nb,
+                              _stream())
     _check(st, "molt_verify_step")
+    return out
+
+
+class Mtp:
+    """The MTP draft head: enorm, hnorm [d] f32, eh_proj [d, 2d] (row-major; packed here
+    into its tiled copy, or already tiled with packed=True), and its decoder layer as a
+    one-layer Model whose head holds the output norm (final_norm)."""
+
+    def __init__(self, enorm, hnorm, eh_proj, layer, final_norm, n_q_heads, n_kv_heads, head_dim,
+                 top_k, rms_eps=1e-6, rope_theta=1e6, packed=False):
+        self.enorm, self.hnorm = enorm, hnorm
+        self.eh_proj = eh_proj if packed else pack_weights(eh_proj)
+        self.layer = Model([layer], {"final_norm": final_norm}, n_q_heads=n_q_heads,
+                           n_kv_heads=n_kv_heads, head_dim=head_dim, top_k=top_k, rms_eps=rms_eps,
+                           rope_theta=rope_theta, packed=packed, vocab=0)
+        s = MoltMtp()
+        s.enorm, s.hnorm, s.eh_proj = enorm.data_ptr(), hnorm.data_ptr(), self.eh_proj.data_ptr()
+        s.layer = ctypes.pointer(self.layer.struct)
+        self.struct = s
+
+
+def mtp_draft_workspace_size(target, mtp, B, k, max_blocks):
+    return load().molt_mtp_draft_workspace_size(ctypes.byref(target.struct), ctypes.byref(mtp.struct),
+                                                B, k, max_blocks)
+
+
+def mtp_draft(target, mtp, kv, hidden, tokens, n_accepted, next_tokens, uniforms=None,
+              greedy=False, workspace=None, out=None):
+    """One draft step after a verify step (molt_mtp_draft). hidden [B*(1+k), d] f32,
+    tokens [B, 1+k] i32, n_accepted [B] i32, next_tokens [B] i32, uniforms [B, k] f32
+    (unused when greedy). Returns dict(drafts [B, k] i32, draft_probs [B, k, V] f32 or None)."""
+    lib = load()
+    B, kp1 = tokens.shape
+    k = kp1 - 1
+    V, d = target.struct.vocab, target.struct.d_model
+    dev = tokens.device
+    _dev(hidden, torch.float32, (B * kp1, d), "hidden")
+    _dev(tokens, torch.int32, name="tokens")
+    _dev(n_accepted, torch.int32, (B,), "n_accepted")
+    _dev(next_tokens, torch.int32, (B,), "next_tokens")
+    if not greedy:
+        _dev(uniforms, torch.float32, (B, k), "uniforms")
+    if out is None:
+        out = {"drafts": torch.empty(B, k, dtype=torch.int32, device=dev),
+               "draft_probs": None if greedy else torch.empty(B, k, V, dtype=torch.float32, device=dev)}
+    ws, nb = _workspace(mtp_draft_workspace_size(target, mtp, B, k, kv.struct.max_blocks_per_seq), dev,
+                        workspace)
+    st = lib.molt_mtp_draft(ctypes.byref(target.struct), ctypes.byref(mtp.struct), ctypes.byref(kv.struct),
+                            B, k, _ptr(hidden), _ptr(tokens), _ptr(n_accepted), _ptr(next_tokens),
+                            _ptr(None if greedy else uniforms), _ptr(out["drafts"]),
+                            _ptr(out["draft_probs"]), _ptr(ws), nb, _stream())
+    _check(st, "molt_mtp_draft")
     return out
 
 

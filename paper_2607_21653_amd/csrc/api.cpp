@@ -598,8 +598,8 @@ size_t molt_verify_step_workspace_size(const molt_model* m, int B, int k, int ma
 int molt_verify_step(const molt_model* m, const molt_kv* kv, int B, int k, const int32_t* tokens,
                      const float* draft_probs, const float* uniforms, float* out_logits,
                      int32_t* out_tokens, int32_t* out_num_accepted, float* out_logprobs,
-                     int32_t* out_routes, void* workspace, size_t workspace_bytes,
-                     molt_stream_t stream) {
+                     int32_t* out_routes, float* out_hidden, void* workspace,
+                     size_t workspace_bytes, molt_stream_t stream) {
   if (int r = model_ok(m, kv, B, k, true)) return r;
   if (int r = spec_accept_shape_ok(B, k, m->vocab)) return r;
   REQUIRE(tokens && uniforms && out_tokens && out_num_accepted, "a required pointer is NULL");
@@ -610,9 +610,10 @@ int molt_verify_step(const molt_model* m, const molt_kv* kv, int B, int k, const
   molt::Carver c(workspace, workspace_bytes);
   StepWs w = carve_step(c, m, B, k, kv->max_blocks_per_seq, true);
   float* logits = out_logits ? out_logits : w.logits;
+  float* x = out_hidden ? out_hidden : w.x;   // the residual stream
   const int T = B * (k + 1);
-  hipError_t e = molt::launch_embed(m->embed, tokens, T, m->d_model, m->vocab, m->dtype, w.x, s);
-  if (e == hipSuccess) e = run_decoder(w.dec, m, kv, B, k, w.x, out_routes, m->final_norm, w.yf, s);
+  hipError_t e = molt::launch_embed(m->embed, tokens, T, m->d_model, m->vocab, m->dtype, x, s);
+  if (e == hipSuccess) e = run_decoder(w.dec, m, kv, B, k, x, out_routes, m->final_norm, w.yf, s);
   if (e == hipSuccess) {
     ProfScope ps(MOLT_PROF_LM_HEAD, s);
     e = molt::launch_gemm(w.yf, m->lm_head, logits, T, m->vocab, m->d_model, m->dtype, false,
@@ -625,6 +626,132 @@ int molt_verify_step(const molt_model* m, const molt_kv* kv, int B, int k, const
                                  out_num_accepted, out_logprobs, w.samp, s, k + 1, 1);
   }
   return hip_status(e, "molt_verify_step");
+}
+
+// ------------------------------------------------------------------ MTP draft head
+
+namespace {
+
+struct MtpWs {
+  int32_t* row_tok; float* u_col; int32_t* ctx_next; int32_t* tok;
+  void* y2; float* part; long part_elems;
+  float* x; void* yf; float* hsel; void* ysel; float* logits; void* draw;
+  DecWs cat, one;   // decoder workspaces of the catch-up rows (B, k) and a drafting row (B, 0)
+};
+
+MtpWs carve_mtp(molt::Carver& c, const molt_model* t, const molt_model* L, int B, int k,
+                int max_blocks) {
+  MtpWs w{};
+  const long T = long(B) * (k + 1);
+  const int d = t->d_model;
+  const size_t es = dt_size(t->dtype);
+  w.row_tok = c.take<int32_t>(T);
+  w.u_col = c.take<float>(B);
+  w.ctx_next = c.take<int32_t>(B);
+  w.tok = c.take<int32_t>(B);
+  w.y2 = c.take<uint8_t>(pad32(T) * 2 * d * es);
+  w.part_elems = gemm_part_elems(int(T), d, 2 * d, t->dtype);
+  w.part = c.take<float>(w.part_elems);
+  w.x = c.take<float>(T * d);
+  w.yf = c.take<uint8_t>(pad32(T) * d * es);
+  w.hsel = c.take<float>(long(B) * d);
+  w.ysel = c.take<uint8_t>(pad32(B) * d * es);
+  w.logits = c.take<float>(long(B) * t->vocab);
+  w.draw = c.take<uint8_t>(molt::draft_draw_ws_bytes(B, t->vocab));
+  w.cat = carve_dec(c, L, B, k, max_blocks);
+  w.one = carve_dec(c, L, B, 0, max_blocks);
+  return w;
+}
+
+int mtp_ok(const molt_model* t, const molt_mtp* mtp, const molt_kv* kv, int B, int k) {
+  REQUIRE(t && mtp && kv, "target, mtp and mtp_kv are required");
+  REQUIRE(mtp->layer, "mtp->layer is NULL");
+  const molt_model* L = mtp->layer;
+  REQUIRE(k >= 1, "k = %d must be >= 1 to draft", k);
+  REQUIRE(act_ok(t->dtype), "target dtype must be F32 or BF16");
+  REQUIRE(t->vocab >= 1 && t->embed && t->lm_head, "the target's embed, lm_head and vocab are required");
+  REQUIRE(L->n_layers == 1, "the head has n_layers = %d, must be 1", L->n_layers);
+  REQUIRE(L->d_model == t->d_model && L->dtype == t->dtype,
+          "the head's d_model/dtype (%d, %d) differ from the target's (%d, %d)", L->d_model,
+          int(L->dtype), t->d_model, int(t->dtype));
+  REQUIRE(mtp->enorm && mtp->hnorm && mtp->eh_proj && L->final_norm,
+          "enorm, hnorm, eh_proj and layer->final_norm are required");
+  REQUIRE(2L * t->d_model * long(dt_size(t->dtype)) % 128 == 0, "2 d * sizeof(dtype) must be a multiple of 128");
+  if (int r = spec_accept_shape_ok(B, 0, t->vocab)) return r;
+  return model_ok(L, kv, B, k, false);
+}
+
+}  // namespace
+
+size_t molt_mtp_draft_workspace_size(const molt_model* target, const molt_mtp* mtp, int B, int k,
+                                     int max_blocks) {
+  if (!target || !mtp || !mtp->layer || B < 1 || k < 1 || max_blocks < 1 || target->vocab < 1 ||
+      !pair_ok(mtp->layer->dtype, mtp->layer->expert_dtype))
+    return 0;
+  molt::Carver c(nullptr, 0);
+  carve_mtp(c, target, mtp->layer, B, k, max_blocks);
+  return c.used + 256;
+}
+
+int molt_mtp_draft(const molt_model* target, const molt_mtp* mtp, const molt_kv* mtp_kv, int B,
+                   int k, const float* hidden, const int32_t* tokens, const int32_t* n_accepted,
+                   const int32_t* next_tokens, const float* uniforms, int32_t* out_drafts,
+                   float* out_draft_probs, void* workspace, size_t workspace_bytes,
+                   molt_stream_t stream) {
+  if (int r = mtp_ok(target, mtp, mtp_kv, B, k)) return r;
+  REQUIRE(hidden && tokens && n_accepted && next_tokens && out_drafts, "a required pointer is NULL");
+  REQUIRE(out_draft_probs == nullptr || uniforms, "sampled drafts (out_draft_probs) need uniforms");
+  if (int r = check_ws(workspace, workspace_bytes,
+                       molt_mtp_draft_workspace_size(target, mtp, B, k, mtp_kv->max_blocks_per_seq)))
+    return r;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  molt::Carver c(workspace, workspace_bytes);
+  MtpWs w = carve_mtp(c, target, mtp->layer, B, k, mtp_kv->max_blocks_per_seq);
+  const molt_model* L = mtp->layer;
+  const int d = target->d_model, V = target->vocab, T = B * (k + 1);
+  const molt_dtype dt = target->dtype;
+  const float* u = out_draft_probs ? uniforms : nullptr;   // greedy drafts draw nothing
+  molt_kv one = *mtp_kv;        // drafting rows: context c_b + n_b + i per sequence
+  one.context_lens = w.ctx_next;
+  hipError_t e = hipSuccess;
+#define RUN(call) do { if ((e = (call)) != hipSuccess) return hip_status(e, "molt_mtp_draft"); } while (0)
+  // catch-up rows
+  RUN(molt::launch_mtp_catchup(tokens, n_accepted, next_tokens, u, B, k, w.row_tok, w.u_col, s));
+  RUN(molt::launch_mtp_input(target->embed, w.row_tok, hidden, mtp->enorm, mtp->hnorm, T, d, V,
+                             L->rms_eps, dt, w.y2, s));
+  {
+    ProfScope ps(MOLT_PROF_PROJECTIONS, s);
+    RUN(molt::launch_gemm(w.y2, mtp->eh_proj, w.x, T, d, 2 * d, dt, false, w.part, w.part_elems, s));
+  }
+  RUN(run_decoder(w.cat, L, mtp_kv, B, k, w.x, nullptr, L->final_norm, w.yf, s));
+  RUN(molt::launch_mtp_select(w.x, w.yf, n_accepted, B, k, d, dt, w.hsel, w.ysel, s));
+  for (int i = 0; i < k; ++i) {
+    {
+      ProfScope ps(MOLT_PROF_LM_HEAD, s);
+      RUN(molt::launch_gemm(i == 0 ? w.ysel : w.yf, target->lm_head, w.logits, B, V, d, dt, false,
+                            nullptr, 0, s));
+    }
+    {
+      ProfScope ps(MOLT_PROF_SAMPLER, s);
+      RUN(molt::launch_draft_draw(w.logits, B, V, u ? w.u_col : nullptr, w.tok,
+                                  out_draft_probs ? out_draft_probs + long(i) * V : nullptr,
+                                  long(k) * V, w.draw, s));
+    }
+    RUN(molt::launch_mtp_record(w.tok, i, B, k, mtp_kv->context_lens, n_accepted, u, out_drafts,
+                                w.row_tok, w.ctx_next, w.u_col, s));
+    if (i + 1 == k) break;
+    // drafting row: the head's previous output and draft i + 1 (the input kernel has read
+    // x before the projection overwrites it)
+    RUN(molt::launch_mtp_input(target->embed, w.row_tok, i == 0 ? w.hsel : w.x, mtp->enorm,
+                               mtp->hnorm, B, d, V, L->rms_eps, dt, w.y2, s));
+    {
+      ProfScope ps(MOLT_PROF_PROJECTIONS, s);
+      RUN(molt::launch_gemm(w.y2, mtp->eh_proj, w.x, B, d, 2 * d, dt, false, w.part, w.part_elems, s));
+    }
+    RUN(run_decoder(w.one, L, &one, B, 0, w.x, nullptr, L->final_norm, w.yf, s));
+  }
+#undef RUN
+  return ok();
 }
 
 }  // extern "C"

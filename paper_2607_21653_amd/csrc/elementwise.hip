@@ -1,6 +1,7 @@
 // Row-wise kernels of the verify step: token embedding, RMSNorm (+ per-row fp8
 // quantisation), fp8 quantisation of tiled rows, RoPE with the paged-KV write of the 1+k
-// new positions, and the weighted expert combine. All are HBM-bound with a few bytes per element; one
+// new positions, and the weighted expert combine; and the MTP draft head's row
+// bookkeeping and input normalisation. All are HBM-bound with a few bytes per element; one
 // workgroup per token row.
 #include "device_common.h"
 #include "internal.h"
@@ -261,6 +262,134 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(const float* __restri
   }
 }
 
+
+// ---------------------------------------------------------------- MTP draft head rows
+// (the head's input halves and the row bookkeeping of its catch-up and drafting rows)
+
+MOLT_DEV int clamp_n(int n, int k) { return n < 0 ? 0 : n > k ? k : n; }
+
+// catch-up row r = b(k+1) + j takes token x_{j+1} (j < n_b) or y_b; u_col[b] = u[b, 0]
+__global__ void mtp_catchup_kernel(const int32_t* __restrict__ tokens,
+                                   const int32_t* __restrict__ n_acc,
+                                   const int32_t* __restrict__ next, const float* __restrict__ u,
+                                   int B, int k, int32_t* __restrict__ row_tok,
+                                   float* __restrict__ u_col) {
+  const int r = blockIdx.x * blockDim.x + threadIdx.x;
+  if (r >= B * (k + 1)) return;
+  const int b = r / (k + 1), j = r % (k + 1);
+  const int nb = clamp_n(n_acc[b], k);
+  row_tok[r] = j < nb ? tokens[r + 1] : next[b];
+  if (j == 0 && u) u_col[b] = u[long(b) * k];
+}
+
+// One normalised half of a head input row: v (8 consecutive elements per run) scaled by
+// 1 / sqrt(mean(v^2) + eps) and g, rounded to dt, stored at columns [col0, col0 + d) of the
+// tiled [rows, 2d] matrix y.
+MOLT_DEV void norm_half_store(float (&v)[kNormRuns][8], const float* __restrict__ g, int d,
+                              float eps, molt_dtype dt, void* __restrict__ y, int t, int col0,
+                              float* red) {
+  float ss = 0.f;
+#pragma unroll
+  for (int r = 0; r < kNormRuns; ++r) {
+    const int i = (threadIdx.x + r * kThreads) * 8;
+    if (i >= d) break;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) ss += v[r][e] * v[r][e];
+  }
+  ss = block_sum<kThreads / kWave, float>(ss, red);
+  const float rs = 1.0f / sqrtf(ss / float(d) + eps);
+  const long es = dt == MOLT_BF16 ? 2 : 4, rb = 2L * d * es;
+#pragma unroll
+  for (int r = 0; r < kNormRuns; ++r) {
+    const int i = (threadIdx.x + r * kThreads) * 8;
+    if (i >= d) break;
+    float o[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      o[e] = v[r][e] * rs * g[i + e];
+      if (dt == MOLT_BF16) o[e] = round_to_bf16(o[e]);
+    }
+    uint8_t* yb = static_cast<uint8_t*>(y);
+    if (dt == MOLT_BF16) {
+      uint32_t pk[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        pk[e] = uint32_t(f32_to_bf16(o[2 * e])) | (uint32_t(f32_to_bf16(o[2 * e + 1])) << 16);
+      *reinterpret_cast<uint4*>(yb + tiled_offset(t, 2L * (col0 + i), rb)) =
+          make_uint4(pk[0], pk[1], pk[2], pk[3]);
+    } else {
+      *reinterpret_cast<float4*>(yb + tiled_offset(t, 4L * (col0 + i), rb)) =
+          make_float4(o[0], o[1], o[2], o[3]);
+      *reinterpret_cast<float4*>(yb + tiled_offset(t, 4L * (col0 + i + 4), rb)) =
+          make_float4(o[4], o[5], o[6], o[7]);
+    }
+  }
+}
+
+// y[t] = [RMSNorm(Emb[tok[t]]; ge) ; RMSNorm(h[t]; gh)], each half rounded to dt, tiled
+// [rows padded to 32, 2d] (an out-of-range token gives a zero embedding half)
+__global__ __launch_bounds__(kThreads) void mtp_input_kernel(
+    const void* __restrict__ embed, const int32_t* __restrict__ tok, const float* __restrict__ h,
+    const float* __restrict__ ge, const float* __restrict__ gh, int d, int V, float eps,
+    molt_dtype dt, void* __restrict__ y) {
+  __shared__ float red[kThreads / kWave];
+  const int t = blockIdx.x;
+  const int id = tok[t];
+  const bool ok = id >= 0 && id < V;
+  float v[kNormRuns][8];
+#pragma unroll
+  for (int r = 0; r < kNormRuns; ++r) {
+    const int i = (threadIdx.x + r * kThreads) * 8;
+    if (i >= d) break;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[r][e] = ok ? load_act(embed, long(id) * d + i + e, dt) : 0.f;
+  }
+  norm_half_store(v, ge, d, eps, dt, y, t, 0, red);
+  const float* hr = h + long(t) * d;
+#pragma unroll
+  for (int r = 0; r < kNormRuns; ++r) {
+    const int i = (threadIdx.x + r * kThreads) * 8;
+    if (i >= d) break;
+    const float4 a = *reinterpret_cast<const float4*>(hr + i);
+    const float4 b = *reinterpret_cast<const float4*>(hr + i + 4);
+    v[r][0] = a.x; v[r][1] = a.y; v[r][2] = a.z; v[r][3] = a.w;
+    v[r][4] = b.x; v[r][5] = b.y; v[r][6] = b.z; v[r][7] = b.w;
+  }
+  norm_half_store(v, gh, d, eps, dt, y, t, d, red);
+}
+
+// row b of hsel / ysel = catch-up row b(k+1) + n_b of x (f32 [T, d]) / yf (tiled [T, d] dt)
+__global__ __launch_bounds__(kThreads) void mtp_select_kernel(
+    const float* __restrict__ x, const uint8_t* __restrict__ yf, const int32_t* __restrict__ n_acc,
+    int k, int d, int es, float* __restrict__ hsel, uint8_t* __restrict__ ysel) {
+  const int b = blockIdx.x;
+  const long src = long(b) * (k + 1) + clamp_n(n_acc[b], k);
+  for (int i = threadIdx.x * 4; i < d; i += kThreads * 4)
+    *reinterpret_cast<float4*>(hsel + long(b) * d + i) = *reinterpret_cast<const float4*>(x + src * d + i);
+  const long rb = long(d) * es;
+  for (long c = threadIdx.x; c < rb / 16; c += kThreads)   // 16 bytes of a row are contiguous
+    *reinterpret_cast<uint4*>(ysel + tiled_offset(b, 16 * c, rb)) =
+        *reinterpret_cast<const uint4*>(yf + tiled_offset(src, 16 * c, rb));
+}
+
+// after draft i + 1 is drawn (tok): drafts[b, i] = tok[b]; for the next drafting row its
+// token, its context (position c_b + n_b + i + 1 is the row's own) and its uniform
+__global__ void mtp_record_kernel(const int32_t* __restrict__ tok, int i, int B, int k,
+                                  const int32_t* __restrict__ ctx, const int32_t* __restrict__ n_acc,
+                                  const float* __restrict__ u, int32_t* __restrict__ drafts,
+                                  int32_t* __restrict__ row_tok, int32_t* __restrict__ ctx_next,
+                                  float* __restrict__ u_col) {
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b >= B) return;
+  const int t = tok[b];
+  drafts[long(b) * k + i] = t;
+  if (i + 1 < k) {
+    row_tok[b] = t;
+    ctx_next[b] = ctx[b] + clamp_n(n_acc[b], k) + i + 1;
+    if (u) u_col[b] = u[long(b) * k + i + 1];
+  }
+}
+
 }  // namespace
 
 hipError_t launch_embed(const void* table, const int32_t* tokens, int T, int d, int V,
@@ -309,6 +438,38 @@ hipError_t launch_quant_rows_tiled(const uint16_t* h, const int32_t* pperm, cons
 hipError_t launch_combine(const float* o, const float* w, int T, int K, int d, float* out,
                           bool accumulate, hipStream_t s) {
   combine_kernel<<<T, kThreads, 0, s>>>(o, w, K, d, out, accumulate);
+  return hipGetLastError();
+}
+
+hipError_t launch_mtp_catchup(const int32_t* tokens, const int32_t* n_acc, const int32_t* next,
+                              const float* u, int B, int k, int32_t* row_tok, float* u_col,
+                              hipStream_t s) {
+  const int T = B * (k + 1);
+  mtp_catchup_kernel<<<(T + kThreads - 1) / kThreads, kThreads, 0, s>>>(tokens, n_acc, next, u, B, k,
+                                                                       row_tok, u_col);
+  return hipGetLastError();
+}
+
+hipError_t launch_mtp_input(const void* embed, const int32_t* tok, const float* h, const float* ge,
+                            const float* gh, int T, int d, int V, float eps, molt_dtype dt,
+                            void* y, hipStream_t s) {
+  mtp_input_kernel<<<T, kThreads, 0, s>>>(embed, tok, h, ge, gh, d, V, eps, dt, y);
+  return hipGetLastError();
+}
+
+hipError_t launch_mtp_select(const float* x, const void* yf, const int32_t* n_acc, int B, int k,
+                             int d, molt_dtype dt, float* hsel, void* ysel, hipStream_t s) {
+  mtp_select_kernel<<<B, kThreads, 0, s>>>(x, static_cast<const uint8_t*>(yf), n_acc, k, d,
+                                           dt == MOLT_BF16 ? 2 : 4, hsel,
+                                           static_cast<uint8_t*>(ysel));
+  return hipGetLastError();
+}
+
+hipError_t launch_mtp_record(const int32_t* tok, int i, int B, int k, const int32_t* ctx,
+                             const int32_t* n_acc, const float* u, int32_t* drafts,
+                             int32_t* row_tok, int32_t* ctx_next, float* u_col, hipStream_t s) {
+  mtp_record_kernel<<<(B + kThreads - 1) / kThreads, kThreads, 0, s>>>(tok, i, B, k, ctx, n_acc, u,
+                                                                      drafts, row_tok, ctx_next, u_col);
   return hipGetLastError();
 }
 

@@ -31,6 +31,13 @@ hipError_t launch_spec_accept(const float* logits, const float* q, const int32_t
                               int32_t* out_n, float* out_lp, void* ws, hipStream_t s,
                               int draft_stride = -1, int draft_offset = 0);
 
+// Draws of the MTP draft head, one per row: token ~ softmax(logits[b]) by the integer
+// inverse CDF of launch_spec_accept (a step without drafts, uniform u[b]); with q_out also
+// q_out[b * q_stride + t] = softmax(logits[b])_t. u == nullptr: greedy, token = first argmax.
+size_t draft_draw_ws_bytes(int B, int V);
+hipError_t launch_draft_draw(const float* logits, int B, int V, const float* u, int32_t* out_tok,
+                             float* q_out, long q_stride, void* ws, hipStream_t s);
+
 // ------------------------------------------------------------- elementwise
 hipError_t launch_embed(const void* table, const int32_t* tokens, int T, int d, int V,
                         molt_dtype dt, float* x, hipStream_t s);
@@ -59,6 +66,24 @@ hipError_t launch_quant_rows_tiled(const uint16_t* h, const int32_t* pperm, cons
 // out[t] (+)= sum_j w[t, j] o[t * K + j]
 hipError_t launch_combine(const float* o, const float* w, int T, int K, int d, float* out,
                           bool accumulate, hipStream_t s);
+
+// MTP draft head rows. Catch-up row b(k+1)+j takes token tokens[b, j+1] (j < n_b) or
+// next[b], and u_col[b] = u[b, 0] (u may be null).
+hipError_t launch_mtp_catchup(const int32_t* tokens, const int32_t* n_acc, const int32_t* next,
+                              const float* u, int B, int k, int32_t* row_tok, float* u_col,
+                              hipStream_t s);
+// y[t] = [RMSNorm(Emb[tok[t]]; ge) ; RMSNorm(h[t]; gh)] rounded to dt, tiled [T, 2d]
+hipError_t launch_mtp_input(const void* embed, const int32_t* tok, const float* h, const float* ge,
+                            const float* gh, int T, int d, int V, float eps, molt_dtype dt,
+                            void* y, hipStream_t s);
+// hsel[b] = x[b(k+1) + n_b] (f32), ysel row b = yf row b(k+1) + n_b (tiled, dt)
+hipError_t launch_mtp_select(const float* x, const void* yf, const int32_t* n_acc, int B, int k,
+                             int d, molt_dtype dt, float* hsel, void* ysel, hipStream_t s);
+// drafts[b, i] = tok[b]; then (i + 1 < k) row_tok[b] = tok[b], ctx_next[b] = ctx[b] + n_b +
+// i + 1, u_col[b] = u[b, i + 1]
+hipError_t launch_mtp_record(const int32_t* tok, int i, int B, int k, const int32_t* ctx,
+                             const int32_t* n_acc, const float* u, int32_t* drafts,
+                             int32_t* row_tok, int32_t* ctx_next, float* u_col, hipStream_t s);
 
 // ------------------------------------------------------------- routing
 // top-K + softmax of router logits (the sum, in order, of nparts split-K partials

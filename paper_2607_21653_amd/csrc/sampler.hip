@@ -507,6 +507,88 @@ __global__ __launch_bounds__(kWave) void draw_pick_kernel(
   }
 }
 
+
+// ---- MTP draft draws --------------------------------------------------------------------
+// q[b * q_stride + t] = softmax(logits[b])_t in f32: (m, S) combined from the chunk
+// statistics exactly as the accept decisions combine them, exp(l - m) by the table exp.
+template <bool kVec>
+__global__ __launch_bounds__(kThreads) void softmax_write_kernel(const float* __restrict__ logits,
+                                                                 int V, int nch,
+                                                                 const float* __restrict__ cmax,
+                                                                 const double* __restrict__ csum,
+                                                                 float* __restrict__ q, long q_stride) {
+  __shared__ double tab[256];
+  __shared__ double s_m, s_inv;
+  const long row = blockIdx.x / nch;
+  const int c = int(blockIdx.x % nch);
+  exp_table_init(tab, threadIdx.x, kThreads);
+  if (threadIdx.x < kWave) {
+    const int lane = threadIdx.x;
+    float mx = -INFINITY;
+    for (int cc = lane; cc < nch; cc += kWave) mx = fmaxf(mx, cmax[row * nch + cc]);
+    mx = wave_max(mx);
+    double acc = 0.0;
+    for (int cc = lane; cc < nch; cc += kWave) {
+      const float v = cmax[row * nch + cc];
+      if (v != -INFINITY) acc += csum[row * nch + cc] * exp(double(v) - double(mx));
+    }
+    acc = wave_sum(acc);
+    if (lane == 0) {
+      s_m = double(mx);
+      s_inv = 1.0 / acc;
+    }
+  }
+  __syncthreads();
+  const double m = s_m, inv = s_inv;
+  const float* src = logits + row * long(V) + long(c) * kChunk;
+  float* dst = q + row * q_stride + long(c) * kChunk;
+  const int n = min(kChunk, V - c * kChunk);
+  if (kVec) {
+#pragma unroll 2
+    for (int i = 0; i < kPerThread / 4; ++i) {
+      const int e0 = 4 * (threadIdx.x + kThreads * i);
+      if (e0 >= n) break;
+      const floatx4_t l = __builtin_nontemporal_load(reinterpret_cast<const floatx4_t*>(src + e0));
+      floatx4_t o;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) o[e] = float(exp_nonpos(double(l[e]) - m, tab) * inv);
+      *reinterpret_cast<floatx4_t*>(dst + e0) = o;
+    }
+  } else {
+    for (int e = threadIdx.x; e < n; e += kThreads)
+      dst[e] = float(exp_nonpos(double(src[e]) - m, tab) * inv);
+  }
+}
+
+// out[b] = the first index of the largest logit of row b (0 for a row with no finite max)
+__global__ __launch_bounds__(kThreads) void argmax_kernel(const float* __restrict__ logits, int V,
+                                                          int32_t* __restrict__ out) {
+  __shared__ float s_v[kThreads / kWave];
+  __shared__ int s_i[kThreads / kWave];
+  const long row = blockIdx.x;
+  const float* src = logits + row * long(V);
+  float best = -INFINITY;
+  int bi = V;
+  for (int t = threadIdx.x; t < V; t += kThreads) {   // a thread's indices increase
+    const float v = src[t];
+    if (v > best) { best = v; bi = t; }
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const float ov = __shfl_xor(best, o, kWave);
+    const int oi = __shfl_xor(bi, o, kWave);
+    if (ov > best || (ov == best && oi < bi)) { best = ov; bi = oi; }
+  }
+  const int w = threadIdx.x / kWave;
+  if (threadIdx.x % kWave == 0) { s_v[w] = best; s_i[w] = bi; }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int j = 1; j < kThreads / kWave; ++j)
+      if (s_v[j] > best || (s_v[j] == best && s_i[j] < bi)) { best = s_v[j]; bi = s_i[j]; }
+    out[row] = bi < V ? bi : 0;
+  }
+}
+
 }  // namespace
 
 int sampler_chunk_elems() { return kChunk; }
@@ -554,6 +636,41 @@ hipError_t launch_spec_accept(const float* logits, const float* q, const int32_t
     draw_pick_kernel<false><<<g3, kWave, 0, s>>>(logits, q, u, k, V, nch, fin, ctot, stot,
                                                  out_tokens, out_lp);
   }
+  return hipGetLastError();
+}
+
+size_t draft_draw_ws_bytes(int B, int V) {
+  Carver c(nullptr, 0);
+  c.take<uint8_t>(sampler_ws_bytes(B, 0, V));
+  c.take<int32_t>(B);
+  c.take<float>(B);
+  return c.used + 256;
+}
+
+hipError_t launch_draft_draw(const float* logits, int B, int V, const float* u, int32_t* out_tok,
+                             float* q_out, long q_stride, void* ws, hipStream_t s) {
+  if (u == nullptr) {
+    argmax_kernel<<<B, kThreads, 0, s>>>(logits, V, out_tok);
+    return hipGetLastError();
+  }
+  Carver c(ws, 0);
+  void* samp = c.take<uint8_t>(sampler_ws_bytes(B, 0, V));
+  int32_t* n = c.take<int32_t>(B);
+  float* lp = c.take<float>(B);
+  // a draw from p is the bonus draw of a step without drafts (k = 0, one uniform per row)
+  hipError_t e = launch_spec_accept(logits, nullptr, out_tok, u, B, 0, V, out_tok, n, lp, samp, s);
+  if (e != hipSuccess || q_out == nullptr) return e;
+  // the row statistics of pass 1 sit at the start of the sampler's workspace
+  const int nch = (V + kChunk - 1) / kChunk;
+  Carver cs(samp, 0);
+  const float* cmax = cs.take<float>(long(B) * nch);
+  const double* csum = cs.take<double>(long(B) * nch);
+  const bool vec = (V % 4 == 0) && (q_stride % 4 == 0) &&
+                   ((reinterpret_cast<uintptr_t>(logits) & 15) == 0) &&
+                   ((reinterpret_cast<uintptr_t>(q_out) & 15) == 0);
+  const dim3 g{unsigned(long(B) * nch)};
+  if (vec) softmax_write_kernel<true><<<g, kThreads, 0, s>>>(logits, V, nch, cmax, csum, q_out, q_stride);
+  else softmax_write_kernel<false><<<g, kThreads, 0, s>>>(logits, V, nch, cmax, csum, q_out, q_stride);
   return hipGetLastError();
 }
 

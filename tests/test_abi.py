@@ -116,4 +116,32 @@ def test_model_validation(L):
     assert L.molt_decoder_forward(ctypes.byref(m), ctypes.byref(kv), 1, 1, ctypes.c_void_p(1), None,
                                   None, 0, None) == INVALID
     assert L.molt_verify_step(ctypes.byref(m), ctypes.byref(kv), 1, 1, None, None, None, None, None,
-                              None, None, None, None, 0, None) == INVALID
+                              None, None, None, None, None, 0, None) == INVALID
+
+
+def test_mtp_validation(L):
+    """Host-side checks of molt_mtp_draft: nothing is enqueued for a bad request."""
+    t, lay, kv = _lib.MoltModel(), _lib.MoltModel(), _lib.MoltKV()
+    t.d_model, t.vocab, t.dtype = 256, 2048, _lib.MOLT_BF16
+    t.embed = t.lm_head = ctypes.c_void_p(0x1000)
+    lay.n_layers, lay.d_model, lay.dtype = 2, 256, _lib.MOLT_BF16
+    mtp = _lib.MoltMtp()
+    mtp.enorm = mtp.hnorm = mtp.eh_proj = ctypes.c_void_p(0x2000)
+    mtp.layer = ctypes.pointer(lay)
+    args = (ctypes.c_void_p(1),) * 4 + (None, ctypes.c_void_p(1), None, None, 0, None)
+    assert L.molt_mtp_draft(ctypes.byref(t), None, ctypes.byref(kv), 4, 3, *args) == INVALID
+    assert L.molt_mtp_draft(ctypes.byref(t), ctypes.byref(mtp), ctypes.byref(kv), 4, 0, *args) == INVALID
+    assert "k = 0" in L.molt_last_error().decode()
+    # a two-layer head
+    assert L.molt_mtp_draft(ctypes.byref(t), ctypes.byref(mtp), ctypes.byref(kv), 4, 3, *args) == INVALID
+    assert "n_layers = 2" in L.molt_last_error().decode()
+    lay.n_layers, lay.d_model = 1, 512
+    assert L.molt_mtp_draft(ctypes.byref(t), ctypes.byref(mtp), ctypes.byref(kv), 4, 3, *args) == INVALID
+    assert "d_model" in L.molt_last_error().decode()
+    # sampled drafts without uniforms
+    lay.d_model = 256
+    probs = ctypes.c_void_p(0x3000)
+    a2 = (ctypes.c_void_p(1),) * 4 + (None, ctypes.c_void_p(1), probs, None, 0, None)
+    assert L.molt_mtp_draft(ctypes.byref(t), ctypes.byref(mtp), ctypes.byref(kv), 4, 3, *a2) == INVALID
+    assert L.molt_mtp_draft_workspace_size(ctypes.byref(t), None, 4, 3, 8) == 0
+    assert L.molt_mtp_draft_workspace_size(ctypes.byref(t), ctypes.byref(mtp), 4, 0, 8) == 0
