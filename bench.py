@@ -125,6 +125,65 @@ def other_rooflines(w, groups, samp):
     return out
 
 
+def mtp_measure(w, seed, molt, model, layout, kv, tokens, u, q, reps=5):
+    """The MTP draft step (molt_mtp_draft) after this verify step: one head layer of the
+    target's shape with its own cache, sampled drafts with their q. Timed with HIP events on
+    the library's stream after the timed region (inputs resident: the verify step's hidden
+    rows, accepted counts and emitted tokens). Algorithmic bytes: the head's K/V read once
+    per row batch (the catch-up rows, then each drafting row), every expert's weights and
+    eh_proj once per row batch, the LM head once per draft, and q written."""
+    import torch
+    dev = "cuda"
+    B, k, V, d = w.batch, w.k, w.vocab, w.d_model
+    mt = workloads.make_mtp_weights(w, seed, device=dev)
+    mtp = molt.Mtp(mt["enorm"], mt["hnorm"], mt["eh_proj"], mt["layer"], mt["final_norm"],
+                   n_q_heads=w.n_q_heads, n_kv_heads=w.n_kv_heads, head_dim=w.head_dim,
+                   top_k=w.top_k, rms_eps=w.rms_eps, rope_theta=w.rope_theta)
+    del mt
+    hkc, hvc = workloads.make_kv_cache(w, layout, seed, w.n_layers, device=dev)
+    hkv = molt.KVCache([hkc], [hvc], kv.block_tables, kv.context_lens)
+    vs = molt.verify_step(model, kv, tokens, u, q, want_logits=False, want_hidden=True)
+    n = vs["n_accepted"]
+    nxt = vs["tokens"].gather(1, n.long()[:, None])[:, 0].contiguous()
+    ud = workloads.make_uniforms(B, k - 1, seed, tag="mtp_u", device=dev)
+    ws = torch.empty(molt.mtp_draft_workspace_size(model, mtp, B, k, layout.block_tables.shape[1]),
+                     dtype=torch.uint8, device=dev)
+    res = molt.mtp_draft(model, mtp, hkv, vs["hidden"], tokens, n, nxt, ud, workspace=ws)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        molt.mtp_draft(model, mtp, hkv, vs["hidden"], tokens, n, nxt, ud, workspace=ws, out=res)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    molt.profile_enable(True)
+    molt.mtp_draft(model, mtp, hkv, vs["hidden"], tokens, n, nxt, ud, workspace=ws, out=res)
+    torch.cuda.synchronize()
+    molt.profile_enable(False)
+    groups = {g: molt.profile_read(g) for g in molt._lib.PROF_GROUPS}
+    e = 1 if w.expert_dtype == "fp8" else 2
+    ctx = layout.context_lens.astype(np.int64)
+    na = n.cpu().numpy().astype(np.int64)
+    kvrow = w.n_kv_heads * w.head_dim * 2 * 2          # K and V bytes per cached position
+    abytes = int((ctx + k + 1).sum()) * kvrow + sum(int((ctx + na + i + 1).sum()) * kvrow for i in range(1, k))
+    ebytes = k * (w.n_experts * 3 * w.d_ff * d * e + 2 * d * d * 2
+                  + ((w.n_q_heads + 2 * w.n_kv_heads) * w.head_dim * d + d * w.n_q_heads * w.head_dim) * 2)
+    hbytes = k * V * d * 2 + B * k * V * 4
+    nbytes = abytes + ebytes + hbytes
+    gbs = nbytes / (ms / 1e3) / 1e9
+    drafts = res["drafts"].cpu().numpy()
+    assert ((drafts >= 0) & (drafts < V)).all()
+    return {"avg_ms": round(ms, 3), "drafts_per_s": round(B * k / (ms / 1e3), 1),
+            "bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": round(gbs / HBM_PEAK_GBS, 4), "algorithmic_bytes": nbytes,
+            "groups_ms": {g: round(t, 3) for g, (t, _) in groups.items()},
+            "note": f"one MTP draft step (k = {k} sampled drafts with q, B = {B}) after the verify "
+                    "step: catch-up rows + k-1 drafting rows of one head layer, the shared LM head "
+                    "and the draws; bytes = head K/V per row batch + weights per row batch + LM "
+                    "head per draft + q"}
+
+
 CPU_SAMPLE_SEQS, CPU_SAMPLE_LAYERS = 8, 12
 
 
@@ -138,7 +197,8 @@ def build(w, seed, molt, keep_host=0):
     layout in place of the row-major ones. Row-major host copies of the head and of the
     first `keep_host` layers are kept for the CPU baseline."""
     dev = "cuda"
-    layout = workloads.make_kv_layout(w, seed)
+    # room for the draft head's rows too (up to k - 1 positions past the verify window)
+    layout = workloads.make_kv_layout(w, seed, extra_tokens=w.k)
     layers, kcs, vcs, host_layers = [], [], [], []
     for l in range(w.n_layers):
         lw = workloads.make_layer_weights(w, seed, l, device=dev)
@@ -310,6 +370,8 @@ def main():
     n_break = min(a.steps, 3)
     samp = sampler_roofline(w, molt, out, tokens, q, u)
     n_acc = out["n_accepted"].cpu().numpy()
+    log("[bench] MTP draft step")
+    mtp = mtp_measure(w, a.seed, molt, model, layout, kv, tokens, u, q) if k > 0 else None
     positions = B * (k + 1)
     value = positions / (ms / 1e3)
     emitted = float((n_acc + 1).sum()) / (ms / 1e3)
@@ -349,6 +411,7 @@ def main():
         "kernel_groups_note": f"HIP-event times of each group over {n_break} untimed steps after the timed region",
         "lm_head_tflops": round(lm_flops / (lm_ms / max(lm_n, 1) / 1e3) / 1e12, 1) if lm_n else None,
         "other_rooflines": other_rooflines(w, groups, samp),
+        "mtp_draft": mtp,
     }
     if not a.no_cpu_baseline:
         log("[bench] timing the CPU oracle on a bounded sample")
