@@ -184,6 +184,28 @@ def mtp_measure(w, seed, molt, model, layout, kv, tokens, u, q, reps=5):
                     "head per draft + q"}
 
 
+def replay_measure(molt, model, kv, tokens, u, q, reps=3):
+    """The actor's recompute of the step's emitted tokens with routing replay
+    (molt_score_tokens with the verify step's tokens, out_tokens and out_routes), timed with
+    HIP events after the timed region; also whether it reproduced the recorded behavior
+    log-probabilities bit for bit (the consistency diagnostic)."""
+    import torch
+    v = molt.verify_step(model, kv, tokens, u, q, want_logits=False, want_routes=True)
+    r = molt.score_tokens(model, kv, tokens, v["tokens"], replay_routes=v["routes"])
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        molt.score_tokens(model, kv, tokens, v["tokens"], replay_routes=v["routes"])
+    e1.record()
+    torch.cuda.synchronize()
+    emitted = v["tokens"] >= 0
+    same = bool(torch.equal(r["logprobs"][emitted], v["logprobs"][emitted]))
+    return {"avg_ms": round(e0.elapsed_time(e1) / reps, 3), "reproduces_behavior_logprobs": same,
+            "note": "molt_score_tokens over the verify step's tokens with its emitted tokens as "
+                    "targets and its recorded routes replayed"}
+
+
 CPU_SAMPLE_SEQS, CPU_SAMPLE_LAYERS = 8, 12
 
 
@@ -372,6 +394,8 @@ def main():
     n_acc = out["n_accepted"].cpu().numpy()
     log("[bench] MTP draft step")
     mtp = mtp_measure(w, a.seed, molt, model, layout, kv, tokens, u, q) if k > 0 else None
+    log("[bench] replay recompute")
+    rep = replay_measure(molt, model, kv, tokens, u, q)
     positions = B * (k + 1)
     value = positions / (ms / 1e3)
     emitted = float((n_acc + 1).sum()) / (ms / 1e3)
@@ -412,6 +436,7 @@ def main():
         "lm_head_tflops": round(lm_flops / (lm_ms / max(lm_n, 1) / 1e3) / 1e12, 1) if lm_n else None,
         "other_rooflines": other_rooflines(w, groups, samp),
         "mtp_draft": mtp,
+        "replay_recompute": rep,
     }
     if not a.no_cpu_baseline:
         log("[bench] timing the CPU oracle on a bounded sample")

@@ -276,6 +276,31 @@ int molt_verify_step(const molt_model* m, const molt_kv* kv, int B, int k, const
                      size_t workspace_bytes, molt_stream_t stream);
 
 /* ------------------------------------------------------------------------------
+ * molt_score_tokens -- behavior-log-prob recompute with routing replay: the actor's pass
+ * over the tokens the engine emitted (Sec. 4.1: rollout routing replay records expert
+ * choices during generation and reuses them in the actor, with route alignment and
+ * numerical-consistency diagnostics; Sec. 4.2, Eq. 1: recorded token IDs and behavior
+ * log-probabilities). The verify step's forward over tokens[b, 0..k] at positions
+ * context_lens[b] + j, with each MoE layer's experts taken from replay_routes (their
+ * weights still come from the router, a softmax over the router logits of the given
+ * experts; replay_routes NULL: the router chooses), then
+ *   out_logprobs[b, j] = log softmax(logits[b, j])[targets[b, j]]   (NaN for a target
+ *                        outside [0, V)), computed exactly as molt_spec_accept's log-probs.
+ * On the weights that generated them, tokens = the verify step's tokens, targets = its
+ * out_tokens and replay_routes = its out_routes reproduce its out_logprobs and logits bit
+ * for bit. Writes the window's keys/values into the cache like molt_verify_step.
+ *   tokens, targets  [B, 1+k] i32;  replay_routes [n_layers, B*(1+k), top_k] i32 or NULL
+ *                    (an id outside [0, E) is taken as expert 0)
+ *   out_logprobs     [B, 1+k] f32;  out_logits [B, 1+k, V] f32 or NULL;
+ *   out_routes       [n_layers, B*(1+k), top_k] i32 or NULL (the routes used)
+ * ---------------------------------------------------------------------------- */
+size_t molt_score_tokens_workspace_size(const molt_model* m, int B, int k, int max_blocks_per_seq);
+int molt_score_tokens(const molt_model* m, const molt_kv* kv, int B, int k, const int32_t* tokens,
+                      const int32_t* targets, const int32_t* replay_routes, float* out_logprobs,
+                      float* out_logits, int32_t* out_routes, void* workspace,
+                      size_t workspace_bytes, molt_stream_t stream);
+
+/* ------------------------------------------------------------------------------
  * MTP draft head: the checkpoint's multi-token-prediction head that drafts the k
  * tokens the next verify step checks (Sec. 4.1 control table: number of
  * speculative tokens; Sec. 5.4: the MTP head shortens generation about five-fold).

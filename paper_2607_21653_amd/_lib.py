@@ -68,6 +68,9 @@ _SIGS = {
     "molt_verify_step": (c_int, [ctypes.POINTER(MoltModel), ctypes.POINTER(MoltKV), c_int, c_int,
                                  c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp,
                                  c_size, c_vp]),
+    "molt_score_tokens_workspace_size": (c_size, [ctypes.POINTER(MoltModel), c_int, c_int, c_int]),
+    "molt_score_tokens": (c_int, [ctypes.POINTER(MoltModel), ctypes.POINTER(MoltKV), c_int, c_int,
+                                  c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_size, c_vp]),
     "molt_mtp_draft_workspace_size": (c_size, [ctypes.POINTER(MoltModel), ctypes.POINTER(MoltMtp),
                                                c_int, c_int, c_int]),
     "molt_mtp_draft": (c_int, [ctypes.POINTER(MoltModel), ctypes.POINTER(MoltMtp),
@@ -400,6 +403,37 @@ def verify_step(model, kv, tokens, uniforms, draft_probs=None, want_logits=True,
                               _ptr(out.get("routes")), _ptr(out.get("hidden")), _ptr(ws), nb,
                               _stream())
     _check(st, "molt_verify_step")
+    return out
+
+
+def score_tokens_workspace_size(model, B, k, max_blocks):
+    return load().molt_score_tokens_workspace_size(ctypes.byref(model.struct), B, k, max_blocks)
+
+
+def score_tokens(model, kv, tokens, targets, replay_routes=None, want_logits=False, want_routes=False,
+                 workspace=None):
+    """Behavior-log-prob recompute (molt_score_tokens): tokens, targets [B, 1+k] i32,
+    replay_routes [L, B*(1+k), K] i32 or None. Returns dict(logprobs, logits?, routes?)."""
+    lib = load()
+    B, kp1 = tokens.shape
+    k = kp1 - 1
+    m = model.struct
+    dev = tokens.device
+    _dev(tokens, torch.int32, name="tokens")
+    _dev(targets, torch.int32, (B, kp1), "targets")
+    _dev(replay_routes, torch.int32, (m.n_layers, B * kp1, m.top_k), "replay_routes")
+    out = {"logprobs": torch.empty(B, kp1, dtype=torch.float32, device=dev)}
+    if want_logits:
+        out["logits"] = torch.empty(B, kp1, m.vocab, dtype=torch.float32, device=dev)
+    if want_routes:
+        out["routes"] = torch.empty(m.n_layers, B * kp1, m.top_k, dtype=torch.int32, device=dev)
+    ws, nb = _workspace(score_tokens_workspace_size(model, B, k, kv.struct.max_blocks_per_seq), dev,
+                        workspace)
+    st = lib.molt_score_tokens(ctypes.byref(m), ctypes.byref(kv.struct), B, k, _ptr(tokens),
+                               _ptr(targets), _ptr(replay_routes), _ptr(out["logprobs"]),
+                               _ptr(out.get("logits")), _ptr(out.get("routes")), _ptr(ws), nb,
+                               _stream())
+    _check(st, "molt_score_tokens")
     return out
 
 

@@ -488,10 +488,11 @@ DecWs carve_dec(molt::Carver& c, const molt_model* m, int B, int k, int max_bloc
 }
 
 // All layers on the residual stream x. With final_g, the last layer's MoE combine is fused
-// with the final RMSNorm, whose tiled output goes to final_y.
+// with the final RMSNorm, whose tiled output goes to final_y. With replay ([L, T, K] expert
+// ids), every MoE layer takes its experts from it (routing replay).
 hipError_t run_decoder(const DecWs& w, const molt_model* m, const molt_kv* kv, int B, int k,
                        float* x, int32_t* routes, const float* final_g, void* final_y,
-                       hipStream_t s) {
+                       hipStream_t s, const int32_t* replay = nullptr) {
   const int T = B * (k + 1);
   const int d = m->d_model, D = m->head_dim, Hq = m->n_q_heads, Hkv = m->n_kv_heads;
   const int K = m->top_k, L = m->n_layers;
@@ -537,7 +538,8 @@ hipError_t run_decoder(const DecWs& w, const molt_model* m, const molt_kv* kv, i
     RUN(run_moe(w.moe, w.y, fp8 ? w.yq : nullptr, fp8 ? w.ys : nullptr, m->w_router[l],
                 m->router_bias ? m->router_bias[l] : nullptr, m->w_gate_up[l], m->w_down[l],
                 fp8 ? m->s_gate_up[l] : nullptr, fp8 ? m->s_down[l] : nullptr, T, d,
-                m->n_experts, K, m->d_ff, m->dtype, m->expert_dtype, nullptr, nullptr, false, s));
+                m->n_experts, K, m->d_ff, m->dtype, m->expert_dtype,
+                replay ? replay + size_t(l) * T * K : nullptr, nullptr, false, s));
     if (routes) RUN(copy_out(routes + size_t(l) * T * K, w.moe.ids, size_t(T) * K * 4, s));
     // x += MoE combine; then the next layer's attention norm (or the final norm)
     const bool last = l + 1 == L;
@@ -626,6 +628,60 @@ int molt_verify_step(const molt_model* m, const molt_kv* kv, int B, int k, const
                                  out_num_accepted, out_logprobs, w.samp, s, k + 1, 1);
   }
   return hip_status(e, "molt_verify_step");
+}
+
+// ------------------------------------------------------------------ replay recompute
+
+namespace {
+struct ScoreWs { float* x; void* yf; float* logits; void* lp; DecWs dec; };
+ScoreWs carve_score(molt::Carver& c, const molt_model* m, int B, int k, int max_blocks) {
+  ScoreWs w{};
+  const long T = long(B) * (k + 1);
+  w.x = c.take<float>(T * m->d_model);
+  w.yf = c.take<uint8_t>(pad32(T) * m->d_model * dt_size(m->dtype));
+  w.logits = c.take<float>(T * long(m->vocab));
+  w.lp = c.take<uint8_t>(molt::token_logprob_ws_bytes(T, m->vocab));
+  w.dec = carve_dec(c, m, B, k, max_blocks);
+  return w;
+}
+}  // namespace
+
+size_t molt_score_tokens_workspace_size(const molt_model* m, int B, int k, int max_blocks) {
+  if (!m || B < 1 || k < 0 || max_blocks < 1 || m->vocab < 1 || !pair_ok(m->dtype, m->expert_dtype))
+    return 0;
+  molt::Carver c(nullptr, 0);
+  carve_score(c, m, B, k, max_blocks);
+  return c.used + 256;
+}
+
+int molt_score_tokens(const molt_model* m, const molt_kv* kv, int B, int k, const int32_t* tokens,
+                      const int32_t* targets, const int32_t* replay_routes, float* out_logprobs,
+                      float* out_logits, int32_t* out_routes, void* workspace,
+                      size_t workspace_bytes, molt_stream_t stream) {
+  if (int r = model_ok(m, kv, B, k, true)) return r;
+  if (int r = spec_accept_shape_ok(B, k, m->vocab)) return r;
+  REQUIRE(tokens && targets && out_logprobs, "a required pointer is NULL");
+  if (int r = check_ws(workspace, workspace_bytes,
+                       molt_score_tokens_workspace_size(m, B, k, kv->max_blocks_per_seq)))
+    return r;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  molt::Carver c(workspace, workspace_bytes);
+  ScoreWs w = carve_score(c, m, B, k, kv->max_blocks_per_seq);
+  float* logits = out_logits ? out_logits : w.logits;
+  const int T = B * (k + 1);
+  hipError_t e = molt::launch_embed(m->embed, tokens, T, m->d_model, m->vocab, m->dtype, w.x, s);
+  if (e == hipSuccess)
+    e = run_decoder(w.dec, m, kv, B, k, w.x, out_routes, m->final_norm, w.yf, s, replay_routes);
+  if (e == hipSuccess) {
+    ProfScope ps(MOLT_PROF_LM_HEAD, s);
+    e = molt::launch_gemm(w.yf, m->lm_head, logits, T, m->vocab, m->d_model, m->dtype, false,
+                          nullptr, 0, s);
+  }
+  if (e == hipSuccess) {
+    ProfScope ps(MOLT_PROF_SAMPLER, s);
+    e = molt::launch_token_logprobs(logits, T, m->vocab, targets, out_logprobs, w.lp, s);
+  }
+  return hip_status(e, "molt_score_tokens");
 }
 
 // ------------------------------------------------------------------ MTP draft head

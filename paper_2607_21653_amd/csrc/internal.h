@@ -31,6 +31,12 @@ hipError_t launch_spec_accept(const float* logits, const float* q, const int32_t
                               int32_t* out_n, float* out_lp, void* ws, hipStream_t s,
                               int draft_stride = -1, int draft_offset = 0);
 
+// Scores of given tokens: out[r] = log softmax(logits[r])[targets[r]] with the accept
+// decisions' row moments (NaN for a target outside [0, V)).
+size_t token_logprob_ws_bytes(long rows, int V);
+hipError_t launch_token_logprobs(const float* logits, long rows, int V, const int32_t* targets,
+                                 float* out, void* ws, hipStream_t s);
+
 // Draws of the MTP draft head, one per row: token ~ softmax(logits[b]) by the integer
 // inverse CDF of launch_spec_accept (a step without drafts, uniform u[b]); with q_out also
 // q_out[b * q_stride + t] = softmax(logits[b])_t. u == nullptr: greedy, token = first argmax.

@@ -589,6 +589,36 @@ __global__ __launch_bounds__(kThreads) void argmax_kernel(const float* __restric
   }
 }
 
+
+// ---- scores of given tokens -------------------------------------------------------------
+// lp[r] = (l[r, y] - m) - ln S for y = targets[r] in [0, V), else NaN: one wavefront per row,
+// (m, S) combined from the chunk statistics exactly as the accept decisions combine them,
+// so that a recompute of emitted tokens reproduces the recorded log-probs bit for bit.
+__global__ __launch_bounds__(kWave) void token_logprob_kernel(const float* __restrict__ logits,
+                                                              int V, int nch,
+                                                              const float* __restrict__ cmax,
+                                                              const double* __restrict__ csum,
+                                                              const int32_t* __restrict__ targets,
+                                                              float* __restrict__ out) {
+  const long row = blockIdx.x;
+  const int lane = threadIdx.x;
+  float mx = -INFINITY;
+  for (int cc = lane; cc < nch; cc += kWave) mx = fmaxf(mx, cmax[row * nch + cc]);
+  mx = wave_max(mx);
+  double acc = 0.0;
+  for (int cc = lane; cc < nch; cc += kWave) {
+    const float v = cmax[row * nch + cc];
+    if (v != -INFINITY) acc += csum[row * nch + cc] * exp(double(v) - double(mx));
+  }
+  acc = wave_sum(acc);
+  if (lane == 0) {
+    const int y = targets[row];
+    out[row] = (y >= 0 && y < V)
+                   ? float((double(logits[row * long(V) + y]) - double(mx)) - log(acc))
+                   : __builtin_nanf("");
+  }
+}
+
 }  // namespace
 
 int sampler_chunk_elems() { return kChunk; }
@@ -671,6 +701,28 @@ hipError_t launch_draft_draw(const float* logits, int B, int V, const float* u, 
   const dim3 g{unsigned(long(B) * nch)};
   if (vec) softmax_write_kernel<true><<<g, kThreads, 0, s>>>(logits, V, nch, cmax, csum, q_out, q_stride);
   else softmax_write_kernel<false><<<g, kThreads, 0, s>>>(logits, V, nch, cmax, csum, q_out, q_stride);
+  return hipGetLastError();
+}
+
+size_t token_logprob_ws_bytes(long rows, int V) {
+  const long nch = (V + kChunk - 1) / kChunk;
+  Carver c(nullptr, 0);
+  c.take<float>(rows * nch);
+  c.take<double>(rows * nch);
+  return c.used + 256;
+}
+
+hipError_t launch_token_logprobs(const float* logits, long rows, int V, const int32_t* targets,
+                                 float* out, void* ws, hipStream_t s) {
+  const int nch = (V + kChunk - 1) / kChunk;
+  Carver c(ws, 0);
+  float* cmax = c.take<float>(rows * nch);
+  double* csum = c.take<double>(rows * nch);
+  const bool vec = (V % 4 == 0) && ((reinterpret_cast<uintptr_t>(logits) & 15) == 0);
+  const dim3 g1{unsigned(rows * nch)}, g2{unsigned(rows)};
+  if (vec) chunk_stats_kernel<true><<<g1, kThreads, 0, s>>>(logits, rows, V, nch, cmax, csum);
+  else chunk_stats_kernel<false><<<g1, kThreads, 0, s>>>(logits, rows, V, nch, cmax, csum);
+  token_logprob_kernel<<<g2, kWave, 0, s>>>(logits, V, nch, cmax, csum, targets, out);
   return hipGetLastError();
 }
 
