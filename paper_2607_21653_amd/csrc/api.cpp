@@ -385,7 +385,8 @@ static int attn_shape_ok(int B, int k, int Hq, int Hkv, int D, int max_blocks, m
   REQUIRE(act_ok(dt), "attention dtype must be F32 or BF16");
   REQUIRE(D == 64 || D == 128, "head_dim = %d must be 64 or 128", D);
   REQUIRE(Hkv >= 1 && Hq >= Hkv && Hq % Hkv == 0, "n_q_heads %d must be a multiple of n_kv_heads %d", Hq, Hkv);
-  REQUIRE(dt == MOLT_F32 || (Hq / Hkv) * (k + 1) <= 128, "(Hq/Hkv)*(1+k) = %d exceeds 128", (Hq / Hkv) * (k + 1));
+  REQUIRE(dt == MOLT_F32 || Hq / Hkv <= 128, "Hq/Hkv = %d exceeds 128", Hq / Hkv);
+  REQUIRE(double(B) * (k + 1) * Hq < 2.0e9, "B * (1+k) * Hq too large");
   REQUIRE(max_blocks >= 1, "max_blocks_per_seq = %d must be >= 1", max_blocks);
   REQUIRE(double(B) * Hkv * ((max_blocks + 63) / 64) < 2.0e9, "grid too large");
   return MOLT_OK;

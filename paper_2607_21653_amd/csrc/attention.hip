@@ -3,9 +3,11 @@
 // R = G*(1+k) query rows (G = Hq/Hkv query heads, 1+k positions) share every key/value
 // block, so each K/V byte is read once per (b, h) and reused by all R rows on MFMA.
 //
-// Work split: workgroup = (b, h, split of the key range), 4 wavefronts; the number of
-// splits is chosen so the grid holds ~512 workgroups (at B*Hkv >= 512 there is no split and
-// no merge pass) and no split exceeds 2048 blocks. The wavefronts split the R query rows and
+// Work split: workgroup = (b, h, query tile, split of the key range), 4 wavefronts. A query
+// tile holds all R rows when R <= 128 (the verify step); longer windows (prefill) are cut
+// into tiles of floor(128 / G) positions, each reading the keys its last position sees.
+// The number of splits is chosen so the grid holds ~512 workgroups (at B*Hkv*tiles >= 512
+// there is no split and no merge pass) and no split exceeds 2048 blocks. The wavefronts split the R query rows and
 // share every 32-key block pair through a double-buffered LDS ring (details at the kernel).
 // Per pair, on v_mfma_f32_16x16x32_bf16:
 //   S^T[32 keys x 16 rows] = K Q^T   (A = K rows from LDS, B = Q^T held in registers)
@@ -42,6 +44,7 @@ struct AttnParams {
   float* part_o;           // [B, Hkv, S, R, D]
   float* part_ml;          // [B, Hkv, S, R, 2]
   int k, Hq, Hkv, max_blocks, splits, blocks_per_split;
+  int qtiles, tq;          // query tiles per (b, h) and positions per tile (tq * G <= 128)
   float scale_log2;        // log2(e) / sqrt(D)
   int out_tiled;           // output in the GEMM operand layout (input of the O projection)
 };
@@ -82,13 +85,17 @@ __global__ __launch_bounds__(kThreads) void attn_lds_kernel(AttnParams p) {
   __shared__ __attribute__((aligned(16))) uint8_t lds[2][PAIR];
 
   const int split = blockIdx.x % p.splits;
-  const int bh = blockIdx.x / p.splits;
+  const int qt = (blockIdx.x / p.splits) % p.qtiles;
+  const int bh = blockIdx.x / p.splits / p.qtiles;
   const int b = bh / p.Hkv, h = bh % p.Hkv;
   const int G = p.Hq / p.Hkv;
   const int kp1 = p.k + 1;
-  const int R = G * kp1;
+  const int R = G * kp1;                   // rows of (b, h); this tile holds rows r0 .. r0 + Rt
+  const int j0 = qt * p.tq;                // the tile's first position
+  const int Rt = G * min(p.tq, kp1 - j0);
+  const int r0 = G * j0;
   const int ctx = p.ctx[b];
-  const int nkeys = ctx + kp1;
+  const int nkeys = ctx + j0 + Rt / G;     // keys the tile's last position sees
   const int nblk = (nkeys + 15) / 16;
   const int blk0 = split * p.blocks_per_split;
   const int blk1 = min(blk0 + p.blocks_per_split, nblk);
@@ -103,12 +110,12 @@ __global__ __launch_bounds__(kThreads) void attn_lds_kernel(AttnParams p) {
   int lim[RTW];
 #pragma unroll
   for (int i = 0; i < RTW; ++i) {
-    const int r = 16 * (wave + 4 * i) + l16;
-    const int j = r / G, gi = r % G;
-    lim[i] = r < R ? ctx + j : -1;
+    const int r = 16 * (wave + 4 * i) + l16;     // row of the tile
+    const int j = j0 + r / G, gi = r % G;
+    lim[i] = r < Rt ? ctx + j : -1;
 #pragma unroll
     for (int s = 0; s < DS; ++s) {
-      if (r < R) {
+      if (r < Rt) {
         qf[i][s] = *reinterpret_cast<const bf16x8_t*>(
             p.q + ((long(b) * kp1 + j) * p.Hq + h * G + gi) * D + s * 32 + g4 * 8);
       } else {
@@ -125,7 +132,8 @@ __global__ __launch_bounds__(kThreads) void attn_lds_kernel(AttnParams p) {
   float m_run[RTW], l_run[RTW];
 #pragma unroll
   for (int i = 0; i < RTW; ++i) { m_run[i] = kNegBig; l_run[i] = 0.f; }
-  const bool active = 16 * wave < R;    // wavefronts without rows only help with the loads
+  const bool active = 16 * wave < Rt;   // wavefronts without rows only help with the loads
+  const int lim_lo = ctx + j0;          // keys up to here are visible to every row of the tile
 
   __shared__ int s_bt[kMaxSplitBlocks];
   const int* btab = p.bt + long(b) * p.max_blocks;
@@ -211,7 +219,7 @@ __global__ __launch_bounds__(kThreads) void attn_lds_kernel(AttnParams p) {
       }
     }
     // lane's 8 keys: block pb + g4 / 2, keys 8 (g4 % 2) + 4 t + e
-    if (!(pb * 16 + 31 <= ctx)) {
+    if (!(pb * 16 + 31 <= lim_lo)) {
       const bool blk_ok = (g4 / 2 == 0) || (pb + 1 < blk1);
 #pragma unroll
       for (int i = 0; i < RTW; ++i)
@@ -307,8 +315,8 @@ __global__ __launch_bounds__(kThreads) void attn_lds_kernel(AttnParams p) {
     lt += __shfl_xor(lt, 16, kWave);
     lt += __shfl_xor(lt, 32, kWave);
     const int r = 16 * (wave + 4 * i) + l16;
-    if (r >= R) continue;
-    const int j = r / G, gi = r % G;
+    if (r >= Rt) continue;
+    const int j = j0 + r / G, gi = r % G;
     // O^T element e of tile dt: dim 16 dt + 4 g4 + e
     if (p.splits == 1) {
       const float inv = lt > 0.f ? 1.f / lt : 0.f;
@@ -319,7 +327,7 @@ __global__ __launch_bounds__(kThreads) void attn_lds_kernel(AttnParams p) {
           p.out[out_index(p, long(b) * kp1 + j, (h * G + gi) * D + 16 * dt + 4 * g4 + e, long(p.Hq) * D, 2)] =
               f32_to_bf16(o[dt][i][e] * inv);
     } else {
-      const long pr = (long(bh) * p.splits + split) * R + r;
+      const long pr = (long(bh) * p.splits + split) * R + r0 + r;
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
@@ -341,7 +349,8 @@ __global__ __launch_bounds__(D) void attn_merge_kernel(AttnParams p, int out_f32
   const int r = blockIdx.x % R;
   const int bh = blockIdx.x / R;
   const int b = bh / p.Hkv, h = bh % p.Hkv;
-  const int nblk = (p.ctx[b] + kp1 + 15) / 16;
+  const int j_end = min(kp1, (r / G / p.tq + 1) * p.tq);      // end of the row's query tile
+  const int nblk = (p.ctx[b] + j_end + 15) / 16;
   const int ns = min(p.splits, (nblk + p.blocks_per_split - 1) / p.blocks_per_split);
   float M = kNegBig;
   for (int s = 0; s < ns; ++s) M = fmaxf(M, p.part_ml[((long(bh) * p.splits + s) * R + r) * 2]);
@@ -415,9 +424,9 @@ __global__ __launch_bounds__(kWave) void attn_f32_kernel(const float* __restrict
 
 // Splits of the key range: enough workgroups to fill the chip twice over (512), each split a
 // multiple of 8 blocks (4 wavefronts x one 32-key pair) and at least 32 blocks long.
-void split_plan(int B, int Hkv, int max_blocks, int& splits, int& bps) {
-  const int pairs = B * Hkv;
-  int s = (512 + pairs - 1) / pairs;
+void split_plan(long units, int max_blocks, int& splits, int& bps) {
+  const long pairs = units;
+  int s = int((512 + pairs - 1) / pairs);
   const int cap = (max_blocks + 31) / 32;
   if (s > cap) s = cap;
   if (s < 1) s = 1;
@@ -430,17 +439,27 @@ void split_plan(int B, int Hkv, int max_blocks, int& splits, int& bps) {
 
 template <int D>
 hipError_t launch_d(const AttnParams& p, int B, int R, hipStream_t s) {
-  if (R <= 64) attn_lds_kernel<D, 1><<<B * p.Hkv * p.splits, kThreads, 0, s>>>(p);
-  else attn_lds_kernel<D, 2><<<B * p.Hkv * p.splits, kThreads, 0, s>>>(p);
+  const int Rt = (p.Hq / p.Hkv) * p.tq;     // rows of a query tile
+  const long grid = long(B) * p.Hkv * p.qtiles * p.splits;
+  if (Rt <= 64) attn_lds_kernel<D, 1><<<grid, kThreads, 0, s>>>(p);
+  else attn_lds_kernel<D, 2><<<grid, kThreads, 0, s>>>(p);
   if (p.splits > 1) attn_merge_kernel<D><<<B * p.Hkv * R, D, 0, s>>>(p, 0);
   return hipGetLastError();
 }
 
 }  // namespace
 
+// Query tiles of (b, h): all G(1+k) rows in one tile when they fit in 128, else tiles of
+// floor(128 / G) positions (prefill windows).
+static void qtile_plan(int G, int kp1, int& qtiles, int& tq) {
+  tq = G * kp1 <= 128 ? kp1 : 128 / G;
+  qtiles = (kp1 + tq - 1) / tq;
+}
+
 size_t attention_ws_bytes(int B, int k, int Hq, int Hkv, int D, int max_blocks) {
-  int S, bps;
-  split_plan(B, Hkv, max_blocks, S, bps);
+  int S, bps, qtiles, tq;
+  qtile_plan(Hq / Hkv, k + 1, qtiles, tq);
+  split_plan(long(B) * Hkv * qtiles, max_blocks, S, bps);
   if (S <= 1) return 0;
   const long rows = long(B) * (k + 1) * Hq;   // = B * Hkv * R
   Carver c(nullptr, 0);
@@ -470,7 +489,8 @@ hipError_t launch_paged_attention(const void* q, const void* kc, const void* vc,
                                                         static_cast<const float*>(vc), p, D);
     return hipGetLastError();
   }
-  split_plan(B, Hkv, max_blocks, p.splits, p.blocks_per_split);
+  qtile_plan(Hq / Hkv, k + 1, p.qtiles, p.tq);
+  split_plan(long(B) * Hkv * p.qtiles, max_blocks, p.splits, p.blocks_per_split);
   if (p.splits > 1) {
     const long rows = long(B) * (k + 1) * Hq;
     Carver c(ws, 0);

@@ -2,8 +2,10 @@
 paged blocks with split-KV merge) against the oracle's float64 paged attention: bf16
 within 1e-2 max-abs (probabilities are rounded to bf16 for the MFMA, outputs to bf16),
 f32 within 1e-5; ragged contexts, one-key and empty-context edges, k = 0, 8 drafts
-(72 query rows), head dim 64, many splits; shuffled and contiguous block tables give
-bit-identical outputs."""
+(72 query rows), head dim 64, many splits; prefill windows longer than one 128-row query
+tile (64, 41, 101 and 256 positions: several tiles, a partial last tile, tiles with splits,
+an empty cached context); shuffled and contiguous block tables give bit-identical
+outputs."""
 import numpy as np
 import pytest
 import torch
@@ -45,6 +47,10 @@ def _gpu(molt, w, layout, kc, vc, q, bt=None):
     (4, 0, 32, 4, 128, 0, 40),          # plain decode, empty context allowed
     (2, 3, 8, 2, 64, 200, 1500),        # head dim 64
     (1, 4, 32, 4, 128, 9000, 9000),     # 9 splits
+    (2, 63, 32, 4, 128, 0, 300),        # prefill window: 4 query tiles, empty context allowed
+    (3, 40, 16, 4, 128, 10, 700),       # G = 4: tiles of 32 positions, partial last tile
+    (1, 255, 32, 4, 128, 2000, 2000),   # 16 query tiles x 5 splits
+    (2, 100, 8, 2, 64, 50, 400),        # head dim 64, 4 tiles
 ])
 def test_bf16_parity(molt_lib, B, k, Hq, Hkv, D, lo, hi):
     print(f"case B={B} k={k} Hq={Hq} Hkv={Hkv} D={D} ctx=[{lo},{hi}]", flush=True)
@@ -56,8 +62,9 @@ def test_bf16_parity(molt_lib, B, k, Hq, Hkv, D, lo, hi):
     assert err <= 1e-2
 
 
-def test_f32_parity(molt_lib):
-    w, layout, kc, vc, q = _setup(4, 3, 4, 4, 64, 64, 128, "f32", 7)
+@pytest.mark.parametrize("B,k,lo,hi", [(4, 3, 64, 128), (2, 40, 0, 100)])
+def test_f32_parity(molt_lib, B, k, lo, hi):
+    w, layout, kc, vc, q = _setup(B, k, 4, 4, 64, lo, hi, "f32", 7)
     err = max_abs(_gpu(molt_lib, w, layout, kc, vc, q), _oracle(w, layout, kc, vc, q))
     assert err <= 1e-5, err
 
