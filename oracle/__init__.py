@@ -14,4 +14,4 @@ Only ``tests/``, ``__graft_entry__.smoke()`` and the benchmark's ``cpu_baseline`
 leg may import this package. The GPU library never calls it and shares no code
 with it: the only common module is ``workloads`` (seeded random inputs).
 """
-from . import codecs, sampler, routing, moe, attention, model, mtp, replay  # noqa: F401
+from . import codecs, sampler, routing, moe, attention, model, mtp, replay, prefix  # noqa: F401
