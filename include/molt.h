@@ -57,7 +57,8 @@ typedef enum {
   MOLT_ERR_INVALID_ARG = -1, /* NULL required pointer, bad size, bad combination  */
   MOLT_ERR_UNSUPPORTED = -2, /* valid request this build does not implement       */
   MOLT_ERR_WORKSPACE = -3,   /* workspace missing or smaller than *_workspace_size */
-  MOLT_ERR_HIP = -4          /* a HIP runtime call or kernel launch failed         */
+  MOLT_ERR_HIP = -4,         /* a HIP runtime call or kernel launch failed         */
+  MOLT_ERR_CAPACITY = -5     /* the block pool has no free or evictable block left  */
 } molt_status;
 
 typedef enum {
@@ -274,6 +275,64 @@ int molt_verify_step(const molt_model* m, const molt_kv* kv, int B, int k, const
                      int32_t* out_tokens, int32_t* out_num_accepted, float* out_logprobs,
                      int32_t* out_routes, float* out_hidden, void* workspace,
                      size_t workspace_bytes, molt_stream_t stream);
+
+/* ------------------------------------------------------------------------------
+ * molt_prefill -- paged prefill of a window of new tokens per sequence: the verify step's
+ * forward over tokens[b, 0..n) at positions context_lens[b] + j (cached positions below
+ * context_lens[b], e.g. a prefix-cache hit, are read, not recomputed), then the final norm
+ * and LM head of each sequence's last new row (row lens[b] - 1). Prefix caching enters the
+ * serving engine (Sec. 4.1, Sec. 5.3); a cache-hit re-prefill of an agent's growing context
+ * computes only the positions past the hit (Sec. 5.4).
+ *   tokens      [B, n] i32; rows j >= lens[b] are padding (computed, their cache slots
+ *               written; the caller advances context_lens[b] by lens[b] only)
+ *   lens        [B] i32 in [1, n]
+ *   out_logits  [B, V] f32: logits of row lens[b] - 1
+ *   out_hidden  [B*n, d] f32 final residual stream (before the final norm), or NULL
+ *   out_routes  [n_layers, B*n, top_k] i32, or NULL
+ * Writes the cache at positions context_lens[b] .. context_lens[b] + n - 1;
+ * context_lens[b] + n <= 16 * max_blocks_per_seq is the caller's duty.
+ * ---------------------------------------------------------------------------- */
+size_t molt_prefill_workspace_size(const molt_model* m, int B, int n, int max_blocks_per_seq);
+int molt_prefill(const molt_model* m, const molt_kv* kv, int B, int n, const int32_t* tokens,
+                 const int32_t* lens, float* out_logits, float* out_hidden, int32_t* out_routes,
+                 void* workspace, size_t workspace_bytes, molt_stream_t stream);
+
+/* ------------------------------------------------------------------------------
+ * Session-consistent prefix cache (HOST side: every pointer below is a host pointer; no
+ * device memory, no stream). Hands out physical block ids of a pool of num_blocks blocks
+ * of 16 positions for the callers' block tables, reusing the blocks of a cached prefix
+ * only when its token IDs match exactly (Sec. 4.2: a rewritten history starts anew).
+ *  - A full block is identified by its 16 token IDs and its parent (the cached block of
+ *    the preceding 16 tokens); cached blocks form a tree, and dropping a block's entry
+ *    drops its subtree's.
+ *  - acquire: the longest chain of cached full blocks matching tokens[0..n), at most
+ *    (n - 1) / 16 blocks (at least one position is left to compute), each gaining a
+ *    reference; then ceil((n + extra_tokens) / 16) blocks in all, each missing one the
+ *    lowest free block id, or, with none free, after evicting the least recently released
+ *    cached block without references. Writes block_table[0..max_blocks) (-1 past the
+ *    row), *n_cached = 16 * hits (the caller prefills tokens[n_cached..n) at context
+ *    n_cached); returns the row's block count, MOLT_ERR_INVALID_ARG (bad argument, or more
+ *    than max_blocks blocks needed) or MOLT_ERR_CAPACITY (pool exhausted; nothing changed
+ *    but the hit blocks' recency).
+ *  - commit: once the keys/values of tokens[0..n) are in the row's blocks, every full
+ *    block whose prefix is not cached yet becomes cached (a prefix cached elsewhere keeps
+ *    that block).
+ *  - release: the row's blocks lose a reference (last block first); a block left without
+ *    references becomes evictable (cached) or free.
+ *  - stats: out[7] = free blocks, cached blocks, referenced blocks, evictable blocks,
+ *    tokens looked up, tokens hit, evictions.
+ * Not thread-safe: one host thread per cache.
+ * ---------------------------------------------------------------------------- */
+typedef struct molt_prefix_cache molt_prefix_cache;
+molt_prefix_cache* molt_prefix_cache_create(int num_blocks);   /* NULL if num_blocks < 1 */
+void molt_prefix_cache_destroy(molt_prefix_cache* cache);
+int molt_prefix_cache_acquire(molt_prefix_cache* cache, const int32_t* tokens, int n,
+                              int extra_tokens, int32_t* block_table, int max_blocks,
+                              int* n_cached);
+int molt_prefix_cache_commit(molt_prefix_cache* cache, const int32_t* tokens, int n,
+                             const int32_t* block_table, int n_blocks);
+int molt_prefix_cache_release(molt_prefix_cache* cache, const int32_t* block_table, int n_blocks);
+int molt_prefix_cache_stats(const molt_prefix_cache* cache, long long* out);
 
 /* ------------------------------------------------------------------------------
  * molt_score_tokens -- behavior-log-prob recompute with routing replay: the actor's pass

@@ -68,6 +68,16 @@ _SIGS = {
     "molt_verify_step": (c_int, [ctypes.POINTER(MoltModel), ctypes.POINTER(MoltKV), c_int, c_int,
                                  c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp,
                                  c_size, c_vp]),
+    "molt_prefill_workspace_size": (c_size, [ctypes.POINTER(MoltModel), c_int, c_int, c_int]),
+    "molt_prefill": (c_int, [ctypes.POINTER(MoltModel), ctypes.POINTER(MoltKV), c_int, c_int, c_vp,
+                             c_vp, c_vp, c_vp, c_vp, c_vp, c_size, c_vp]),
+    "molt_prefix_cache_create": (c_vp, [c_int]),
+    "molt_prefix_cache_destroy": (None, [c_vp]),
+    "molt_prefix_cache_acquire": (c_int, [c_vp, c_vp, c_int, c_int, c_vp, c_int,
+                                          ctypes.POINTER(c_int)]),
+    "molt_prefix_cache_commit": (c_int, [c_vp, c_vp, c_int, c_vp, c_int]),
+    "molt_prefix_cache_release": (c_int, [c_vp, c_vp, c_int]),
+    "molt_prefix_cache_stats": (c_int, [c_vp, ctypes.POINTER(ctypes.c_longlong)]),
     "molt_score_tokens_workspace_size": (c_size, [ctypes.POINTER(MoltModel), c_int, c_int, c_int]),
     "molt_score_tokens": (c_int, [ctypes.POINTER(MoltModel), ctypes.POINTER(MoltKV), c_int, c_int,
                                   c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_size, c_vp]),
@@ -404,6 +414,84 @@ def verify_step(model, kv, tokens, uniforms, draft_probs=None, want_logits=True,
                               _stream())
     _check(st, "molt_verify_step")
     return out
+
+
+def prefill_workspace_size(model, B, n, max_blocks):
+    return load().molt_prefill_workspace_size(ctypes.byref(model.struct), B, n, max_blocks)
+
+
+def prefill(model, kv, tokens, lens, want_hidden=False, want_routes=False, workspace=None):
+    """Paged prefill (molt_prefill): tokens [B, n] i32 at positions context_lens[b] + j,
+    lens [B] i32 in [1, n]. Returns dict(logits [B, V] of each last new row, hidden?, routes?)."""
+    lib = load()
+    B, n = tokens.shape
+    m = model.struct
+    dev = tokens.device
+    _dev(tokens, torch.int32, name="tokens")
+    _dev(lens, torch.int32, (B,), "lens")
+    out = {"logits": torch.empty(B, m.vocab, dtype=torch.float32, device=dev)}
+    if want_hidden:
+        out["hidden"] = torch.empty(B * n, m.d_model, dtype=torch.float32, device=dev)
+    if want_routes:
+        out["routes"] = torch.empty(m.n_layers, B * n, m.top_k, dtype=torch.int32, device=dev)
+    ws, nb = _workspace(prefill_workspace_size(model, B, n, kv.struct.max_blocks_per_seq), dev, workspace)
+    st = lib.molt_prefill(ctypes.byref(m), ctypes.byref(kv.struct), B, n, _ptr(tokens), _ptr(lens),
+                          _ptr(out["logits"]), _ptr(out.get("hidden")), _ptr(out.get("routes")),
+                          _ptr(ws), nb, _stream())
+    _check(st, "molt_prefill")
+    return out
+
+
+class PrefixCache:
+    """The session-consistent prefix cache (host side, molt_prefix_cache_*): block ids of a
+    pool of num_blocks blocks for the callers' block tables. Token lists and rows are host
+    (numpy / Python) values."""
+
+    def __init__(self, num_blocks):
+        self._lib = load()
+        self._c = self._lib.molt_prefix_cache_create(num_blocks)
+        if not self._c:
+            raise MoltError("molt_prefix_cache_create failed")
+        self.num_blocks = num_blocks
+
+    def __del__(self):
+        if getattr(self, "_c", None):
+            self._lib.molt_prefix_cache_destroy(self._c)
+            self._c = None
+
+    def acquire(self, tokens, extra_tokens=0, max_blocks=None):
+        """-> (row [n_blocks] int32, n_cached), or None when the pool is exhausted or the row
+        would need more than max_blocks blocks."""
+        import numpy as np
+        toks = np.ascontiguousarray(tokens, dtype=np.int32)
+        n = len(toks)
+        mb = max_blocks if max_blocks is not None else (n + extra_tokens + 15) // 16
+        row = np.empty(max(mb, 1), dtype=np.int32)
+        hit = c_int(0)
+        r = self._lib.molt_prefix_cache_acquire(self._c, toks.ctypes.data, n, extra_tokens,
+                                                row.ctypes.data, mb, ctypes.byref(hit))
+        if r < 0:
+            return None
+        return row[:r].copy(), hit.value
+
+    def commit(self, tokens, row):
+        import numpy as np
+        toks = np.ascontiguousarray(tokens, dtype=np.int32)
+        row = np.ascontiguousarray(row, dtype=np.int32)
+        _check(self._lib.molt_prefix_cache_commit(self._c, toks.ctypes.data, len(toks), row.ctypes.data,
+                                                  len(row)), "molt_prefix_cache_commit")
+
+    def release(self, row):
+        import numpy as np
+        row = np.ascontiguousarray(row, dtype=np.int32)
+        _check(self._lib.molt_prefix_cache_release(self._c, row.ctypes.data, len(row)),
+               "molt_prefix_cache_release")
+
+    def stats(self):
+        out = (ctypes.c_longlong * 7)()
+        _check(self._lib.molt_prefix_cache_stats(self._c, out), "molt_prefix_cache_stats")
+        keys = ("free", "cached", "referenced", "evictable", "lookup_tokens", "hit_tokens", "evictions")
+        return dict(zip(keys, list(out)))
 
 
 def score_tokens_workspace_size(model, B, k, max_blocks):

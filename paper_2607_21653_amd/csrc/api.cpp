@@ -631,6 +631,58 @@ int molt_verify_step(const molt_model* m, const molt_kv* kv, int B, int k, const
   return hip_status(e, "molt_verify_step");
 }
 
+// ------------------------------------------------------------------ prefill
+
+namespace {
+struct PrefillWs { float* x; void* yf; float* hsel; void* ysel; DecWs dec; };
+PrefillWs carve_prefill(molt::Carver& c, const molt_model* m, int B, int n, int max_blocks,
+                        bool own_x) {
+  PrefillWs w{};
+  const long T = long(B) * n;
+  const size_t es = dt_size(m->dtype);
+  w.x = own_x ? c.take<float>(T * m->d_model) : nullptr;
+  w.yf = c.take<uint8_t>(pad32(T) * m->d_model * es);
+  w.hsel = c.take<float>(long(B) * m->d_model);
+  w.ysel = c.take<uint8_t>(pad32(B) * m->d_model * es);
+  w.dec = carve_dec(c, m, B, n - 1, max_blocks);
+  return w;
+}
+}  // namespace
+
+size_t molt_prefill_workspace_size(const molt_model* m, int B, int n, int max_blocks) {
+  if (!m || B < 1 || n < 1 || max_blocks < 1 || m->vocab < 1 || !pair_ok(m->dtype, m->expert_dtype))
+    return 0;
+  molt::Carver c(nullptr, 0);
+  carve_prefill(c, m, B, n, max_blocks, true);
+  return c.used + 256;
+}
+
+int molt_prefill(const molt_model* m, const molt_kv* kv, int B, int n, const int32_t* tokens,
+                 const int32_t* lens, float* out_logits, float* out_hidden, int32_t* out_routes,
+                 void* workspace, size_t workspace_bytes, molt_stream_t stream) {
+  REQUIRE(n >= 1, "n = %d must be >= 1", n);
+  if (int r = model_ok(m, kv, B, n - 1, true)) return r;
+  REQUIRE(tokens && lens && out_logits, "a required pointer is NULL");
+  if (int r = check_ws(workspace, workspace_bytes,
+                       molt_prefill_workspace_size(m, B, n, kv->max_blocks_per_seq)))
+    return r;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  molt::Carver c(workspace, workspace_bytes);
+  PrefillWs w = carve_prefill(c, m, B, n, kv->max_blocks_per_seq, true);
+  float* x = out_hidden ? out_hidden : w.x;
+  const int T = B * n;
+  hipError_t e = molt::launch_embed(m->embed, tokens, T, m->d_model, m->vocab, m->dtype, x, s);
+  if (e == hipSuccess) e = run_decoder(w.dec, m, kv, B, n - 1, x, out_routes, m->final_norm, w.yf, s);
+  if (e == hipSuccess)   // each sequence's last new row: row b n + lens[b] - 1
+    e = molt::launch_mtp_select(x, w.yf, lens, B, n - 1, m->d_model, m->dtype, w.hsel, w.ysel, s, -1);
+  if (e == hipSuccess) {
+    ProfScope ps(MOLT_PROF_LM_HEAD, s);
+    e = molt::launch_gemm(w.ysel, m->lm_head, out_logits, B, m->vocab, m->d_model, m->dtype, false,
+                          nullptr, 0, s);
+  }
+  return hip_status(e, "molt_prefill");
+}
+
 // ------------------------------------------------------------------ replay recompute
 
 namespace {

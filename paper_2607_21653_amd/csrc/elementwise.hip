@@ -358,12 +358,13 @@ __global__ __launch_bounds__(kThreads) void mtp_input_kernel(
   norm_half_store(v, gh, d, eps, dt, y, t, d, red);
 }
 
-// row b of hsel / ysel = catch-up row b(k+1) + n_b of x (f32 [T, d]) / yf (tiled [T, d] dt)
+// row b of hsel / ysel = row b(k+1) + clamp(n_b + delta) of x (f32 [T, d]) / yf (tiled
+// [T, d] dt): the draft head's catch-up row n_b (delta 0), a prefill's last row (delta -1)
 __global__ __launch_bounds__(kThreads) void mtp_select_kernel(
     const float* __restrict__ x, const uint8_t* __restrict__ yf, const int32_t* __restrict__ n_acc,
-    int k, int d, int es, float* __restrict__ hsel, uint8_t* __restrict__ ysel) {
+    int delta, int k, int d, int es, float* __restrict__ hsel, uint8_t* __restrict__ ysel) {
   const int b = blockIdx.x;
-  const long src = long(b) * (k + 1) + clamp_n(n_acc[b], k);
+  const long src = long(b) * (k + 1) + clamp_n(n_acc[b] + delta, k);
   for (int i = threadIdx.x * 4; i < d; i += kThreads * 4)
     *reinterpret_cast<float4*>(hsel + long(b) * d + i) = *reinterpret_cast<const float4*>(x + src * d + i);
   const long rb = long(d) * es;
@@ -458,8 +459,9 @@ hipError_t launch_mtp_input(const void* embed, const int32_t* tok, const float* 
 }
 
 hipError_t launch_mtp_select(const float* x, const void* yf, const int32_t* n_acc, int B, int k,
-                             int d, molt_dtype dt, float* hsel, void* ysel, hipStream_t s) {
-  mtp_select_kernel<<<B, kThreads, 0, s>>>(x, static_cast<const uint8_t*>(yf), n_acc, k, d,
+                             int d, molt_dtype dt, float* hsel, void* ysel, hipStream_t s,
+                             int delta) {
+  mtp_select_kernel<<<B, kThreads, 0, s>>>(x, static_cast<const uint8_t*>(yf), n_acc, delta, k, d,
                                            dt == MOLT_BF16 ? 2 : 4, hsel,
                                            static_cast<uint8_t*>(ysel));
   return hipGetLastError();

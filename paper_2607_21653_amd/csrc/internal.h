@@ -82,9 +82,11 @@ hipError_t launch_mtp_catchup(const int32_t* tokens, const int32_t* n_acc, const
 hipError_t launch_mtp_input(const void* embed, const int32_t* tok, const float* h, const float* ge,
                             const float* gh, int T, int d, int V, float eps, molt_dtype dt,
                             void* y, hipStream_t s);
-// hsel[b] = x[b(k+1) + n_b] (f32), ysel row b = yf row b(k+1) + n_b (tiled, dt)
+// hsel[b] = x[b(k+1) + n_b + delta] (f32), ysel row b = yf row b(k+1) + n_b + delta (tiled,
+// dt); n_b + delta clamped to [0, k]
 hipError_t launch_mtp_select(const float* x, const void* yf, const int32_t* n_acc, int B, int k,
-                             int d, molt_dtype dt, float* hsel, void* ysel, hipStream_t s);
+                             int d, molt_dtype dt, float* hsel, void* ysel, hipStream_t s,
+                             int delta = 0);
 // drafts[b, i] = tok[b]; then (i + 1 < k) row_tok[b] = tok[b], ctx_next[b] = ctx[b] + n_b +
 // i + 1, u_col[b] = u[b, i + 1]
 hipError_t launch_mtp_record(const int32_t* tok, int i, int B, int k, const int32_t* ctx,

@@ -94,7 +94,7 @@ def test_attention_validation(L):
     assert call(D=96) == INVALID
     assert call(Hq=30) == INVALID
     assert call(k=-1) == INVALID
-    assert call(Hq=64, Hkv=2, k=4) == INVALID     # 160 query rows per kv head
+    assert call(Hq=256, Hkv=1, k=0) == INVALID    # 256 query heads per kv head (a tile holds 128 rows)
     assert call(dt=2) == INVALID
     assert call(B=2, mb=2000, ws=None, wsb=0) == WORKSPACE
 
