@@ -206,6 +206,42 @@ def replay_measure(molt, model, kv, tokens, u, q, reps=3):
                     "targets and its recorded routes replayed"}
 
 
+REPREFILL_TOKENS = 256
+
+
+def reprefill_measure(w, seed, molt, model, layout, kv, reps=3):
+    """Cache-hit re-prefill of an agent's growing context: sequence 0's cached 16-token
+    blocks below its context (8192 positions) are the hit, and a new turn of
+    REPREFILL_TOKENS tokens is prefilled at that context into spare blocks (molt_prefill,
+    B = 1). Timed with HIP events after the timed region."""
+    import torch
+    dev = "cuda"
+    ctx = int(layout.context_lens[0]) // 16 * 16
+    used = set(int(b) for b in layout.block_tables.ravel() if b >= 0)
+    spare = [b for b in range(layout.num_blocks) if b not in used][:REPREFILL_TOKENS // 16]
+    row = np.concatenate([layout.block_tables[0][:ctx // 16], np.array(spare, np.int32)]).astype(np.int32)
+    kv1 = molt.KVCache(kv.k_caches, kv.v_caches, torch.from_numpy(row[None, :].copy()).to(dev),
+                       torch.tensor([ctx], dtype=torch.int32, device=dev))
+    g = np.random.Generator(np.random.Philox(workloads._seed(seed, w.name, "reprefill")))
+    toks = torch.from_numpy(g.integers(0, w.vocab, (1, REPREFILL_TOKENS)).astype(np.int32)).to(dev)
+    lens = torch.tensor([REPREFILL_TOKENS], dtype=torch.int32, device=dev)
+    ws = torch.empty(molt.prefill_workspace_size(model, 1, REPREFILL_TOKENS, len(row)), dtype=torch.uint8,
+                     device=dev)
+    out = molt.prefill(model, kv1, toks, lens, workspace=ws)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        molt.prefill(model, kv1, toks, lens, workspace=ws)
+    e1.record()
+    torch.cuda.synchronize()
+    assert torch.isfinite(out["logits"]).all()
+    return {"avg_ms": round(e0.elapsed_time(e1) / reps, 3), "cached_tokens": ctx,
+            "new_tokens": REPREFILL_TOKENS,
+            "note": "molt_prefill of one session's new turn at context 8192 (its cached prefix read "
+                    "from the paged cache, not recomputed): the cache-hit re-prefill latency"}
+
+
 CPU_SAMPLE_SEQS, CPU_SAMPLE_LAYERS = 8, 12
 
 
@@ -219,8 +255,9 @@ def build(w, seed, molt, keep_host=0):
     layout in place of the row-major ones. Row-major host copies of the head and of the
     first `keep_host` layers are kept for the CPU baseline."""
     dev = "cuda"
-    # room for the draft head's rows too (up to k - 1 positions past the verify window)
-    layout = workloads.make_kv_layout(w, seed, extra_tokens=w.k)
+    # room for the draft head's rows too (up to k - 1 positions past the verify window), and
+    # spare blocks for the re-prefill measurement
+    layout = workloads.make_kv_layout(w, seed, spare_blocks=REPREFILL_TOKENS // 16, extra_tokens=w.k)
     layers, kcs, vcs, host_layers = [], [], [], []
     for l in range(w.n_layers):
         lw = workloads.make_layer_weights(w, seed, l, device=dev)
@@ -396,6 +433,8 @@ def main():
     mtp = mtp_measure(w, a.seed, molt, model, layout, kv, tokens, u, q) if k > 0 else None
     log("[bench] replay recompute")
     rep = replay_measure(molt, model, kv, tokens, u, q)
+    log("[bench] cache-hit re-prefill")
+    rpf = reprefill_measure(w, a.seed, molt, model, layout, kv)
     positions = B * (k + 1)
     value = positions / (ms / 1e3)
     emitted = float((n_acc + 1).sum()) / (ms / 1e3)
@@ -437,6 +476,7 @@ def main():
         "other_rooflines": other_rooflines(w, groups, samp),
         "mtp_draft": mtp,
         "replay_recompute": rep,
+        "reprefill": rpf,
     }
     if not a.no_cpu_baseline:
         log("[bench] timing the CPU oracle on a bounded sample")
