@@ -363,6 +363,8 @@ def main():
     ap.add_argument("--workload", default="full_depth_bf16", choices=sorted(workloads.WORKLOADS))
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--verify-only", action="store_true",
+                    help="skip the draft-head, replay and re-prefill measurements (profiling runs)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a 1 GiB device-to-device copy (HBM counter calibration)")
     a = ap.parse_args()
@@ -429,12 +431,14 @@ def main():
     n_break = min(a.steps, 3)
     samp = sampler_roofline(w, molt, out, tokens, q, u)
     n_acc = out["n_accepted"].cpu().numpy()
-    log("[bench] MTP draft step")
-    mtp = mtp_measure(w, a.seed, molt, model, layout, kv, tokens, u, q) if k > 0 else None
-    log("[bench] replay recompute")
-    rep = replay_measure(molt, model, kv, tokens, u, q)
-    log("[bench] cache-hit re-prefill")
-    rpf = reprefill_measure(w, a.seed, molt, model, layout, kv)
+    mtp = rep = rpf = None
+    if not a.verify_only:
+        log("[bench] MTP draft step")
+        mtp = mtp_measure(w, a.seed, molt, model, layout, kv, tokens, u, q) if k > 0 else None
+        log("[bench] replay recompute")
+        rep = replay_measure(molt, model, kv, tokens, u, q)
+        log("[bench] cache-hit re-prefill")
+        rpf = reprefill_measure(w, a.seed, molt, model, layout, kv)
     positions = B * (k + 1)
     value = positions / (ms / 1e3)
     emitted = float((n_acc + 1).sum()) / (ms / 1e3)
