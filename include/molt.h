@@ -405,6 +405,20 @@ typedef struct molt_mtp {
  * - 1; c_b + max(k, n_b + k - 1) < 16 * max_blocks_per_seq is the caller's duty
  * (positions past the block table are computed and not written).
  * ---------------------------------------------------------------------------- */
+/* molt_mtp_draft_window -- the same step with a catch-up window of `window` rows per
+ * sequence instead of 1+k: hidden [B*window, d] and tokens [B, window] at positions
+ * c_b .. c_b + window - 1, n_accepted[b] in [0, window - 1] the row that yields draft 1.
+ * After a prefill (window = its n, n_accepted = lens - 1, next_tokens = the token sampled
+ * from its logits, hidden = its out_hidden) it fills the head's cache for the prompt and
+ * drafts the first k tokens; molt_mtp_draft is window = k + 1. Positions written:
+ * c_b .. c_b + window - 1 and c_b + n_b + 1 .. c_b + n_b + k - 1. */
+size_t molt_mtp_draft_window_workspace_size(const molt_model* target, const molt_mtp* mtp, int B,
+                                            int window, int k, int max_blocks_per_seq);
+int molt_mtp_draft_window(const molt_model* target, const molt_mtp* mtp, const molt_kv* mtp_kv,
+                          int B, int window, int k, const float* hidden, const int32_t* tokens,
+                          const int32_t* n_accepted, const int32_t* next_tokens,
+                          const float* uniforms, int32_t* out_drafts, float* out_draft_probs,
+                          void* workspace, size_t workspace_bytes, molt_stream_t stream);
 size_t molt_mtp_draft_workspace_size(const molt_model* target, const molt_mtp* mtp, int B, int k,
                                      int max_blocks_per_seq);
 int molt_mtp_draft(const molt_model* target, const molt_mtp* mtp, const molt_kv* mtp_kv, int B,

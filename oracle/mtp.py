@@ -17,7 +17,8 @@ Row (h_p, token at p+1) sits at cache position p and predicts the token at p+2.
 
 After a verify step of sequence b (context c_b; tokens x_0..x_k at positions c_b..c_b+k;
 n_b accepted drafts; the emitted token y_b, the bonus or replacement, at position
-c_b + n_b + 1) one draft step runs:
+c_b + n_b + 1) one draft step runs (after a prefill the catch-up window is the prompt's
+instead of k+1 rows, with n_b = its length - 1 and y_b the token sampled from its logits):
   * catch-up: k+1 rows per sequence at positions c_b + j, j = 0..k, with h = the target's
     final residual stream (before its final norm) at row j and token x_{j+1} for j < n_b,
     y_b for j >= n_b. Row n_b predicts draft 1. Rows past n_b carry rejected drafts' hidden
@@ -55,8 +56,9 @@ def head_logits(x, mtp, head, cfg):
 
 
 def mtp_draft(hidden, tokens, n_accepted, next_tokens, mtp, head, kcache, vcache, block_tables,
-              context_lens, cfg, uniforms=None, forced=None):
-    """hidden [B(1+k), d] f32 (the verify step's final residual stream); tokens [B, 1+k];
+              context_lens, cfg, uniforms=None, forced=None, k=None):
+    """hidden [B W, d] f32 (the verify step's final residual stream: W = 1+k; or a prefill's,
+    W = its window, with n_accepted = lens - 1); tokens [B, W]; k drafts (default W - 1);
     n_accepted [B]; next_tokens [B]; kcache/vcache: the head's cache as float64 arrays
     (updated in place); uniforms [B, k] (None: greedy drafts). forced [B, k]: feed these
     tokens to the following rows instead of the drawn drafts (teacher forcing, to compare
@@ -67,8 +69,8 @@ def mtp_draft(hidden, tokens, n_accepted, next_tokens, mtp, head, kcache, vcache
     (the draw's margin relative to its total mass; greedy: the gap between the two largest
     logits)."""
     tokens = np.asarray(tokens)
-    B, kp1 = tokens.shape
-    k = kp1 - 1
+    B, kp1 = tokens.shape                      # kp1: the catch-up window W
+    k = kp1 - 1 if k is None else k
     n = np.asarray(n_accepted).astype(np.int64)
     nxt = np.asarray(next_tokens).astype(np.int64)
     ctx = np.asarray(context_lens).astype(np.int64)
@@ -76,7 +78,7 @@ def mtp_draft(hidden, tokens, n_accepted, next_tokens, mtp, head, kcache, vcache
     row_tok = np.array([[tokens[b, j + 1] if j < n[b] else nxt[b] for j in range(kp1)]
                         for b in range(B)]).reshape(-1)
     x = head_input(row_tok, np.asarray(hidden, np.float32), mtp, head, cfg)
-    x = head_layer(x, mtp, kcache, vcache, block_tables, ctx, k, cfg)
+    x = head_layer(x, mtp, kcache, vcache, block_tables, ctx, kp1 - 1, cfg)
     h = x[np.arange(B) * kp1 + n]
     drafts = np.zeros((B, k), np.int32)
     logits_all, qs, hs, margins = [], [], [], np.zeros((B, k))

@@ -83,6 +83,11 @@ _SIGS = {
                                   c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_size, c_vp]),
     "molt_mtp_draft_workspace_size": (c_size, [ctypes.POINTER(MoltModel), ctypes.POINTER(MoltMtp),
                                                c_int, c_int, c_int]),
+    "molt_mtp_draft_window_workspace_size": (c_size, [ctypes.POINTER(MoltModel), ctypes.POINTER(MoltMtp),
+                                                      c_int, c_int, c_int, c_int]),
+    "molt_mtp_draft_window": (c_int, [ctypes.POINTER(MoltModel), ctypes.POINTER(MoltMtp),
+                                      ctypes.POINTER(MoltKV), c_int, c_int, c_int, c_vp, c_vp, c_vp,
+                                      c_vp, c_vp, c_vp, c_vp, c_vp, c_size, c_vp]),
     "molt_mtp_draft": (c_int, [ctypes.POINTER(MoltModel), ctypes.POINTER(MoltMtp),
                                ctypes.POINTER(MoltKV), c_int, c_int, c_vp, c_vp, c_vp, c_vp, c_vp,
                                c_vp, c_vp, c_vp, c_size, c_vp]),
@@ -543,22 +548,24 @@ class Mtp:
         self.struct = s
 
 
-def mtp_draft_workspace_size(target, mtp, B, k, max_blocks):
-    return load().molt_mtp_draft_workspace_size(ctypes.byref(target.struct), ctypes.byref(mtp.struct),
-                                                B, k, max_blocks)
+def mtp_draft_workspace_size(target, mtp, B, k, max_blocks, window=None):
+    return load().molt_mtp_draft_window_workspace_size(
+        ctypes.byref(target.struct), ctypes.byref(mtp.struct), B, k + 1 if window is None else window,
+        k, max_blocks)
 
 
 def mtp_draft(target, mtp, kv, hidden, tokens, n_accepted, next_tokens, uniforms=None,
-              greedy=False, workspace=None, out=None):
-    """One draft step after a verify step (molt_mtp_draft). hidden [B*(1+k), d] f32,
-    tokens [B, 1+k] i32, n_accepted [B] i32, next_tokens [B] i32, uniforms [B, k] f32
-    (unused when greedy). Returns dict(drafts [B, k] i32, draft_probs [B, k, V] f32 or None)."""
+              greedy=False, k=None, workspace=None, out=None):
+    """One draft step (molt_mtp_draft_window): after a verify step (tokens [B, 1+k], the
+    default k) or after a prefill (tokens [B, n] = its window, n_accepted = lens - 1, k given).
+    hidden [B*W, d] f32, n_accepted [B] i32, next_tokens [B] i32, uniforms [B, k] f32 (unused
+    when greedy). Returns dict(drafts [B, k] i32, draft_probs [B, k, V] f32 or None)."""
     lib = load()
-    B, kp1 = tokens.shape
-    k = kp1 - 1
+    B, W = tokens.shape
+    k = W - 1 if k is None else k
     V, d = target.struct.vocab, target.struct.d_model
     dev = tokens.device
-    _dev(hidden, torch.float32, (B * kp1, d), "hidden")
+    _dev(hidden, torch.float32, (B * W, d), "hidden")
     _dev(tokens, torch.int32, name="tokens")
     _dev(n_accepted, torch.int32, (B,), "n_accepted")
     _dev(next_tokens, torch.int32, (B,), "next_tokens")
@@ -567,12 +574,13 @@ def mtp_draft(target, mtp, kv, hidden, tokens, n_accepted, next_tokens, uniforms
     if out is None:
         out = {"drafts": torch.empty(B, k, dtype=torch.int32, device=dev),
                "draft_probs": None if greedy else torch.empty(B, k, V, dtype=torch.float32, device=dev)}
-    ws, nb = _workspace(mtp_draft_workspace_size(target, mtp, B, k, kv.struct.max_blocks_per_seq), dev,
+    ws, nb = _workspace(mtp_draft_workspace_size(target, mtp, B, k, kv.struct.max_blocks_per_seq, W), dev,
                         workspace)
-    st = lib.molt_mtp_draft(ctypes.byref(target.struct), ctypes.byref(mtp.struct), ctypes.byref(kv.struct),
-                            B, k, _ptr(hidden), _ptr(tokens), _ptr(n_accepted), _ptr(next_tokens),
-                            _ptr(None if greedy else uniforms), _ptr(out["drafts"]),
-                            _ptr(out["draft_probs"]), _ptr(ws), nb, _stream())
+    st = lib.molt_mtp_draft_window(ctypes.byref(target.struct), ctypes.byref(mtp.struct),
+                                   ctypes.byref(kv.struct), B, W, k, _ptr(hidden), _ptr(tokens),
+                                   _ptr(n_accepted), _ptr(next_tokens),
+                                   _ptr(None if greedy else uniforms), _ptr(out["drafts"]),
+                                   _ptr(out["draft_probs"]), _ptr(ws), nb, _stream())
     _check(st, "molt_mtp_draft")
     return out
 

@@ -745,13 +745,13 @@ struct MtpWs {
   int32_t* row_tok; float* u_col; int32_t* ctx_next; int32_t* tok;
   void* y2; float* part; long part_elems;
   float* x; void* yf; float* hsel; void* ysel; float* logits; void* draw;
-  DecWs cat, one;   // decoder workspaces of the catch-up rows (B, k) and a drafting row (B, 0)
+  DecWs cat, one;   // decoder workspaces of the catch-up rows (B, W) and a drafting row (B, 1)
 };
 
-MtpWs carve_mtp(molt::Carver& c, const molt_model* t, const molt_model* L, int B, int k,
+MtpWs carve_mtp(molt::Carver& c, const molt_model* t, const molt_model* L, int B, int W,
                 int max_blocks) {
   MtpWs w{};
-  const long T = long(B) * (k + 1);
+  const long T = long(B) * W;
   const int d = t->d_model;
   const size_t es = dt_size(t->dtype);
   w.row_tok = c.take<int32_t>(T);
@@ -767,16 +767,17 @@ MtpWs carve_mtp(molt::Carver& c, const molt_model* t, const molt_model* L, int B
   w.ysel = c.take<uint8_t>(pad32(B) * d * es);
   w.logits = c.take<float>(long(B) * t->vocab);
   w.draw = c.take<uint8_t>(molt::draft_draw_ws_bytes(B, t->vocab));
-  w.cat = carve_dec(c, L, B, k, max_blocks);
+  w.cat = carve_dec(c, L, B, W - 1, max_blocks);
   w.one = carve_dec(c, L, B, 0, max_blocks);
   return w;
 }
 
-int mtp_ok(const molt_model* t, const molt_mtp* mtp, const molt_kv* kv, int B, int k) {
+int mtp_ok(const molt_model* t, const molt_mtp* mtp, const molt_kv* kv, int B, int W, int k) {
   REQUIRE(t && mtp && kv, "target, mtp and mtp_kv are required");
   REQUIRE(mtp->layer, "mtp->layer is NULL");
   const molt_model* L = mtp->layer;
   REQUIRE(k >= 1, "k = %d must be >= 1 to draft", k);
+  REQUIRE(W >= 1, "window = %d must be >= 1", W);
   REQUIRE(act_ok(t->dtype), "target dtype must be F32 or BF16");
   REQUIRE(t->vocab >= 1 && t->embed && t->lm_head, "the target's embed, lm_head and vocab are required");
   REQUIRE(L->n_layers == 1, "the head has n_layers = %d, must be 1", L->n_layers);
@@ -787,37 +788,44 @@ int mtp_ok(const molt_model* t, const molt_mtp* mtp, const molt_kv* kv, int B, i
           "enorm, hnorm, eh_proj and layer->final_norm are required");
   REQUIRE(2L * t->d_model * long(dt_size(t->dtype)) % 128 == 0, "2 d * sizeof(dtype) must be a multiple of 128");
   if (int r = spec_accept_shape_ok(B, 0, t->vocab)) return r;
-  return model_ok(L, kv, B, k, false);
+  return model_ok(L, kv, B, W - 1, false);
 }
 
 }  // namespace
 
-size_t molt_mtp_draft_workspace_size(const molt_model* target, const molt_mtp* mtp, int B, int k,
-                                     int max_blocks) {
-  if (!target || !mtp || !mtp->layer || B < 1 || k < 1 || max_blocks < 1 || target->vocab < 1 ||
-      !pair_ok(mtp->layer->dtype, mtp->layer->expert_dtype))
+size_t molt_mtp_draft_window_workspace_size(const molt_model* target, const molt_mtp* mtp, int B,
+                                            int window, int k, int max_blocks) {
+  if (!target || !mtp || !mtp->layer || B < 1 || window < 1 || k < 1 || max_blocks < 1 ||
+      target->vocab < 1 || !pair_ok(mtp->layer->dtype, mtp->layer->expert_dtype))
     return 0;
   molt::Carver c(nullptr, 0);
-  carve_mtp(c, target, mtp->layer, B, k, max_blocks);
+  carve_mtp(c, target, mtp->layer, B, window, max_blocks);
   return c.used + 256;
 }
 
-int molt_mtp_draft(const molt_model* target, const molt_mtp* mtp, const molt_kv* mtp_kv, int B,
-                   int k, const float* hidden, const int32_t* tokens, const int32_t* n_accepted,
-                   const int32_t* next_tokens, const float* uniforms, int32_t* out_drafts,
-                   float* out_draft_probs, void* workspace, size_t workspace_bytes,
-                   molt_stream_t stream) {
-  if (int r = mtp_ok(target, mtp, mtp_kv, B, k)) return r;
+size_t molt_mtp_draft_workspace_size(const molt_model* target, const molt_mtp* mtp, int B, int k,
+                                     int max_blocks) {
+  return molt_mtp_draft_window_workspace_size(target, mtp, B, k + 1, k, max_blocks);
+}
+
+int molt_mtp_draft_window(const molt_model* target, const molt_mtp* mtp, const molt_kv* mtp_kv,
+                          int B, int window, int k, const float* hidden, const int32_t* tokens,
+                          const int32_t* n_accepted, const int32_t* next_tokens,
+                          const float* uniforms, int32_t* out_drafts, float* out_draft_probs,
+                          void* workspace, size_t workspace_bytes, molt_stream_t stream) {
+  const int W = window;
+  if (int r = mtp_ok(target, mtp, mtp_kv, B, W, k)) return r;
   REQUIRE(hidden && tokens && n_accepted && next_tokens && out_drafts, "a required pointer is NULL");
   REQUIRE(out_draft_probs == nullptr || uniforms, "sampled drafts (out_draft_probs) need uniforms");
   if (int r = check_ws(workspace, workspace_bytes,
-                       molt_mtp_draft_workspace_size(target, mtp, B, k, mtp_kv->max_blocks_per_seq)))
+                       molt_mtp_draft_window_workspace_size(target, mtp, B, W, k,
+                                                            mtp_kv->max_blocks_per_seq)))
     return r;
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   molt::Carver c(workspace, workspace_bytes);
-  MtpWs w = carve_mtp(c, target, mtp->layer, B, k, mtp_kv->max_blocks_per_seq);
+  MtpWs w = carve_mtp(c, target, mtp->layer, B, W, mtp_kv->max_blocks_per_seq);
   const molt_model* L = mtp->layer;
-  const int d = target->d_model, V = target->vocab, T = B * (k + 1);
+  const int d = target->d_model, V = target->vocab, T = B * W;
   const molt_dtype dt = target->dtype;
   const float* u = out_draft_probs ? uniforms : nullptr;   // greedy drafts draw nothing
   molt_kv one = *mtp_kv;        // drafting rows: context c_b + n_b + i per sequence
@@ -825,15 +833,15 @@ int molt_mtp_draft(const molt_model* target, const molt_mtp* mtp, const molt_kv*
   hipError_t e = hipSuccess;
 #define RUN(call) do { if ((e = (call)) != hipSuccess) return hip_status(e, "molt_mtp_draft"); } while (0)
   // catch-up rows
-  RUN(molt::launch_mtp_catchup(tokens, n_accepted, next_tokens, u, B, k, w.row_tok, w.u_col, s));
+  RUN(molt::launch_mtp_catchup(tokens, n_accepted, next_tokens, u, B, W, k, w.row_tok, w.u_col, s));
   RUN(molt::launch_mtp_input(target->embed, w.row_tok, hidden, mtp->enorm, mtp->hnorm, T, d, V,
                              L->rms_eps, dt, w.y2, s));
   {
     ProfScope ps(MOLT_PROF_PROJECTIONS, s);
     RUN(molt::launch_gemm(w.y2, mtp->eh_proj, w.x, T, d, 2 * d, dt, false, w.part, w.part_elems, s));
   }
-  RUN(run_decoder(w.cat, L, mtp_kv, B, k, w.x, nullptr, L->final_norm, w.yf, s));
-  RUN(molt::launch_mtp_select(w.x, w.yf, n_accepted, B, k, d, dt, w.hsel, w.ysel, s));
+  RUN(run_decoder(w.cat, L, mtp_kv, B, W - 1, w.x, nullptr, L->final_norm, w.yf, s));
+  RUN(molt::launch_mtp_select(w.x, w.yf, n_accepted, B, W - 1, d, dt, w.hsel, w.ysel, s));
   for (int i = 0; i < k; ++i) {
     {
       ProfScope ps(MOLT_PROF_LM_HEAD, s);
@@ -846,7 +854,7 @@ int molt_mtp_draft(const molt_model* target, const molt_mtp* mtp, const molt_kv*
                                   out_draft_probs ? out_draft_probs + long(i) * V : nullptr,
                                   long(k) * V, w.draw, s));
     }
-    RUN(molt::launch_mtp_record(w.tok, i, B, k, mtp_kv->context_lens, n_accepted, u, out_drafts,
+    RUN(molt::launch_mtp_record(w.tok, i, B, W, k, mtp_kv->context_lens, n_accepted, u, out_drafts,
                                 w.row_tok, w.ctx_next, w.u_col, s));
     if (i + 1 == k) break;
     // drafting row: the head's previous output and draft i + 1 (the input kernel has read
@@ -861,6 +869,16 @@ int molt_mtp_draft(const molt_model* target, const molt_mtp* mtp, const molt_kv*
   }
 #undef RUN
   return ok();
+}
+
+int molt_mtp_draft(const molt_model* target, const molt_mtp* mtp, const molt_kv* mtp_kv, int B,
+                   int k, const float* hidden, const int32_t* tokens, const int32_t* n_accepted,
+                   const int32_t* next_tokens, const float* uniforms, int32_t* out_drafts,
+                   float* out_draft_probs, void* workspace, size_t workspace_bytes,
+                   molt_stream_t stream) {
+  return molt_mtp_draft_window(target, mtp, mtp_kv, B, k + 1, k, hidden, tokens, n_accepted,
+                               next_tokens, uniforms, out_drafts, out_draft_probs, workspace,
+                               workspace_bytes, stream);
 }
 
 }  // extern "C"

@@ -268,16 +268,17 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(const float* __restri
 
 MOLT_DEV int clamp_n(int n, int k) { return n < 0 ? 0 : n > k ? k : n; }
 
-// catch-up row r = b(k+1) + j takes token x_{j+1} (j < n_b) or y_b; u_col[b] = u[b, 0]
+// catch-up row r = b W + j (W rows per sequence) takes token x_{j+1} (j < n_b) or y_b;
+// u_col[b] = u[b, 0] (u: [B, k] draft uniforms)
 __global__ void mtp_catchup_kernel(const int32_t* __restrict__ tokens,
                                    const int32_t* __restrict__ n_acc,
                                    const int32_t* __restrict__ next, const float* __restrict__ u,
-                                   int B, int k, int32_t* __restrict__ row_tok,
+                                   int B, int W, int k, int32_t* __restrict__ row_tok,
                                    float* __restrict__ u_col) {
   const int r = blockIdx.x * blockDim.x + threadIdx.x;
-  if (r >= B * (k + 1)) return;
-  const int b = r / (k + 1), j = r % (k + 1);
-  const int nb = clamp_n(n_acc[b], k);
+  if (r >= B * W) return;
+  const int b = r / W, j = r % W;
+  const int nb = clamp_n(n_acc[b], W - 1);
   row_tok[r] = j < nb ? tokens[r + 1] : next[b];
   if (j == 0 && u) u_col[b] = u[long(b) * k];
 }
@@ -375,7 +376,7 @@ __global__ __launch_bounds__(kThreads) void mtp_select_kernel(
 
 // after draft i + 1 is drawn (tok): drafts[b, i] = tok[b]; for the next drafting row its
 // token, its context (position c_b + n_b + i + 1 is the row's own) and its uniform
-__global__ void mtp_record_kernel(const int32_t* __restrict__ tok, int i, int B, int k,
+__global__ void mtp_record_kernel(const int32_t* __restrict__ tok, int i, int B, int W, int k,
                                   const int32_t* __restrict__ ctx, const int32_t* __restrict__ n_acc,
                                   const float* __restrict__ u, int32_t* __restrict__ drafts,
                                   int32_t* __restrict__ row_tok, int32_t* __restrict__ ctx_next,
@@ -386,7 +387,7 @@ __global__ void mtp_record_kernel(const int32_t* __restrict__ tok, int i, int B,
   drafts[long(b) * k + i] = t;
   if (i + 1 < k) {
     row_tok[b] = t;
-    ctx_next[b] = ctx[b] + clamp_n(n_acc[b], k) + i + 1;
+    ctx_next[b] = ctx[b] + clamp_n(n_acc[b], W - 1) + i + 1;
     if (u) u_col[b] = u[long(b) * k + i + 1];
   }
 }
@@ -443,11 +444,11 @@ hipError_t launch_combine(const float* o, const float* w, int T, int K, int d, f
 }
 
 hipError_t launch_mtp_catchup(const int32_t* tokens, const int32_t* n_acc, const int32_t* next,
-                              const float* u, int B, int k, int32_t* row_tok, float* u_col,
+                              const float* u, int B, int W, int k, int32_t* row_tok, float* u_col,
                               hipStream_t s) {
-  const int T = B * (k + 1);
-  mtp_catchup_kernel<<<(T + kThreads - 1) / kThreads, kThreads, 0, s>>>(tokens, n_acc, next, u, B, k,
-                                                                       row_tok, u_col);
+  const int T = B * W;
+  mtp_catchup_kernel<<<(T + kThreads - 1) / kThreads, kThreads, 0, s>>>(tokens, n_acc, next, u, B, W,
+                                                                       k, row_tok, u_col);
   return hipGetLastError();
 }
 
@@ -467,10 +468,10 @@ hipError_t launch_mtp_select(const float* x, const void* yf, const int32_t* n_ac
   return hipGetLastError();
 }
 
-hipError_t launch_mtp_record(const int32_t* tok, int i, int B, int k, const int32_t* ctx,
+hipError_t launch_mtp_record(const int32_t* tok, int i, int B, int W, int k, const int32_t* ctx,
                              const int32_t* n_acc, const float* u, int32_t* drafts,
                              int32_t* row_tok, int32_t* ctx_next, float* u_col, hipStream_t s) {
-  mtp_record_kernel<<<(B + kThreads - 1) / kThreads, kThreads, 0, s>>>(tok, i, B, k, ctx, n_acc, u,
+  mtp_record_kernel<<<(B + kThreads - 1) / kThreads, kThreads, 0, s>>>(tok, i, B, W, k, ctx, n_acc, u,
                                                                       drafts, row_tok, ctx_next, u_col);
   return hipGetLastError();
 }

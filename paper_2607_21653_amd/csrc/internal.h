@@ -73,10 +73,10 @@ hipError_t launch_quant_rows_tiled(const uint16_t* h, const int32_t* pperm, cons
 hipError_t launch_combine(const float* o, const float* w, int T, int K, int d, float* out,
                           bool accumulate, hipStream_t s);
 
-// MTP draft head rows. Catch-up row b(k+1)+j takes token tokens[b, j+1] (j < n_b) or
-// next[b], and u_col[b] = u[b, 0] (u may be null).
+// MTP draft head rows. Catch-up row bW+j (W rows per sequence) takes token tokens[b, j+1]
+// (j < n_b) or next[b], and u_col[b] = u[b, 0] (u: [B, k], may be null).
 hipError_t launch_mtp_catchup(const int32_t* tokens, const int32_t* n_acc, const int32_t* next,
-                              const float* u, int B, int k, int32_t* row_tok, float* u_col,
+                              const float* u, int B, int W, int k, int32_t* row_tok, float* u_col,
                               hipStream_t s);
 // y[t] = [RMSNorm(Emb[tok[t]]; ge) ; RMSNorm(h[t]; gh)] rounded to dt, tiled [T, 2d]
 hipError_t launch_mtp_input(const void* embed, const int32_t* tok, const float* h, const float* ge,
@@ -88,8 +88,8 @@ hipError_t launch_mtp_select(const float* x, const void* yf, const int32_t* n_ac
                              int d, molt_dtype dt, float* hsel, void* ysel, hipStream_t s,
                              int delta = 0);
 // drafts[b, i] = tok[b]; then (i + 1 < k) row_tok[b] = tok[b], ctx_next[b] = ctx[b] + n_b +
-// i + 1, u_col[b] = u[b, i + 1]
-hipError_t launch_mtp_record(const int32_t* tok, int i, int B, int k, const int32_t* ctx,
+// i + 1 (n_b clamped to [0, W - 1]), u_col[b] = u[b, i + 1]
+hipError_t launch_mtp_record(const int32_t* tok, int i, int B, int W, int k, const int32_t* ctx,
                              const int32_t* n_acc, const float* u, int32_t* drafts,
                              int32_t* row_tok, int32_t* ctx_next, float* u_col, hipStream_t s);
 
