@@ -217,3 +217,24 @@ def test_full_shape_synthetic(molt_lib):
                        forced=drafts[seqs])
     _check_q(q[seqs].cpu().numpy(), o["q"], 5e-2, 1e-6)
     _drafts_in_cdf(drafts[seqs], o["q"], host(ud)[seqs], 1e-3)
+
+
+def test_tiny_one_draft(molt_lib):
+    """k = 1: the catch-up rows alone give the only draft (no drafting row)."""
+    molt = molt_lib
+    w = workloads.TINY_FP32.scaled(k=1)
+    s = _setup(molt, w, 15)
+    toks, hidden, n, nxt = _verify(molt, s, 16)
+    ud = workloads.make_uniforms(w.batch, 0, 17, tag="mtp_u")
+    hc0 = tuple(host(c) for c in (s["hkv"].k_caches[0], s["hkv"].v_caches[0]))
+    g = molt.mtp_draft(s["model"], s["mtp"], s["hkv"], hidden, dev(torch.from_numpy(toks)), n, nxt, dev(ud))
+    gg = molt.mtp_draft(s["model"], s["mtp"], s["hkv"], hidden, dev(torch.from_numpy(toks)), n, nxt, greedy=True)
+    torch.cuda.synchronize()
+    drafts = g["drafts"].cpu().numpy()
+    o, _, _ = _oracle(s, host(hidden), toks, host(n), host(nxt), hc0, host(ud), drafts)
+    _check_q(g["draft_probs"].cpu().numpy(), o["q"], 1e-4, 1e-7)
+    ok = o["margin"] > 1e-6
+    np.testing.assert_array_equal(drafts[ok], o["drafts"][ok])
+    og, _, _ = _oracle(s, host(hidden), toks, host(n), host(nxt), hc0, None, gg["drafts"].cpu().numpy())
+    ok = og["margin"] > 1e-4
+    np.testing.assert_array_equal(gg["drafts"].cpu().numpy()[ok], og["drafts"][ok])

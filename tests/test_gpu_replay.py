@@ -76,3 +76,20 @@ def test_recompute_reproduces_verify_and_oracle(molt_lib, wname):
         err = max_abs(g["logprobs"].cpu().numpy(), o["logprobs"])
         print(f"{name} routes: max |logprob - oracle| = {err:.3e}", flush=True)
         assert err <= tol
+
+
+def test_recompute_single_position(molt_lib):
+    """k = 0: one position per sequence (a plain decode step's recompute)."""
+    molt = molt_lib
+    w = workloads.TINY_FP32.scaled(k=0)
+    seed = 43
+    layout, layers, head, caches, kv, model = _setup(molt, w, seed)
+    toks = workloads.make_step_tokens(w, seed)
+    targets = np.random.default_rng(seed).integers(0, w.vocab, toks.shape).astype(np.int32)
+    g = molt.score_tokens(model, kv, dev(torch.from_numpy(toks)), dev(torch.from_numpy(targets)),
+                          want_routes=True)
+    torch.cuda.synchronize()
+    o = _oracle(w, layout, layers, head, caches, toks, targets, None)
+    clear = g["routes"].cpu().numpy() == o["routes"]
+    assert clear.all()
+    assert max_abs(g["logprobs"].cpu().numpy(), o["logprobs"]) <= 1e-4
