@@ -124,7 +124,10 @@ def test_full_depth_step(molt_lib):
     ok = ~near
     print(f"sampler: {near.sum()} near-tie sequences excluded; mean accepted fraction "
           f"{a['n_accepted'].mean() / k:.3f}", flush=True)
-    assert near.sum() <= 2
+    # near-ties are a property of the logits, not an error: with near-uniform rows over
+    # 151936 tokens a draw lands within 2e-8 of a CDF boundary with probability ~0.6% per
+    # sequence (~0.8 of 128 expected); 7 or more has probability ~1e-4
+    assert near.sum() <= 6
     assert (a["n_accepted"][ok] == o["n_accepted"][ok]).all()
     assert (a["tokens"][ok] == o["tokens"][ok]).all()
     np.testing.assert_allclose(a["logprobs"][ok], o["logprobs"][ok], rtol=1e-6, atol=1e-6,
