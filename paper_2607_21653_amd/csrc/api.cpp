@@ -77,7 +77,7 @@ extern "C" {
 
 const char* molt_last_error(void) { return g_err.c_str(); }
 
-int molt_version(void) { return 101; }
+int molt_version(void) { return 102; }
 
 // ------------------------------------------------------------------ profiling
 

@@ -35,7 +35,7 @@ def test_exports_every_declared_symbol(L):
 
 
 def test_version_and_error_string(L):
-    assert L.molt_version() == 101
+    assert L.molt_version() == 102
     assert isinstance(L.molt_last_error(), bytes)
 
 
