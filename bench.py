@@ -62,6 +62,24 @@ def attention_bytes(w, ctx):
     return kv + qo
 
 
+def layer_weight_bytes(w):
+    """Weights one layer reads at this batch: every expert (T*K = 5120 pairs over 128
+    experts leave none untouched), the attention projections and the router."""
+    eb = 1 if w.expert_dtype == "fp8" else 2
+    d, D = w.d_model, w.head_dim
+    experts = w.n_experts * 3 * w.d_ff * d * eb
+    dense = ((w.n_q_heads + 2 * w.n_kv_heads) * D * d + d * w.n_q_heads * D + w.n_experts * d) * 2
+    return experts + dense
+
+
+def step_bytes(w, ctx, samp_bytes):
+    """Algorithmic HBM bytes of one whole verify step: every layer's attention (K/V, q, out)
+    and weights, the LM head's weights and logits, the sampler's reads."""
+    T = w.batch * (w.k + 1)
+    return (w.n_layers * (attention_bytes(w, ctx) + layer_weight_bytes(w))
+            + w.vocab * w.d_model * 2 + T * w.vocab * 4 + samp_bytes)
+
+
 def sampler_roofline(w, molt, out, tokens, q, u, reps=20):
     """The standalone sampler (molt_spec_accept) on the step's own logits, drafts, q and
     uniforms, timed with HIP events on the library's stream after the timed region.
@@ -236,8 +254,14 @@ def reprefill_measure(w, seed, molt, model, layout, kv, reps=3):
     e1.record()
     torch.cuda.synchronize()
     assert torch.isfinite(out["logits"]).all()
-    return {"avg_ms": round(e0.elapsed_time(e1) / reps, 3), "cached_tokens": ctx,
-            "new_tokens": REPREFILL_TOKENS,
+    ms = e0.elapsed_time(e1) / reps
+    kvrow = w.n_kv_heads * w.head_dim * 2 * 2
+    nbytes = (w.n_layers * (layer_weight_bytes(w) + (ctx + REPREFILL_TOKENS) * kvrow)
+              + w.vocab * w.d_model * 2)
+    gbs = nbytes / (ms / 1e3) / 1e9
+    return {"avg_ms": round(ms, 3), "cached_tokens": ctx, "new_tokens": REPREFILL_TOKENS,
+            "bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": round(gbs / HBM_PEAK_GBS, 4), "algorithmic_bytes": int(nbytes),
             "note": "molt_prefill of one session's new turn at context 8192 (its cached prefix read "
                     "from the paged cache, not recomputed): the cache-hit re-prefill latency"}
 
@@ -478,6 +502,13 @@ def main():
         "kernel_groups_note": f"HIP-event times of each group over {n_break} untimed steps after the timed region",
         "lm_head_tflops": round(lm_flops / (lm_ms / max(lm_n, 1) / 1e3) / 1e12, 1) if lm_n else None,
         "other_rooflines": other_rooflines(w, groups, samp),
+        "step_roofline": (lambda nb: {"bound": "hbm", "achieved": round(nb / (ms / 1e3) / 1e9, 1),
+                                      "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                                      "frac": round(nb / (ms / 1e3) / 1e9 / HBM_PEAK_GBS, 4),
+                                      "algorithmic_bytes": int(nb),
+                                      "note": "the whole step: every layer's attention K/V + q + out "
+                                              "and weights, LM head weights + logits, sampler reads"})(
+            step_bytes(w, layout.context_lens, samp["bytes"])),
         "mtp_draft": mtp,
         "replay_recompute": rep,
         "reprefill": rpf,
