@@ -62,88 +62,142 @@ MOLT_DEV floatx16_t mfma(const int32x8_t& a, const int32x8_t& b, const floatx16_
 // translation requests, not HBM, set the pace) and every LDS fragment read is a
 // contiguous 1 KB. Tiles start at multiples of 32 rows (padded expert order), so each
 // 32-row block of A is one tile column of the tiled activation buffer.
+// The grid is persistent (see stream_gemm_kernel) and, for the bf16 down GEMM when the K
+// slices come in multiples of 4, chained: the last steps of a tile issue the first weight and activation
+// loads of the workgroup's next tile into the slots where its prologue would put them, so
+// a tile starts with its first 4 slices in flight or landed instead of waiting out a fresh
+// HBM latency (an unchained tile carried a fixed cost of about a fifth of its time).
+// Nothing after those loads waits for them before the next tile's first step: the
+// epilogues use LDS-only barriers, and down reads its output rows' pair indices from LDS,
+// copied there early in the tile.
 struct Slice16 { int32x4_t c[4]; };   // one lane's 64 bytes of a 32-row x 128-byte tile
 
-// One (m-tile, n-tile) pair of a grouped launch.
-template <int BM, bool FP8, int MODE>
-MOLT_DEV void stream_tile(const GemmParams& p, int id) {
-  static_assert(MODE == kGateUp || MODE == kDown, "grouped modes");
-  constexpr int MS = BM / 32;                        // 32-row MFMA tiles per wavefront
-  constexpr int kElem = FP8 ? 1 : 2;
-  __shared__ __attribute__((aligned(16))) float upbuf[MODE == kGateUp ? BM * 64 : 1];
-  const int mt = id / p.n_ntiles;
-  const int nt = id % p.n_ntiles;
+// Where one (m-tile, n-tile) pair of a grouped launch reads (all wavefront-uniform).
+struct StreamTile {
+  const uint8_t* b;     // the wavefront's 32 weight rows (gate_up: waves 0-1 gate, 2-3 up)
+  const uint8_t* a;     // the tile's first 32-row activation block
+  int a_last;           // its last 32-row block that holds rows (0 .. BM / 32 - 1)
+  int rot;              // first K slice visited
+  int expert, row0, row1, n0;
+};
+
+template <int MODE>
+MOLT_DEV StreamTile stream_geometry(const GemmParams& p, int id, int nk, int wave) {
+  StreamTile g;
+  const int mt = id / p.n_ntiles, nt = id % p.n_ntiles;
   const int4 t = p.tiles[mt];
-  const int expert = t.x, row0 = t.y, row1 = t.z;     // row0 % 32 == 0
-  const long RB = long(p.K) * kElem;                  // bytes per operand row
-  const int nk = int(RB / kRowBytes);                 // 128-byte K slices
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
-  const int lane = threadIdx.x % kWave;
-  // first of the wavefront's 32 weight rows (gate_up: waves 0-1 gate, 2-3 up)
+  g.expert = t.x;
+  g.row0 = t.y;                                       // a multiple of 32
+  g.row1 = t.z;
+  const long RB = long(nk) * kRowBytes;               // bytes per operand row
   long wrow;
-  int n0;
   if (MODE == kGateUp) {
-    n0 = nt * (kBN / 2);
-    wrow = long(expert) * 2 * p.N + (wave < 2 ? n0 + 32 * wave : p.N + n0 + 32 * (wave - 2));
+    g.n0 = nt * (kBN / 2);
+    wrow = long(g.expert) * 2 * p.N + (wave < 2 ? g.n0 + 32 * wave : p.N + g.n0 + 32 * (wave - 2));
   } else {
-    n0 = nt * kBN;
-    wrow = long(expert) * p.N + n0 + 32 * wave;
+    g.n0 = nt * kBN;
+    wrow = long(g.expert) * p.N + g.n0 + 32 * wave;
   }
-  const uint8_t* bsrc = static_cast<const uint8_t*>(p.B) + wrow * RB + lane * 16;
-  const int last_block = (row1 - 1) & ~31;
-  const uint8_t* asrc[MS];
-#pragma unroll
-  for (int i = 0; i < MS; ++i)
-    asrc[i] = static_cast<const uint8_t*>(p.A) + long(min(row0 + 32 * i, last_block)) * RB + threadIdx.x * 16;
-  __shared__ __attribute__((aligned(16))) uint8_t alds[2][MS * 4096];
-  int32x4_t st0[MS], st1[MS];
-  // weight slices in flight per wavefront (each 4 KB slice of a wavefront's 32 weight rows
-  // is 16 registers; 8 in flight measured slower than 4)
-  constexpr int WD = 4;
-  Slice16 wb[WD];
-  // weights are read once per step: nontemporal loads
+  g.b = static_cast<const uint8_t*>(p.B) + wrow * RB;
+  g.a = static_cast<const uint8_t*>(p.A) + long(g.row0) * RB;
+  g.a_last = (((g.row1 - 1) & ~31) - g.row0) / 32;
   // K slices are visited in an order rotated by the column tile, so the workgroups of one
   // row tile (running side by side on one XCD) read different activation blocks at any
   // moment instead of all hitting the same L2 lines
-  const int rot = int((long(nt) * nk) / p.n_ntiles);
-  auto rs = [&](int kb) __attribute__((always_inline)) {
-    const int k = min(kb, nk - 1) + rot;
+  g.rot = int((long(nt) * nk) / p.n_ntiles);
+  return g;
+}
+
+// Persistent grouped GEMM: the grid is what the chip holds at once (a multiple of 8, see
+// run_stream). Workgroup b runs on XCD b % 8 and walks that XCD's contiguous eighth of the
+// live (m-tile, n-tile) pairs, m-tile major, with the XCD's workgroup count as stride: the
+// n-tiles of one row tile run side by side on one XCD, so its activation tile is read from
+// HBM once and then hits that XCD's L2. Launching one workgroup per pair left the chip
+// at 50-80% of its resident workgroups on average (dispatch gaps between short tiles).
+// CHAIN requires K slices in multiples of 4 (the slot pattern then lines up across tiles).
+template <int BM, bool FP8, int MODE, bool CHAIN>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(BM <= 64 ? 3 : 2)))
+void stream_gemm_kernel(GemmParams p) {
+  static_assert(MODE == kGateUp || MODE == kDown, "grouped modes");
+  constexpr int MS = BM / 32;                        // 32-row MFMA tiles per wavefront
+  constexpr int kElem = FP8 ? 1 : 2;
+  // weight slices in flight per wavefront (each 4 KB slice of a wavefront's 32 weight rows
+  // is 16 registers; 8 in flight measured slower than 4)
+  constexpr int WD = 4;
+  __shared__ __attribute__((aligned(16))) float upbuf[MODE == kGateUp ? BM * 64 : 1];
+  __shared__ __attribute__((aligned(16))) uint8_t alds[2][MS * 4096];
+  __shared__ int prow[MODE == kDown ? BM : 1];       // down: pair index of each tile row
+  const int total = *p.n_tiles_live * p.n_ntiles;
+  const int chunk = (total + 7) / 8;
+  const int stride = gridDim.x / 8;
+  const int first = (blockIdx.x % 8) * chunk;
+  int k8 = blockIdx.x / 8;
+  if (k8 >= chunk || first + k8 >= total) return;
+  const int nk = int(long(p.K) * kElem / kRowBytes);  // 128-byte K slices
+  const long RB = long(nk) * kRowBytes;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+  const int lane = threadIdx.x % kWave;
+  const unsigned boff = lane * 16u, aoff = threadIdx.x * 16u;
+  auto slice = [&](const StreamTile& t, int kb) __attribute__((always_inline)) {
+    const int k = min(kb, nk - 1) + t.rot;
     return long(k >= nk ? k - nk : k) * 4096;
   };
-  auto wld = [&](Slice16& f, int kb) __attribute__((always_inline)) {
-    const uint8_t* src = bsrc + rs(kb);
+  // weights are read once per step: nontemporal loads
+  auto wld = [&](Slice16& f, const StreamTile& t, int kb) __attribute__((always_inline)) {
+    const uint8_t* src = t.b + slice(t, kb) + boff;
 #pragma unroll
     for (int c = 0; c < 4; ++c) f.c[c] = __builtin_nontemporal_load(reinterpret_cast<const int32x4_t*>(src + 1024 * c));
   };
-#define MOLT_GLOAD(ST, KB)                                                            \
+#define MOLT_GLOAD(ST, T, KB)                                                         \
   {                                                                                   \
-    const long off_ = rs(KB);                                                         \
+    const long off_ = slice(T, KB);                                                   \
     _Pragma("unroll") for (int b_ = 0; b_ < MS; ++b_)                                 \
-        ST[b_] = *reinterpret_cast<const int32x4_t*>(asrc[b_] + off_);                \
+        ST[b_] = *reinterpret_cast<const int32x4_t*>((T).a + long(min(b_, (T).a_last)) * 32 * RB + off_ + aoff); \
   }
 #define MOLT_SSTORE(ST, BUF)                                                          \
   {                                                                                   \
     _Pragma("unroll") for (int b_ = 0; b_ < MS; ++b_)                                 \
         *reinterpret_cast<int32x4_t*>(&alds[BUF][b_ * 4096 + threadIdx.x * 16]) = ST[b_]; \
   }
+  int32x4_t st0[MS], st1[MS];
+  Slice16 wb[WD];
   floatx16_t acc[MS];
+  StreamTile g = stream_geometry<MODE>(p, first + k8, nk, wave);
+  StreamTile gn = g;
+  bool more = false;
+  bool primed = false;                               // g's first slices already loaded
+  for (;;) {
+    // down: the pair index of each of the tile's rows, loaded before the tile's own loads
+    int pv = -1;
+    if (MODE == kDown && threadIdx.x < BM && g.row0 + int(threadIdx.x) < g.row1)
+      pv = p.perm[g.row0 + threadIdx.x];
+    auto put_prow = [&]() __attribute__((always_inline)) {
+      if (MODE == kDown && threadIdx.x < BM) prow[threadIdx.x] = pv;
+    };
+    {
+      const int kn = k8 + stride;
+      more = kn < chunk && first + kn < total;
+      if (CHAIN && more) gn = stream_geometry<MODE>(p, first + kn, nk, wave);
+    }
+    if (!primed) {
+      MOLT_GLOAD(st0, g, 0);
+      MOLT_GLOAD(st1, g, 1);
 #pragma unroll
-  for (int i = 0; i < MS; ++i)
+      for (int s = 0; s < WD; ++s) wld(wb[s], g, s);
+      MOLT_SSTORE(st0, 0);
+      MOLT_GLOAD(st0, g, 2);
+      lds_barrier();
+    }
 #pragma unroll
-    for (int e = 0; e < 16; ++e) acc[i][e] = 0.f;
-  MOLT_GLOAD(st0, 0);
-  MOLT_GLOAD(st1, 1);
+    for (int i = 0; i < MS; ++i)
 #pragma unroll
-  for (int s = 0; s < WD; ++s) wld(wb[s], s);
-  MOLT_SSTORE(st0, 0);
-  MOLT_GLOAD(st0, 2);
-  lds_barrier();
-  // Step over slice k: LDS buffer U holds its activations, weight slot W its weights,
-  // register slot ST_NEXT slice k + 1 (the other slot k + 2). It computes, refills W with
-  // slice k + WD, stores slice k + 1 into buffer 1 - U (last read before the previous
-  // barrier) and refills ST_NEXT with slice k + 3. In the last WD + 3 steps (TAIL = 1) the
-  // refills past the end are skipped: re-reading the last slice instead cost the short down
-  // GEMM (12 slices) a third more weight loads, part of them missing L2.
+      for (int e = 0; e < 16; ++e) acc[i][e] = 0.f;
+    // Step over slice k: LDS buffer U holds its activations, weight slot W its weights,
+    // register slot ST_NEXT slice k + 1 (the other slot k + 2). It computes, refills W with
+    // slice k + WD, stores slice k + 1 into buffer 1 - U (last read before the previous
+    // barrier) and refills ST_NEXT with slice k + 3. In the last WD + 3 steps (TAIL = 1) a
+    // refill past the end loads the next tile's slice (chained) or nothing: re-reading the
+    // last slice instead cost the 12-slice down GEMM a third more weight loads.
 #define MOLT_STEP(U, ST_NEXT, W, K, TAIL)                                                           \
   {                                                                                                  \
     const uint8_t* base_ = alds[U] + lane * 16;                                                      \
@@ -164,99 +218,95 @@ MOLT_DEV void stream_tile(const GemmParams& p, int id) {
         }                                                                                            \
       }                                                                                              \
     }                                                                                                \
-    if (!(TAIL) || (K) + WD < nk) wld(wb[W], (K) + WD);                                              \
+    if (!(TAIL) || (K) + WD < nk) wld(wb[W], g, (K) + WD);                                           \
+    else if (CHAIN && more) wld(wb[W], gn, (K) + WD - nk);                                           \
     MOLT_SSTORE(ST_NEXT, 1 - (U));                                                                   \
-    if (!(TAIL) || (K) + 3 < nk) MOLT_GLOAD(ST_NEXT, (K) + 3);                                       \
+    if (!(TAIL) || (K) + 3 < nk) MOLT_GLOAD(ST_NEXT, g, (K) + 3)                                     \
+    else if (CHAIN && more) MOLT_GLOAD(ST_NEXT, gn, (K) + 3 - nk)                                    \
     lds_barrier();                                                                                   \
   }
-  static_assert(WD == 4, "the step sequence cycles through 4 weight slots");
-  int kb = 0;
-  for (; kb + WD + 3 < nk; kb += 4) {      // every refill of these 4 steps is in range
-    MOLT_STEP(0, st1, 0, kb, 0);
-    MOLT_STEP(1, st0, 1, kb + 1, 0);
-    MOLT_STEP(0, st1, 2, kb + 2, 0);
-    MOLT_STEP(1, st0, 3, kb + 3, 0);
-  }
-  // the last 1..7 slices (kb % 4 == 0, so the slot pattern continues)
-  if (kb < nk) MOLT_STEP(0, st1, 0, kb, 1);
-  if (kb + 1 < nk) MOLT_STEP(1, st0, 1, kb + 1, 1);
-  if (kb + 2 < nk) MOLT_STEP(0, st1, 2, kb + 2, 1);
-  if (kb + 3 < nk) MOLT_STEP(1, st0, 3, kb + 3, 1);
-  if (kb + 4 < nk) MOLT_STEP(0, st1, 0, kb + 4, 1);
-  if (kb + 5 < nk) MOLT_STEP(1, st0, 1, kb + 5, 1);
-  if (kb + 6 < nk) MOLT_STEP(0, st1, 2, kb + 6, 1);
+    static_assert(WD == 4, "the step sequence cycles through 4 weight slots");
+    int kb = 0;
+    for (; kb + WD + 3 < nk; kb += 4) {    // every refill of these 4 steps is in this tile
+      MOLT_STEP(0, st1, 0, kb, 0);
+      if (kb == 0) put_prow();             // waits for the row load, not for the step's own
+      MOLT_STEP(1, st0, 1, kb + 1, 0);
+      MOLT_STEP(0, st1, 2, kb + 2, 0);
+      MOLT_STEP(1, st0, 3, kb + 3, 0);
+    }
+    if (kb == 0) {                         // no full 4 steps: a chained tile has had no
+      if (primed) lds_barrier();           // barrier since the last tile's epilogue read prow
+      put_prow();
+    }
+    // the last 1..7 slices (kb % 4 == 0, so the slot pattern continues)
+    if (kb < nk) MOLT_STEP(0, st1, 0, kb, 1);
+    if (kb + 1 < nk) MOLT_STEP(1, st0, 1, kb + 1, 1);
+    if (kb + 2 < nk) MOLT_STEP(0, st1, 2, kb + 2, 1);
+    if (kb + 3 < nk) MOLT_STEP(1, st0, 3, kb + 3, 1);
+    if (kb + 4 < nk) MOLT_STEP(0, st1, 0, kb + 4, 1);
+    if (kb + 5 < nk) MOLT_STEP(1, st0, 1, kb + 5, 1);
+    if (kb + 6 < nk) MOLT_STEP(0, st1, 2, kb + 6, 1);
 #undef MOLT_STEP
+    // accumulator element e of lane (lcol, lgrp) in tile i: row 32 i + 8 (e / 4) + 4 lgrp + e % 4
+    int lcol = lane % 32, lgrp = lane / 32;
+    // opaque per tile: the epilogue's address arithmetic stays here instead of being hoisted
+    // out of the tile loop into registers held across the K steps (gate_up spilled them)
+    asm volatile("" : "+v"(lcol), "+v"(lgrp));
+    if (MODE == kGateUp) {
+      // h = silu(gate) * up, bf16, tiled layout over padded rows; up columns go through LDS
+      if (wave >= 2) {
+#pragma unroll
+        for (int i = 0; i < MS; ++i)
+#pragma unroll
+          for (int e = 0; e < 16; ++e) {
+            const int r = 32 * i + 8 * (e / 4) + 4 * lgrp + (e % 4);
+            upbuf[r * 64 + 32 * (wave - 2) + lcol] = acc[i][e];
+          }
+      }
+      lds_barrier();
+      if (wave < 2) {
+        const int c = 32 * wave + lcol;
+        const long hrb = 2L * p.N;
+#pragma unroll
+        for (int i = 0; i < MS; ++i)
+#pragma unroll
+          for (int e = 0; e < 16; ++e) {
+            const int r = 32 * i + 8 * (e / 4) + 4 * lgrp + (e % 4);
+            const int grow = g.row0 + r;
+            if (grow >= g.row1) continue;
+            float gt = acc[i][e], u = upbuf[r * 64 + c];
+            if (FP8) {
+              const float sx = p.a_scale[p.perm[grow] / p.ktop];
+              const float* sw = p.b_scale + long(g.expert) * p.b_scale_ld;
+              gt = gt * sx * sw[g.n0 + c];
+              u = u * sx * sw[p.N + g.n0 + c];
+            }
+            *reinterpret_cast<uint16_t*>(static_cast<uint8_t*>(p.C) +
+                                         tiled_offset(grow, 2L * (g.n0 + c), hrb)) = f32_to_bf16(silu(gt) * u);
+          }
+      }
+    } else {
+      // per-pair expert output, f32, row = pair index (token * K + slot)
+      const int c = g.n0 + 32 * wave + lcol;
+#pragma unroll
+      for (int i = 0; i < MS; ++i)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int r = 32 * i + 8 * (e / 4) + 4 * lgrp + (e % 4);
+          const int grow = g.row0 + r;
+          if (grow >= g.row1) continue;
+          float v = acc[i][e];
+          if (FP8) v = v * p.a_scale[grow] * p.b_scale[long(g.expert) * p.b_scale_ld + c];
+          static_cast<float*>(p.C)[long(prow[r]) * p.ldc + c] = v;
+        }
+    }
+    if (!more) break;
+    k8 += stride;
+    g = CHAIN ? gn : stream_geometry<MODE>(p, first + k8, nk, wave);
+    primed = CHAIN;
+  }
 #undef MOLT_SSTORE
 #undef MOLT_GLOAD
-  // accumulator element e of lane (lcol, lgrp) in tile i: row 32 i + 8 (e / 4) + 4 lgrp + e % 4
-  const int lcol = lane % 32, lgrp = lane / 32;
-  if (MODE == kGateUp) {
-    // h = silu(gate) * up, bf16, tiled layout over padded rows; up columns go through LDS
-    if (wave >= 2) {
-#pragma unroll
-      for (int i = 0; i < MS; ++i)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const int r = 32 * i + 8 * (e / 4) + 4 * lgrp + (e % 4);
-          upbuf[r * 64 + 32 * (wave - 2) + lcol] = acc[i][e];
-        }
-    }
-    __syncthreads();
-    if (wave < 2) {
-      const int c = 32 * wave + lcol;
-      const long hrb = 2L * p.N;
-#pragma unroll
-      for (int i = 0; i < MS; ++i)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const int r = 32 * i + 8 * (e / 4) + 4 * lgrp + (e % 4);
-          const int grow = row0 + r;
-          if (grow >= row1) continue;
-          float g = acc[i][e], u = upbuf[r * 64 + c];
-          if (FP8) {
-            const float sx = p.a_scale[p.perm[grow] / p.ktop];
-            const float* sw = p.b_scale + long(expert) * p.b_scale_ld;
-            g = g * sx * sw[n0 + c];
-            u = u * sx * sw[p.N + n0 + c];
-          }
-          *reinterpret_cast<uint16_t*>(static_cast<uint8_t*>(p.C) +
-                                       tiled_offset(grow, 2L * (n0 + c), hrb)) = f32_to_bf16(silu(g) * u);
-        }
-    }
-  } else {
-    // per-pair expert output, f32, row = pair index (token * K + slot)
-    const int c = n0 + 32 * wave + lcol;
-#pragma unroll
-    for (int i = 0; i < MS; ++i)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const int r = 32 * i + 8 * (e / 4) + 4 * lgrp + (e % 4);
-        const int grow = row0 + r;
-        if (grow >= row1) continue;
-        float v = acc[i][e];
-        if (FP8) v = v * p.a_scale[grow] * p.b_scale[long(expert) * p.b_scale_ld + c];
-        static_cast<float*>(p.C)[long(p.perm[grow]) * p.ldc + c] = v;
-      }
-  }
-}
-
-// Persistent grouped GEMM: the grid is what the chip holds at once (a multiple of 8, see
-// run_stream). Workgroup b runs on XCD b % 8 and walks that XCD's contiguous eighth of the
-// live (m-tile, n-tile) pairs, m-tile major, with the XCD's workgroup count as stride: the
-// n-tiles of one row tile run side by side on one XCD, so its activation tile is read from
-// HBM once and then hits that XCD's L2. Launching one workgroup per pair left the chip
-// at 50-80% of its resident workgroups on average (dispatch gaps between short tiles).
-template <int BM, bool FP8, int MODE>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(BM <= 64 ? 3 : 2)))
-void stream_gemm_kernel(GemmParams p) {
-  const int total = *p.n_tiles_live * p.n_ntiles;
-  const int chunk = (total + 7) / 8;
-  const int stride = gridDim.x / 8;
-  for (int k8 = blockIdx.x / 8; k8 < chunk; k8 += stride) {
-    const int id = (blockIdx.x % 8) * chunk + k8;
-    if (id >= total) break;
-    stream_tile<BM, FP8, MODE>(p, id);
-  }
 }
 
 // Workgroups of `kernel` (kThreads each) resident on the whole device at once, rounded
@@ -271,19 +321,28 @@ int resident_grid(K kernel) {
   return (cus * per_cu) / 8 * 8 > 8 ? (cus * per_cu) / 8 * 8 : 8;
 }
 
-template <bool FP8, int MODE>
-hipError_t run_stream(GemmParams p, int tile_m, hipStream_t s) {
+template <bool FP8, int MODE, bool CHAIN>
+hipError_t run_stream_k(GemmParams p, int tile_m, hipStream_t s) {
   // resident workgroups per kernel, queried once per process (one device model)
-  static const int r32 = resident_grid(stream_gemm_kernel<32, FP8, MODE>);
-  static const int r64 = resident_grid(stream_gemm_kernel<64, FP8, MODE>);
-  static const int r128 = resident_grid(stream_gemm_kernel<128, FP8, MODE>);
+  static const int r32 = resident_grid(stream_gemm_kernel<32, FP8, MODE, CHAIN>);
+  static const int r64 = resident_grid(stream_gemm_kernel<64, FP8, MODE, CHAIN>);
+  static const int r128 = resident_grid(stream_gemm_kernel<128, FP8, MODE, CHAIN>);
   const int pairs = (p.n_mtiles * p.n_ntiles + 7) / 8 * 8;   // upper bound of the live pairs
   const int cap = tile_m == 32 ? r32 : tile_m == 64 ? r64 : r128;
   const int grid = pairs < cap ? pairs : cap;
-  if (tile_m == 32) stream_gemm_kernel<32, FP8, MODE><<<grid, kThreads, 0, s>>>(p);
-  else if (tile_m == 64) stream_gemm_kernel<64, FP8, MODE><<<grid, kThreads, 0, s>>>(p);
-  else stream_gemm_kernel<128, FP8, MODE><<<grid, kThreads, 0, s>>>(p);
+  if (tile_m == 32) stream_gemm_kernel<32, FP8, MODE, CHAIN><<<grid, kThreads, 0, s>>>(p);
+  else if (tile_m == 64) stream_gemm_kernel<64, FP8, MODE, CHAIN><<<grid, kThreads, 0, s>>>(p);
+  else stream_gemm_kernel<128, FP8, MODE, CHAIN><<<grid, kThreads, 0, s>>>(p);
   return hipGetLastError();
+}
+
+template <bool FP8, int MODE>
+hipError_t run_stream(GemmParams p, int tile_m, hipStream_t s) {
+  const long nk = long(p.K) * (FP8 ? 1 : 2) / kRowBytes;
+  // chained in bf16 for down only: its 12-slice tiles gained (85 -> 82 us per launch at
+  // T*K = 5120), gate_up's 32-slice tiles did not (159 -> 161 us)
+  if (!FP8 && MODE == kDown && nk % 4 == 0) return run_stream_k<false, MODE, true>(p, tile_m, s);
+  return run_stream_k<FP8, MODE, false>(p, tile_m, s);
 }
 
 // ---------------------------------------------------------------- LDS-tiled dense GEMM
