@@ -3,7 +3,8 @@ GEMMs on MFMA, combine) against the oracle, at the 35B-A3B-like layer shape with
 tokens (several 32-row tiles and ragged expert segments): routes bit-exact except where
 the oracle's K-th/(K+1)-th router-logit gap is below 1e-4 (fp32 summation order), outputs
 within 2e-2 max-abs (bf16/fp8) or 1e-4 (f32); routing on exactly representable inputs is
-bit-exact with ties; replay ids; fp8 experts with Zipf-skewed routing."""
+bit-exact with ties; replay ids; fp8 experts with Zipf-skewed routing; bf16 at 1024 tokens (several tiles per
+persistent workgroup), uniform and Zipf-skewed."""
 import numpy as np
 import pytest
 import torch
@@ -71,6 +72,25 @@ def test_fp8_zipf(molt_lib):
     counts = g[3].cpu().numpy()
     print("max/mean expert load", counts.max() / counts.mean(), flush=True)
     assert counts.max() > 4 * counts.mean()          # skewed
+
+
+@pytest.mark.parametrize("zipf", [None, 1.2])
+def test_bf16_many_tiles_per_workgroup(molt_lib, zipf):
+    """T = 1024 (8192 pairs): every persistent workgroup of the expert GEMMs runs several tiles,
+    so the down GEMM's loads of the next tile's first slices (into another expert, another row
+    tile of the same expert) are exercised; with Zipf-skewed routing popular experts span many
+    row tiles and about 50 experts get no rows."""
+    w = workloads.LAYER_BF16.scaled(name="bf16_chained" if zipf is None else "bf16_zipf_chained", zipf=zipf)
+    T = 1024
+    lw, x = _layer(w, 4, T)
+    print(f"case bf16 T={T} zipf={zipf}", flush=True)
+    g = _gpu(molt_lib, lw, x, w.top_k)
+    o = _oracle(w, lw, x, T)
+    _check(w, o, g, 2e-2)
+    counts = g[3].cpu().numpy()
+    print("max/mean expert load", counts.max() / counts.mean(), "empty experts", (counts == 0).sum(), flush=True)
+    if zipf is not None:
+        assert counts.max() > 4 * counts.mean() and (counts == 0).any()
 
 
 def test_f32_tiny(molt_lib):
