@@ -107,7 +107,7 @@ def sampler_roofline(w, molt, out, tokens, q, u, reps=20):
 
 
 def other_rooflines(w, groups, samp):
-    """Fractions of roofline of the other spec kernels: the sampler (HBM), the expert
+    """Fractions of roofline of the other headline kernels: the sampler (HBM), the expert
     GEMMs (HBM: every expert's weights read once per layer; also their raw MFMA rate) and the
     LM head (MFMA, bf16 dense peak)."""
     B, k, V, d = w.batch, w.k, w.vocab, w.d_model

@@ -55,7 +55,7 @@ typedef struct ihipStream_t* molt_stream_t; /* the same type as hipStream_t */
 typedef enum {
   MOLT_OK = 0,
   MOLT_ERR_INVALID_ARG = -1, /* NULL required pointer, bad size, bad combination  */
-  MOLT_ERR_UNSUPPORTED = -2, /* valid request this build does not implement       */
+  MOLT_ERR_UNSUPPORTED = -2, /* valid request this library does not implement     */
   MOLT_ERR_WORKSPACE = -3,   /* workspace missing or smaller than *_workspace_size */
   MOLT_ERR_HIP = -4,         /* a HIP runtime call or kernel launch failed         */
   MOLT_ERR_CAPACITY = -5     /* the block pool has no free or evictable block left  */
