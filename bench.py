@@ -255,6 +255,12 @@ def reprefill_measure(w, seed, molt, model, layout, kv, reps=3):
     torch.cuda.synchronize()
     assert torch.isfinite(out["logits"]).all()
     ms = e0.elapsed_time(e1) / reps
+    # per-group breakdown from one more call with every group bracketed (untimed above)
+    molt.profile_enable(True)
+    molt.prefill(model, kv1, toks, lens, workspace=ws)
+    torch.cuda.synchronize()
+    molt.profile_enable(False)
+    groups = {gr: molt.profile_read(gr) for gr in molt._lib.PROF_GROUPS}
     kvrow = w.n_kv_heads * w.head_dim * 2 * 2
     nbytes = (w.n_layers * (layer_weight_bytes(w) + (ctx + REPREFILL_TOKENS) * kvrow)
               + w.vocab * w.d_model * 2)
@@ -262,6 +268,7 @@ def reprefill_measure(w, seed, molt, model, layout, kv, reps=3):
     return {"avg_ms": round(ms, 3), "cached_tokens": ctx, "new_tokens": REPREFILL_TOKENS,
             "bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
             "frac": round(gbs / HBM_PEAK_GBS, 4), "algorithmic_bytes": int(nbytes),
+            "groups_ms": {gr: round(t, 3) for gr, (t, _) in groups.items()},
             "note": "molt_prefill of one session's new turn at context 8192 (its cached prefix read "
                     "from the paged cache, not recomputed): the cache-hit re-prefill latency"}
 

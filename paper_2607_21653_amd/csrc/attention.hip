@@ -5,7 +5,7 @@
 //
 // Work split: workgroup = (b, h, query tile, split of the key range), 4 wavefronts. A query
 // tile holds all R rows when R <= 128 (the verify step); longer windows (prefill) are cut
-// into tiles of floor(128 / G) positions, each reading the keys its last position sees.
+// into tiles of floor(64 / G) positions, each reading the keys its last position sees.
 // The number of splits is chosen so the grid holds ~512 workgroups (at B*Hkv*tiles >= 512
 // there is no split and no merge pass) and no split exceeds 2048 blocks. The wavefronts split the R query rows and
 // share every 32-key block pair through a double-buffered LDS ring (details at the kernel).
@@ -449,10 +449,13 @@ hipError_t launch_d(const AttnParams& p, int B, int R, hipStream_t s) {
 
 }  // namespace
 
-// Query tiles of (b, h): all G(1+k) rows in one tile when they fit in 128, else tiles of
-// floor(128 / G) positions (prefill windows).
+// Query tiles of (b, h): all G(1+k) rows in one tile when they fit in 128 (every key and
+// value read once), else tiles of floor(64 / G) positions (at least one): a 128-row tile
+// takes 334 registers per lane, one workgroup per CU; a 256-position window at context
+// 8192 (G = 8) took 135 us in such tiles and 112 us in 64-row ones, which read the keys
+// twice as often (mostly from L2/MALL).
 static void qtile_plan(int G, int kp1, int& qtiles, int& tq) {
-  tq = G * kp1 <= 128 ? kp1 : 128 / G;
+  tq = G * kp1 <= 128 ? kp1 : (G <= 64 ? 64 / G : 1);
   qtiles = (kp1 + tq - 1) / tq;
 }
 
