@@ -47,10 +47,12 @@ def _gpu(molt, w, layout, kc, vc, q, bt=None):
     (4, 0, 32, 4, 128, 0, 40),          # plain decode, empty context allowed
     (2, 3, 8, 2, 64, 200, 1500),        # head dim 64
     (1, 4, 32, 4, 128, 9000, 9000),     # 9 splits
-    (2, 63, 32, 4, 128, 0, 300),        # prefill window: 4 query tiles, empty context allowed
-    (3, 40, 16, 4, 128, 10, 700),       # G = 4: tiles of 32 positions, partial last tile
-    (1, 255, 32, 4, 128, 2000, 2000),   # 16 query tiles x 5 splits
-    (2, 100, 8, 2, 64, 50, 400),        # head dim 64, 4 tiles
+    (2, 63, 32, 4, 128, 0, 300),        # prefill window: 8 query tiles of 64 rows, empty context allowed
+    (3, 40, 16, 4, 128, 10, 700),       # G = 4: tiles of 16 positions, partial last tile
+    (1, 255, 32, 4, 128, 2000, 2000),   # 32 query tiles x 4 splits
+    (2, 100, 8, 2, 64, 50, 400),        # head dim 64, 7 tiles of 16 positions
+    (2, 5, 64, 1, 128, 30, 500),        # G = 64: one position per 64-row tile
+    (1, 3, 128, 1, 128, 100, 100),      # G = 128: one position per 128-row tile
 ])
 def test_bf16_parity(molt_lib, B, k, Hq, Hkv, D, lo, hi):
     print(f"case B={B} k={k} Hq={Hq} Hkv={Hkv} D={D} ctx=[{lo},{hi}]", flush=True)
