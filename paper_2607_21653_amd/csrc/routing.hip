@@ -137,6 +137,12 @@ __global__ __launch_bounds__(kPermThreads) void permute_kernel(
   // same expert, found with 8 ballots over the id bits). The rank is parked in inv[p] (each
   // thread reads back only what it wrote).
   constexpr int kBatch = 8;                // loads of a batch issue together
+  // with one batch (P <= 8 * kPermThreads) pass 2 reuses the ids and ranks held here
+  // instead of reading them back from global memory
+  const bool one_batch = steps <= kBatch;
+  int ev1[kBatch], rk1[kBatch];
+#pragma unroll
+  for (int u = 0; u < kBatch; ++u) { ev1[u] = -1; rk1[u] = 0; }
   for (int s0 = 0; s0 < steps; s0 += kBatch) {
     int ev[kBatch];
 #pragma unroll
@@ -160,7 +166,11 @@ __global__ __launch_bounds__(kPermThreads) void permute_kernel(
       int before = 0;
       if (valid) before = wc[wave][e];
       if (valid && below == 0) wc[wave][e] = before + __popcll(mask);
-      if (valid) inv[p0 + (s0 + u) * kWave + lane] = before + below;
+      if (s0 == 0) {
+        ev1[u] = e;
+        rk1[u] = before + below;
+      }
+      if (valid && !one_batch) inv[p0 + (s0 + u) * kWave + lane] = before + below;
     }
   }
   __syncthreads();
@@ -229,6 +239,19 @@ __global__ __launch_bounds__(kPermThreads) void permute_kernel(
   }
   if (tid == 0) offsets_out[E] = off[E];
   // pass 2: position = offset of the expert + earlier wavefronts' pairs of it + rank
+  if (one_batch) {
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) {
+      const int e = ev1[u];
+      if (e < 0) continue;
+      const int p = p0 + u * kWave + lane;
+      const int pos = off[e] + wc[wave][e] + rk1[u];
+      perm[pos] = p;
+      inv[p] = pos;
+      pperm[pos - off[e] + poff[e]] = p;
+    }
+    return;
+  }
   for (int s0 = 0; s0 < steps; s0 += kBatch) {
     int ev[kBatch], rk[kBatch];
 #pragma unroll
