@@ -19,7 +19,9 @@ Block cache over a pool of `num_blocks` physical blocks of 16 positions.
     needs ceil((n + extra) / 16) blocks in all; each missing one takes the lowest free block
     id, or, with none free, the least recently released cached block with no references is
     evicted (its entry and the entries under it dropped, their blocks freed) and the lowest
-    free id taken. Returns the block table row and n_cached = 16 * hits.
+    free id taken. Returns the block table row and n_cached = 16 * hits. When the free
+    and evictable blocks together cannot cover the request, nothing is evicted and the
+    request fails (only the hit blocks' recency changes).
   * commit(tokens[0..n), row): every full block of the row (16 (i+1) <= n) whose prefix is
     not cached yet becomes the cached block of that prefix; a prefix already cached under
     another block keeps that block.
@@ -75,13 +77,13 @@ class BlockCache:
                 self.lru.remove(b)
             self.ref[b] += 1
         row = list(hits)
+        if need - len(hits) > len(self.free) + len(self.lru):
+            self.release(row)              # the pool cannot hold it: undo, evict nothing
+            return None
         while len(row) < need:
-            if not self.free and self.lru:
+            if not self.free:
                 self.evictions += 1
                 self._drop(self.key_of[self.lru[0]])
-            if not self.free:
-                self.release(row)          # out of blocks: undo
-                return None
             b = min(self.free)
             self.free.remove(b)
             self.ref[b] += 1

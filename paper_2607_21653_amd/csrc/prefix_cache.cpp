@@ -145,14 +145,16 @@ int molt_prefix_cache_acquire(molt_prefix_cache* c, const int32_t* tokens, int n
     if (c->ref[b] == 0) c->lru_remove(b);
     ++c->ref[b];
   }
+  // Only free blocks and unreferenced cached blocks can be handed out; when they cannot
+  // cover the request, fail before evicting anything, so no cached prefix is lost.
+  if (need - hits > long(c->free.size() + c->lru.size())) {
+    c->release_row(row.data(), hits);
+    return MOLT_ERR_CAPACITY;
+  }
   while (long(row.size()) < need) {
-    if (c->free.empty() && !c->lru.empty()) {
+    if (c->free.empty()) {                    // the evicted block itself becomes free
       ++c->evictions;
       c->drop(c->lru.front());
-    }
-    if (c->free.empty()) {                    // the pool is exhausted: undo
-      c->release_row(row.data(), int(row.size()));
-      return MOLT_ERR_CAPACITY;
     }
     const int b = *c->free.begin();
     c->free.erase(c->free.begin());

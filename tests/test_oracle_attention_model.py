@@ -90,6 +90,57 @@ def test_rope_invariants():
     np.testing.assert_allclose(dot(5000, 4990), dot(15, 5), rtol=1e-9)
 
 
+def test_rope_hand_worked():
+    """Worked rotations that fix the frequency schedule, the pairing and the direction
+    (the decoder's rotary embedding: rotate-half pairs (i, i + D/2), inverse frequency
+    theta^(-2i/D), angle = position * inverse frequency).
+
+    D = 4, theta = 100, position 2: inverse frequencies 100^0 = 1 and 100^(-1/2) = 0.1, so
+    pair (x0, x2) turns by 2 rad and pair (x1, x3) by 0.2 rad:
+        cos 2 = -0.4161468365471424   sin 2 = 0.9092974268256817
+        cos .2 = 0.9800665778412416   sin .2 = 0.19866933079506122
+    x = (1, 2, 3, 4):
+        y0 = 1 cos 2 - 3 sin 2   = -3.1440391170241875
+        y2 = 3 cos 2 + 1 sin 2   = -0.33914308281574557
+        y1 = 2 cos .2 - 4 sin .2 =  1.1654558325022384
+        y3 = 4 cos .2 + 2 sin .2 =  4.317604972955089
+    An exponent of -i/D (0.316 for the second pair), interleaved pairs (x0, x1), or the
+    opposite rotation (y0 = cos 2 + 3 sin 2) each give different values.
+
+    D = 8, theta = 1e6 (the workloads' base), position 3: inverse frequencies 1,
+    10^-1.5, 10^-3, 10^-4.5; angles 3, 0.09486832980505137, 0.003, 9.486832980505139e-05:
+        cos = -0.9899924966004454, 0.9955033739876628, 0.999995500003375, 0.9999999955
+        sin =  0.1411200080598672, 0.0947260913327461, 0.002999995500002025,
+               9.48683296627489e-05
+    x = (1, -2, .5, 3, -1.5, 2.5, 4, -.25) rotates pairwise to the values below."""
+    y = attention.apply_rope(np.array([[[1.0, 2.0, 3.0, 4.0]]]), [2], 100.0)[0, 0]
+    np.testing.assert_allclose(y, [-3.1440391170241875, 1.1654558325022384,
+                                   -0.33914308281574557, 4.317604972955089], rtol=0, atol=1e-14)
+    x = np.array([[[1.0, -2.0, 0.5, 3.0, -1.5, 2.5, 4.0, -0.25]]])
+    y = attention.apply_rope(x, [3], 1e6)[0, 0]
+    np.testing.assert_allclose(y, [-0.7783124845106446, -2.2278219763071907, 0.4879977680016794,
+                                   3.0000237035824155, 1.6261087529605354, 2.2993062523036647,
+                                   4.001481997763501, -0.24971539388601174], rtol=0, atol=1e-14)
+    # the angle table itself: position * theta^(-2i/D)
+    np.testing.assert_allclose(attention.rope_angles([3], 8, 1e6)[0],
+                               [3.0, 0.09486832980505137, 0.003, 9.486832980505139e-05],
+                               rtol=1e-15, atol=0)
+
+
+def test_rmsnorm_hand_worked_eps():
+    """The epsilon sits inside the square root, added to the mean square; gains multiply
+    element-wise. x = (2, -2, 2, -2): mean square 4; with eps = 5 the scale is 1/sqrt(9) =
+    1/3 (eps outside the root would give 1/7, eps added to each square before the mean the
+    same 1/3 only because it is added once per element), so with g = (1, 2, 3, 4)
+    y = (2/3, -4/3, 2, -8/3). x = (3, 4, 0, 0), eps = 0.25, g = 1: mean square 25/4, scale
+    1/sqrt(6.5); y0 = 3/sqrt(6.5) = 1.1766968108291043."""
+    y = model.rmsnorm(np.array([[2.0, -2.0, 2.0, -2.0]]), np.array([1.0, 2.0, 3.0, 4.0]), 5.0)
+    np.testing.assert_allclose(y[0], [2 / 3, -4 / 3, 2.0, -8 / 3], rtol=0, atol=1e-15)
+    y = model.rmsnorm(np.array([[3.0, 4.0, 0.0, 0.0]]), np.ones(4), 0.25)
+    np.testing.assert_allclose(y[0], [1.1766968108291043, 1.5689290811054724, 0.0, 0.0],
+                               rtol=0, atol=1e-15)
+
+
 def test_rmsnorm_unit_rms():
     x = np.random.default_rng(6).normal(size=(10, 256)) * 7
     y = model.rmsnorm(x, np.ones(256), 0.0)

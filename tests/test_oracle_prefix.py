@@ -57,6 +57,32 @@ def test_lru_eviction():
     assert hit == 16 and row2[0] == 0
 
 
+def test_failed_acquire_evicts_nothing():
+    """A request larger than the free plus evictable blocks fails without dropping any
+    cached prefix: on a 4-block pool holding 2 cached unreferenced blocks, an 80-token
+    prompt needs 5 blocks; afterwards both entries, the free set and the eviction count
+    are as before, and the cached prefix still hits."""
+    c = BlockCache(4)
+    A = list(range(32))
+    row, _ = c.acquire(A, 32)
+    c.commit(A, 32, row)
+    c.release(row)
+    before = (dict(c.block_of), set(c.free), list(c.lru), c.evictions)
+    assert c.acquire(list(range(1000, 1080)), 80) is None
+    assert (dict(c.block_of), set(c.free), list(c.lru), c.evictions) == before
+    assert c.acquire(A + [7], 33)[1] == 32
+    # with one of the two cached blocks referenced by a live row, 3 free + evictable
+    # blocks cannot hold a 64-token prompt either; the hit block's recency alone moves
+    c = BlockCache(4)
+    c.commit(A, 32, c.acquire(A, 32)[0])
+    c.release([0, 1])
+    live, hit = c.acquire(A[:20], 20)
+    assert (live, hit) == ([0, 2], 16)
+    before = (dict(c.block_of), set(c.free), c.evictions)
+    assert c.acquire(A[:16] + list(range(500, 548)), 64) is None
+    assert (dict(c.block_of), set(c.free), c.evictions) == before and c.ref[0] == 1
+
+
 def test_random_sessions_keep_invariants():
     rng = np.random.default_rng(0)
     c = BlockCache(48)

@@ -64,3 +64,20 @@ def test_invalid_release_is_rejected(molt):
     c.release(row)
     with pytest.raises(molt.MoltError):
         c.release(row)                                      # no references left
+
+
+def test_failed_acquire_changes_nothing(molt):
+    """An acquire that the free and evictable blocks cannot cover returns CAPACITY before
+    evicting: the cached entries, counts and evictions are unchanged and the prefix still
+    hits (4-block pool, 2 cached blocks, an 80-token request)."""
+    c = molt.PrefixCache(4)
+    A = list(range(32))
+    row, _ = c.acquire(A)
+    c.commit(A, row)
+    c.release(row)
+    before = c.stats()
+    assert c.acquire(list(range(1000, 1080))) is None
+    after = c.stats()
+    assert {k: after[k] for k in ("free", "cached", "referenced", "evictable", "evictions")} == \
+        {k: before[k] for k in ("free", "cached", "referenced", "evictable", "evictions")}
+    assert c.acquire(A + [7])[1] == 32
