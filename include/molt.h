@@ -16,7 +16,9 @@
  *  - Pointers are DEVICE pointers unless marked "host". Arrays are row-major.
  *  - The caller owns every buffer. The library allocates no device memory: each
  *    call takes a caller-provided workspace of at least *_workspace_size() bytes
- *    (256-byte aligned start recommended; any alignment is accepted).
+ *    (256-byte aligned start recommended; any alignment is accepted). The one
+ *    exception, molt_spec_accept_noalloc, uses a fixed array the library holds
+ *    per GPU instead.
  *  - Calls are asynchronous on `stream` and never synchronise. Results are valid
  *    after the stream is synchronised. The library keeps no state between calls
  *    (weights and KV cache may be overwritten between calls, e.g. on a weight
@@ -107,6 +109,30 @@ int molt_spec_accept(const float* logits, const float* draft_probs, const int32_
                      const float* uniforms, int B, int k, int V, int32_t* out_tokens,
                      int32_t* out_num_accepted, float* out_logprobs, void* workspace,
                      size_t workspace_bytes, molt_stream_t stream);
+
+/* ------------------------------------------------------------------------------
+ * molt_spec_accept_noalloc -- molt_spec_accept for callers that cannot allocate device
+ * memory: code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc. The same rule, kernels and results (bit for bit) as molt_spec_accept, with
+ * the workspace replaced by a fixed array of MOLT_NOALLOC_SCRATCH_BYTES (8 MiB) of device
+ * memory that the library holds on every GPU it runs on until the process ends. The call
+ * allocates nothing (no hipMalloc, no allocating library routine); its first call on a
+ * device looks up that device's array, so the current device must be the stream's.
+ * Every call on one GPU shares that GPU's array, which keeps the last call's contents
+ * (each call writes every entry before reading it, so nothing needs clearing): calls that
+ * overlap in time on one GPU (several streams or host threads) race and give undefined
+ * results.
+ * Arguments as molt_spec_accept, without the workspace.
+ * Errors: as molt_spec_accept, and INVALID_ARG when molt_spec_accept_workspace_size(B, k,
+ * V) exceeds MOLT_NOALLOC_SCRATCH_BYTES (B = 128, k = 8, V = 151936 needs 0.9 MB; the
+ * need grows as B * (k + 1) * ceil(V / 8192) * 12 + B * ceil(V / 8192) * 264 bytes);
+ * HIP when the array cannot be looked up.
+ * ---------------------------------------------------------------------------- */
+#define MOLT_NOALLOC_SCRATCH_BYTES (8u << 20)
+int molt_spec_accept_noalloc(const float* logits, const float* draft_probs,
+                             const int32_t* draft_tokens, const float* uniforms, int B, int k,
+                             int V, int32_t* out_tokens, int32_t* out_num_accepted,
+                             float* out_logprobs, molt_stream_t stream);
 
 /* ------------------------------------------------------------------------------
  * molt_moe_layer -- top-K routed SwiGLU mixture-of-experts on normalised input

@@ -14,6 +14,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libmolt.so")
 
 MOLT_F32, MOLT_BF16, MOLT_FP8_E4M3 = 0, 1, 2
+NOALLOC_SCRATCH_BYTES = 8 << 20   # MOLT_NOALLOC_SCRATCH_BYTES of include/molt.h
 DTYPE_CODE = {torch.float32: MOLT_F32, torch.bfloat16: MOLT_BF16, torch.uint8: MOLT_FP8_E4M3}
 NAME_CODE = {"f32": MOLT_F32, "bf16": MOLT_BF16, "fp8": MOLT_FP8_E4M3}
 
@@ -49,6 +50,8 @@ _SIGS = {
     "molt_spec_accept_workspace_size": (c_size, [c_int, c_int, c_int]),
     "molt_spec_accept": (c_int, [c_vp, c_vp, c_vp, c_vp, c_int, c_int, c_int, c_vp, c_vp, c_vp,
                                  c_vp, c_size, c_vp]),
+    "molt_spec_accept_noalloc": (c_int, [c_vp, c_vp, c_vp, c_vp, c_int, c_int, c_int, c_vp, c_vp,
+                                         c_vp, c_vp]),
     "molt_moe_layer_workspace_size": (c_size, [c_int] * 5 + [c_int, c_int]),
     "molt_moe_layer": (c_int, [c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_int, c_int, c_int,
                                c_int, c_int, c_int, c_int, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp,
@@ -179,6 +182,30 @@ def spec_accept(logits, draft_tokens, uniforms, draft_probs=None, out=None, work
                               _ptr(uniforms), B, k, V, _ptr(toks), _ptr(n), _ptr(lp), _ptr(ws), nb,
                               _stream())
     _check(st, "molt_spec_accept")
+    return toks, n, lp
+
+
+def spec_accept_noalloc(logits, draft_tokens, uniforms, draft_probs=None, out=None):
+    """molt_spec_accept_noalloc: spec_accept with the library's fixed per-GPU scratch array
+    instead of a workspace (no device allocation inside the call when `out` is given)."""
+    lib = load()
+    B, kp1, V = logits.shape
+    k = kp1 - 1
+    _dev(logits, torch.float32, name="logits")
+    _dev(uniforms, torch.float32, (B, kp1), "uniforms")
+    if k > 0:
+        _dev(draft_tokens, torch.int32, (B, k), "draft_tokens")
+    _dev(draft_probs, torch.float32, (B, k, V), "draft_probs")
+    dev = logits.device
+    if out is None:
+        out = (torch.empty(B, kp1, dtype=torch.int32, device=dev),
+               torch.empty(B, dtype=torch.int32, device=dev),
+               torch.empty(B, kp1, dtype=torch.float32, device=dev))
+    toks, n, lp = out
+    st = lib.molt_spec_accept_noalloc(_ptr(logits), _ptr(draft_probs),
+                                      _ptr(draft_tokens) if k > 0 else None, _ptr(uniforms), B, k, V,
+                                      _ptr(toks), _ptr(n), _ptr(lp), _stream())
+    _check(st, "molt_spec_accept_noalloc")
     return toks, n, lp
 
 

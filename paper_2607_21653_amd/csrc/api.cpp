@@ -6,6 +6,7 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <mutex>
 #include <string>
 
 #include "internal.h"
@@ -77,7 +78,7 @@ extern "C" {
 
 const char* molt_last_error(void) { return g_err.c_str(); }
 
-int molt_version(void) { return 102; }
+int molt_version(void) { return 103; }
 
 // ------------------------------------------------------------------ profiling
 
@@ -153,6 +154,69 @@ int molt_spec_accept(const float* logits, const float* draft_probs, const int32_
                                  reinterpret_cast<hipStream_t>(stream));
   }
   return hip_status(e, "molt_spec_accept");
+}
+
+// ------------------------------------------------------------------ spec accept, no allocation
+
+// The fixed scratch array of the allocation-free accept: one copy per GPU, held until the
+// process ends. In host code `scratch` names a host-side stand-in, not device memory: host
+// code reaches the array only through the address hipGetSymbolAddress returns for the
+// current device.
+static __device__ __align__(256) unsigned char scratch[MOLT_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+
+struct ScratchSlot {
+  std::once_flag once;
+  void* ptr = nullptr;
+  hipError_t err = hipSuccess;
+};
+ScratchSlot g_scratch[kMaxDevices];
+
+// Device address of the current device's scratch array, looked up on the first call on
+// that device (with it current) and kept.
+hipError_t scratch_on_current_device(void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  ScratchSlot& slot = g_scratch[dev];
+  std::call_once(slot.once, [&slot] {
+    slot.err = hipGetSymbolAddress(&slot.ptr, HIP_SYMBOL(scratch));
+  });
+  *out = slot.ptr;
+  return slot.err;
+}
+
+}  // namespace
+
+int molt_spec_accept_noalloc(const float* logits, const float* draft_probs,
+                             const int32_t* draft_tokens, const float* uniforms, int B, int k,
+                             int V, int32_t* out_tokens, int32_t* out_num_accepted,
+                             float* out_logprobs, molt_stream_t stream) {
+  if (int r = spec_accept_shape_ok(B, k, V)) return r;
+  REQUIRE(logits, "logits is NULL");
+  REQUIRE(uniforms, "uniforms is NULL");
+  REQUIRE(k == 0 || draft_tokens, "draft_tokens is NULL with k = %d", k);
+  REQUIRE(out_tokens, "out_tokens is NULL");
+  REQUIRE(out_num_accepted, "out_num_accepted is NULL");
+  const size_t need = molt_spec_accept_workspace_size(B, k, V);
+  REQUIRE(need <= size_t(MOLT_NOALLOC_SCRATCH_BYTES),
+          "B = %d, k = %d, V = %d need %zu bytes of scratch; the allocation-free entry point "
+          "holds %zu (use molt_spec_accept with a workspace)",
+          B, k, V, need, size_t(MOLT_NOALLOC_SCRATCH_BYTES));
+  void* ws = nullptr;
+  hipError_t e = scratch_on_current_device(&ws);
+  if (e != hipSuccess) return hip_status(e, "molt_spec_accept_noalloc: scratch lookup");
+  {
+    ProfScope ps(MOLT_PROF_SAMPLER, reinterpret_cast<hipStream_t>(stream));
+    e = molt::launch_spec_accept(logits, draft_probs, draft_tokens, uniforms, B, k, V, out_tokens,
+                                 out_num_accepted, out_logprobs, ws,
+                                 reinterpret_cast<hipStream_t>(stream));
+  }
+  return hip_status(e, "molt_spec_accept_noalloc");
 }
 
 // ------------------------------------------------------------------ helpers

@@ -35,7 +35,7 @@ def test_exports_every_declared_symbol(L):
 
 
 def test_version_and_error_string(L):
-    assert L.molt_version() == 102
+    assert L.molt_version() == 103
     assert isinstance(L.molt_last_error(), bytes)
 
 
@@ -145,3 +145,20 @@ def test_mtp_validation(L):
     assert L.molt_mtp_draft(ctypes.byref(t), ctypes.byref(mtp), ctypes.byref(kv), 4, 3, *a2) == INVALID
     assert L.molt_mtp_draft_workspace_size(ctypes.byref(t), None, 4, 3, 8) == 0
     assert L.molt_mtp_draft_workspace_size(ctypes.byref(t), ctypes.byref(mtp), 4, 0, 8) == 0
+
+
+def test_spec_accept_noalloc_validation(L):
+    """The allocation-free accept validates like molt_spec_accept and rejects shapes whose
+    scratch need exceeds its fixed array, before any GPU call."""
+    p = ctypes.c_void_p(0x1000)
+    call = lambda B, k, V, logits=p, u=p, toks=p: L.molt_spec_accept_noalloc(
+        logits, None, p, u, B, k, V, toks, p, None, None)
+    assert call(0, 1, 10) == INVALID
+    assert call(2, 1, 10, logits=None) == INVALID
+    assert call(2, 1, 10, u=None) == INVALID
+    assert call(2, 1, 10, toks=None) == INVALID
+    limit = _lib.NOALLOC_SCRATCH_BYTES
+    assert L.molt_spec_accept_workspace_size(128, 8, 151936) <= limit
+    assert L.molt_spec_accept_workspace_size(4096, 8, 151936) > limit
+    assert call(4096, 8, 151936) == INVALID
+    assert b"scratch" in L.molt_last_error()
