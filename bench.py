@@ -13,6 +13,14 @@ Prints one JSON line: verified tokens/s (= B*(1+k) positions scored per second),
 roofline of the dominant kernel (paged attention, HBM-bound; its average launch time
 measured with HIP events on the library's stream during the timed region), and the
 CPU oracle timed on a bounded sample of the same workload (cpu_baseline).
+
+The same line carries `configs`: the other seeded workloads measured beside it, each
+with its own oracle baseline -- the tiny f32 decoder (the whole step), one bf16 layer
+at the 35B-A3B-like shape (B 64, k 4, context 4096), that layer at long agent contexts
+(B 16, context U[32768, 65536]) and with fp8 experts under Zipf(1.2) routing (B 256,
+k 8, context 2048; plus a one-expert fp8 GEMM at that row count). A layer workload's
+step is one molt_decoder_forward call over its B(1+k) positions; `--workload <name>`
+measures one of them alone (profiling runs).
 """
 import argparse
 import json
@@ -343,11 +351,7 @@ def cpu_baseline(w, layout, host_layers, head, kv, tokens, q, u, n_seq=CPU_SAMPL
     measured, threads, description)."""
     import oracle.model as omodel
     from oracle import sampler as osamp
-    try:
-        from threadpoolctl import threadpool_info
-        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
-    except Exception:
-        threads = os.cpu_count() or 1
+    threads = blas_threads()
 
     sample_layers = min(sample_layers, len(host_layers))
     cfg = dict(dtype=w.dtype, expert_dtype=w.expert_dtype, n_layers=sample_layers,
@@ -386,6 +390,314 @@ def cpu_baseline(w, layout, host_layers, head, kv, tokens, q, u, n_seq=CPU_SAMPL
     return value, t2 - t0, threads, desc
 
 
+# ------------------------------------------------------------------ host description
+
+def host_info():
+    """The host the oracle runs on: core counts, BLAS library and threads, CPU model."""
+    info = {"os_cpu_count": os.cpu_count(), "sched_affinity": len(os.sched_getaffinity(0))}
+    try:
+        from threadpoolctl import threadpool_info
+        info["blas"] = [{k_: i.get(k_) for k_ in ("internal_api", "version", "num_threads",
+                                                  "threading_layer")} for i in threadpool_info()]
+    except Exception as e:                                    # noqa: BLE001
+        info["blas"] = f"unknown ({e})"
+    try:
+        with open("/proc/cpuinfo") as f:
+            info["cpu_model"] = next(l.split(":", 1)[1].strip() for l in f if l.startswith("model name"))
+    except (OSError, StopIteration):
+        info["cpu_model"] = None
+    return info
+
+
+def blas_threads():
+    try:
+        from threadpoolctl import threadpool_info
+        return max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:                                         # noqa: BLE001
+        return os.cpu_count() or 1
+
+
+# ------------------------------------------------------------------ layer workloads
+
+FLUSH_BYTES = 1 << 30          # written between timed iterations: evicts L2 and the MALL
+LAYER_ITERS, LAYER_WARMUP = 20, 3
+CPU_LAYER_SEQS = {"layer_bf16": 4, "long_ctx_bf16": 2, "fp8_zipf": 4}
+
+
+def _timed(fn, flush, iters, warmup, prep=None):
+    """Median and mean of `iters` calls of fn(), each bracketed by HIP events on torch's
+    current stream (the library's stream), with the flush buffer rewritten and prep() run
+    before each, outside the events."""
+    for _ in range(warmup):
+        if prep:
+            prep()
+        fn()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(iters)]
+    for e0, e1 in ev:
+        flush.zero_()
+        if prep:
+            prep()
+        e0.record()
+        fn()
+        e1.record()
+    torch.cuda.synchronize()
+    t = np.array([e0.elapsed_time(e1) for e0, e1 in ev])
+    return float(np.median(t)), float(t.mean())
+
+
+def _groups(molt, fn, flush, reps=3, prep=None):
+    """Per-kernel-group times of `reps` further calls, every group bracketed."""
+    molt.profile_enable(True)
+    for _ in range(reps):
+        flush.zero_()
+        if prep:
+            prep()
+        fn()
+    torch.cuda.synchronize()
+    molt.profile_enable(False)
+    return {g: (t / reps, n // reps) for g, (t, n) in
+            ((g, molt.profile_read(g)) for g in molt._lib.PROF_GROUPS)}
+
+
+def _frac(achieved, peak):
+    return round(achieved / peak, 4)
+
+
+def dense_weight_bytes(w):
+    D, d = w.head_dim, w.d_model
+    return ((w.n_q_heads + 2 * w.n_kv_heads) * D * d + d * w.n_q_heads * D + w.n_experts * d) * 2
+
+
+def dense_flops(w, T):
+    return 2.0 * T * dense_weight_bytes(w) / 2
+
+
+def layer_cpu_baseline(w, layout, lh, kc, vc, x0, n_seq):
+    """The oracle's attention block and MoE block for the first n_seq sequences of the
+    layer workload (their (1+k) positions, their own cache blocks), timed on the host."""
+    import oracle.model as omodel
+    seqs = list(range(n_seq))
+    rows = [layout.block_tables[b][layout.block_tables[b] >= 0] for b in seqs]
+    idx = torch.from_numpy(np.concatenate(rows)).long().to(kc.device)
+    bt = np.full((n_seq, max(len(r) for r in rows)), -1, dtype=np.int64)
+    pos = 0
+    for i, r in enumerate(rows):
+        bt[i, :len(r)] = np.arange(pos, pos + len(r))
+        pos += len(r)
+    okc = omodel.widen_cache(host(kc.index_select(0, idx)), w.dtype)
+    ovc = omodel.widen_cache(host(vc.index_select(0, idx)), w.dtype)
+    kp1 = w.k + 1
+    xr = host(x0)[np.concatenate([np.arange(b * kp1, (b + 1) * kp1) for b in seqs])]
+    cfg = dict(dtype=w.dtype, expert_dtype=w.expert_dtype, n_layers=1, n_q_heads=w.n_q_heads,
+               n_kv_heads=w.n_kv_heads, head_dim=w.head_dim, top_k=w.top_k, rms_eps=w.rms_eps,
+               rope_theta=w.rope_theta, block_size=16)
+    t0 = time.perf_counter()
+    xo = omodel.attention_block(xr, lh, okc, ovc, bt, layout.context_lens[seqs], w.k, cfg)
+    omodel.moe_block(xo, lh, cfg)
+    secs = time.perf_counter() - t0
+    return {"value": round(len(xr) / secs, 2), "unit": "verified tokens/s", "cores": blas_threads(),
+            "kind": "oracle",
+            "sample": f"{n_seq} of {w.batch} sequences ({len(xr)} positions) through the layer "
+                      f"(attention block + MoE block), float64 NumPy oracle",
+            "seconds": round(secs, 2)}
+
+
+def hot_expert_gemm(w, seed, molt, flush, M):
+    """One fp8 expert of the layer's shape with every one of M rows routed to it (E = K = 1
+    through molt_moe_layer): the dense limit of a Zipf-hot expert. Its two GEMMs are timed
+    as the expert-GEMM kernel group."""
+    dev = "cuda"
+    one = w.scaled(n_experts=1, top_k=1, zipf=None)
+    lw = workloads.make_layer_weights(one, seed, 0, device=dev)
+    x = workloads.make_hidden(one, seed, T=M, device=dev).to(torch.bfloat16)
+    wr, wgu, wd = (molt.pack_weights(lw[k_]) for k_ in ("w_router", "w_gate_up", "w_down"))
+    ws = torch.empty(molt._lib.load().molt_moe_layer_workspace_size(M, w.d_model, 1, 1, w.d_ff, 1, 2),
+                     dtype=torch.uint8, device=dev)
+
+    def call():
+        molt.moe_layer(x, wr, wgu, wd, 1, s_gate_up=lw["s_gate_up"], s_down=lw["s_down"],
+                       workspace=ws, packed=True, n_experts=1)
+
+    _timed(call, flush, 5, 3)
+    t, n = _groups(molt, call, flush, reps=10)["expert_gemm"]
+    flops = 2.0 * M * 3 * w.d_ff * w.d_model
+    tf = flops / (t / 1e3) / 1e12
+    return {"rows": M, "gemm_ms": round(t, 4), "tflops": round(tf, 1), "peak": 5000.0,
+            "unit": "TFLOP/s", "frac": _frac(tf, 5000.0), "flops": flops,
+            "note": "gate_up + down of one fp8 expert with every row routed to it "
+                    "(arithmetic intensity ~4600 flop/B: MFMA-bound)"}
+
+
+def layer_measure(w, seed, molt, flush, cpu=True):
+    """One decoder layer of a layer workload: the residual stream x [B(1+k), d] N(0,1), the
+    layer's weights, and a random paged cache, all resident; median of LAYER_ITERS timed
+    molt_decoder_forward calls (x restored before each, outside the events)."""
+    dev = "cuda"
+    B, k = w.batch, w.k
+    T = B * (k + 1)
+    layout = workloads.make_kv_layout(w, seed)
+    lw = workloads.make_layer_weights(w, seed, 0, device=dev)
+    lh = {k_: (None if v is None else host(v)) for k_, v in lw.items()} if cpu else None
+    for key in molt.Model.PACKED:
+        lw[key] = molt.pack_weights(lw[key])
+    model = molt.Model([lw], None, n_q_heads=w.n_q_heads, n_kv_heads=w.n_kv_heads,
+                       head_dim=w.head_dim, top_k=w.top_k, rms_eps=w.rms_eps,
+                       rope_theta=w.rope_theta, packed=True)
+    kc, vc = workloads.make_kv_cache(w, layout, seed, 0, device=dev)
+    kv = molt.KVCache([kc], [vc], torch.from_numpy(layout.block_tables).to(dev),
+                      torch.from_numpy(layout.context_lens).to(dev))
+    x0 = workloads.make_hidden(w, seed, device=dev)
+    x = x0.clone()
+    ws = torch.empty(molt.decoder_workspace_size(model, B, k, layout.block_tables.shape[1]),
+                     dtype=torch.uint8, device=dev)
+    routes = molt.decoder_forward(model, kv, B, k, x, want_routes=True, workspace=ws)
+    torch.cuda.synchronize()
+    counts = np.bincount(routes.cpu().numpy().ravel(), minlength=w.n_experts)
+
+    def call():
+        molt.decoder_forward(model, kv, B, k, x, workspace=ws)
+
+    def restore():
+        x.copy_(x0)
+
+    log(f"[bench] {w.name}: timing {LAYER_ITERS} layer calls")
+    med, mean = _timed(call, flush, LAYER_ITERS, LAYER_WARMUP, prep=restore)
+    groups = _groups(molt, call, flush, prep=restore)
+    eb = 1 if w.expert_dtype == "fp8" else 2
+    touched = int((counts > 0).sum())
+    ebytes = touched * 3 * w.d_ff * w.d_model * eb
+    abytes = attention_bytes(w, layout.context_lens)
+    dbytes = dense_weight_bytes(w)
+    nbytes = abytes + ebytes + dbytes
+    eflops = 2.0 * T * w.top_k * 3 * w.d_ff * w.d_model
+    epeak = 5000.0 if eb == 1 else BF16_PEAK_TFLOPS
+    out = {"workload": w.name, "batch": B, "k": k,
+           "context": [int(layout.context_lens.min()), int(layout.context_lens.max())],
+           "positions": T, "layer_us": round(med * 1e3, 1), "layer_us_mean": round(mean * 1e3, 1),
+           "verified_tokens_per_s": round(T / (med / 1e3), 1),
+           "roofline": {"bound": "hbm", "algorithmic_bytes": int(nbytes),
+                        "roofline_us": round(nbytes / (HBM_PEAK_GBS * 1e9) * 1e6, 1),
+                        "achieved": round(nbytes / (med / 1e3) / 1e9, 1), "peak": HBM_PEAK_GBS,
+                        "unit": "GB/s", "frac": _frac(nbytes / (med / 1e3) / 1e9, HBM_PEAK_GBS),
+                        "note": "attention K/V + q + out, touched experts' weights, attention "
+                                "projections and router, each once"}}
+    ta, na = groups["attention"]
+    if na:
+        a = abytes / (ta / na / 1e3) / 1e9
+        out["attention"] = {"avg_launch_us": round(ta / na * 1e3, 1), "algorithmic_bytes": int(abytes),
+                            "achieved": round(a, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                            "frac": _frac(a, HBM_PEAK_GBS)}
+    te, ne = groups["expert_gemm"]
+    if ne:
+        a = ebytes / (te / 1e3) / 1e9
+        tf = eflops / (te / 1e3) / 1e12
+        ai = eflops / ebytes
+        attain = min(epeak, ai * HBM_PEAK_GBS / 1e3)
+        out["expert_gemm"] = {"gate_up_plus_down_us": round(te * 1e3, 1), "touched_experts": touched,
+                              "weight_bytes": int(ebytes), "achieved": round(a, 1), "peak": HBM_PEAK_GBS,
+                              "unit": "GB/s", "frac": _frac(a, HBM_PEAK_GBS),
+                              "mfma_tflops": round(tf, 1), "mfma_peak": epeak,
+                              "mfma_frac": _frac(tf, epeak),
+                              "attainable_tflops": round(attain, 1),
+                              "frac_of_attainable": _frac(tf, attain)}
+    tp, npj = groups["projections"]
+    if npj:
+        tf = dense_flops(w, T) / (tp / 1e3) / 1e12
+        attain = min(BF16_PEAK_TFLOPS, dense_flops(w, T) / dbytes * HBM_PEAK_GBS / 1e3)
+        out["projections"] = {"qkv_o_router_us": round(tp * 1e3, 1), "mfma_tflops": round(tf, 1),
+                              "mfma_peak": BF16_PEAK_TFLOPS, "mfma_frac": _frac(tf, BF16_PEAK_TFLOPS),
+                              "attainable_tflops": round(attain, 1), "frac_of_attainable": _frac(tf, attain)}
+    out["other_kernels_us"] = round((med - ta - te - tp) * 1e3, 1)
+    if w.zipf is not None:
+        srt = np.sort(counts)[::-1]
+        out["expert_load"] = {"max_over_mean": round(float(counts.max() / counts.mean()), 2),
+                              "top8_rows": srt[:8].tolist(), "empty_experts": int((counts == 0).sum())}
+        out["hot_expert_gemm"] = hot_expert_gemm(w, seed, molt, flush, int(counts.max()))
+        out["dense_expert_gemm"] = hot_expert_gemm(w, seed, molt, flush, T)
+    if cpu:
+        log(f"[bench] {w.name}: timing the CPU oracle")
+        out["cpu_baseline"] = layer_cpu_baseline(w, layout, lh, kc, vc, x0, CPU_LAYER_SEQS[w.name])
+    del model, kv, kc, vc, lw
+    torch.cuda.empty_cache()
+    return out
+
+
+def tiny_measure(w, seed, molt, flush, cpu=True):
+    """The tiny f32 decoder's whole verify step (2 layers, B 4, k 3, vocab 2048): the cache is
+    filled by molt_prefill of the seeded prompts, then molt_verify_step is timed (a
+    latency-bound configuration); the oracle's whole step on all cores and on one thread."""
+    dev = "cuda"
+    B, k = w.batch, w.k
+    layout = workloads.make_kv_layout(w, seed)
+    layers = [workloads.make_layer_weights(w, seed, l, device=dev) for l in range(w.n_layers)]
+    head = workloads.make_head_weights(w, seed, device=dev)
+    lh = [{k_: (None if v is None else host(v)) for k_, v in lw.items()} for lw in layers]
+    hh = {k_: host(v) for k_, v in head.items()}
+    model = molt.Model(layers, head, n_q_heads=w.n_q_heads, n_kv_heads=w.n_kv_heads,
+                       head_dim=w.head_dim, top_k=w.top_k, rms_eps=w.rms_eps, rope_theta=w.rope_theta)
+    caches = [workloads.empty_kv_cache(w, layout, device=dev) for _ in range(w.n_layers)]
+    bt = torch.from_numpy(layout.block_tables).to(dev)
+    kcs, vcs = [c[0] for c in caches], [c[1] for c in caches]
+    for b, p in enumerate(workloads.make_prompts(w, layout, seed)):   # one sequence at a time
+        kvb = molt.KVCache(kcs, vcs, bt[b:b + 1].contiguous(), torch.zeros(1, dtype=torch.int32, device=dev))
+        molt.prefill(model, kvb, torch.from_numpy(p[None, :].copy()).to(dev),
+                     torch.tensor([len(p)], dtype=torch.int32, device=dev))
+    kv = molt.KVCache(kcs, vcs, bt, torch.from_numpy(layout.context_lens).to(dev))
+    toks = torch.from_numpy(workloads.make_step_tokens(w, seed)).to(dev)
+    q = workloads.make_softmax_q(B, k, w.vocab, seed, device=dev)
+    u = workloads.make_uniforms(B, k, seed, device=dev)
+    ws = torch.empty(molt.verify_step_workspace_size(model, B, k, layout.block_tables.shape[1]),
+                     dtype=torch.uint8, device=dev)
+    res = molt.verify_step(model, kv, toks, u, q, workspace=ws)
+    med, mean = _timed(lambda: molt.verify_step(model, kv, toks, u, q, workspace=ws, out=res),
+                       flush, LAYER_ITERS, LAYER_WARMUP)
+    T = B * (k + 1)
+    out = {"workload": w.name, "positions": T, "step_us": round(med * 1e3, 1),
+           "verified_tokens_per_s": round(T / (med / 1e3), 1),
+           "note": "latency-bound (31 MB of weights): no roofline fraction is claimed"}
+    if cpu:
+        import oracle.model as omodel
+        cfg = dict(dtype=w.dtype, expert_dtype=w.expert_dtype, n_layers=w.n_layers,
+                   n_q_heads=w.n_q_heads, n_kv_heads=w.n_kv_heads, head_dim=w.head_dim,
+                   top_k=w.top_k, rms_eps=w.rms_eps, rope_theta=w.rope_theta, block_size=16)
+        kch = [(omodel.widen_cache(host(a), w.dtype), omodel.widen_cache(host(b), w.dtype))
+               for a, b in zip(kv.k_caches, kv.v_caches)]
+
+        def run():
+            c = [(a.copy(), b.copy()) for a, b in kch]
+            t0 = time.perf_counter()
+            omodel.verify_step(host(toks), lambda l: lh[l], hh, c, layout.block_tables,
+                               layout.context_lens, cfg, host(q), host(u))
+            return time.perf_counter() - t0
+
+        secs = run()
+        try:
+            from threadpoolctl import threadpool_limits
+            with threadpool_limits(limits=1):
+                secs1 = run()
+            one = {"value": round(T / secs1, 2), "cores": 1, "seconds": round(secs1, 3)}
+        except Exception as e:                                # noqa: BLE001
+            one = f"unavailable ({e})"
+        out["cpu_baseline"] = {"value": round(T / secs, 2), "unit": "verified tokens/s",
+                               "cores": blas_threads(), "kind": "oracle",
+                               "sample": f"the whole step ({T} positions), float64 NumPy oracle",
+                               "seconds": round(secs, 3), "single_thread": one}
+    return out
+
+
+def acceptance_prediction(out, q, k):
+    """Closed form of the expected accepted count from the step's own rows: a draft drawn
+    from q_i passes with probability alpha_i = sum_t min(p_t, q_t) = 1 - TV(p, q) (p =
+    softmax of logits row i-1), so E[n] = sum_i prod_{j<=i} alpha_j per sequence."""
+    alpha = torch.stack([torch.minimum(torch.softmax(out["logits"][:, i].double(), dim=-1),
+                                       q[:, i].double()).sum(dim=-1) for i in range(k)], dim=1)
+    en = torch.cumprod(alpha, dim=1).sum(dim=1)
+    return {"predicted_mean_accepted_fraction": round(float(en.mean()) / k, 4),
+            "mean_alpha": round(float(alpha.mean()), 4),
+            "note": "E[n]/k from alpha_i = 1 - TV(p_{i-1}, q_i) of the step's own logits and q"}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -398,6 +710,8 @@ def main():
                     help="skip the draft-head, replay and re-prefill measurements (profiling runs)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a 1 GiB device-to-device copy (HBM counter calibration)")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="skip the other workloads measured beside the headline")
     a = ap.parse_args()
     if a.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for {a.gpus}): the verify step shards by "
@@ -416,8 +730,27 @@ def main():
     import paper_2607_21653_amd as molt
     molt.load()
     w = workloads.WORKLOADS[a.workload]
-    if not w.full_model:
-        sys.exit(f"{a.workload} is a single-layer workload; the bench step is the full verify step")
+    flush = torch.empty(FLUSH_BYTES, dtype=torch.uint8, device="cuda")
+    info = None if a.no_cpu_baseline else host_info()
+    if w.name != workloads.FULL_DEPTH_BF16.name:
+        # one of the other workloads alone (profiling runs)
+        m = (tiny_measure if w.name == workloads.TINY_FP32.name else layer_measure)(
+            w, a.seed, molt, flush, cpu=not a.no_cpu_baseline)
+        if info is not None:
+            m["cpu_baseline"]["host"] = info
+        print(json.dumps({"metric": "verified tokens/s per MI355X (verify step) + % HBM/MFMA roofline",
+                          "value": m["verified_tokens_per_s"], "unit": "verified tokens/s", "n_gpus": 1,
+                          "higher_is_better": True, "dtype": w.dtype, "data": "synthetic",
+                          "config": {"workload": w.name}, "measurement": m}))
+        return
+    configs = {}
+    if not a.no_configs:
+        for cw in (workloads.TINY_FP32, workloads.LAYER_BF16, workloads.LONG_CTX_BF16, workloads.FP8_ZIPF):
+            log(f"[bench] workload {cw.name}")
+            configs[cw.name] = (tiny_measure if cw.name == workloads.TINY_FP32.name else layer_measure)(
+                cw, a.seed, molt, flush, cpu=not a.no_cpu_baseline)
+    del flush
+    torch.cuda.empty_cache()
     t_setup = time.time()
     layout, host_layers, head, model, kv = build(
         w, a.seed, molt, keep_host=0 if a.no_cpu_baseline else CPU_SAMPLE_LAYERS)
@@ -451,6 +784,13 @@ def main():
     molt.profile_enable(False)
     ms = (t1 - t0) * 1e3 / a.steps
     attn_ms, attn_n = molt.profile_read("attention")
+    # the same steps again with no event inside, for the instrumentation's cost
+    torch.cuda.synchronize()
+    t2 = time.perf_counter()
+    for _ in range(a.steps):
+        molt.verify_step(model, kv, tokens, u, q, workspace=ws, out=out)
+    torch.cuda.synchronize()
+    ms_plain = (time.perf_counter() - t2) * 1e3 / a.steps
     # per-group breakdown from separate, untimed steps with every group bracketed
     log("[bench] kernel-group breakdown (untimed steps)")
     molt.profile_enable(True)
@@ -462,6 +802,7 @@ def main():
     n_break = min(a.steps, 3)
     samp = sampler_roofline(w, molt, out, tokens, q, u)
     n_acc = out["n_accepted"].cpu().numpy()
+    accept = acceptance_prediction(out, q, k) if k > 0 else None
     mtp = rep = rpf = None
     if not a.verify_only:
         log("[bench] MTP draft step")
@@ -503,8 +844,10 @@ def main():
                      "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": attention_traffic(),
                      "algorithmic_bytes_per_launch": abytes, "avg_launch_ms": round(attn_avg, 4)},
+        "ms_per_step_without_events": round(ms_plain, 3),
         "emitted_tokens_per_s": round(emitted, 1),
         "mean_accepted_fraction": round(float(n_acc.mean()) / k, 4) if k else None,
+        "acceptance_closed_form": accept,
         "kernel_groups": per_group,
         "kernel_groups_note": f"HIP-event times of each group over {n_break} untimed steps after the timed region",
         "lm_head_tflops": round(lm_flops / (lm_ms / max(lm_n, 1) / 1e3) / 1e12, 1) if lm_n else None,
@@ -519,12 +862,14 @@ def main():
         "mtp_draft": mtp,
         "replay_recompute": rep,
         "reprefill": rpf,
+        "configs": configs or None,
     }
     if not a.no_cpu_baseline:
         log("[bench] timing the CPU oracle on a bounded sample")
         v, secs, threads, desc = cpu_baseline(w, layout, host_layers, head, kv, tokens, q, u)
         res["cpu_baseline"] = {"value": round(v, 3), "unit": "verified tokens/s", "cores": threads,
-                               "kind": "oracle", "sample": desc, "seconds": round(secs, 2)}
+                               "kind": "oracle", "sample": desc, "seconds": round(secs, 2),
+                               "host": info}
     print(json.dumps(res))
 
 

@@ -175,11 +175,16 @@ def empty_kv_cache(w: Workload, layout: KVLayout, device="cpu"):
 # weights
 # ----------------------------------------------------------------------------------------
 
-def make_fp8_codes(shape, g, device) -> torch.Tensor:
-    """Random OCP e4m3fn codes with the top exponent bit cleared: magnitudes in
-    [2^-9, 1.875], subnormals included, no NaN code. A synthetic fp8 checkpoint."""
-    b = torch.randint(0, 256, shape, generator=g, device=device, dtype=torch.int32)
-    return (b & 0xBF).to(torch.uint8)
+def make_fp8_weights(shape, std, g, device):
+    """A synthetic fp8 checkpoint: N(0, std^2) weights quantised per output channel (every
+    row of the last axis): s = amax / 448, codes = e4m3fn(w / s) by torch's float8_e4m3fn
+    conversion (round to nearest even; |w / s| <= 448 up to one rounding, which rounds to
+    448). Returns (uint8 codes, f32 scales of shape[:-1])."""
+    wt = torch.randn(*shape, generator=g, device=device, dtype=torch.float32).mul_(std)
+    s = wt.abs().amax(dim=-1) / 448.0
+    s = torch.where(s > 0, s, torch.ones_like(s))
+    codes = (wt / s.unsqueeze(-1)).to(torch.float8_e4m3fn).view(torch.uint8)
+    return codes, s
 
 
 def make_layer_weights(w: Workload, seed: int, layer: int, device="cpu") -> dict:
@@ -194,13 +199,10 @@ def make_layer_weights(w: Workload, seed: int, layer: int, device="cpu") -> dict
         "w_router": _normal((E, d), std, rng(seed, w.name, "wrouter", layer, device=device), device, dt),
     }
     if w.expert_dtype == "fp8":
-        out["w_gate_up"] = make_fp8_codes((E, 2 * F, d), rng(seed, w.name, "wgu", layer, device=device), device)
-        out["w_down"] = make_fp8_codes((E, d, F), rng(seed, w.name, "wd", layer, device=device), device)
-        # per-output-channel scales: codes have rms ~0.58, so scale ~ std/0.58 with +-50% spread
-        g = rng(seed, w.name, "scales", layer, device=device)
-        base = std / 0.58
-        out["s_gate_up"] = (torch.rand(E, 2 * F, generator=g, device=device) + 0.5) * base
-        out["s_down"] = (torch.rand(E, d, generator=g, device=device) + 0.5) * base
+        out["w_gate_up"], out["s_gate_up"] = make_fp8_weights(
+            (E, 2 * F, d), std, rng(seed, w.name, "wgu", layer, device=device), device)
+        out["w_down"], out["s_down"] = make_fp8_weights(
+            (E, d, F), std, rng(seed, w.name, "wd", layer, device=device), device)
     else:
         edt = torch_dtype(w.expert_dtype)
         out["w_gate_up"] = _normal((E, 2 * F, d), std, rng(seed, w.name, "wgu", layer, device=device), device, edt)
