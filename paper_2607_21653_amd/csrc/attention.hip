@@ -3,9 +3,10 @@
 // R = G*(1+k) query rows (G = Hq/Hkv query heads, 1+k positions) share every key/value
 // block, so each K/V byte is read once per (b, h) and reused by all R rows on MFMA.
 //
-// Work split: workgroup = (b, h, query tile, split of the key range), 4 wavefronts. A query
-// tile holds all R rows when R <= 128 (the verify step); longer windows (prefill) are cut
-// into tiles of floor(64 / G) positions, each reading the keys its last position sees.
+// Work split: workgroup = (b, h, query tile, split of the key range), 4 wavefronts for up to
+// 64 rows, 8 for up to 128 (one 16-row tile per wavefront either way). A query tile holds
+// all R rows when R <= 128 (the verify step); longer windows (prefill) are cut into tiles
+// of floor(128 / G) positions, each reading the keys its last position sees.
 // The number of splits is chosen so the grid holds ~512 workgroups (at B*Hkv*tiles >= 512
 // there is no split and no merge pass) and no split exceeds 2048 blocks. The wavefronts split the R query rows and
 // share every 32-key block pair through a double-buffered LDS ring (details at the kernel).
@@ -26,8 +27,6 @@
 namespace molt {
 namespace {
 
-constexpr int kThreads = 256;
-constexpr int kWaves = 4;
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kNegBig = -1.0e30f;   // finite "minus infinity" for running maxima
 constexpr float kRescaleSlack = 8.0f; // probabilities may grow to 2^8 before O is rescaled
@@ -55,12 +54,15 @@ MOLT_DEV long out_index(const AttnParams& p, long t, long c, long cols, int esiz
 }
 
 // ---------------------------------------------------------------- MFMA kernel
-// Workgroup = (b, h, split), 4 wavefronts that split the R query rows (wavefront w owns
-// row tiles w and w + 4) and share every 32-key block pair through LDS: per pair the 256
-// threads copy its K and V blocks (4 x 16 D bytes) with coalesced 16-byte loads, kept
-// kDepth pairs ahead in registers, into a double-buffered ring; one LDS-only barrier per
-// pair. Each wavefront keeps only its own rows' Q fragments and O accumulator, so a
-// workgroup needs few registers and two fit per CU; no cross-wavefront merge at the end.
+// Workgroup = (b, h, query tile, split), NW wavefronts that split the query rows (wavefront
+// w owns the 16-row tile w) and share every 32-key block pair through LDS: per pair the
+// 64 NW threads copy its K and V blocks (4 x 16 D bytes) with coalesced 16-byte loads,
+// kept kDepth pairs ahead in registers, into a double-buffered ring; one LDS-only barrier
+// per pair. Each wavefront keeps only its own rows' Q fragments and O accumulator (about
+// 210 registers: two wavefronts per SIMD, i.e. two 4-wavefront or one 8-wavefront
+// workgroup per CU); no cross-wavefront merge at the end. Holding two row tiles per
+// wavefront instead (334 registers) left one wavefront per SIMD, which could not hide the
+// per-pair latency chain (72 rows at context 2048: 36% of HBM bandwidth).
 // Key order inside a pair for the MFMA k-index: lane group g (of 4) holds keys
 // 8 (g % 2) .. +7 of block g / 2. S^T MFMA t (t = 0, 1) computes rows m = 4 g + i for keys
 // 8 (g % 2) + 4 t + i of block g / 2, so the 8 scores of a lane are those 8 contiguous keys
@@ -74,13 +76,16 @@ MOLT_DEV int kswz(int key, int blk) {
 }
 MOLT_DEV int vswz(int dim) { return ((dim >> 2) ^ (dim >> 3)) & 1; }
 
-template <int D, int RTW>
-__global__ __launch_bounds__(kThreads) void attn_lds_kernel(AttnParams p) {
+template <int D, int NW>
+__global__ __launch_bounds__(64 * NW) void attn_lds_kernel(AttnParams p) {
+  constexpr int kThreads = 64 * NW;
+  constexpr int RTW = 1;                // 16-row tiles per wavefront
   constexpr int DS = D / 32;            // 32-dim k-steps for S
   constexpr int DT = D / 16;            // 16-dim tiles of O^T
   constexpr int KB = 16 * D * 2;        // bytes of one K (or V) block
   constexpr int PAIR = 4 * KB;          // K0, K1, V0, V1
   constexpr int CPT = PAIR / 16 / kThreads;   // 16-byte chunks per thread per pair
+  static_assert(CPT >= 1 && CPT * 16 * kThreads == PAIR, "chunks per thread");
   constexpr int kDepth = 6;             // pairs loaded ahead into registers
   __shared__ __attribute__((aligned(16))) uint8_t lds[2][PAIR];
 
@@ -105,12 +110,12 @@ __global__ __launch_bounds__(kThreads) void attn_lds_kernel(AttnParams p) {
   const int l16 = lane % 16, g4 = lane / 16;
   const float c = p.scale_log2;
 
-  // Q^T fragments of the wavefront's rows r = 16 (wave + 4 i) + l16, dims [32 s + 8 g4, +8)
+  // Q^T fragments of the wavefront's rows r = 16 (wave + NW i) + l16, dims [32 s + 8 g4, +8)
   bf16x8_t qf[RTW][DS];
   int lim[RTW];
 #pragma unroll
   for (int i = 0; i < RTW; ++i) {
-    const int r = 16 * (wave + 4 * i) + l16;     // row of the tile
+    const int r = 16 * (wave + NW * i) + l16;    // row of the tile
     const int j = j0 + r / G, gi = r % G;
     lim[i] = r < Rt ? ctx + j : -1;
 #pragma unroll
@@ -140,53 +145,46 @@ __global__ __launch_bounds__(kThreads) void attn_lds_kernel(AttnParams p) {
   for (int i = threadIdx.x; i < blk1 - blk0; i += kThreads) s_bt[i] = btab[blk0 + i];
   __syncthreads();
   const long kv_blk_stride = long(p.Hkv) * 16 * D;    // elements per physical block
-  // staging: thread t copies 16-byte chunk t (and t + 256 for D = 64) of each of the 4
-  // blocks K0, K1, V0, V1; the K (V) chunks of the two blocks sit at the same offsets
-  static_assert(KB / 16 == kThreads || KB / 16 == kThreads / 2, "chunks per block");
-  constexpr int CPB = CPT / 4 > 0 ? CPT / 4 : 1;      // chunks per thread per block (D=128: 1)
-  int k_src[CPB], v_src[CPB], k_dst[CPB], v_dst[CPB];
-  bool has[CPB];
+  // staging: the pair's 4 KB / 16 chunks per block (K0, K1, V0, V1 in that order) are
+  // numbered c = 0 .. PAIR / 16 - 1; thread t copies chunks t + kThreads u, u < CPT, each from
+  // its block (q = c / (KB / 16)) to its swizzled LDS place
+  int src_off[CPT], dst_off[CPT];
+  bool from_v[CPT], second[CPT];
 #pragma unroll
-  for (int u = 0; u < CPB; ++u) {
-    const int chu = threadIdx.x + kThreads * u;
-    has[u] = chu < KB / 16;
-    const int ch = chu % (KB / 16);                    // chunk inside a block (threads past the
-                                                       // block's chunks re-load one, store none)
-    const int key = ch / (D / 8), kc = ch % (D / 8);
-    k_src[u] = (h * 16 + key) * D + kc * 8;
-    k_dst[u] = key * (2 * D) + ((kc ^ kswz<D>(key, 0)) * 16);
-    const int dim = ch / 2, vc = ch % 2;
-    v_src[u] = (h * D + dim) * 16 + vc * 8;
-    v_dst[u] = dim * 32 + ((vc ^ vswz(dim)) * 16);
+  for (int u = 0; u < CPT; ++u) {
+    const int c = threadIdx.x + kThreads * u;
+    const int q = c / (KB / 16), ch = c % (KB / 16);
+    from_v[u] = q >= 2;
+    second[u] = q & 1;
+    if (!from_v[u]) {
+      const int key = ch / (D / 8), kc = ch % (D / 8);
+      src_off[u] = (h * 16 + key) * D + kc * 8;
+      dst_off[u] = q * KB + key * (2 * D) + ((kc ^ kswz<D>(key, q & 1)) * 16);
+    } else {
+      const int dim = ch / 2, vc = ch % 2;
+      src_off[u] = (h * D + dim) * 16 + vc * 8;
+      dst_off[u] = q * KB + dim * 32 + ((vc ^ vswz(dim)) * 16);
+    }
   }
-  // kswz depends on the block for D = 128 (bit 3): K1's chunk index is XORed with 8
-  int32x4_t st[kDepth][4 * CPB];
+  int32x4_t st[kDepth][CPT];
   // The split's block-table entries are read from LDS: a global load of them, issued behind
   // the K/V prefetches, would have its wait drain every load in flight (the vector memory
   // counter retires in order).
-  auto gload = [&](int32x4_t (&dst)[4 * CPB], int pi) __attribute__((always_inline)) {
+  auto gload = [&](int32x4_t (&dst)[CPT], int pi) __attribute__((always_inline)) {
     const int rel = 2 * min(pi, npairs - 1);
     const long phys0 = s_bt[rel];
     const long phys1r = s_bt[min(rel + 1, blk1 - blk0 - 1)];
     const long phys1 = blk0 + rel + 1 < blk1 ? phys1r : phys0;
 #pragma unroll
-    for (int u = 0; u < CPB; ++u) {
-      dst[4 * u + 0] = __builtin_nontemporal_load(reinterpret_cast<const int32x4_t*>(p.kc + phys0 * kv_blk_stride + k_src[u]));
-      dst[4 * u + 1] = __builtin_nontemporal_load(reinterpret_cast<const int32x4_t*>(p.kc + phys1 * kv_blk_stride + k_src[u]));
-      dst[4 * u + 2] = __builtin_nontemporal_load(reinterpret_cast<const int32x4_t*>(p.vc + phys0 * kv_blk_stride + v_src[u]));
-      dst[4 * u + 3] = __builtin_nontemporal_load(reinterpret_cast<const int32x4_t*>(p.vc + phys1 * kv_blk_stride + v_src[u]));
+    for (int u = 0; u < CPT; ++u) {
+      const uint16_t* base = from_v[u] ? p.vc : p.kc;
+      dst[u] = __builtin_nontemporal_load(reinterpret_cast<const int32x4_t*>(
+          base + (second[u] ? phys1 : phys0) * kv_blk_stride + src_off[u]));
     }
   };
-  auto sstore = [&](const int32x4_t (&src)[4 * CPB], int buf) __attribute__((always_inline)) {
+  auto sstore = [&](const int32x4_t (&src)[CPT], int buf) __attribute__((always_inline)) {
 #pragma unroll
-    for (int u = 0; u < CPB; ++u) {
-      if (!has[u]) continue;
-      uint8_t* base = lds[buf];
-      *reinterpret_cast<int32x4_t*>(base + k_dst[u]) = src[4 * u + 0];
-      *reinterpret_cast<int32x4_t*>(base + KB + (D == 128 ? (k_dst[u] ^ 128) : k_dst[u])) = src[4 * u + 1];
-      *reinterpret_cast<int32x4_t*>(base + 2 * KB + v_dst[u]) = src[4 * u + 2];
-      *reinterpret_cast<int32x4_t*>(base + 3 * KB + v_dst[u]) = src[4 * u + 3];
-    }
+    for (int u = 0; u < CPT; ++u) *reinterpret_cast<int32x4_t*>(lds[buf] + dst_off[u]) = src[u];
   };
 
   // K fragment: block j = l16 / 8, key 8 ((l16 / 4) % 2) + 4 t + l16 % 4 (the swizzle is the
@@ -314,7 +312,7 @@ __global__ __launch_bounds__(kThreads) void attn_lds_kernel(AttnParams p) {
     float lt = l_run[i];
     lt += __shfl_xor(lt, 16, kWave);
     lt += __shfl_xor(lt, 32, kWave);
-    const int r = 16 * (wave + 4 * i) + l16;
+    const int r = 16 * (wave + NW * i) + l16;
     if (r >= Rt) continue;
     const int j = j0 + r / G, gi = r % G;
     // O^T element e of tile dt: dim 16 dt + 4 g4 + e
@@ -441,8 +439,8 @@ template <int D>
 hipError_t launch_d(const AttnParams& p, int B, int R, hipStream_t s) {
   const int Rt = (p.Hq / p.Hkv) * p.tq;     // rows of a query tile
   const long grid = long(B) * p.Hkv * p.qtiles * p.splits;
-  if (Rt <= 64) attn_lds_kernel<D, 1><<<grid, kThreads, 0, s>>>(p);
-  else attn_lds_kernel<D, 2><<<grid, kThreads, 0, s>>>(p);
+  if (Rt <= 64) attn_lds_kernel<D, 4><<<grid, 256, 0, s>>>(p);
+  else attn_lds_kernel<D, 8><<<grid, 512, 0, s>>>(p);
   if (p.splits > 1) attn_merge_kernel<D><<<B * p.Hkv * R, D, 0, s>>>(p, 0);
   return hipGetLastError();
 }
@@ -450,12 +448,10 @@ hipError_t launch_d(const AttnParams& p, int B, int R, hipStream_t s) {
 }  // namespace
 
 // Query tiles of (b, h): all G(1+k) rows in one tile when they fit in 128 (every key and
-// value read once), else tiles of floor(64 / G) positions (at least one): a 128-row tile
-// takes 334 registers per lane, one workgroup per CU; a 256-position window at context
-// 8192 (G = 8) took 135 us in such tiles and 112 us in 64-row ones, which read the keys
-// twice as often (mostly from L2/MALL).
+// value read once), else tiles of floor(128 / G) positions (at least one), each read by an
+// 8-wavefront workgroup.
 static void qtile_plan(int G, int kp1, int& qtiles, int& tq) {
-  tq = G * kp1 <= 128 ? kp1 : (G <= 64 ? 64 / G : 1);
+  tq = G * kp1 <= 128 ? kp1 : (G <= 128 ? 128 / G : 1);
   qtiles = (kp1 + tq - 1) / tq;
 }
 
