@@ -14,8 +14,13 @@
 //   S^T[32 keys x 16 rows] = K Q^T   (A = K rows from LDS, B = Q^T held in registers)
 //   O^T[D x 16 rows]      += V^T P^T (A = V^T: the V cache stores a block as [D][16 tokens],
 //                                    so 8 consecutive keys of one dim are 16 contiguous
-//                                    bytes; B = P^T is the S^T accumulator layout rounded to
-//                                    bf16: no cross-lane shuffles)
+//                                    bytes; B = P^T is the S^T accumulator layout: no
+//                                    cross-lane shuffles)
+// P is split into two bf16 parts, hi = bf16(p) and lo = bf16(p - hi) (16 significant bits),
+// and V^T P^T takes one MFMA per part, so the output is the f32 softmax product up to
+// accumulation order. With P rounded to bf16 alone (one MFMA) the end-to-end logits of a
+// 2-layer bf16 step moved by up to 1.7e-2 against the exact product (the final RMSNorm
+// scales up the residual differences that bf16 flips of the attention output leave).
 // Causality: row r = j*G + g (position j) sees keys <= ctx_b + j; only pairs reaching past
 // ctx_b need masks. Softmax in f32 with exp2 of log2(e)-scaled scores; the output is
 // rescaled lazily, only when a row maximum grows by more than 8 (in log2 units) over the
@@ -251,7 +256,7 @@ __global__ __launch_bounds__(64 * NW) void attn_lds_kernel(AttnParams p) {
         for (int dt = 0; dt < DT; ++dt) o[dt][i] *= alpha;
       }
     }
-    bf16x8_t pf[RTW];
+    bf16x8_t pf[RTW], pl[RTW];   // P = hi + lo
 #pragma unroll
     for (int i = 0; i < RTW; ++i) {
       const float nm = -m_run[i];
@@ -260,9 +265,11 @@ __global__ __launch_bounds__(64 * NW) void attn_lds_kernel(AttnParams p) {
       for (int t = 0; t < 2; ++t)
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          const __bf16 w = __bf16(exp2f(fmaf(sv[t][i][e], c, nm)));
-          pf[i][t * 4 + e] = w;
-          ps += float(w);   // the normaliser sums the same rounded weights the MFMA uses
+          const float w = exp2f(fmaf(sv[t][i][e], c, nm));
+          const __bf16 hi = __bf16(w);
+          pf[i][t * 4 + e] = hi;
+          pl[i][t * 4 + e] = __bf16(w - float(hi));   // w - hi is exact in f32
+          ps += w;
         }
       l_run[i] += ps;
     }
@@ -270,7 +277,10 @@ __global__ __launch_bounds__(64 * NW) void attn_lds_kernel(AttnParams p) {
     for (int dt = 0; dt < DT; ++dt) {
       const bf16x8_t vf = *reinterpret_cast<const bf16x8_t*>(base + voff + dt * 16 * 32);
 #pragma unroll
-      for (int i = 0; i < RTW; ++i) o[dt][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[i], o[dt][i], 0, 0, 0);
+      for (int i = 0; i < RTW; ++i) {
+        o[dt][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[i], o[dt][i], 0, 0, 0);
+        o[dt][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pl[i], o[dt][i], 0, 0, 0);
+      }
     }
   };
 

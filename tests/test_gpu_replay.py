@@ -3,7 +3,7 @@
 * the consistency diagnostic: after a GPU verify step, scoring its tokens with its emitted
   tokens as targets and its recorded routes as replay reproduces the recorded logits and
   behavior log-probabilities bit for bit (NaN past each sequence's emitted token);
-* against the oracle (oracle/replay.py): log-probs within 1e-4 (f32) / 5e-2 (bf16: logits
+* against the oracle (oracle/replay.py): log-probs within 1e-4 (f32) / 4e-2 (bf16: logits
   within 2e-2 move (l_y - m) - ln S by at most twice that), with the router's own routes
   and with foreign replayed routes (every expert id shifted), where the routes used must be
   exactly the replayed ones."""
@@ -63,7 +63,7 @@ def test_recompute_reproduces_verify_and_oracle(molt_lib, wname):
     print(f"recompute == verify: {emitted.sum()} emitted tokens bit-exact", flush=True)
     # against the oracle, with the GPU's routes replayed on both sides (the routes are then
     # the same by construction) and with foreign routes
-    tol = 1e-4 if w.dtype == "f32" else 5e-2
+    tol = 1e-4 if w.dtype == "f32" else 2 * 2e-2
     targets = np.roll(toks, -1, axis=1)
     targets[:, -1] = v["tokens"].cpu().numpy()[np.arange(w.batch), v["n_accepted"].cpu().numpy()]
     routes = v["routes"].cpu().numpy()

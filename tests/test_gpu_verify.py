@@ -167,11 +167,13 @@ def test_bf16_full_step_small_vocab(molt_lib):
     """Whole bf16 verify step (2 layers of the 35B-A3B-like shape, vocab 4096) against the
     oracle for sequences whose routes are clear.
 
-    Teacher-forced (each layer, and the final norm + LM head, given the GPU's own input):
-    within the 2e-2 logit bar. End to end: within 3e-2, 1.5x the measured noise floor of
-    this composition (perturbing every value the oracle rounds to bf16 by 1e-6 relative,
-    the size of f32-versus-f64 accumulation differences, moves the oracle's own logits by up
-    to 1.8e-2 here: bf16 rounding-boundary flips carried through two layers)."""
+    End to end and teacher-forced (each layer, and the final norm + LM head, given the
+    GPU's own input): within the 2e-2 logit bar. The composition's own noise floor is close
+    to it: computing only the attention scores and probabilities in f32 instead of f64 moves
+    the oracle's logits by 1.1e-2 here (bf16 flips of the attention output reach the
+    residual stream through the O projection, and the final RMSNorm scales the residual
+    differences up), and rounding the attention probabilities to bf16 moves them by 1.7e-2,
+    which is why the attention kernel keeps them to 16 bits (hi + lo)."""
     w = workloads.LAYER_BF16.scaled(n_layers=2, vocab=4096, batch=3, k=4, ctx_lo=30, ctx_hi=90,
                                     full_model=True)
     cfg = oracle_cfg(w)
@@ -209,7 +211,7 @@ def test_bf16_full_step_small_vocab(molt_lib):
     err = max_abs(logits[ok], o["logits"][ok])
     print(f"end to end: max |logits - oracle| = {err:.3e} over {ok.sum()} of {w.batch} sequences",
           flush=True)
-    assert err <= 3e-2
+    assert err <= 2e-2
     # teacher-forced: layer by layer on the GPU (one-layer models over the same caches), each
     # checked against the oracle's layer applied to the GPU's own input
     kv = fresh_kv()
