@@ -79,6 +79,85 @@ MOLT_DEV void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" :
 
 // ---------------------------------------------------------------- reductions
 
+// Wavefront all-reductions on DPP: an inclusive scan along each 16-lane row (row_shr 1, 2,
+// 4, 8), then the rows combined by row_bcast15 (rows 1 and 3) and row_bcast31 (rows 2 and
+// 3), so lane 63 ends with the whole wavefront's result, read back wave-uniform. A lane
+// whose DPP source lies outside its row (or whose row is masked off) takes the identity.
+// Each step is a register move with a few cycles of latency, where a __shfl_xor step is a
+// permute through the LDS crossbar.
+template <int CTRL, int ROWS>
+MOLT_DEV uint32_t dpp_u32(uint32_t v, uint32_t ident) {
+  return uint32_t(__builtin_amdgcn_update_dpp(int(ident), int(v), CTRL, ROWS, 0xF, false));
+}
+
+template <int CTRL, int ROWS>
+MOLT_DEV unsigned long long dpp_max_step(unsigned long long v) {
+  const uint32_t lo = dpp_u32<CTRL, ROWS>(uint32_t(v), 0u);
+  const uint32_t hi = dpp_u32<CTRL, ROWS>(uint32_t(v >> 32), 0u);
+  const unsigned long long o = (static_cast<unsigned long long>(hi) << 32) | lo;
+  return o > v ? o : v;
+}
+
+template <int CTRL, int ROWS>
+MOLT_DEV float dpp_max_step(float v) {
+  return fmaxf(v, __uint_as_float(dpp_u32<CTRL, ROWS>(__float_as_uint(v), 0xff800000u)));
+}
+
+template <int CTRL, int ROWS>
+MOLT_DEV float dpp_sum_step(float v) {
+  return v + __uint_as_float(dpp_u32<CTRL, ROWS>(__float_as_uint(v), 0u));
+}
+
+MOLT_DEV uint32_t lane63(uint32_t v) { return uint32_t(__builtin_amdgcn_readlane(int(v), 63)); }
+
+template <int CTRL, int ROWS>
+MOLT_DEV int dpp_add_step(int v) {
+  return v + int(dpp_u32<CTRL, ROWS>(uint32_t(v), 0u));
+}
+
+// inclusive prefix sum over the lanes (lane i gets lanes 0..i): the same DPP steps, every
+// lane keeping its partial result
+MOLT_DEV int wave_scan_dpp(int v) {
+  v = dpp_add_step<0x111, 0xF>(v);
+  v = dpp_add_step<0x112, 0xF>(v);
+  v = dpp_add_step<0x114, 0xF>(v);
+  v = dpp_add_step<0x118, 0xF>(v);
+  v = dpp_add_step<0x142, 0xA>(v);
+  v = dpp_add_step<0x143, 0xC>(v);
+  return v;
+}
+
+// unsigned 64-bit maximum over the wavefront (every lane gets it)
+MOLT_DEV unsigned long long wave_max_dpp(unsigned long long v) {
+  v = dpp_max_step<0x111, 0xF>(v);
+  v = dpp_max_step<0x112, 0xF>(v);
+  v = dpp_max_step<0x114, 0xF>(v);
+  v = dpp_max_step<0x118, 0xF>(v);
+  v = dpp_max_step<0x142, 0xA>(v);
+  v = dpp_max_step<0x143, 0xC>(v);
+  return (static_cast<unsigned long long>(lane63(uint32_t(v >> 32))) << 32) | lane63(uint32_t(v));
+}
+
+MOLT_DEV float wave_max_dpp(float v) {
+  v = dpp_max_step<0x111, 0xF>(v);
+  v = dpp_max_step<0x112, 0xF>(v);
+  v = dpp_max_step<0x114, 0xF>(v);
+  v = dpp_max_step<0x118, 0xF>(v);
+  v = dpp_max_step<0x142, 0xA>(v);
+  v = dpp_max_step<0x143, 0xC>(v);
+  return __uint_as_float(lane63(__float_as_uint(v)));
+}
+
+MOLT_DEV float wave_sum_dpp(float v) {
+  v = dpp_sum_step<0x111, 0xF>(v);
+  v = dpp_sum_step<0x112, 0xF>(v);
+  v = dpp_sum_step<0x114, 0xF>(v);
+  v = dpp_sum_step<0x118, 0xF>(v);
+  v = dpp_sum_step<0x142, 0xA>(v);
+  v = dpp_sum_step<0x143, 0xC>(v);
+  return __uint_as_float(lane63(__float_as_uint(v)));
+}
+
 MOLT_DEV float wave_max(float v) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, kWave));

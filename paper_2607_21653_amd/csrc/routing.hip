@@ -6,7 +6,8 @@
 // (E <= 256) as 64-bit keys: order-preserving f32 bits (with -0 folded into +0) in
 // the high word, 0xFFFFFFFF - expert id in the low word, so the maximum key is the
 // largest logit with ties resolved to the lower expert id. K rounds of a wavefront
-// max-reduction select the experts in descending order.
+// max-reduction (DPP: with LDS-crossbar shuffles the K rounds were one long chain of
+// permute round trips) select the experts in descending order.
 //
 // permute_kernel: one 1024-thread workgroup, one pass over the ids. Wavefront w owns a
 // contiguous range of the T*K pairs (in (token, slot) order) and visits it 64 pairs at a
@@ -41,15 +42,6 @@ MOLT_DEV unsigned long long route_key(float v, int e) {
 MOLT_DEV float key_value(unsigned long long key) {
   const uint32_t ord = uint32_t(key >> 32);
   return __uint_as_float((ord >> 31) ? (ord & 0x7fffffffu) : ~ord);
-}
-
-MOLT_DEV unsigned long long wave_max_u64(unsigned long long v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
-    unsigned long long w = __shfl_xor(v, o, kWave);
-    v = w > v ? w : v;
-  }
-  return v;
 }
 
 __global__ __launch_bounds__(256) void topk_kernel(const float* __restrict__ logits, int nparts,
@@ -91,7 +83,7 @@ __global__ __launch_bounds__(256) void topk_kernel(const float* __restrict__ log
 #pragma unroll
       for (int i = 1; i < 4; ++i)
         if (key[i] > mine) { mine = key[i]; which = i; }
-      const unsigned long long best = wave_max_u64(mine);
+      const unsigned long long best = wave_max_dpp(mine);
       if (mine == best && best != 0ull) key[which] = 0ull;   // the unique owner drops it
       if (lane == j) {
         // the key holds the logit's order-preserving bits: decode instead of re-reading
@@ -101,9 +93,9 @@ __global__ __launch_bounds__(256) void topk_kernel(const float* __restrict__ log
     }
   }
   // softmax over the K selected logits
-  const float m = wave_max(lane < K ? sel_v : -INFINITY);
+  const float m = wave_max_dpp(lane < K ? sel_v : -INFINITY);
   const float ex = lane < K ? expf(sel_v - m) : 0.f;
-  const float sum = wave_sum(ex);
+  const float sum = wave_sum_dpp(ex);
   if (lane < K) {
     ids[long(t) * K + lane] = sel_e;
     w[long(t) * K + lane] = ex / sum;
@@ -174,13 +166,17 @@ __global__ __launch_bounds__(kPermThreads) void permute_kernel(
     }
   }
   __syncthreads();
-  // per expert: exclusive prefix of the wavefront counts, and the total
+  // per expert: exclusive prefix of the wavefront counts (all 16 read before any write),
+  // and the total
   if (tid < kMaxE) {
+    int c[kPermWaves];
+#pragma unroll
+    for (int w2 = 0; w2 < kPermWaves; ++w2) c[w2] = wc[w2][tid];
     int run = 0;
+#pragma unroll
     for (int w2 = 0; w2 < kPermWaves; ++w2) {
-      const int c = wc[w2][tid];
       wc[w2][tid] = run;
-      run += c;
+      run += c[w2];
     }
     cnt[tid] = tid < E ? run : 0;
   }
@@ -193,11 +189,7 @@ __global__ __launch_bounds__(kPermThreads) void permute_kernel(
     int v[3] = {c, (c + 31) / 32 * 32, (c + tile_m - 1) / tile_m};
 #pragma unroll
     for (int q = 0; q < 3; ++q) {
-#pragma unroll
-      for (int o = 1; o < kWave; o <<= 1) {
-        const int u = __shfl_up(v[q], o, kWave);
-        if (lane >= o) v[q] += u;
-      }
+      v[q] = wave_scan_dpp(v[q]);
       if (lane == kWave - 1) wsum[q][wave] = v[q];
     }
     wtmp[0][tid] = v[0];
