@@ -1,8 +1,10 @@
 """GPU parity of molt_paged_attention (MFMA multi-query decode attention over shuffled
 paged blocks with split-KV merge) against the oracle's float64 paged attention: bf16
-within 1e-2 max-abs (probabilities are rounded to bf16 for the MFMA, outputs to bf16),
-f32 within 1e-5; ragged contexts, one-key and empty-context edges, k = 0, 8 drafts
-(72 query rows), head dim 64, many splits; prefill windows longer than one 128-row query
+within 1e-2 max-abs (outputs are rounded to bf16), f32 within 1e-5; ragged contexts,
+one-key and empty-context edges, k = 0, 8 drafts (72 query rows, also ragged with splits),
+9 drafts with many splits and 11 (96 rows) on the 8-wavefront tiles, head dim 64, many
+splits; prefill
+windows longer than one 128-row query
 tile (64, 41, 101 and 256 positions: several tiles, a partial last tile, tiles with splits,
 an empty cached context); shuffled and contiguous block tables give bit-identical
 outputs."""
@@ -44,6 +46,9 @@ def _gpu(molt, w, layout, kc, vc, q, bt=None):
 @pytest.mark.parametrize("B,k,Hq,Hkv,D,lo,hi", [
     (3, 4, 32, 4, 128, 1, 3000),        # ragged, several splits
     (2, 8, 32, 4, 128, 900, 2100),      # 72 query rows
+    (3, 8, 32, 4, 128, 1, 3000),        # 72 rows, ragged, splits
+    (1, 9, 32, 4, 128, 9000, 9000),     # 80 rows, many splits
+    (2, 11, 32, 4, 128, 300, 2500),     # 96 rows
     (4, 0, 32, 4, 128, 0, 40),          # plain decode, empty context allowed
     (2, 3, 8, 2, 64, 200, 1500),        # head dim 64
     (1, 4, 32, 4, 128, 9000, 9000),     # 9 splits
