@@ -206,6 +206,32 @@ MOLT_DEV T block_sum(T v, T* red) {
   return r;
 }
 
+// the same over NW wavefronts, each wavefront's share reduced on DPP
+template <int NW>
+MOLT_DEV float block_sum_dpp(float v, float* red) {
+  v = wave_sum_dpp(v);
+  const int w = threadIdx.x / kWave, l = threadIdx.x % kWave;
+  __syncthreads();
+  if (l == 0) red[w] = v;
+  __syncthreads();
+  float r = red[0];
+#pragma unroll
+  for (int i = 1; i < NW; ++i) r += red[i];   // fixed order: deterministic
+  return r;
+}
+template <int NW>
+MOLT_DEV float block_max_dpp(float v, float* red) {
+  v = wave_max_dpp(v);
+  const int w = threadIdx.x / kWave, l = threadIdx.x % kWave;
+  __syncthreads();
+  if (l == 0) red[w] = v;
+  __syncthreads();
+  float r = red[0];
+#pragma unroll
+  for (int i = 1; i < NW; ++i) r = fmaxf(r, red[i]);
+  return r;
+}
+
 MOLT_DEV float silu(float x) { return x / (1.0f + expf(-x)); }
 
 // ---------------------------------------------------------------- tiled operand layout

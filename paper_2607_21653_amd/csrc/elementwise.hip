@@ -87,7 +87,7 @@ __global__ __launch_bounds__(kThreads) void residual_norm_kernel(
     for (int e = 0; e < 8; ++e) ss += v[r][e] * v[r][e];
   }
   if (g == nullptr) return;
-  ss = block_sum<kThreads / kWave, float>(ss, red);
+  ss = block_sum_dpp<kThreads / kWave>(ss, red);
   const float rs = 1.0f / sqrtf(ss / float(d) + eps);
   float amax = 0.f;
 #pragma unroll
@@ -120,7 +120,7 @@ __global__ __launch_bounds__(kThreads) void residual_norm_kernel(
     }
   }
   if (yq == nullptr) return;
-  amax = block_max<kThreads / kWave>(amax, red);
+  amax = block_max_dpp<kThreads / kWave>(amax, red);
   const float sc = amax / 448.0f;
 #pragma unroll
   for (int r = 0; r < kNormRuns; ++r) {
@@ -297,7 +297,7 @@ MOLT_DEV void norm_half_store(float (&v)[kNormRuns][8], const float* __restrict_
 #pragma unroll
     for (int e = 0; e < 8; ++e) ss += v[r][e] * v[r][e];
   }
-  ss = block_sum<kThreads / kWave, float>(ss, red);
+  ss = block_sum_dpp<kThreads / kWave>(ss, red);
   const float rs = 1.0f / sqrtf(ss / float(d) + eps);
   const long es = dt == MOLT_BF16 ? 2 : 4, rb = 2L * d * es;
 #pragma unroll
