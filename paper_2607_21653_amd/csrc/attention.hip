@@ -82,7 +82,7 @@ MOLT_DEV int kswz(int key, int blk) {
 MOLT_DEV int vswz(int dim) { return ((dim >> 2) ^ (dim >> 3)) & 1; }
 
 template <int D, int NW>
-__global__ __launch_bounds__(64 * NW) void attn_lds_kernel(AttnParams p) {
+__global__ __launch_bounds__(64 * NW, NW == 8 ? 2 : 1) void attn_lds_kernel(AttnParams p) {
   constexpr int kThreads = 64 * NW;
   constexpr int RTW = 1;                // 16-row tiles per wavefront
   constexpr int DS = D / 32;            // 32-dim k-steps for S
@@ -91,7 +91,9 @@ __global__ __launch_bounds__(64 * NW) void attn_lds_kernel(AttnParams p) {
   constexpr int PAIR = 4 * KB;          // K0, K1, V0, V1
   constexpr int CPT = PAIR / 16 / kThreads;   // 16-byte chunks per thread per pair
   static_assert(CPT >= 1 && CPT * 16 * kThreads == PAIR, "chunks per thread");
-  constexpr int kDepth = 6;             // pairs loaded ahead into registers
+  // pairs loaded ahead into registers: 8-wavefront workgroups hold 3, which keeps them at
+  // 122 registers, so two fit per CU (6 pairs in flight per CU either way)
+  constexpr int kDepth = NW == 8 ? 3 : 6;
   __shared__ __attribute__((aligned(16))) uint8_t lds[2][PAIR];
 
   const int split = blockIdx.x % p.splits;
@@ -295,21 +297,24 @@ __global__ __launch_bounds__(64 * NW) void attn_lds_kernel(AttnParams p) {
 #pragma unroll
     for (int u = 1; u <= kDepth; ++u) gload(st[u % kDepth], u);
     lds_barrier();
+    // pair p sits in LDS buffer p % 2 (kDepth may be odd, so the parity comes from pi)
     int pi = 0;
     for (; pi + kDepth - 1 < npairs; pi += kDepth) {
+      const int par = pi & 1;
 #pragma unroll
       for (int u = 0; u < kDepth; ++u) {
-        sstore(st[(u + 1) % kDepth], 1 - u % 2);
+        sstore(st[(u + 1) % kDepth], 1 - (par ^ (u & 1)));
         gload(st[(u + 1) % kDepth], pi + u + 1 + kDepth);
-        compute(u % 2, pi + u);
+        compute(par ^ (u & 1), pi + u);
         lds_barrier();
       }
     }
+    const int par = pi & 1;
 #pragma unroll
     for (int u = 0; u < kDepth - 1; ++u) {
       if (pi + u < npairs) {
-        sstore(st[(u + 1) % kDepth], 1 - u % 2);
-        compute(u % 2, pi + u);
+        sstore(st[(u + 1) % kDepth], 1 - (par ^ (u & 1)));
+        compute(par ^ (u & 1), pi + u);
         lds_barrier();
       }
     }
