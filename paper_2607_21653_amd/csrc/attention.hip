@@ -3,10 +3,10 @@
 // R = G*(1+k) query rows (G = Hq/Hkv query heads, 1+k positions) share every key/value
 // block, so each K/V byte is read once per (b, h) and reused by all R rows on MFMA.
 //
-// Work split: workgroup = (b, h, query tile, split of the key range), 4 wavefronts for up to
-// 64 rows, 8 for up to 128 (one 16-row tile per wavefront either way). A query tile holds
-// all R rows when R <= 128 (the verify step); longer windows (prefill) are cut into tiles
-// of floor(128 / G) positions, each reading the keys its last position sees.
+// Work split: workgroup = (b, h, query tile, split of the key range), 8 wavefronts (one
+// 16-row tile each; those without rows only load). A query tile holds all R rows when
+// R <= 128 (the verify step); longer windows (prefill) are cut into tiles of floor(128 / G)
+// positions, each reading the keys its last position sees.
 // The number of splits is chosen so the grid holds ~512 workgroups (at B*Hkv*tiles >= 512
 // there is no split and no merge pass) and no split exceeds 2048 blocks. The wavefronts split the R query rows and
 // share every 32-key block pair through a double-buffered LDS ring (details at the kernel).
@@ -63,11 +63,15 @@ MOLT_DEV long out_index(const AttnParams& p, long t, long c, long cols, int esiz
 // w owns the 16-row tile w) and share every 32-key block pair through LDS: per pair the
 // 64 NW threads copy its K and V blocks (4 x 16 D bytes) with coalesced 16-byte loads,
 // kept kDepth pairs ahead in registers, into a double-buffered ring; one LDS-only barrier
-// per pair. Each wavefront keeps only its own rows' Q fragments and O accumulator (about
-// 210 registers: two wavefronts per SIMD, i.e. two 4-wavefront or one 8-wavefront
-// workgroup per CU); no cross-wavefront merge at the end. Holding two row tiles per
-// wavefront instead (334 registers) left one wavefront per SIMD, which could not hide the
-// per-pair latency chain (72 rows at context 2048: 36% of HBM bandwidth).
+// per pair. Each wavefront keeps only its own rows' Q fragments and O accumulator; with 3
+// pairs in flight the 8-wavefront kernel takes 122 registers, so two workgroups (16
+// wavefronts, 6 pairs in flight) share a CU; no cross-wavefront merge at the end. The
+// kernel is bound by the latency of each wavefront's per-pair chain (counters: LDS active
+// ~25%, MFMA busy ~17% of cycles), so wavefronts per CU set its pace: at 72 rows and
+// context 2048 two row tiles per wavefront of 4 (334 registers, one wavefront per SIMD)
+// reached 36% of HBM bandwidth, one 8-wavefront workgroup per CU (6 pairs in flight)
+// 45%, two per CU 62%; at 40 rows two 4-wavefront workgroups per CU (6 pairs each) reached
+// 56-59% at contexts 4096-65536, two 8-wavefront ones 60-61%.
 // Key order inside a pair for the MFMA k-index: lane group g (of 4) holds keys
 // 8 (g % 2) .. +7 of block g / 2. S^T MFMA t (t = 0, 1) computes rows m = 4 g + i for keys
 // 8 (g % 2) + 4 t + i of block g / 2, so the 8 scores of a lane are those 8 contiguous keys
@@ -454,8 +458,8 @@ template <int D>
 hipError_t launch_d(const AttnParams& p, int B, int R, hipStream_t s) {
   const int Rt = (p.Hq / p.Hkv) * p.tq;     // rows of a query tile
   const long grid = long(B) * p.Hkv * p.qtiles * p.splits;
-  if (Rt <= 64) attn_lds_kernel<D, 4><<<grid, 256, 0, s>>>(p);
-  else attn_lds_kernel<D, 8><<<grid, 512, 0, s>>>(p);
+  (void)Rt;
+  attn_lds_kernel<D, 8><<<grid, 512, 0, s>>>(p);
   if (p.splits > 1) attn_merge_kernel<D><<<B * p.Hkv * R, D, 0, s>>>(p, 0);
   return hipGetLastError();
 }
