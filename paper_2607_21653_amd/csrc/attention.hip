@@ -440,7 +440,7 @@ __global__ __launch_bounds__(kWave) void attn_f32_kernel(const float* __restrict
 }
 
 // Splits of the key range: enough workgroups to fill the chip twice over (512), each split a
-// multiple of 8 blocks (4 wavefronts x one 32-key pair) and at least 32 blocks long.
+// multiple of 8 blocks and at least 32 blocks long.
 void split_plan(long units, int max_blocks, int& splits, int& bps) {
   const long pairs = units;
   int s = int((512 + pairs - 1) / pairs);
