@@ -1,7 +1,8 @@
 """GPU parity of molt_dense_gemm (the decoder's dense projections and LM head) against a
 float64 product of the same bf16/f32 operands: |C - ref| <= 1e-4 * sqrt(K) * max|a||b|
 (f32 accumulation), at the verify step's shapes and ragged row/column counts, with and
-without split-K."""
+without split-K, on the LDS-tiled kernel (also at the fp8 layer's 2304 rows) and on the
+big-tile one (the LM head)."""
 import numpy as np
 import pytest
 import torch
@@ -15,6 +16,10 @@ pytestmark = pytest.mark.gpu
     (77, 128, 2048, torch.bfloat16, False),     # router, 64-row tiles
     (25, 256, 2048, torch.bfloat16, False),     # 32-row tiles
     (640, 151936, 2048, torch.bfloat16, False), # LM head
+    (2304, 5120, 2048, torch.bfloat16, False),  # QKV at 2304 rows: 128-row tiles
+    (2304, 2048, 4096, torch.bfloat16, True),   # O at 2304 rows, accumulate
+    (1100, 2048, 4096, torch.bfloat16, True),   # ragged rows, accumulate
+    (1024, 1024, 1024, torch.bfloat16, False),
     (200, 131195, 512, torch.bfloat16, True),   # many columns: ragged rows and columns, accumulate
     (130, 131104, 192, torch.bfloat16, False),  # odd slice count
     (33, 200, 128, torch.bfloat16, False),      # N not a multiple of 128
