@@ -124,9 +124,14 @@ void stream_gemm_kernel(GemmParams p) {
   // weight slices in flight per wavefront (each 4 KB slice of a wavefront's 32 weight rows
   // is 16 registers; 8 in flight measured slower than 4)
   constexpr int WD = 4;
-  __shared__ __attribute__((aligned(16))) float upbuf[MODE == kGateUp ? BM * 64 : 1];
-  __shared__ __attribute__((aligned(16))) uint8_t alds[2][MS * 4096];
+  // activation staging: 2 buffers of MS 4 KB blocks; gate_up's epilogue reuses them, with
+  // the space after them, as a BM x 128 f32 tile (2 * BM * 256 bytes)
+  __shared__ __attribute__((aligned(16))) uint8_t smem[(MODE == kGateUp ? 4 : 2) * MS * 4096];
+  uint8_t (*alds)[MS * 4096] = reinterpret_cast<uint8_t (*)[MS * 4096]>(smem);
   __shared__ int prow[MODE == kDown ? BM : 1];       // down: pair index of each tile row
+  // down epilogue: the tile's outputs (BM x 128 f32; 128-row tiles in two 64-column passes)
+  constexpr int kEpCols = BM == 128 ? 64 : 128;
+  __shared__ __attribute__((aligned(16))) float dep[MODE == kDown ? BM * kEpCols : 1];
   const int total = *p.n_tiles_live * p.n_ntiles;
   const int chunk = (total + 7) / 8;
   const int stride = gridDim.x / 8;
@@ -184,6 +189,8 @@ void stream_gemm_kernel(GemmParams p) {
       MOLT_GLOAD(st1, g, 1);
 #pragma unroll
       for (int s = 0; s < WD; ++s) wld(wb[s], g, s);
+      // gate_up: every wavefront is done reading the last tile's epilogue tile from LDS
+      if (MODE == kGateUp && k8 != int(blockIdx.x / 8)) lds_barrier();
       MOLT_SSTORE(st0, 0);
       MOLT_GLOAD(st0, g, 2);
       lds_barrier();
@@ -253,52 +260,80 @@ void stream_gemm_kernel(GemmParams p) {
     // out of the tile loop into registers held across the K steps (gate_up spilled them)
     asm volatile("" : "+v"(lcol), "+v"(lgrp));
     if (MODE == kGateUp) {
-      // h = silu(gate) * up, bf16, tiled layout over padded rows; up columns go through LDS
-      if (wave >= 2) {
-#pragma unroll
-        for (int i = 0; i < MS; ++i)
-#pragma unroll
-          for (int e = 0; e < 16; ++e) {
-            const int r = 32 * i + 8 * (e / 4) + 4 * lgrp + (e % 4);
-            upbuf[r * 64 + 32 * (wave - 2) + lcol] = acc[i][e];
-          }
-      }
-      lds_barrier();
-      if (wave < 2) {
-        const int c = 32 * wave + lcol;
-        const long hrb = 2L * p.N;
-#pragma unroll
-        for (int i = 0; i < MS; ++i)
-#pragma unroll
-          for (int e = 0; e < 16; ++e) {
-            const int r = 32 * i + 8 * (e / 4) + 4 * lgrp + (e % 4);
-            const int grow = g.row0 + r;
-            if (grow >= g.row1) continue;
-            float gt = acc[i][e], u = upbuf[r * 64 + c];
-            if (FP8) {
-              const float sx = p.a_scale[p.perm[grow] / p.ktop];
-              const float* sw = p.b_scale + long(g.expert) * p.b_scale_ld;
-              gt = gt * sx * sw[g.n0 + c];
-              u = u * sx * sw[p.N + g.n0 + c];
-            }
-            *reinterpret_cast<uint16_t*>(static_cast<uint8_t*>(p.C) +
-                                         tiled_offset(grow, 2L * (g.n0 + c), hrb)) = f32_to_bf16(silu(gt) * u);
-          }
-      }
-    } else {
-      // per-pair expert output, f32, row = pair index (token * K + slot)
-      const int c = g.n0 + 32 * wave + lcol;
+      // h = silu(gate) * up, bf16, tiled layout over padded rows. The accumulators go to LDS
+      // as a BM x 128 tile (gate columns 0-63 from wavefronts 0-1, up columns 64-127 from
+      // 2-3; the last step's barrier freed the staging buffers); then each thread finishes
+      // 8 consecutive columns of a row per pass and writes them with one 16-byte store.
+      float* ep = reinterpret_cast<float*>(smem);
 #pragma unroll
       for (int i = 0; i < MS; ++i)
 #pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const int r = 32 * i + 8 * (e / 4) + 4 * lgrp + (e % 4);
+        for (int e = 0; e < 16; ++e) ep[(32 * i + 8 * (e / 4) + 4 * lgrp + (e % 4)) * 128 + 32 * wave + lcol] = acc[i][e];
+      lds_barrier();
+      const long hrb = 2L * p.N;
+#pragma unroll
+      for (int j = 0; j < MS; ++j) {
+        const int u = int(threadIdx.x) + kThreads * j;   // BM * 8 units of 8 columns
+        const int r = u >> 3, cb = (u & 7) * 8;
+        const int grow = g.row0 + r;
+        if (grow >= g.row1) continue;
+        const float4* gp = reinterpret_cast<const float4*>(ep + r * 128 + cb);
+        const float4* up = reinterpret_cast<const float4*>(ep + r * 128 + 64 + cb);
+        const float4 g0 = gp[0], g1 = gp[1], u0 = up[0], u1 = up[1];
+        float gv[8] = {g0.x, g0.y, g0.z, g0.w, g1.x, g1.y, g1.z, g1.w};
+        float uv[8] = {u0.x, u0.y, u0.z, u0.w, u1.x, u1.y, u1.z, u1.w};
+        if (FP8) {
+          const float sx = p.a_scale[p.perm[grow] / p.ktop];
+          const float* sw = p.b_scale + long(g.expert) * p.b_scale_ld + g.n0 + cb;
+#pragma unroll
+          for (int q = 0; q < 8; ++q) {
+            gv[q] *= sx * sw[q];
+            uv[q] *= sx * sw[p.N + q];
+          }
+        }
+        uint32_t packed[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          packed[q] = uint32_t(f32_to_bf16(silu(gv[2 * q]) * uv[2 * q])) |
+                      (uint32_t(f32_to_bf16(silu(gv[2 * q + 1]) * uv[2 * q + 1])) << 16);
+        *reinterpret_cast<int32x4_t*>(static_cast<uint8_t*>(p.C) + tiled_offset(grow, 2L * (g.n0 + cb), hrb)) =
+            int32x4_t{int(packed[0]), int(packed[1]), int(packed[2]), int(packed[3])};
+      }
+    } else {
+      // per-pair expert output, f32, row = pair index (token * K + slot). Through LDS, so
+      // that each thread writes 4 consecutive columns of a row with one 16-byte store.
+#pragma unroll
+      for (int pass = 0; pass < 128 / kEpCols; ++pass) {
+        const int c0 = pass * kEpCols;                 // first column of this pass
+        if (32 * wave >= c0 && 32 * wave < c0 + kEpCols) {
+#pragma unroll
+          for (int i = 0; i < MS; ++i)
+#pragma unroll
+            for (int e = 0; e < 16; ++e)
+              dep[(32 * i + 8 * (e / 4) + 4 * lgrp + (e % 4)) * kEpCols + 32 * wave - c0 + lcol] = acc[i][e];
+        }
+        lds_barrier();
+        constexpr int kUnits = BM * kEpCols / 4;       // 4-column units
+#pragma unroll 4
+        for (int j = 0; j < kUnits / kThreads; ++j) {
+          const int u = int(threadIdx.x) + kThreads * j;
+          const int r = u / (kEpCols / 4), c4 = (u % (kEpCols / 4)) * 4;
           const int grow = g.row0 + r;
           if (grow >= g.row1) continue;
-          float v = acc[i][e];
-          if (FP8) v = v * p.a_scale[grow] * p.b_scale[long(g.expert) * p.b_scale_ld + c];
-          static_cast<float*>(p.C)[long(prow[r]) * p.ldc + c] = v;
+          float4 v = *reinterpret_cast<const float4*>(dep + r * kEpCols + c4);
+          const int c = g.n0 + c0 + c4;
+          if (FP8) {
+            const float sx = p.a_scale[grow];
+            const float* sw = p.b_scale + long(g.expert) * p.b_scale_ld + c;
+            v.x *= sx * sw[0];
+            v.y *= sx * sw[1];
+            v.z *= sx * sw[2];
+            v.w *= sx * sw[3];
+          }
+          *reinterpret_cast<float4*>(static_cast<float*>(p.C) + long(prow[r]) * p.ldc + c) = v;
         }
+        if (pass + 1 < 128 / kEpCols) lds_barrier();
+      }
     }
     if (!more) break;
     k8 += stride;
@@ -341,7 +376,8 @@ hipError_t run_stream(GemmParams p, int tile_m, hipStream_t s) {
   const long nk = long(p.K) * (FP8 ? 1 : 2) / kRowBytes;
   // chained in bf16 for down only: its 12-slice tiles gained (85 -> 82 us per launch at
   // T*K = 5120), gate_up's 32-slice tiles did not (159 -> 161 us)
-  if (!FP8 && MODE == kDown && nk % 4 == 0) return run_stream_k<false, MODE, true>(p, tile_m, s);
+  if constexpr (!FP8 && MODE == kDown)
+    if (nk % 4 == 0) return run_stream_k<false, MODE, true>(p, tile_m, s);
   return run_stream_k<FP8, MODE, false>(p, tile_m, s);
 }
 
