@@ -85,20 +85,22 @@ MOLT_DEV int kswz(int key, int blk) {
 }
 MOLT_DEV int vswz(int dim) { return ((dim >> 2) ^ (dim >> 3)) & 1; }
 
-template <int D, int NW>
+template <int D, int NW, int KS>
 __global__ __launch_bounds__(64 * NW, NW == 8 ? 2 : 1) void attn_lds_kernel(AttnParams p) {
   constexpr int kThreads = 64 * NW;
   constexpr int RTW = 1;                // 16-row tiles per wavefront
+  constexpr int NRT = NW / KS;          // row tiles per key group
   constexpr int DS = D / 32;            // 32-dim k-steps for S
   constexpr int DT = D / 16;            // 16-dim tiles of O^T
   constexpr int KB = 16 * D * 2;        // bytes of one K (or V) block
   constexpr int PAIR = 4 * KB;          // K0, K1, V0, V1
   constexpr int CPT = PAIR / 16 / kThreads;   // 16-byte chunks per thread per pair
   static_assert(CPT >= 1 && CPT * 16 * kThreads == PAIR, "chunks per thread");
-  // pairs loaded ahead into registers: 8-wavefront workgroups hold 3, which keeps them at
-  // 122 registers, so two fit per CU (6 pairs in flight per CU either way)
-  constexpr int kDepth = NW == 8 ? 3 : 6;
-  __shared__ __attribute__((aligned(16))) uint8_t lds[2][PAIR];
+  // steps (KS pairs each) loaded ahead into registers: 8-wavefront workgroups hold 3 pairs
+  // with one key group, which keeps them at 122 registers, so two fit per CU; with two key
+  // groups one step (2 pairs) ahead
+  constexpr int kDepth = KS == 2 ? 1 : NW == 8 ? 3 : 6;
+  __shared__ __attribute__((aligned(16))) uint8_t lds[2 * KS][PAIR];
 
   const int split = blockIdx.x % p.splits;
   const int qt = (blockIdx.x / p.splits) % p.qtiles;
@@ -120,13 +122,15 @@ __global__ __launch_bounds__(64 * NW, NW == 8 ? 2 : 1) void attn_lds_kernel(Attn
   const int lane = threadIdx.x % kWave;
   const int l16 = lane % 16, g4 = lane / 16;
   const float c = p.scale_log2;
+  // key group kg takes pairs kg, kg + KS, ...; its wavefront rt holds 16-row tile rt
+  const int kg = wave / NRT, rtile = wave % NRT;
 
-  // Q^T fragments of the wavefront's rows r = 16 (wave + NW i) + l16, dims [32 s + 8 g4, +8)
+  // Q^T fragments of the wavefront's rows r = 16 (rtile + NRT i) + l16, dims [32 s + 8 g4, +8)
   bf16x8_t qf[RTW][DS];
   int lim[RTW];
 #pragma unroll
   for (int i = 0; i < RTW; ++i) {
-    const int r = 16 * (wave + NW * i) + l16;    // row of the tile
+    const int r = 16 * (rtile + NRT * i) + l16;  // row of the tile
     const int j = j0 + r / G, gi = r % G;
     lim[i] = r < Rt ? ctx + j : -1;
 #pragma unroll
@@ -148,7 +152,7 @@ __global__ __launch_bounds__(64 * NW, NW == 8 ? 2 : 1) void attn_lds_kernel(Attn
   float m_run[RTW], l_run[RTW];
 #pragma unroll
   for (int i = 0; i < RTW; ++i) { m_run[i] = kNegBig; l_run[i] = 0.f; }
-  const bool active = 16 * wave < Rt;   // wavefronts without rows only help with the loads
+  const bool active = 16 * rtile < Rt;  // wavefronts without rows only help with the loads
   const int lim_lo = ctx + j0;          // keys up to here are visible to every row of the tile
 
   __shared__ int s_bt[kMaxSplitBlocks];
@@ -177,11 +181,11 @@ __global__ __launch_bounds__(64 * NW, NW == 8 ? 2 : 1) void attn_lds_kernel(Attn
       dst_off[u] = q * KB + dim * 32 + ((vc ^ vswz(dim)) * 16);
     }
   }
-  int32x4_t st[kDepth][CPT];
+  int32x4_t st[kDepth][KS][CPT];
   // The split's block-table entries are read from LDS: a global load of them, issued behind
   // the K/V prefetches, would have its wait drain every load in flight (the vector memory
   // counter retires in order).
-  auto gload = [&](int32x4_t (&dst)[CPT], int pi) __attribute__((always_inline)) {
+  auto gload_pair = [&](int32x4_t (&dst)[CPT], int pi) __attribute__((always_inline)) {
     const int rel = 2 * min(pi, npairs - 1);
     const long phys0 = s_bt[rel];
     const long phys1r = s_bt[min(rel + 1, blk1 - blk0 - 1)];
@@ -193,9 +197,17 @@ __global__ __launch_bounds__(64 * NW, NW == 8 ? 2 : 1) void attn_lds_kernel(Attn
           base + (second[u] ? phys1 : phys0) * kv_blk_stride + src_off[u]));
     }
   };
-  auto sstore = [&](const int32x4_t (&src)[CPT], int buf) __attribute__((always_inline)) {
+  // step si covers pairs KS si .. KS si + KS - 1; LDS half hf holds a step's pairs in
+  // buffers KS hf .. KS hf + KS - 1
+  auto gload = [&](int32x4_t (&dst)[KS][CPT], int si) __attribute__((always_inline)) {
 #pragma unroll
-    for (int u = 0; u < CPT; ++u) *reinterpret_cast<int32x4_t*>(lds[buf] + dst_off[u]) = src[u];
+    for (int g = 0; g < KS; ++g) gload_pair(dst[g], KS * si + g);
+  };
+  auto sstore = [&](const int32x4_t (&src)[KS][CPT], int hf) __attribute__((always_inline)) {
+#pragma unroll
+    for (int g = 0; g < KS; ++g)
+#pragma unroll
+      for (int u = 0; u < CPT; ++u) *reinterpret_cast<int32x4_t*>(lds[KS * hf + g] + dst_off[u]) = src[g][u];
   };
 
   // K fragment: block j = l16 / 8, key 8 ((l16 / 4) % 2) + 4 t + l16 % 4 (the swizzle is the
@@ -246,8 +258,7 @@ __global__ __launch_bounds__(64 * NW, NW == 8 ? 2 : 1) void attn_lds_kernel(Attn
     for (int i = 0; i < RTW; ++i) {
       float v = fmaxf(fmaxf(fmaxf(sv[0][i][0], sv[0][i][1]), fmaxf(sv[0][i][2], sv[0][i][3])),
                       fmaxf(fmaxf(sv[1][i][0], sv[1][i][1]), fmaxf(sv[1][i][2], sv[1][i][3])));
-      v = fmaxf(v, __shfl_xor(v, 16, kWave));
-      v = fmaxf(v, __shfl_xor(v, 32, kWave));
+      v = rows_max4(v);
       mx[i] = v * c;
       grow |= mx[i] > m_run[i] + kRescaleSlack;
     }
@@ -290,37 +301,69 @@ __global__ __launch_bounds__(64 * NW, NW == 8 ? 2 : 1) void attn_lds_kernel(Attn
     }
   };
 
-  // pipeline: pair pi sits in LDS buffer pi % 2; register slot (pi + 1) % kDepth holds pair
-  // pi + 1 (slots hold pi + 1 .. pi + kDepth). Step pi first stores pair pi + 1 into the
-  // other buffer (last read before the previous barrier) and refills its slot with pair
-  // pi + 1 + kDepth, so the new loads are in flight during the compute; then it computes
-  // pair pi. Loads past the last pair re-read it.
-  if (npairs > 0) {
+  // pipeline: step si sits in LDS half si % 2; register slot (si + 1) % kDepth holds step
+  // si + 1 (slots hold si + 1 .. si + kDepth). Step si first stores step si + 1 into the
+  // other half (last read before the previous barrier) and refills its slot with step
+  // si + 1 + kDepth, so the new loads are in flight during the compute; then each key group
+  // computes its pair of step si. Loads past the last pair re-read it.
+  const int nsteps = (npairs + KS - 1) / KS;
+  auto step = [&](int hf, int si) __attribute__((always_inline)) {
+    if (KS * si + kg < npairs) compute(KS * hf + kg, KS * si + kg);
+  };
+  if (nsteps > 0) {
     gload(st[0], 0);
     sstore(st[0], 0);
 #pragma unroll
     for (int u = 1; u <= kDepth; ++u) gload(st[u % kDepth], u);
     lds_barrier();
-    // pair p sits in LDS buffer p % 2 (kDepth may be odd, so the parity comes from pi)
-    int pi = 0;
-    for (; pi + kDepth - 1 < npairs; pi += kDepth) {
-      const int par = pi & 1;
+    // step s sits in LDS half s % 2 (kDepth may be odd, so the parity comes from si)
+    int si = 0;
+    for (; si + kDepth - 1 < nsteps; si += kDepth) {
+      const int par = si & 1;
 #pragma unroll
       for (int u = 0; u < kDepth; ++u) {
         sstore(st[(u + 1) % kDepth], 1 - (par ^ (u & 1)));
-        gload(st[(u + 1) % kDepth], pi + u + 1 + kDepth);
-        compute(par ^ (u & 1), pi + u);
+        gload(st[(u + 1) % kDepth], si + u + 1 + kDepth);
+        step(par ^ (u & 1), si + u);
         lds_barrier();
       }
     }
-    const int par = pi & 1;
+    const int par = si & 1;
 #pragma unroll
     for (int u = 0; u < kDepth - 1; ++u) {
-      if (pi + u < npairs) {
+      if (si + u < nsteps) {
         sstore(st[(u + 1) % kDepth], 1 - (par ^ (u & 1)));
-        compute(par ^ (u & 1), pi + u);
+        step(par ^ (u & 1), si + u);
         lds_barrier();
       }
+    }
+  }
+  if constexpr (KS == 2) {
+    // merge the key groups: group 1 leaves its running max, partial sums and O^T in LDS
+    // (free after the last barrier), group 0 combines them with its own
+    constexpr int kMergeF = DT * 4 + 2;    // floats per lane
+    static_assert(NRT * kMergeF * 64 * 4 <= 2 * KS * PAIR, "merge state fits the ring");
+    float* mg = reinterpret_cast<float*>(&lds[0][0]) + rtile * kMergeF * 64 + lane;
+    if (kg == 1 && active) {
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) mg[(dt * 4 + e) * 64] = o[dt][0][e];
+      mg[DT * 4 * 64] = m_run[0];
+      mg[(DT * 4 + 1) * 64] = l_run[0];
+    }
+    lds_barrier();
+    if (kg == 1) return;
+    if (active) {
+      const float m1 = mg[DT * 4 * 64], l1 = mg[(DT * 4 + 1) * 64];
+      const float mm = fmaxf(m_run[0], m1);
+      const float a0 = exp2f(m_run[0] - mm), a1 = exp2f(m1 - mm);
+      m_run[0] = mm;
+      l_run[0] = l_run[0] * a0 + l1 * a1;
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) o[dt][0][e] = o[dt][0][e] * a0 + mg[(dt * 4 + e) * 64] * a1;
     }
   }
   if (!active) return;
@@ -329,9 +372,8 @@ __global__ __launch_bounds__(64 * NW, NW == 8 ? 2 : 1) void attn_lds_kernel(Attn
 #pragma unroll
   for (int i = 0; i < RTW; ++i) {
     float lt = l_run[i];
-    lt += __shfl_xor(lt, 16, kWave);
-    lt += __shfl_xor(lt, 32, kWave);
-    const int r = 16 * (wave + NW * i) + l16;
+    lt = rows_sum4(lt);
+    const int r = 16 * (rtile + NRT * i) + l16;
     if (r >= Rt) continue;
     const int j = j0 + r / G, gi = r % G;
     // O^T element e of tile dt: dim 16 dt + 4 g4 + e
@@ -458,8 +500,9 @@ template <int D>
 hipError_t launch_d(const AttnParams& p, int B, int R, hipStream_t s) {
   const int Rt = (p.Hq / p.Hkv) * p.tq;     // rows of a query tile
   const long grid = long(B) * p.Hkv * p.qtiles * p.splits;
-  (void)Rt;
-  attn_lds_kernel<D, 8><<<grid, 512, 0, s>>>(p);
+  // two key groups when a query tile's row tiles fit half the wavefronts
+  if ((Rt + 15) / 16 <= 4) attn_lds_kernel<D, 8, 2><<<grid, 512, 0, s>>>(p);
+  else attn_lds_kernel<D, 8, 1><<<grid, 512, 0, s>>>(p);
   if (p.splits > 1) attn_merge_kernel<D><<<B * p.Hkv * R, D, 0, s>>>(p, 0);
   return hipGetLastError();
 }

@@ -158,6 +158,24 @@ MOLT_DEV float wave_sum_dpp(float v) {
   return __uint_as_float(lane63(__float_as_uint(v)));
 }
 
+// Maximum (sum) over the lanes l, l ^ 16, l ^ 32 and l ^ 48: the four 16-lane rows of a
+// wavefront combined lane by lane, on gfx950's row swaps (VALU moves, no LDS permute).
+// permlane16_swap(a, b) exchanges rows 1 and 3 of a with rows 0 and 2 of b, permlane32_swap
+// rows 2-3 of a with rows 0-1 of b; given the same value twice, the two results hold each
+// row's value and its partner's. Every lane gets (x0 op x1) op (x2 op x3) for its rows.
+MOLT_DEV float rows_max4(float v) {
+  const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  v = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+MOLT_DEV float rows_sum4(float v) {
+  const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  v = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+  const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(b[0]) + __uint_as_float(b[1]);
+}
+
 MOLT_DEV float wave_max(float v) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, kWave));
