@@ -45,10 +45,11 @@ def head_input(tokens, h, mtp, head, cfg):
 
 
 def head_layer(x, mtp, kcache, vcache, block_tables, context_lens, k, cfg):
-    """The head's decoder layer on rows b*(k+1)+j at positions context_lens[b] + j."""
+    """The head's decoder layer on rows b*(k+1)+j at positions context_lens[b] + j.
+    Returns the rows and their route-set margins (the router's gap at the top-K boundary)."""
     x = model.attention_block(x, mtp["layer"], kcache, vcache, block_tables, context_lens, k, cfg)
-    x, _ = model.moe_block(x, mtp["layer"], cfg)
-    return x
+    x, r = model.moe_block(x, mtp["layer"], cfg)
+    return x, r["margin"]
 
 
 def head_logits(x, mtp, head, cfg):
@@ -67,7 +68,8 @@ def mtp_draft(hidden, tokens, n_accepted, next_tokens, mtp, head, kcache, vcache
     Returns dict: drafts [B, k] int32, q [B, k, V] float64 (None when greedy), logits
     [B, k, V] f32, h [B, k, d] f32 (the head's output row behind each draft), margin [B, k]
     (the draw's margin relative to its total mass; greedy: the gap between the two largest
-    logits)."""
+    logits), route_margin [B, k] (the route-set margin of the head row behind each draft: a
+    near-tie there lets rounding pick another expert set)."""
     tokens = np.asarray(tokens)
     B, kp1 = tokens.shape                      # kp1: the catch-up window W
     k = kp1 - 1 if k is None else k
@@ -78,10 +80,12 @@ def mtp_draft(hidden, tokens, n_accepted, next_tokens, mtp, head, kcache, vcache
     row_tok = np.array([[tokens[b, j + 1] if j < n[b] else nxt[b] for j in range(kp1)]
                         for b in range(B)]).reshape(-1)
     x = head_input(row_tok, np.asarray(hidden, np.float32), mtp, head, cfg)
-    x = head_layer(x, mtp, kcache, vcache, block_tables, ctx, kp1 - 1, cfg)
+    x, rm = head_layer(x, mtp, kcache, vcache, block_tables, ctx, kp1 - 1, cfg)
     h = x[np.arange(B) * kp1 + n]
     drafts = np.zeros((B, k), np.int32)
     logits_all, qs, hs, margins = [], [], [], np.zeros((B, k))
+    route_margin = np.zeros((B, k))
+    route_margin[:, 0] = rm[np.arange(B) * kp1 + n]
     for i in range(k):
         lg = head_logits(h, mtp, head, cfg)                   # [B, V] f32
         logits_all.append(lg)
@@ -101,7 +105,9 @@ def mtp_draft(hidden, tokens, n_accepted, next_tokens, mtp, head, kcache, vcache
             break
         tok = np.asarray(forced)[:, i] if forced is not None else d
         x = head_input(tok, h, mtp, head, cfg)
-        x = head_layer(x, mtp, kcache, vcache, block_tables, ctx + n + i + 1, 0, cfg)
+        x, rm = head_layer(x, mtp, kcache, vcache, block_tables, ctx + n + i + 1, 0, cfg)
+        route_margin[:, i + 1] = rm
         h = x
     return {"drafts": drafts, "q": None if uniforms is None else np.stack(qs, axis=1),
-            "logits": np.stack(logits_all, axis=1), "h": np.stack(hs, axis=1), "margin": margins}
+            "logits": np.stack(logits_all, axis=1), "h": np.stack(hs, axis=1), "margin": margins,
+            "route_margin": route_margin}

@@ -165,9 +165,17 @@ def test_small_bf16_after_verify(molt_lib, seed):
     assert ((drafts >= 0) & (drafts < w.vocab)).all()
 
 
+# A head row whose top-K route set sits within this router-logit gap of the next expert may
+# take another set under rounding (its output, and every later draft's input, then moves
+# by far more than the logits' tolerance): such a row and the drafts after it are compared
+# only for validity, as in the full-shape decoder test.
+ROUTE_TIE = 1e-2
+
+
 def test_full_shape_synthetic(molt_lib):
     """B 128, k 4, context 8192, vocabulary 151936 (the benchmark's step), one head layer;
-    the oracle on three sampled sequences with n_accepted 0, 2 and 4."""
+    the oracle on six sampled sequences with n_accepted 0 to 4, each compared up to its
+    first head row at a route near-tie."""
     molt = molt_lib
     w = workloads.FULL_DEPTH_BF16.scaled(n_layers=1)
     seed = 31
@@ -182,8 +190,8 @@ def test_full_shape_synthetic(molt_lib):
     B, k, V = w.batch, w.k, w.vocab
     g = np.random.default_rng(seed)
     n = g.integers(0, k + 1, B).astype(np.int32)
-    seqs = [3, 40, 77]
-    n[seqs] = [0, 2, 4]
+    seqs = [3, 40, 77, 90, 101, 120]
+    n[seqs] = [0, 2, 4, 1, 3, 0]
     nxt = g.integers(0, V, B).astype(np.int32)
     toks = workloads.make_step_tokens(w, seed)
     hidden = workloads.make_hidden(w, seed, device="cuda")
@@ -215,8 +223,17 @@ def test_full_shape_synthetic(molt_lib):
     o = omtp.mtp_draft(hid, toks[seqs], n[seqs], nxt[seqs], _mtp_host(mt), hh, okc, ovc, bt2,
                        layout.context_lens[seqs], oracle_cfg(w), uniforms=host(ud)[seqs],
                        forced=drafts[seqs])
-    _check_q(q[seqs].cpu().numpy(), o["q"], 5e-2, 1e-6)
-    _drafts_in_cdf(drafts[seqs], o["q"], host(ud)[seqs], 1e-3)
+    tie = o["route_margin"] < ROUTE_TIE
+    upto = np.where(tie.any(axis=1), tie.argmax(axis=1), k)   # drafts before the first near-tie
+    print(f"route margins {np.array2string(o['route_margin'], precision=3)}; compared drafts per "
+          f"sequence {upto.tolist()}", flush=True)
+    assert upto.sum() >= 12, "too few drafts away from route near-ties"
+    qg = q[seqs].cpu().numpy()
+    for i in range(len(seqs)):
+        if upto[i]:
+            _check_q(qg[i:i + 1, :upto[i]], o["q"][i:i + 1, :upto[i]], 5e-2, 1e-6)
+            _drafts_in_cdf(drafts[seqs][i:i + 1, :upto[i]], o["q"][i:i + 1, :upto[i]],
+                           host(ud)[seqs][i:i + 1, :upto[i]], 1e-3)
 
 
 def test_tiny_one_draft(molt_lib):
