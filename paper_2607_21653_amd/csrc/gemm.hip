@@ -772,8 +772,10 @@ __global__ __launch_bounds__(kThreads) void pack_tiled_kernel(const uint8_t* __r
 }
 
 // gather: tiled activation rows in padded expert order from tiled token rows,
-// row = src[pperm[row] / ktop] (zeros for padding rows); one workgroup per 4 KB tile of
-// the destination, thread = 16-byte chunk of it
+// row = src[pperm[row] / ktop]; one workgroup per 4 KB tile of the destination, thread =
+// 16-byte chunk of it. Padding rows are left unwritten: a GEMM output row depends on its
+// own operand row only, and the rows computed from padding are never stored. (Workgroups
+// over 8 slices of a 32-row block, each thread with 8 loads in flight, took twice as long.)
 __global__ __launch_bounds__(kThreads) void gather_tiled_kernel(
     const uint8_t* __restrict__ src, const int32_t* __restrict__ pperm, int ktop,
     const int32_t* __restrict__ n_rows, long RB, uint8_t* __restrict__ dst) {
@@ -785,9 +787,9 @@ __global__ __launch_bounds__(kThreads) void gather_tiled_kernel(
   const long row = rb * 32 + (l % 32);
   const long j = kb * 128 + (l / 32) * 64 + quarter * 16;
   const int pair = pperm[row];
-  int4 v = make_int4(0, 0, 0, 0);
-  if (pair >= 0) v = *reinterpret_cast<const int4*>(src + tiled_offset(pair / ktop, j, RB));
-  *reinterpret_cast<int4*>(dst + tile * 4096 + threadIdx.x * 16) = v;
+  if (pair < 0) return;
+  *reinterpret_cast<int4*>(dst + tile * 4096 + threadIdx.x * 16) =
+      *reinterpret_cast<const int4*>(src + tiled_offset(pair / ktop, j, RB));
 }
 
 // ---------------------------------------------------------------- f32 VALU path
