@@ -242,7 +242,7 @@ long gemm_part_elems(int M, int N, int K, molt_dtype dt) {
 
 struct MoeWs {
   float* g; int32_t* ids; float* w; int32_t* counts; int32_t* offsets; int32_t* perm;
-  int32_t* inv; int32_t* pperm; int32_t* n_padded; int32_t* tiles; int32_t* n_tiles;
+  int32_t* pperm; int32_t* n_padded; int32_t* tiles; int32_t* n_tiles;
   uint8_t* xq; float* xs; void* xt; void* h; uint8_t* hq; float* hs; float* o;
   float* part; long part_elems;   // split-K partial sums of the router GEMM
   long max_rows; int max_tiles; int tile_m;
@@ -267,7 +267,6 @@ MoeWs carve_moe(molt::Carver& c, int T, int d, int E, int K, int F, molt_dtype a
   m.counts = c.take<int32_t>(E);
   m.offsets = c.take<int32_t>(E + 1);
   m.perm = c.take<int32_t>(P);
-  m.inv = c.take<int32_t>(P);
   m.pperm = c.take<int32_t>(R);
   m.n_padded = c.take<int32_t>(1);
   m.tiles = c.take<int32_t>(long(m.max_tiles) * 4);
@@ -316,7 +315,7 @@ hipError_t run_moe(const MoeWs& m, const void* x, const uint8_t* xq, const float
       return e;
   }
   if ((e = molt::launch_route(nparts > 1 ? m.part : m.g, nparts, bias, replay, T, E, K, m.ids, m.w,
-                              m.counts, m.offsets, m.perm, m.inv, m.pperm, m.n_padded, m.tile_m,
+                              m.counts, m.offsets, m.perm, m.pperm, m.n_padded, m.tile_m,
                               m.tiles, m.max_tiles, m.n_tiles, s)) != hipSuccess)
     return e;
   const bool fp8 = wdt == MOLT_FP8_E4M3;

@@ -16,7 +16,9 @@ struct Carver {
   Carver(void* p, size_t c) : base(static_cast<char*>(p)), cap(c) {}
   template <typename T>
   T* take(size_t n) {
-    used = (used + 255) & ~size_t(255);
+    // 256-byte aligned addresses (the sizes reserve 256 bytes for an unaligned base)
+    const size_t b = reinterpret_cast<size_t>(base);
+    used = ((b + used + 255) & ~size_t(255)) - b;
     T* p = reinterpret_cast<T*>(base ? base + used : nullptr);
     used += n * sizeof(T);
     return p;
@@ -95,13 +97,13 @@ hipError_t launch_mtp_record(const int32_t* tok, int i, int B, int W, int k, con
 
 // ------------------------------------------------------------- routing
 // top-K + softmax of router logits (the sum, in order, of nparts split-K partials
-// logits[s * T * E ..]; or replay ids); stable permutation (perm/inv) and its padded copy
-// (pperm: padded row -> pair or -1, n_padded rows); tile table in padded rows
+// logits[s * T * E ..]; or replay ids); stable permutation perm (position -> pair) and its
+// padded copy (pperm: padded row -> pair or -1, n_padded rows); tile table in padded rows
 hipError_t launch_route(const float* logits, int nparts, const float* bias, const int32_t* replay,
                         int T, int E, int K, int32_t* ids, float* w, int32_t* counts,
-                        int32_t* offsets, int32_t* perm, int32_t* inv, int32_t* pperm,
-                        int32_t* n_padded, int tile_m, int32_t* tiles, int max_tiles,
-                        int32_t* n_tiles, hipStream_t s);
+                        int32_t* offsets, int32_t* perm, int32_t* pperm, int32_t* n_padded,
+                        int tile_m, int32_t* tiles, int max_tiles, int32_t* n_tiles,
+                        hipStream_t s);
 int max_expert_tiles(int T, int E, int K, int tile_m);
 long max_padded_rows(int T, int E, int K);
 
@@ -136,8 +138,8 @@ hipError_t launch_moe_down(const void* a, const float* a_scale, const int32_t* p
 // row-major [rows, row_bytes] -> tiled layout (row_bytes % 128 == 0), rows padded to a
 // multiple of 32 with zeros
 hipError_t launch_pack_tiled(const void* src, void* dst, long rows, long row_bytes, hipStream_t s);
-// tiled rows in padded expert order from tiled token rows: row = src[pperm[row] / K_top],
-// zeros for padding
+// tiled rows in padded expert order from tiled token rows: row = src[pperm[row] / K_top];
+// padding rows are left unwritten
 hipError_t launch_gather_tiled(const void* src, const int32_t* pperm, int K_top,
                                const int32_t* n_rows, long max_rows, long row_bytes, void* dst,
                                hipStream_t s);

@@ -9,14 +9,16 @@
 // max-reduction (DPP: with LDS-crossbar shuffles the K rounds were one long chain of
 // permute round trips) select the experts in descending order.
 //
-// permute_kernel: one 1024-thread workgroup, one pass over the ids. Wavefront w owns a
-// contiguous range of the T*K pairs (in (token, slot) order) and visits it 64 pairs at a
-// time: lanes holding the same expert find each other with 8 ballots over the expert id
-// bits, a popcount of the lower lanes gives the rank inside the step, and a running LDS
-// count per (wavefront, expert) adds the earlier steps. An exclusive prefix of those counts
-// over the wavefronts, and wavefront prefix sums over the experts (offsets, padded offsets,
-// grouped-GEMM tile table), then give position = offset[e] + earlier wavefronts + rank:
-// the stable (expert, token, slot) order, bit-exact, with no atomics.
+// permute_kernel: workgroups of 256 threads, each owning a contiguous range of the T*K
+// pairs (in (token, slot) order; 64 pairs per workgroup up to 512 workgroups). Each counts
+// every pair per expert and the pairs before its range (LDS integer atomics) and scans the
+// counts over the experts (offsets, padded offsets, grouped-GEMM tile table); inside the
+// range, lanes holding the same expert find each other with 8 ballots over the expert id
+// bits, a popcount of the lower lanes gives the rank inside a 64-pair step and a running
+// LDS count per (wavefront, expert) adds the earlier steps. Position = offset[e] + pairs of
+// e before the range + before the wavefront's part + rank: the stable (expert, token,
+// slot) order, bit-exact, with no global atomics. (One 1024-thread workgroup over all
+// pairs took 11.5 us at 5120 pairs, this launch ~6.)
 // The grouped GEMMs work on a padded copy of that order: every expert's rows start at a
 // multiple of 32 (padded offset poff[e] = sum of the earlier counts rounded up to 32), so
 // each 32-row block of a GEMM tile belongs to one expert; padded slots hold pair -1. The
@@ -28,8 +30,14 @@ namespace molt {
 namespace {
 
 constexpr int kMaxE = 256;
-constexpr int kPermThreads = 1024;
+constexpr int kPermThreads = 256;
 constexpr int kPermWaves = kPermThreads / kWave;
+constexpr int kRankSteps = 8;                               // 64-pair steps per wavefront
+constexpr int kMaxRange = kPermWaves * kRankSteps * kWave;  // pairs per workgroup, at most
+constexpr int kHistBatch = 8;                               // 16-byte id loads in flight
+constexpr int kPermRange = 64;                              // pairs per workgroup, at least
+constexpr int kPermGrid = 512;                              // workgroups, at most (while the
+                                                            // range stays <= kMaxRange)
 
 MOLT_DEV unsigned long long route_key(float v, int e) {
   const float c = v + 0.0f;                  // -0.0 -> +0.0
@@ -102,167 +110,165 @@ __global__ __launch_bounds__(256) void topk_kernel(const float* __restrict__ log
   }
 }
 
-__global__ __launch_bounds__(kPermThreads) void permute_kernel(
-    const int32_t* __restrict__ ids, int P, int E, int tile_m, int32_t* __restrict__ counts_out,
-    int32_t* __restrict__ offsets_out, int32_t* __restrict__ perm, int32_t* __restrict__ inv,
-    int32_t* __restrict__ pperm, int32_t* __restrict__ n_padded, int4* __restrict__ tiles,
-    int max_tiles, int32_t* __restrict__ n_tiles) {
-  __shared__ int wc[kPermWaves][kMaxE];    // pass 1: count per (wavefront, expert); then its
-                                           // exclusive prefix over the wavefronts
-  __shared__ int cnt[kMaxE];
+struct PermuteParams {
+  const int32_t* ids;      // [P] expert of pair p = t * K + slot
+  int P, E, K, tile_m;
+  int range;               // pairs per workgroup (<= kMaxRange)
+  int32_t* counts;         // [E]
+  int32_t* offsets;        // [E + 1]
+  int32_t* perm;           // [P] position -> pair
+  int32_t* pperm;          // [padded rows] padded row -> pair, -1 for padding
+  int32_t* n_padded;
+  int4* tiles;             // [max_tiles] (expert, first row, end row, 0) in padded rows
+  int max_tiles;
+  int32_t* n_tiles;
+};
+
+__global__ __launch_bounds__(kPermThreads) void permute_kernel(PermuteParams p) {
+  static_assert(kPermThreads == kMaxE, "one thread per expert in the scans");
+  __shared__ int tot[kMaxE];               // pairs per expert
+  __shared__ int bef[kMaxE];               // pairs per expert before the range
+  __shared__ int wc[kPermWaves][kMaxE];    // per (wavefront, expert): its pairs, then the
+                                           // expert's pairs before the wavefront's part
   __shared__ int off[kMaxE + 1];
   __shared__ int poff[kMaxE + 1];
-  __shared__ int wsum[3][kMaxE / kWave];
-  __shared__ int wtmp[3][kMaxE];
-  __shared__ int s_nt;
+  __shared__ int wsum[3][kPermWaves];
   const int tid = threadIdx.x;
   const int wave = tid / kWave, lane = tid % kWave;
-  // Wavefront w owns the contiguous pair range [w * per, (w + 1) * per), visited 64 at a
-  // time, so pair order = (wavefront, step, lane) order.
-  const int steps = (P + kPermThreads - 1) / kPermThreads;
-  const int per = steps * kWave;
-  const int p0 = wave * per;
-  for (int e = lane; e < kMaxE; e += kWave) wc[wave][e] = 0;   // own row only: no barrier
+  const int p0 = blockIdx.x * p.range, p1 = min(p0 + p.range, p.P);
+  tot[tid] = 0;
+  bef[tid] = 0;
+  for (int e = lane; e < kMaxE; e += kWave) wc[wave][e] = 0;
+  // rank of each pair of the range among the earlier pairs of its expert in its wavefront
+  // (wc rows are per wavefront: no barrier needed). Wavefront w owns the contiguous pairs
+  // [q0, q0 + per), 64 per step; lanes with the same expert find each other with 8 ballots
+  // over the id bits and a popcount of the lower lanes gives the rank inside the step.
+  const int per = (p1 - p0 + kPermWaves * kWave - 1) / (kPermWaves * kWave) * kWave;
+  const int steps = per / kWave;
+  const int q0 = p0 + wave * per;
   const unsigned long long lt = (1ull << lane) - 1ull;
-  // pass 1: the rank of each pair among the earlier pairs of its expert in this wavefront
-  // (earlier steps: the running count in wc; this step: popcount of the lower lanes with the
-  // same expert, found with 8 ballots over the id bits). The rank is parked in inv[p] (each
-  // thread reads back only what it wrote).
-  constexpr int kBatch = 8;                // loads of a batch issue together
-  // with one batch (P <= 8 * kPermThreads) pass 2 reuses the ids and ranks held here
-  // instead of reading them back from global memory
-  const bool one_batch = steps <= kBatch;
-  int ev1[kBatch], rk1[kBatch];
+  int ev[kRankSteps], rk[kRankSteps];
 #pragma unroll
-  for (int u = 0; u < kBatch; ++u) { ev1[u] = -1; rk1[u] = 0; }
-  for (int s0 = 0; s0 < steps; s0 += kBatch) {
-    int ev[kBatch];
+  for (int u = 0; u < kRankSteps; ++u) {
+    const int q = q0 + u * kWave + lane;
+    ev[u] = (u < steps && q < p1) ? p.ids[q] : -1;
+    rk[u] = 0;
+  }
 #pragma unroll
-    for (int u = 0; u < kBatch; ++u) {
-      const int p = p0 + (s0 + u) * kWave + lane;
-      ev[u] = (s0 + u < steps && p < P) ? ids[p] : -1;
+  for (int u = 0; u < kRankSteps; ++u) {
+    if (u >= steps) break;
+    const int e = ev[u];
+    const bool valid = e >= 0;
+    unsigned long long mask = __ballot(valid);
+#pragma unroll
+    for (int bit = 0; bit < 8; ++bit) {
+      const bool on = (e >> bit) & 1;
+      const unsigned long long b = __ballot(valid && on);
+      mask &= on ? b : ~b;
     }
-#pragma unroll
-    for (int u = 0; u < kBatch; ++u) {
-      if (s0 + u >= steps) break;
-      const int e = ev[u];
-      const bool valid = e >= 0;
-      unsigned long long mask = __ballot(valid);
-#pragma unroll
-      for (int bit = 0; bit < 8; ++bit) {
-        const bool on = (e >> bit) & 1;
-        const unsigned long long b = __ballot(valid && on);
-        mask &= on ? b : ~b;
-      }
-      const int below = __popcll(mask & lt);
-      int before = 0;
-      if (valid) before = wc[wave][e];
-      if (valid && below == 0) wc[wave][e] = before + __popcll(mask);
-      if (s0 == 0) {
-        ev1[u] = e;
-        rk1[u] = before + below;
-      }
-      if (valid && !one_batch) inv[p0 + (s0 + u) * kWave + lane] = before + below;
-    }
+    const int below = __popcll(mask & lt);
+    int before = 0;
+    if (valid) before = wc[wave][e];
+    if (valid && below == 0) wc[wave][e] = before + __popcll(mask);
+    rk[u] = before + below;
   }
   __syncthreads();
-  // per expert: exclusive prefix of the wavefront counts (all 16 read before any write),
-  // and the total
-  if (tid < kMaxE) {
-    int c[kPermWaves];
+  // every workgroup counts all pairs per expert and those before its range (LDS atomics on
+  // integers: exact in any order)
+  // (ids read 4 at a time; the allocation holds P ids, so the last group of 4 reads
+  // element-wise)
+  const int P4 = p.P / 4;
+  for (int i0 = 0; i0 < P4; i0 += kPermThreads * kHistBatch) {
+    int32x4_t hv[kHistBatch];
 #pragma unroll
-    for (int w2 = 0; w2 < kPermWaves; ++w2) c[w2] = wc[w2][tid];
-    int run = 0;
+    for (int u = 0; u < kHistBatch; ++u) {
+      const int i = i0 + kPermThreads * u + tid;
+      hv[u] = i < P4 ? reinterpret_cast<const int32x4_t*>(p.ids)[i] : int32x4_t{-1, -1, -1, -1};
+    }
+#pragma unroll
+    for (int u = 0; u < kHistBatch; ++u) {
+      const int i = 4 * (i0 + kPermThreads * u + tid);
+#pragma unroll
+      for (int c4 = 0; c4 < 4; ++c4) {
+        if (hv[u][c4] >= 0) {
+          atomicAdd(&tot[hv[u][c4]], 1);
+          if (i + c4 < p0) atomicAdd(&bef[hv[u][c4]], 1);
+        }
+      }
+    }
+  }
+  if (tid < p.P - 4 * P4) {
+    const int i = 4 * P4 + tid;
+    const int e = p.ids[i];
+    atomicAdd(&tot[e], 1);
+    if (i < p0) atomicAdd(&bef[e], 1);
+  }
+  __syncthreads();
+  // thread e: its expert's pairs before each wavefront's part of the range (all rows read
+  // before any write), and the inclusive scans over experts of the count, the count padded
+  // to 32 rows and the tile count
+  const int c = tid < p.E ? tot[tid] : 0;
+  const int tn = (c + p.tile_m - 1) / p.tile_m;
+  {
+    int cw[kPermWaves];
+#pragma unroll
+    for (int w2 = 0; w2 < kPermWaves; ++w2) cw[w2] = wc[w2][tid];
+    int run = bef[tid];
 #pragma unroll
     for (int w2 = 0; w2 < kPermWaves; ++w2) {
       wc[w2][tid] = run;
-      run += c[w2];
+      run += cw[w2];
     }
-    cnt[tid] = tid < E ? run : 0;
   }
-  __syncthreads();
-  // exclusive prefix sums over experts (threads 0..255, one expert each) of the count, the
-  // padded count and the tile count: offsets, padded offsets, first tile of each expert
-  int tile0 = 0;
-  if (tid < kMaxE) {
-    const int c = cnt[tid];
-    int v[3] = {c, (c + 31) / 32 * 32, (c + tile_m - 1) / tile_m};
+  int v[3] = {c, (c + 31) / 32 * 32, tn};
 #pragma unroll
-    for (int q = 0; q < 3; ++q) {
-      v[q] = wave_scan_dpp(v[q]);
-      if (lane == kWave - 1) wsum[q][wave] = v[q];
-    }
-    wtmp[0][tid] = v[0];
-    wtmp[1][tid] = v[1];
-    wtmp[2][tid] = v[2];
+  for (int q = 0; q < 3; ++q) {
+    v[q] = wave_scan_dpp(v[q]);
+    if (lane == kWave - 1) wsum[q][wave] = v[q];
   }
   __syncthreads();
-  if (tid < kMaxE) {
+  int nt = 0;
+  {
     int add[3] = {0, 0, 0};
-    for (int w2 = 0; w2 < wave; ++w2)
 #pragma unroll
-      for (int q = 0; q < 3; ++q) add[q] += wsum[q][w2];
-    const int c = cnt[tid];
-    const int tn = (c + tile_m - 1) / tile_m;
-    off[tid + 1] = wtmp[0][tid] + add[0];
-    poff[tid + 1] = wtmp[1][tid] + add[1];
-    tile0 = wtmp[2][tid] + add[2] - tn;
+    for (int w2 = 0; w2 < kPermWaves; ++w2) {
+#pragma unroll
+      for (int q = 0; q < 3; ++q) add[q] += w2 < wave ? wsum[q][w2] : 0;
+      nt += wsum[2][w2];
+    }
+    off[tid + 1] = v[0] + add[0];
+    poff[tid + 1] = v[1] + add[1];
+    v[2] += add[2] - tn;                   // this expert's first tile
     if (tid == 0) { off[0] = 0; poff[0] = 0; }
-    if (tid == E - 1) {
-      s_nt = min(tile0 + tn, max_tiles);
-      *n_tiles = s_nt;
-      *n_padded = poff[E];
-    }
   }
+  nt = min(nt, p.max_tiles);
   __syncthreads();
-  if (tid < E) {                                       // this expert's tiles
-    const int c = cnt[tid];
-    for (int m0 = 0, i = tile0; m0 < c && i < max_tiles; m0 += tile_m, ++i)
-      tiles[i] = make_int4(tid, poff[tid] + m0, poff[tid] + min(m0 + tile_m, c), 0);
-  }
-  for (int i = tid; i < E * 32; i += kPermThreads) {   // padding slots of each expert
-    const int e = i / 32, r = cnt[e] + i % 32;
-    if (r < poff[e + 1] - poff[e]) pperm[poff[e] + r] = -1;
-  }
-  for (int i = s_nt + tid; i < max_tiles; i += kPermThreads) tiles[i] = make_int4(-1, 0, 0, 0);
-  for (int e = tid; e < E; e += kPermThreads) {
-    counts_out[e] = cnt[e];
-    offsets_out[e] = off[e];
-  }
-  if (tid == 0) offsets_out[E] = off[E];
-  // pass 2: position = offset of the expert + earlier wavefronts' pairs of it + rank
-  if (one_batch) {
-#pragma unroll
-    for (int u = 0; u < kBatch; ++u) {
-      const int e = ev1[u];
-      if (e < 0) continue;
-      const int p = p0 + u * kWave + lane;
-      const int pos = off[e] + wc[wave][e] + rk1[u];
-      perm[pos] = p;
-      inv[p] = pos;
-      pperm[pos - off[e] + poff[e]] = p;
+  // workgroup 0: counts, offsets, tile table, padding slots
+  if (blockIdx.x == 0) {
+    if (tid < p.E) {
+      p.counts[tid] = c;
+      p.offsets[tid] = off[tid];
+      for (int m0 = 0, i = v[2]; m0 < c && i < p.max_tiles; m0 += p.tile_m, ++i)
+        p.tiles[i] = make_int4(tid, poff[tid] + m0, poff[tid] + min(m0 + p.tile_m, c), 0);
+      for (int r = poff[tid] + c; r < poff[tid + 1]; ++r) p.pperm[r] = -1;
     }
-    return;
+    if (tid == 0) {
+      p.offsets[p.E] = off[p.E];
+      *p.n_padded = poff[p.E];
+      *p.n_tiles = nt;
+    }
+    for (int i = nt + tid; i < p.max_tiles; i += kPermThreads) p.tiles[i] = make_int4(-1, 0, 0, 0);
   }
-  for (int s0 = 0; s0 < steps; s0 += kBatch) {
-    int ev[kBatch], rk[kBatch];
+  // the range's pairs: position = offset + earlier pairs of the expert + rank
 #pragma unroll
-    for (int u = 0; u < kBatch; ++u) {
-      const int p = p0 + (s0 + u) * kWave + lane;
-      const bool ok = s0 + u < steps && p < P;
-      ev[u] = ok ? ids[p] : -1;
-      rk[u] = ok ? inv[p] : 0;
-    }
-#pragma unroll
-    for (int u = 0; u < kBatch; ++u) {
-      const int e = ev[u];
-      if (e < 0) continue;
-      const int p = p0 + (s0 + u) * kWave + lane;
-      const int pos = off[e] + wc[wave][e] + rk[u];
-      perm[pos] = p;
-      inv[p] = pos;
-      pperm[pos - off[e] + poff[e]] = p;
-    }
+  for (int u = 0; u < kRankSteps; ++u) {
+    if (u >= steps) break;
+    const int e = ev[u];
+    if (e < 0) continue;
+    const int q = q0 + u * kWave + lane;
+    const int r = wc[wave][e] + rk[u];
+    p.perm[off[e] + r] = q;
+    p.pperm[poff[e] + r] = q;
   }
 }
 
@@ -280,13 +286,27 @@ long max_padded_rows(int T, int E, int K) {
 
 hipError_t launch_route(const float* logits, int nparts, const float* bias, const int32_t* replay,
                         int T, int E, int K, int32_t* ids, float* w, int32_t* counts,
-                        int32_t* offsets, int32_t* perm, int32_t* inv, int32_t* pperm,
-                        int32_t* n_padded, int tile_m, int32_t* tiles, int max_tiles,
-                        int32_t* n_tiles, hipStream_t s) {
+                        int32_t* offsets, int32_t* perm, int32_t* pperm, int32_t* n_padded,
+                        int tile_m, int32_t* tiles, int max_tiles, int32_t* n_tiles,
+                        hipStream_t s) {
   topk_kernel<<<(T + 3) / 4, 256, 0, s>>>(logits, nparts, bias, replay, T, E, K, ids, w);
-  permute_kernel<<<1, kPermThreads, 0, s>>>(ids, T * K, E, tile_m, counts, offsets, perm, inv,
-                                            pperm, n_padded, reinterpret_cast<int4*>(tiles),
-                                            max_tiles, n_tiles);
+  PermuteParams p;
+  p.ids = ids;
+  p.P = T * K;
+  p.E = E;
+  p.K = K;
+  p.tile_m = tile_m;
+  p.range = max(kPermRange, (p.P + kPermGrid - 1) / kPermGrid);
+  if (p.range > kMaxRange) p.range = kMaxRange;
+  p.counts = counts;
+  p.offsets = offsets;
+  p.perm = perm;
+  p.pperm = pperm;
+  p.n_padded = n_padded;
+  p.tiles = reinterpret_cast<int4*>(tiles);
+  p.max_tiles = max_tiles;
+  p.n_tiles = n_tiles;
+  permute_kernel<<<(p.P + p.range - 1) / p.range, kPermThreads, 0, s>>>(p);
   return hipGetLastError();
 }
 

@@ -151,3 +151,24 @@ def test_fp8_codec_on_gpu_matches_oracle(molt_lib):
     gq = _gpu(molt_lib, lw, x, 1)
     err = max_abs(gq[0].cpu().numpy(), o["out"])
     assert err <= 1e-2 * np.abs(o["out"]).max(), err
+
+
+@pytest.mark.parametrize("T,K,E", [(4683, 7, 128), (2601, 61, 256)])
+def test_permutation_many_pairs(molt_lib, T, K, E):
+    """Pair counts past one 64-pair range per permutation workgroup: 32781 pairs (ranges of
+    65, a count that is not a multiple of 4) and 158661 pairs (ranges of 310: several 64-pair
+    steps per wavefront). Replayed Zipf-skewed routes give hot experts many tiles; counts,
+    offsets and the permutation must equal the oracle's exactly and the outputs match."""
+    w = workloads.LAYER_BF16.scaled(n_experts=E, top_k=K, d_model=128, d_ff=64)
+    lw, x = _layer(w, 8, T)
+    g = np.random.Generator(np.random.Philox(11))
+    pz = 1.0 / np.arange(1, E + 1) ** 1.2
+    pz /= pz.sum()
+    replay = np.stack([g.choice(E, K, replace=False, p=pz) for _ in range(T)]).astype(np.int32)
+    print(f"case T={T} K={K} E={E}", flush=True)
+    o = _oracle(w, lw, x, T, replay)
+    out, ids, wts, counts, offsets, perm = [t.cpu().numpy() for t in _gpu(molt_lib, lw, x, K, torch.from_numpy(replay))]
+    assert (ids == replay).all()
+    assert (counts == o["counts"]).all() and (offsets == o["offsets"]).all()
+    assert (perm == o["perm"]).all()
+    assert max_abs(out, o["out"]) <= 2e-2
