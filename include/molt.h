@@ -474,6 +474,9 @@ typedef enum {
 } molt_prof_group;
 /* group_mask: bit g times group g (-1: all); nonzero starts and clears, 0 stops */
 int molt_profile_enable(int group_mask);
+/* time only every n-th launch of each enabled group (launches 0, n, 2n, ... counted per
+ * group from the last enable; default 1 = every launch). INVALID_ARG for n < 1. */
+int molt_profile_every(int n);
 int molt_profile_read(int group, double* total_ms, int* launches);
 
 #ifdef __cplusplus

@@ -66,6 +66,7 @@ _SIGS = {
     "molt_decoder_forward": (c_int, [ctypes.POINTER(MoltModel), ctypes.POINTER(MoltKV), c_int,
                                      c_int, c_vp, c_vp, c_vp, c_size, c_vp]),
     "molt_profile_enable": (c_int, [c_int]),
+    "molt_profile_every": (c_int, [c_int]),
     "molt_profile_read": (c_int, [c_int, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(c_int)]),
     "molt_verify_step_workspace_size": (c_size, [ctypes.POINTER(MoltModel), c_int, c_int, c_int]),
     "molt_verify_step": (c_int, [ctypes.POINTER(MoltModel), ctypes.POINTER(MoltKV), c_int, c_int,
@@ -617,8 +618,9 @@ def mtp_draft(target, mtp, kv, hidden, tokens, n_accepted, next_tokens, uniforms
 PROF_GROUPS = {"attention": 0, "expert_gemm": 1, "lm_head": 2, "sampler": 3, "projections": 4}
 
 
-def profile_enable(on=True):
-    """on: True (all groups), False (stop), or an iterable of group names to time."""
+def profile_enable(on=True, every=1):
+    """on: True (all groups), False (stop), or an iterable of group names to time; every:
+    time only launches 0, every, 2 every, ... of each group."""
     if on is True:
         mask = -1
     elif not on:
@@ -627,6 +629,7 @@ def profile_enable(on=True):
         mask = 0
         for g in on:
             mask |= 1 << PROF_GROUPS[g]
+    _check(load().molt_profile_every(every), "molt_profile_every")
     _check(load().molt_profile_enable(mask), "molt_profile_enable")
 
 

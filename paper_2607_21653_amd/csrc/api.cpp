@@ -39,6 +39,8 @@ int hip_status(hipError_t e, const char* where) {
 struct Profiler {
   static constexpr int kPairs = 4096;
   int mask = 0;                 // bit g: group g is timed
+  int every = 1;                // time launches 0, every, 2 every, ... of each group
+  int seen[8] = {};             // launches of each group since the last enable
   bool ready = false;
   hipEvent_t ev[2 * kPairs];
   int used = 0;
@@ -51,6 +53,7 @@ struct ProfScope {
   hipStream_t s;
   ProfScope(int grp, hipStream_t st) : s(st) {
     if (!((g_prof.mask >> grp) & 1) || g_prof.used >= Profiler::kPairs) return;
+    if (g_prof.seen[grp]++ % g_prof.every != 0) return;
     slot = g_prof.used++;
     g_prof.group[slot] = grp;
     hipEventRecord(g_prof.ev[2 * slot], s);
@@ -91,8 +94,17 @@ int molt_profile_enable(int group_mask) {
     }
     g_prof.ready = true;
   }
-  if (enable) g_prof.used = 0;
+  if (enable) {
+    g_prof.used = 0;
+    for (int& n : g_prof.seen) n = 0;
+  }
   g_prof.mask = group_mask;
+  return ok();
+}
+
+int molt_profile_every(int n) {
+  REQUIRE(n >= 1, "n = %d must be >= 1", n);
+  g_prof.every = n;
   return ok();
 }
 

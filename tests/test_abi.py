@@ -39,6 +39,12 @@ def test_version_and_error_string(L):
     assert isinstance(L.molt_last_error(), bytes)
 
 
+def test_profile_every_validation(L):
+    assert L.molt_profile_every(0) == INVALID
+    assert L.molt_profile_every(-3) == INVALID
+    assert L.molt_profile_every(1) == OK
+
+
 def test_workspace_queries(L):
     assert L.molt_spec_accept_workspace_size(128, 4, 151936) > 0
     assert L.molt_spec_accept_workspace_size(0, 4, 10) == 0

@@ -172,3 +172,17 @@ def test_permutation_many_pairs(molt_lib, T, K, E):
     assert (counts == o["counts"]).all() and (offsets == o["offsets"]).all()
     assert (perm == o["perm"]).all()
     assert max_abs(out, o["out"]) <= 2e-2
+
+
+def test_profile_every(molt_lib):
+    """Sampled kernel-group timing: with every = 3, four MoE calls (eight expert GEMM
+    launches) bracket launches 0, 3 and 6."""
+    w = workloads.LAYER_BF16
+    lw, x = _layer(w, 1, 64)
+    molt_lib.profile_enable(["expert_gemm"], every=3)
+    for _ in range(4):
+        _gpu(molt_lib, lw, x, w.top_k)
+    torch.cuda.synchronize()
+    molt_lib.profile_enable(False)
+    ms, n = molt_lib.profile_read("expert_gemm")
+    assert n == 3 and ms > 0
