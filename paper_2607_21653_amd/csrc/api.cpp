@@ -317,7 +317,7 @@ hipError_t run_moe(const MoeWs& m, const void* x, const uint8_t* xq, const float
                    const void* w_router, const float* bias, const void* w_gu, const void* w_d,
                    const float* s_gu, const float* s_d, int T, int d, int E, int K, int F,
                    molt_dtype act, molt_dtype wdt, const int32_t* replay, float* out,
-                   bool accumulate, hipStream_t s) {
+                   bool accumulate, hipStream_t s, const void* x_rows = nullptr) {
   hipError_t e;
   int nparts = 1;
   {
@@ -338,14 +338,18 @@ hipError_t run_moe(const MoeWs& m, const void* x, const uint8_t* xq, const float
     xq = m.xq;
     xs = m.xs;
   }
+  // bf16 experts with row-major token rows at hand: gate_up reads them through the
+  // permutation, no gathered copy
+  const bool rows = x_rows != nullptr && act == MOLT_BF16 && wdt == MOLT_BF16;
   const void* src = fp8 ? static_cast<const void*>(xq) : x;
-  if ((e = molt::launch_gather_tiled(src, m.pperm, K, m.n_padded, m.max_rows,
-                                     long(d) * dt_size(wdt), m.xt, s)) != hipSuccess)
+  if (!rows && (e = molt::launch_gather_tiled(src, m.pperm, K, m.n_padded, m.max_rows,
+                                              long(d) * dt_size(wdt), m.xt, s)) != hipSuccess)
     return e;
   {
     ProfScope ps(MOLT_PROF_EXPERT_GEMM, s);
-    if ((e = molt::launch_moe_gate_up(m.xt, xs, m.pperm, K, w_gu, s_gu, d, F, wdt, m.tiles,
-                                      m.n_tiles, m.max_tiles, m.tile_m, m.h, s)) != hipSuccess)
+    if ((e = molt::launch_moe_gate_up(m.xt, rows ? x_rows : nullptr, xs, m.pperm, K, w_gu, s_gu, d,
+                                      F, wdt, m.tiles, m.n_tiles, m.max_tiles, m.tile_m, m.h,
+                                      s)) != hipSuccess)
       return e;
   }
   if (fp8) {
@@ -403,7 +407,7 @@ int molt_moe_layer(const void* x, const void* w_router, const float* router_bias
   hipError_t e = molt::launch_pack_tiled(x, xt, T, long(d) * dt_size(act_dtype), s);
   if (e == hipSuccess)
     e = run_moe(m, xt, nullptr, nullptr, w_router, router_bias, w_gate_up, w_down, s_gate_up,
-                s_down, T, d, E, K, F, act_dtype, w_dtype, replay_ids, out, false, s);
+                s_down, T, d, E, K, F, act_dtype, w_dtype, replay_ids, out, false, s, x);
   const size_t P = size_t(T) * K;
   if (e == hipSuccess) e = copy_out(out_ids, m.ids, P * 4, s);
   if (e == hipSuccess) e = copy_out(out_weights, m.w, P * 4, s);
@@ -531,6 +535,7 @@ int model_ok(const molt_model* m, const molt_kv* kv, int B, int k, bool need_hea
 
 struct DecWs {
   void* y; uint8_t* yq; float* ys; float* qkv; void* q; void* attn; void* attn_ws; MoeWs moe;
+  void* y_rows;                   // bf16 experts: the pre-MoE y row-major (expert GEMM input)
   float* part; long part_elems;   // split-K partial sums of the QKV and O projections
   void* rope;                     // RoPE cos/sin of the step's positions, [T, D/2] f64 pairs
   int32_t* kv_slot;               // KV-cache slot of each token of the step (or -1)
@@ -547,6 +552,7 @@ DecWs carve_dec(molt::Carver& c, const molt_model* m, int B, int k, int max_bloc
     w.yq = c.take<uint8_t>(Tp * d);
     w.ys = c.take<float>(Tp);
   }
+  if (m->dtype == MOLT_BF16 && m->expert_dtype == MOLT_BF16) w.y_rows = c.take<uint8_t>(T * d * es);
   if (!(m->dtype == MOLT_BF16 && D == 128))   // else RoPE is fused into the QKV epilogue
     w.qkv = c.take<float>(T * (Hq + 2 * Hkv) * D);
   w.q = c.take<uint8_t>(T * Hq * D * es);
@@ -610,12 +616,12 @@ hipError_t run_decoder(const DecWs& w, const molt_model* m, const molt_kv* kv, i
     // x += O partials; y = RMSNorm(x) * moe_norm (+ fp8 codes)
     RUN(molt::launch_residual_norm(x, np > 1 ? w.part : nullptr, np > 1 ? np : 0, nullptr, nullptr,
                                    0, m->moe_norm[l], T, d, m->rms_eps, m->dtype, w.y,
-                                   fp8 ? w.yq : nullptr, fp8 ? w.ys : nullptr, s));
+                                   fp8 ? w.yq : nullptr, fp8 ? w.ys : nullptr, s, w.y_rows));
     RUN(run_moe(w.moe, w.y, fp8 ? w.yq : nullptr, fp8 ? w.ys : nullptr, m->w_router[l],
                 m->router_bias ? m->router_bias[l] : nullptr, m->w_gate_up[l], m->w_down[l],
                 fp8 ? m->s_gate_up[l] : nullptr, fp8 ? m->s_down[l] : nullptr, T, d,
                 m->n_experts, K, m->d_ff, m->dtype, m->expert_dtype,
-                replay ? replay + size_t(l) * T * K : nullptr, nullptr, false, s));
+                replay ? replay + size_t(l) * T * K : nullptr, nullptr, false, s, w.y_rows));
     if (routes) RUN(copy_out(routes + size_t(l) * T * K, w.moe.ids, size_t(T) * K * 4, s));
     // x += MoE combine; then the next layer's attention norm (or the final norm)
     const bool last = l + 1 == L;

@@ -37,7 +37,8 @@ __global__ __launch_bounds__(kThreads) void embed_kernel(const void* __restrict_
 //                                            split order; nparts = 0: none)
 //   x[t] += sum_j w[t, j] * o[t * K + j]     (MoE combine, slot order; o = NULL: none)
 //   y = x[t] / sqrt(mean(x[t]^2) + eps) * g  rounded to dt, tiled (g = NULL: no norm)
-// With yq, also the per-row fp8 code of y (s = amax|y| / 448, code = e4m3(y / s)).
+// With yq, also the per-row fp8 code of y (s = amax|y| / 448, code = e4m3(y / s)); with
+// y_rows (bf16), also y in row-major order (read by the expert GEMM through the permutation).
 // Each thread owns runs of 8 consecutive elements (d % 8 == 0, d <= 8 * 256 * kNormRuns),
 // kept in registers from the residual update to the stores: one 16-byte store of y per run
 // (8 bf16 are contiguous in the tiled layout).
@@ -55,7 +56,7 @@ __global__ __launch_bounds__(kThreads) void residual_norm_kernel(
     float* __restrict__ x, const float* __restrict__ part, int nparts, long part_stride,
     const float* __restrict__ o, const float* __restrict__ w, int K, const float* __restrict__ g,
     int d, float eps, molt_dtype dt, void* __restrict__ y, uint8_t* __restrict__ yq,
-    float* __restrict__ ys) {
+    float* __restrict__ ys, void* __restrict__ y_rows) {
   __shared__ float red[kThreads / kWave];
   const int t = blockIdx.x;
   float* xr = x + long(t) * d;
@@ -111,6 +112,9 @@ __global__ __launch_bounds__(kThreads) void residual_norm_kernel(
         pk[e] = uint32_t(f32_to_bf16(v[r][2 * e])) | (uint32_t(f32_to_bf16(v[r][2 * e + 1])) << 16);
       *reinterpret_cast<uint4*>(static_cast<uint8_t*>(y) + tiled_offset(t, 2L * i, 2L * d)) =
           make_uint4(pk[0], pk[1], pk[2], pk[3]);
+      if (y_rows)
+        *reinterpret_cast<uint4*>(static_cast<uint8_t*>(y_rows) + 2L * (long(t) * d + i)) =
+            make_uint4(pk[0], pk[1], pk[2], pk[3]);
     } else {
       uint8_t* yb = static_cast<uint8_t*>(y);
       *reinterpret_cast<float4*>(yb + tiled_offset(t, 4L * i, 4L * d)) =
@@ -402,9 +406,10 @@ hipError_t launch_embed(const void* table, const int32_t* tokens, int T, int d, 
 
 hipError_t launch_residual_norm(float* x, const float* part, int nparts, const float* o,
                                 const float* w, int K, const float* g, int T, int d, float eps,
-                                molt_dtype dt, void* y, uint8_t* yq, float* ys, hipStream_t s) {
+                                molt_dtype dt, void* y, uint8_t* yq, float* ys, hipStream_t s,
+                                void* y_rows) {
   residual_norm_kernel<<<T, kThreads, 0, s>>>(x, part, nparts, long(T) * d, o, w, K, g, d, eps, dt,
-                                              y, yq, ys);
+                                              y, yq, ys, dt == MOLT_BF16 ? y_rows : nullptr);
   return hipGetLastError();
 }
 

@@ -115,10 +115,11 @@ MOLT_DEV StreamTile stream_geometry(const GemmParams& p, int id, int nk, int wav
 // HBM once and then hits that XCD's L2. Launching one workgroup per pair left the chip
 // at 50-80% of its resident workgroups on average (dispatch gaps between short tiles).
 // CHAIN requires K slices in multiples of 4 (the slot pattern then lines up across tiles).
-template <int BM, bool FP8, int MODE, bool CHAIN>
+template <int BM, bool FP8, int MODE, bool CHAIN, bool ROWS>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(BM <= 64 ? 3 : 2)))
 void stream_gemm_kernel(GemmParams p) {
   static_assert(MODE == kGateUp || MODE == kDown, "grouped modes");
+  static_assert(!ROWS || (!FP8 && MODE == kGateUp && !CHAIN), "row gather: bf16 gate_up");
   constexpr int MS = BM / 32;                        // 32-row MFMA tiles per wavefront
   constexpr int kElem = FP8 ? 1 : 2;
   // weight slices in flight per wavefront (each 4 KB slice of a wavefront's 32 weight rows
@@ -153,17 +154,31 @@ void stream_gemm_kernel(GemmParams p) {
 #pragma unroll
     for (int c = 0; c < 4; ++c) f.c[c] = __builtin_nontemporal_load(reinterpret_cast<const int32x4_t*>(src + 1024 * c));
   };
+  // ROWS: thread t copies piece t % 8 (16 bytes) of row t / 8 of each 32-row block from the
+  // token's row-major row (roff: its byte offset, set per tile), so each load instruction
+  // reads 8 whole 128-byte row slices; in LDS the row's 8 pieces sit at piece ^ swz(row)
+  // (conflict-free fragment reads and stores)
+  long roff[ROWS ? MS : 1];
+  const unsigned rsto = ROWS ? (threadIdx.x / 8) * 128 + ((threadIdx.x % 8) ^ ((threadIdx.x / 16) % 8)) * 16
+                             : threadIdx.x * 16;
 #define MOLT_GLOAD(ST, T, KB)                                                         \
   {                                                                                   \
     const long off_ = slice(T, KB);                                                   \
-    _Pragma("unroll") for (int b_ = 0; b_ < MS; ++b_)                                 \
-        ST[b_] = *reinterpret_cast<const int32x4_t*>((T).a + long(min(b_, (T).a_last)) * 32 * RB + off_ + aoff); \
+    if (ROWS) {                                                                       \
+      _Pragma("unroll") for (int b_ = 0; b_ < MS; ++b_)                               \
+          ST[b_] = *reinterpret_cast<const int32x4_t*>(static_cast<const uint8_t*>(p.A) + roff[b_ % (ROWS ? MS : 1)] + (off_ >> 5) + (threadIdx.x % 8) * 16); \
+    } else {                                                                          \
+      _Pragma("unroll") for (int b_ = 0; b_ < MS; ++b_)                               \
+          ST[b_] = *reinterpret_cast<const int32x4_t*>((T).a + long(min(b_, (T).a_last)) * 32 * RB + off_ + aoff); \
+    }                                                                                 \
   }
 #define MOLT_SSTORE(ST, BUF)                                                          \
   {                                                                                   \
     _Pragma("unroll") for (int b_ = 0; b_ < MS; ++b_)                                 \
-        *reinterpret_cast<int32x4_t*>(&alds[BUF][b_ * 4096 + threadIdx.x * 16]) = ST[b_]; \
+        *reinterpret_cast<int32x4_t*>(&alds[BUF][b_ * 4096 + rsto]) = ST[b_];         \
   }
+  // ROWS fragment reads: lane l takes row l % 32, piece 4 (l / 32) + c for k-step c
+  const unsigned rsw = (4 * (lane / 32)) ^ ((lane % 32 / 2) % 8);
   int32x4_t st0[MS], st1[MS];
   Slice16 wb[WD];
   floatx16_t acc[MS];
@@ -183,6 +198,15 @@ void stream_gemm_kernel(GemmParams p) {
       const int kn = k8 + stride;
       more = kn < chunk && first + kn < total;
       if (CHAIN && more) gn = stream_geometry<MODE>(p, first + kn, nk, wave);
+    }
+    if (ROWS) {
+      // rows past the tile's end (and padding rows) read token 0: their outputs are not stored
+#pragma unroll
+      for (int b_ = 0; b_ < MS; ++b_) {
+        const int r = g.row0 + 32 * b_ + int(threadIdx.x / 8);
+        const int pr = r < g.row1 ? p.perm[r] : -1;
+        roff[b_ % (ROWS ? MS : 1)] = pr < 0 ? 0 : long(pr / p.ktop) * RB;
+      }
     }
     if (!primed) {
       MOLT_GLOAD(st0, g, 0);
@@ -207,12 +231,13 @@ void stream_gemm_kernel(GemmParams p) {
     // last slice instead cost the 12-slice down GEMM a third more weight loads.
 #define MOLT_STEP(U, ST_NEXT, W, K, TAIL)                                                           \
   {                                                                                                  \
-    const uint8_t* base_ = alds[U] + lane * 16;                                                      \
+    const uint8_t* base_ = alds[U] + (ROWS ? (lane % 32) * 128 : lane * 16);                         \
     if (!FP8) {                                                                                      \
       _Pragma("unroll") for (int c = 0; c < 4; ++c) {                                                \
         const bf16x8_t bv = *reinterpret_cast<const bf16x8_t*>(&wb[W].c[c]);                         \
+        const unsigned fo_ = ROWS ? ((rsw ^ c) * 16) : c * 1024;                                     \
         _Pragma("unroll") for (int i = 0; i < MS; ++i) acc[i] =                                      \
-            mfma(*reinterpret_cast<const bf16x8_t*>(base_ + i * 4096 + c * 1024), bv, acc[i]);       \
+            mfma(*reinterpret_cast<const bf16x8_t*>(base_ + i * 4096 + fo_), bv, acc[i]);            \
       }                                                                                              \
     } else {                                                                                         \
       _Pragma("unroll") for (int c = 0; c < 2; ++c) {                                                \
@@ -356,28 +381,30 @@ int resident_grid(K kernel) {
   return (cus * per_cu) / 8 * 8 > 8 ? (cus * per_cu) / 8 * 8 : 8;
 }
 
-template <bool FP8, int MODE, bool CHAIN>
+template <bool FP8, int MODE, bool CHAIN, bool ROWS = false>
 hipError_t run_stream_k(GemmParams p, int tile_m, hipStream_t s) {
   // resident workgroups per kernel, queried once per process (one device model)
-  static const int r32 = resident_grid(stream_gemm_kernel<32, FP8, MODE, CHAIN>);
-  static const int r64 = resident_grid(stream_gemm_kernel<64, FP8, MODE, CHAIN>);
-  static const int r128 = resident_grid(stream_gemm_kernel<128, FP8, MODE, CHAIN>);
+  static const int r32 = resident_grid(stream_gemm_kernel<32, FP8, MODE, CHAIN, ROWS>);
+  static const int r64 = resident_grid(stream_gemm_kernel<64, FP8, MODE, CHAIN, ROWS>);
+  static const int r128 = resident_grid(stream_gemm_kernel<128, FP8, MODE, CHAIN, ROWS>);
   const int pairs = (p.n_mtiles * p.n_ntiles + 7) / 8 * 8;   // upper bound of the live pairs
   const int cap = tile_m == 32 ? r32 : tile_m == 64 ? r64 : r128;
   const int grid = pairs < cap ? pairs : cap;
-  if (tile_m == 32) stream_gemm_kernel<32, FP8, MODE, CHAIN><<<grid, kThreads, 0, s>>>(p);
-  else if (tile_m == 64) stream_gemm_kernel<64, FP8, MODE, CHAIN><<<grid, kThreads, 0, s>>>(p);
-  else stream_gemm_kernel<128, FP8, MODE, CHAIN><<<grid, kThreads, 0, s>>>(p);
+  if (tile_m == 32) stream_gemm_kernel<32, FP8, MODE, CHAIN, ROWS><<<grid, kThreads, 0, s>>>(p);
+  else if (tile_m == 64) stream_gemm_kernel<64, FP8, MODE, CHAIN, ROWS><<<grid, kThreads, 0, s>>>(p);
+  else stream_gemm_kernel<128, FP8, MODE, CHAIN, ROWS><<<grid, kThreads, 0, s>>>(p);
   return hipGetLastError();
 }
 
 template <bool FP8, int MODE>
-hipError_t run_stream(GemmParams p, int tile_m, hipStream_t s) {
+hipError_t run_stream(GemmParams p, int tile_m, hipStream_t s, bool rows = false) {
   const long nk = long(p.K) * (FP8 ? 1 : 2) / kRowBytes;
   // chained in bf16 for down only: its 12-slice tiles gained (85 -> 82 us per launch at
   // T*K = 5120), gate_up's 32-slice tiles did not (159 -> 161 us)
   if constexpr (!FP8 && MODE == kDown)
     if (nk % 4 == 0) return run_stream_k<false, MODE, true>(p, tile_m, s);
+  if constexpr (!FP8 && MODE == kGateUp)
+    if (rows) return run_stream_k<false, MODE, false, true>(p, tile_m, s);
   return run_stream_k<FP8, MODE, false>(p, tile_m, s);
 }
 
@@ -920,13 +947,15 @@ hipError_t launch_qkv_rope(const void* A, const void* Bw, int M, int K_in, int H
   return hipGetLastError();
 }
 
-hipError_t launch_moe_gate_up(const void* a, const float* a_scale, const int32_t* pperm, int K_top,
-                              const void* w_gu, const float* s_gu, int d, int F, molt_dtype wdt,
-                              const int32_t* tiles, const int32_t* n_tiles, int max_tiles,
-                              int tile_m, void* h, hipStream_t s) {
+hipError_t launch_moe_gate_up(const void* a, const void* a_rows, const float* a_scale,
+                              const int32_t* pperm, int K_top, const void* w_gu, const float* s_gu,
+                              int d, int F, molt_dtype wdt, const int32_t* tiles,
+                              const int32_t* n_tiles, int max_tiles, int tile_m, void* h,
+                              hipStream_t s) {
   GemmParams p{};
   p.n_tiles_live = n_tiles;
-  p.A = a; p.B = w_gu; p.C = h; p.N = F; p.K = d; p.ldc = F;
+  p.A = a_rows != nullptr && wdt == MOLT_BF16 ? a_rows : a;
+  p.B = w_gu; p.C = h; p.N = F; p.K = d; p.ldc = F;
   p.tiles = reinterpret_cast<const int4*>(tiles);
   p.n_mtiles = max_tiles;
   p.perm = pperm; p.ktop = K_top;
@@ -938,7 +967,7 @@ hipError_t launch_moe_gate_up(const void* a, const float* a_scale, const int32_t
   }
   p.n_ntiles = F / (kBN / 2);
   if (wdt == MOLT_FP8_E4M3) return run_stream<true, kGateUp>(p, tile_m, s);
-  return run_stream<false, kGateUp>(p, tile_m, s);
+  return run_stream<false, kGateUp>(p, tile_m, s, a_rows != nullptr);
 }
 
 hipError_t launch_moe_down(const void* a, const float* a_scale, const int32_t* pperm,
