@@ -331,6 +331,7 @@ hipError_t run_moe(const MoeWs& m, const void* x, const uint8_t* xq, const float
                               m.tiles, m.max_tiles, m.n_tiles, s)) != hipSuccess)
     return e;
   const bool fp8 = wdt == MOLT_FP8_E4M3;
+  const bool xq_given = xq != nullptr;
   if (fp8 && xq == nullptr) {
     if ((e = molt::launch_quant_rows_tiled(static_cast<const uint16_t*>(x), nullptr, nullptr, T, d,
                                            m.xq, m.xs, s)) != hipSuccess)
@@ -338,9 +339,10 @@ hipError_t run_moe(const MoeWs& m, const void* x, const uint8_t* xq, const float
     xq = m.xq;
     xs = m.xs;
   }
-  // bf16 experts with row-major token rows at hand: gate_up reads them through the
-  // permutation, no gathered copy
-  const bool rows = x_rows != nullptr && act == MOLT_BF16 && wdt == MOLT_BF16;
+  // row-major token rows at hand (bf16 rows of x for bf16 experts, the caller's fp8 codes
+  // for fp8 experts): gate_up reads them through the permutation, no gathered copy
+  const bool rows = x_rows != nullptr &&
+                    (wdt == MOLT_BF16 ? act == MOLT_BF16 : wdt == MOLT_FP8_E4M3 && xq_given);
   const void* src = fp8 ? static_cast<const void*>(xq) : x;
   if (!rows && (e = molt::launch_gather_tiled(src, m.pperm, K, m.n_padded, m.max_rows,
                                               long(d) * dt_size(wdt), m.xt, s)) != hipSuccess)
@@ -535,7 +537,8 @@ int model_ok(const molt_model* m, const molt_kv* kv, int B, int k, bool need_hea
 
 struct DecWs {
   void* y; uint8_t* yq; float* ys; float* qkv; void* q; void* attn; void* attn_ws; MoeWs moe;
-  void* y_rows;                   // bf16 experts: the pre-MoE y row-major (expert GEMM input)
+  void* y_rows;                   // the pre-MoE y row-major (bf16 experts) or its fp8 codes
+                                  // row-major (fp8 experts): the expert GEMM's input
   float* part; long part_elems;   // split-K partial sums of the QKV and O projections
   void* rope;                     // RoPE cos/sin of the step's positions, [T, D/2] f64 pairs
   int32_t* kv_slot;               // KV-cache slot of each token of the step (or -1)
@@ -553,6 +556,7 @@ DecWs carve_dec(molt::Carver& c, const molt_model* m, int B, int k, int max_bloc
     w.ys = c.take<float>(Tp);
   }
   if (m->dtype == MOLT_BF16 && m->expert_dtype == MOLT_BF16) w.y_rows = c.take<uint8_t>(T * d * es);
+  if (m->expert_dtype == MOLT_FP8_E4M3) w.y_rows = c.take<uint8_t>(T * d);
   if (!(m->dtype == MOLT_BF16 && D == 128))   // else RoPE is fused into the QKV epilogue
     w.qkv = c.take<float>(T * (Hq + 2 * Hkv) * D);
   w.q = c.take<uint8_t>(T * Hq * D * es);
@@ -616,7 +620,9 @@ hipError_t run_decoder(const DecWs& w, const molt_model* m, const molt_kv* kv, i
     // x += O partials; y = RMSNorm(x) * moe_norm (+ fp8 codes)
     RUN(molt::launch_residual_norm(x, np > 1 ? w.part : nullptr, np > 1 ? np : 0, nullptr, nullptr,
                                    0, m->moe_norm[l], T, d, m->rms_eps, m->dtype, w.y,
-                                   fp8 ? w.yq : nullptr, fp8 ? w.ys : nullptr, s, w.y_rows));
+                                   fp8 ? w.yq : nullptr, fp8 ? w.ys : nullptr, s,
+                                   fp8 ? nullptr : w.y_rows,
+                                   fp8 ? static_cast<uint8_t*>(w.y_rows) : nullptr));
     RUN(run_moe(w.moe, w.y, fp8 ? w.yq : nullptr, fp8 ? w.ys : nullptr, m->w_router[l],
                 m->router_bias ? m->router_bias[l] : nullptr, m->w_gate_up[l], m->w_down[l],
                 fp8 ? m->s_gate_up[l] : nullptr, fp8 ? m->s_down[l] : nullptr, T, d,

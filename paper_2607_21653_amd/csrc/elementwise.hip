@@ -38,7 +38,8 @@ __global__ __launch_bounds__(kThreads) void embed_kernel(const void* __restrict_
 //   x[t] += sum_j w[t, j] * o[t * K + j]     (MoE combine, slot order; o = NULL: none)
 //   y = x[t] / sqrt(mean(x[t]^2) + eps) * g  rounded to dt, tiled (g = NULL: no norm)
 // With yq, also the per-row fp8 code of y (s = amax|y| / 448, code = e4m3(y / s)); with
-// y_rows (bf16), also y in row-major order (read by the expert GEMM through the permutation).
+// y_rows (bf16) and yq_rows, also y and its codes in row-major order (read by the expert
+// GEMM through the permutation).
 // Each thread owns runs of 8 consecutive elements (d % 8 == 0, d <= 8 * 256 * kNormRuns),
 // kept in registers from the residual update to the stores: one 16-byte store of y per run
 // (8 bf16 are contiguous in the tiled layout).
@@ -56,7 +57,7 @@ __global__ __launch_bounds__(kThreads) void residual_norm_kernel(
     float* __restrict__ x, const float* __restrict__ part, int nparts, long part_stride,
     const float* __restrict__ o, const float* __restrict__ w, int K, const float* __restrict__ g,
     int d, float eps, molt_dtype dt, void* __restrict__ y, uint8_t* __restrict__ yq,
-    float* __restrict__ ys, void* __restrict__ y_rows) {
+    float* __restrict__ ys, void* __restrict__ y_rows, uint8_t* __restrict__ yq_rows) {
   __shared__ float red[kThreads / kWave];
   const int t = blockIdx.x;
   float* xr = x + long(t) * d;
@@ -136,6 +137,7 @@ __global__ __launch_bounds__(kThreads) void residual_norm_kernel(
       for (int e = 0; e < 8; ++e) c[e / 4] |= f32_to_fp8e4m3(v[r][e] / sc) << (8 * (e % 4));
     }
     *reinterpret_cast<uint2*>(yq + tiled_offset(t, i, d)) = make_uint2(c[0], c[1]);
+    if (yq_rows) *reinterpret_cast<uint2*>(yq_rows + long(t) * d + i) = make_uint2(c[0], c[1]);
   }
   if (threadIdx.x == 0) ys[t] = sc;
 }
@@ -407,9 +409,10 @@ hipError_t launch_embed(const void* table, const int32_t* tokens, int T, int d, 
 hipError_t launch_residual_norm(float* x, const float* part, int nparts, const float* o,
                                 const float* w, int K, const float* g, int T, int d, float eps,
                                 molt_dtype dt, void* y, uint8_t* yq, float* ys, hipStream_t s,
-                                void* y_rows) {
+                                void* y_rows, uint8_t* yq_rows) {
   residual_norm_kernel<<<T, kThreads, 0, s>>>(x, part, nparts, long(T) * d, o, w, K, g, d, eps, dt,
-                                              y, yq, ys, dt == MOLT_BF16 ? y_rows : nullptr);
+                                              y, yq, ys, dt == MOLT_BF16 ? y_rows : nullptr,
+                                              yq ? yq_rows : nullptr);
   return hipGetLastError();
 }
 

@@ -119,7 +119,7 @@ template <int BM, bool FP8, int MODE, bool CHAIN, bool ROWS>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(BM <= 64 ? 3 : 2)))
 void stream_gemm_kernel(GemmParams p) {
   static_assert(MODE == kGateUp || MODE == kDown, "grouped modes");
-  static_assert(!ROWS || (!FP8 && MODE == kGateUp && !CHAIN), "row gather: bf16 gate_up");
+  static_assert(!ROWS || (MODE == kGateUp && !CHAIN), "row gather: gate_up");
   constexpr int MS = BM / 32;                        // 32-row MFMA tiles per wavefront
   constexpr int kElem = FP8 ? 1 : 2;
   // weight slices in flight per wavefront (each 4 KB slice of a wavefront's 32 weight rows
@@ -243,9 +243,11 @@ void stream_gemm_kernel(GemmParams p) {
       _Pragma("unroll") for (int c = 0; c < 2; ++c) {                                                \
         const int32x4_t w0 = wb[W].c[2 * c], w1 = wb[W].c[2 * c + 1];                                \
         const int32x8_t bv = int32x8_t{w0[0], w0[1], w0[2], w0[3], w1[0], w1[1], w1[2], w1[3]};     \
+        const unsigned lo_ = ROWS ? ((rsw ^ (2 * c)) * 16) : 2 * c * 1024;                          \
+        const unsigned hi_ = ROWS ? ((rsw ^ (2 * c + 1)) * 16) : (2 * c + 1) * 1024;                \
         _Pragma("unroll") for (int i = 0; i < MS; ++i) {                                             \
-          const int32x4_t lo = *reinterpret_cast<const int32x4_t*>(base_ + i * 4096 + 2 * c * 1024); \
-          const int32x4_t hi = *reinterpret_cast<const int32x4_t*>(base_ + i * 4096 + (2 * c + 1) * 1024); \
+          const int32x4_t lo = *reinterpret_cast<const int32x4_t*>(base_ + i * 4096 + lo_);          \
+          const int32x4_t hi = *reinterpret_cast<const int32x4_t*>(base_ + i * 4096 + hi_);          \
           acc[i] = mfma(int32x8_t{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]}, bv, acc[i]); \
         }                                                                                            \
       }                                                                                              \
@@ -403,8 +405,8 @@ hipError_t run_stream(GemmParams p, int tile_m, hipStream_t s, bool rows = false
   // T*K = 5120), gate_up's 32-slice tiles did not (159 -> 161 us)
   if constexpr (!FP8 && MODE == kDown)
     if (nk % 4 == 0) return run_stream_k<false, MODE, true>(p, tile_m, s);
-  if constexpr (!FP8 && MODE == kGateUp)
-    if (rows) return run_stream_k<false, MODE, false, true>(p, tile_m, s);
+  if constexpr (MODE == kGateUp)
+    if (rows) return run_stream_k<FP8, MODE, false, true>(p, tile_m, s);
   return run_stream_k<FP8, MODE, false>(p, tile_m, s);
 }
 
@@ -954,7 +956,7 @@ hipError_t launch_moe_gate_up(const void* a, const void* a_rows, const float* a_
                               hipStream_t s) {
   GemmParams p{};
   p.n_tiles_live = n_tiles;
-  p.A = a_rows != nullptr && wdt == MOLT_BF16 ? a_rows : a;
+  p.A = a_rows != nullptr && wdt != MOLT_F32 ? a_rows : a;
   p.B = w_gu; p.C = h; p.N = F; p.K = d; p.ldc = F;
   p.tiles = reinterpret_cast<const int4*>(tiles);
   p.n_mtiles = max_tiles;
@@ -966,7 +968,7 @@ hipError_t launch_moe_gate_up(const void* a, const void* a_rows, const float* a_
     return hipGetLastError();
   }
   p.n_ntiles = F / (kBN / 2);
-  if (wdt == MOLT_FP8_E4M3) return run_stream<true, kGateUp>(p, tile_m, s);
+  if (wdt == MOLT_FP8_E4M3) return run_stream<true, kGateUp>(p, tile_m, s, a_rows != nullptr);
   return run_stream<false, kGateUp>(p, tile_m, s, a_rows != nullptr);
 }
 

@@ -52,11 +52,12 @@ hipError_t launch_embed(const void* table, const int32_t* tokens, int T, int d, 
 // x[t] += sum of nparts split-K partials (part[s * T * d ..], split order) and, with o, the
 // MoE combine sum_j w[t, j] o[t * K + j]; then with g: y = rmsnorm(x) * g in act dtype,
 // tiled layout (rows padded to 32 by the caller's allocation), optionally with its fp8
-// row codes (tiled) and scales, and (bf16) a row-major copy y_rows
+// row codes (tiled) and scales, and row-major copies of y (y_rows, bf16) and of its codes
+// (yq_rows)
 hipError_t launch_residual_norm(float* x, const float* part, int nparts, const float* o,
                                 const float* w, int K, const float* g, int T, int d, float eps,
                                 molt_dtype dt, void* y, uint8_t* yq, float* ys, hipStream_t s,
-                                void* y_rows = nullptr);
+                                void* y_rows = nullptr, uint8_t* yq_rows = nullptr);
 // RoPE cos/sin of the step's B*(1+k) positions (f64 pairs, [T, D/2]), shared by all layers;
 // with kv_slot also each token's KV-cache slot (block * 16 + position % 16, -1 when the block
 // table entry is out of range)
@@ -127,9 +128,9 @@ hipError_t launch_qkv_rope(const void* A, const void* Bw, int M, int K_in, int H
                            void* v_cache, hipStream_t s);
 // Grouped expert GEMMs over the tile table built by launch_route. bf16/fp8: A and the
 // weights in the tiled layout, gate_up writes h tiled; f32: row-major A and h, tiled
-// weights. Rows are padded-order; down writes o[pair]. bf16 gate_up with a_rows (the
-// token rows, row-major [T, K]) reads each padded row's token row through pperm instead
-// of the gathered copy a.
+// weights. Rows are padded-order; down writes o[pair]. gate_up with a_rows (the token
+// rows in the expert dtype, row-major [T, K]) reads each padded row's token row through
+// pperm instead of the gathered copy a.
 hipError_t launch_moe_gate_up(const void* a, const void* a_rows, const float* a_scale,
                               const int32_t* pperm, int K_top, const void* w_gu, const float* s_gu,
                               int d, int F, molt_dtype wdt, const int32_t* tiles,
