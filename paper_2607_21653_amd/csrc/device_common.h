@@ -250,7 +250,12 @@ MOLT_DEV float block_max_dpp(float v, float* red) {
   return r;
 }
 
-MOLT_DEV float silu(float x) { return x / (1.0f + expf(-x)); }
+// SiLU x * sigmoid(x) with the hardware exp2 and reciprocal (v_exp_f32, v_rcp_f32): exp(-x)
+// = 2^(-x log2 e); relative error ~1e-6 for |x| <= 10, limits x and -0 for large |x|.
+// (A full-precision expf and division made the expert GEMM epilogues VALU-bound.)
+MOLT_DEV float silu(float x) {
+  return x * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(-x * 1.4426950408889634f));
+}
 
 // ---------------------------------------------------------------- tiled operand layout
 // The grouped expert GEMMs keep their operands (expert weights, gathered activations, the

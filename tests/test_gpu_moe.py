@@ -186,3 +186,19 @@ def test_profile_every(molt_lib):
     molt_lib.profile_enable(False)
     ms, n = molt_lib.profile_read("expert_gemm")
     assert n == 3 and ms > 0
+
+
+def test_fp8_zipf_many_tiles(molt_lib):
+    """fp8 experts at T = 1024 (8192 pairs) under Zipf routing: the popular experts hold
+    hundreds of rows (several 128-row tiles each, ragged last tiles), the rest a few."""
+    w = workloads.FP8_ZIPF
+    T = 1024
+    lw, x = _layer(w, 7, T)
+    print(f"case fp8 zipf T={T}", flush=True)
+    g = _gpu(molt_lib, lw, x, w.top_k)
+    o = _oracle(w, lw, x, T)
+    counts = g[3].cpu().numpy()
+    big = np.sort(counts[counts >= 256])[::-1]
+    print("experts with >= 256 pairs", big.tolist(), flush=True)
+    assert len(big) >= 2 and (big % 128 != 0).all()
+    _check(w, o, g, 2e-2)

@@ -137,6 +137,43 @@ def test_bf16_decoder_layer(molt_lib, fp8):
     assert (gr[ordered] == r["ids"][ordered]).all()
 
 
+def test_fp8_decoder_layer_zipf(molt_lib):
+    """fp8 experts, B = 64, k = 8 (576 tokens) under Zipf routing: the popular experts span
+    several 128-row tiles, their rows read through the permutation from the RMSNorm's
+    row-major codes."""
+    w = workloads.FP8_ZIPF.scaled(batch=64, k=8, ctx_lo=100, ctx_hi=600)
+    cfg = oracle_cfg(w)
+    seed = 13
+    layout = workloads.make_kv_layout(w, seed)
+    lw = workloads.make_layer_weights(w, seed, 0)
+    kc, vc = workloads.make_kv_cache(w, layout, seed, 0)
+    x = workloads.make_hidden(w, seed)
+    print(f"case fp8 zipf decoder T={x.shape[0]}", flush=True)
+    model = model_from(w, [lw], None, molt_lib)
+    kv = molt_lib.KVCache([dev(kc)], [dev(vc)], dev(torch.from_numpy(layout.block_tables)),
+                          dev(torch.from_numpy(layout.context_lens)))
+    xg = dev(x.clone())
+    routes = molt_lib.decoder_forward(model, kv, w.batch, w.k, xg, want_routes=True)
+    torch.cuda.synchronize()
+    gr = routes.cpu().numpy()[0]
+    counts = np.bincount(gr.ravel(), minlength=w.n_experts)
+    print("experts with >= 256 pairs:", np.sort(counts[counts >= 256])[::-1].tolist(), flush=True)
+    assert (counts >= 256).sum() >= 2
+    lh = layer_host(lw)
+    xo = omodel.attention_block(host(x), lh, omodel.widen_cache(host(kc), w.dtype),
+                                omodel.widen_cache(host(vc), w.dtype), layout.block_tables,
+                                layout.context_lens, w.k, cfg)
+    xo, r = omodel.moe_block(xo, lh, cfg)
+    same = _route_sets_agree(gr, r["ids"], r["margin"])
+    g = xg.cpu().numpy()
+    d = (g[same] - xo[same]).astype(np.float64)
+    err = max_abs(g[same], xo[same])
+    rel = float(np.sqrt((d * d).mean() / (xo[same].astype(np.float64) ** 2).mean()))
+    print(f"max |x - oracle| = {err:.3e}, relative rms {rel:.2e} ({(~same).sum()} near-tie tokens excluded)",
+          flush=True)
+    assert err <= 5e-2 and rel <= 1e-2
+
+
 def test_bf16_decoder_layer_many_tokens(molt_lib):
     """T = 320 tokens: the dense projections run 128-row tiles with a ragged 64-row tail."""
     w = workloads.LAYER_BF16.scaled(batch=64, k=4, ctx_lo=40, ctx_hi=300)
