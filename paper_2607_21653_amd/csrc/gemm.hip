@@ -22,6 +22,9 @@ constexpr int kRowBytes = 128;   // K-slice, bytes
 
 enum Mode { kDense = 0, kGateUp = 1, kDown = 2 };
 
+// s_waitcnt immediate: vmcnt(0), expcnt(7) and lgkmcnt(15) (no wait on those two)
+constexpr int kWaitVmcnt0 = (7 << 4) | (15 << 8);
+
 struct GemmParams {
   const void* A;           // tiled. dense: [M, K]; gate_up: gathered rows [R, K]; down: h [R, K]
   const void* B;           // tiled. dense: [N, K]; gate_up: [E, 2F, K]; down: [E, N, K]
@@ -197,7 +200,9 @@ void stream_gemm_kernel(GemmParams p) {
     {
       const int kn = k8 + stride;
       more = kn < chunk && first + kn < total;
-      if (CHAIN && more) gn = stream_geometry<MODE>(p, first + kn, nk, wave);
+      // the next tile's table entry is read here, not after the epilogue: a load issued
+      // behind the epilogue's stores would have to wait for all of them
+      if (more) gn = stream_geometry<MODE>(p, first + kn, nk, wave);
     }
     if (ROWS) {
       // rows past the tile's end (and padding rows) read token 0: their outputs are not stored
@@ -296,7 +301,30 @@ void stream_gemm_kernel(GemmParams p) {
       for (int i = 0; i < MS; ++i)
 #pragma unroll
         for (int e = 0; e < 16; ++e) ep[(32 * i + 8 * (e / 4) + 4 * lgrp + (e % 4)) * 128 + 32 * wave + lcol] = acc[i][e];
+      // fp8 scales of the thread's units (its 8 columns are the same in every unit) are all
+      // loaded before the first store: a load issued after a store has to wait for it
+      float sxv[MS];
+      float4 swv[4];
+      if (FP8) {
+        const float* sw = p.b_scale + long(g.expert) * p.b_scale_ld + g.n0 + (threadIdx.x & 7) * 8;
+        swv[0] = *reinterpret_cast<const float4*>(sw);
+        swv[1] = *reinterpret_cast<const float4*>(sw + 4);
+        swv[2] = *reinterpret_cast<const float4*>(sw + p.N);
+        swv[3] = *reinterpret_cast<const float4*>(sw + p.N + 4);
+        int pr[MS];
+#pragma unroll
+        for (int j = 0; j < MS; ++j) {
+          const int grow = g.row0 + int((threadIdx.x + kThreads * j) >> 3);
+          pr[j] = grow < g.row1 ? p.perm[grow] : 0;
+        }
+#pragma unroll
+        for (int j = 0; j < MS; ++j) sxv[j] = p.a_scale[pr[j] / p.ktop];
+      }
       lds_barrier();
+      // the scales are in before the first store: with the stores behind per-unit branches the
+      // compiler would otherwise wait for every earlier store before each unit's scale use
+      // (s_waitcnt vmcnt(0), expcnt and lgkmcnt left open)
+      if (FP8) __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
       const long hrb = 2L * p.N;
 #pragma unroll
       for (int j = 0; j < MS; ++j) {
@@ -310,12 +338,13 @@ void stream_gemm_kernel(GemmParams p) {
         float gv[8] = {g0.x, g0.y, g0.z, g0.w, g1.x, g1.y, g1.z, g1.w};
         float uv[8] = {u0.x, u0.y, u0.z, u0.w, u1.x, u1.y, u1.z, u1.w};
         if (FP8) {
-          const float sx = p.a_scale[p.perm[grow] / p.ktop];
-          const float* sw = p.b_scale + long(g.expert) * p.b_scale_ld + g.n0 + cb;
+          const float sx = sxv[j];
+          const float swg[8] = {swv[0].x, swv[0].y, swv[0].z, swv[0].w, swv[1].x, swv[1].y, swv[1].z, swv[1].w};
+          const float swu[8] = {swv[2].x, swv[2].y, swv[2].z, swv[2].w, swv[3].x, swv[3].y, swv[3].z, swv[3].w};
 #pragma unroll
           for (int q = 0; q < 8; ++q) {
-            gv[q] *= sx * sw[q];
-            uv[q] *= sx * sw[p.N + q];
+            gv[q] *= sx * swg[q];
+            uv[q] *= sx * swu[q];
           }
         }
         uint32_t packed[4];
@@ -329,6 +358,23 @@ void stream_gemm_kernel(GemmParams p) {
     } else {
       // per-pair expert output, f32, row = pair index (token * K + slot). Through LDS, so
       // that each thread writes 4 consecutive columns of a row with one 16-byte store.
+      constexpr int kUnits = BM * kEpCols / 4;         // 4-column units per pass
+      static_assert(kThreads % (kEpCols / 4) == 0, "a thread's columns are fixed per pass");
+      // fp8: the thread's row and channel scales, all loaded before the first store
+      float sxd[kUnits / kThreads];
+      float4 swd[128 / kEpCols];
+      if (FP8) {
+        const int c4 = int(threadIdx.x % (kEpCols / 4)) * 4;
+#pragma unroll
+        for (int q = 0; q < 128 / kEpCols; ++q)
+          swd[q] = *reinterpret_cast<const float4*>(p.b_scale + long(g.expert) * p.b_scale_ld + g.n0 + q * kEpCols + c4);
+#pragma unroll
+        for (int j = 0; j < kUnits / kThreads; ++j) {
+          const int grow = g.row0 + int((threadIdx.x + kThreads * j) / (kEpCols / 4));
+          sxd[j] = grow < g.row1 ? p.a_scale[grow] : 0.f;
+        }
+        __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);   // in before the first store (see gate_up)
+      }
 #pragma unroll
       for (int pass = 0; pass < 128 / kEpCols; ++pass) {
         const int c0 = pass * kEpCols;                 // first column of this pass
@@ -340,31 +386,36 @@ void stream_gemm_kernel(GemmParams p) {
               dep[(32 * i + 8 * (e / 4) + 4 * lgrp + (e % 4)) * kEpCols + 32 * wave - c0 + lcol] = acc[i][e];
         }
         lds_barrier();
-        constexpr int kUnits = BM * kEpCols / 4;       // 4-column units
-#pragma unroll 4
-        for (int j = 0; j < kUnits / kThreads; ++j) {
+        auto unit = [&](int j) __attribute__((always_inline)) {
           const int u = int(threadIdx.x) + kThreads * j;
           const int r = u / (kEpCols / 4), c4 = (u % (kEpCols / 4)) * 4;
           const int grow = g.row0 + r;
-          if (grow >= g.row1) continue;
+          if (grow >= g.row1) return;
           float4 v = *reinterpret_cast<const float4*>(dep + r * kEpCols + c4);
           const int c = g.n0 + c0 + c4;
           if (FP8) {
-            const float sx = p.a_scale[grow];
-            const float* sw = p.b_scale + long(g.expert) * p.b_scale_ld + c;
-            v.x *= sx * sw[0];
-            v.y *= sx * sw[1];
-            v.z *= sx * sw[2];
-            v.w *= sx * sw[3];
+            const float sx = sxd[j];
+            const float4 sw = swd[pass];
+            v.x *= sx * sw.x;
+            v.y *= sx * sw.y;
+            v.z *= sx * sw.z;
+            v.w *= sx * sw.w;
           }
           *reinterpret_cast<float4*>(static_cast<float*>(p.C) + long(prow[r]) * p.ldc + c) = v;
+        };
+        if constexpr (FP8) {
+#pragma unroll
+          for (int j = 0; j < kUnits / kThreads; ++j) unit(j);
+        } else {
+#pragma unroll 4
+          for (int j = 0; j < kUnits / kThreads; ++j) unit(j);
         }
         if (pass + 1 < 128 / kEpCols) lds_barrier();
       }
     }
     if (!more) break;
     k8 += stride;
-    g = CHAIN ? gn : stream_geometry<MODE>(p, first + k8, nk, wave);
+    g = gn;
     primed = CHAIN;
   }
 #undef MOLT_SSTORE
