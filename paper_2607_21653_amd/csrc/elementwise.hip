@@ -62,11 +62,19 @@ __global__ __launch_bounds__(kThreads) void residual_norm_kernel(
   const int t = blockIdx.x;
   float* xr = x + long(t) * d;
   float v[kNormRuns][8];
+  // the gains are loaded with x: loaded after the x stores, they would wait for those
+  float gv[kNormRuns][8];
   float ss = 0.f;
 #pragma unroll
   for (int r = 0; r < kNormRuns; ++r) {
     const int i = (threadIdx.x + r * kThreads) * 8;
     if (i >= d) break;
+    if (g) {
+      const float4 ga = *reinterpret_cast<const float4*>(g + i);
+      const float4 gb = *reinterpret_cast<const float4*>(g + i + 4);
+      gv[r][0] = ga.x; gv[r][1] = ga.y; gv[r][2] = ga.z; gv[r][3] = ga.w;
+      gv[r][4] = gb.x; gv[r][5] = gb.y; gv[r][6] = gb.z; gv[r][7] = gb.w;
+    }
     const float4 a = *reinterpret_cast<const float4*>(xr + i);
     const float4 b = *reinterpret_cast<const float4*>(xr + i + 4);
     v[r][0] = a.x; v[r][1] = a.y; v[r][2] = a.z; v[r][3] = a.w;
@@ -96,12 +104,9 @@ __global__ __launch_bounds__(kThreads) void residual_norm_kernel(
   for (int r = 0; r < kNormRuns; ++r) {
     const int i = (threadIdx.x + r * kThreads) * 8;
     if (i >= d) break;
-    const float4 ga = *reinterpret_cast<const float4*>(g + i);
-    const float4 gb = *reinterpret_cast<const float4*>(g + i + 4);
-    const float gv[8] = {ga.x, ga.y, ga.z, ga.w, gb.x, gb.y, gb.z, gb.w};
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
-      float u = v[r][e] * rs * gv[e];
+      float u = v[r][e] * rs * gv[r][e];
       if (dt == MOLT_BF16) u = round_to_bf16(u);
       v[r][e] = u;
       amax = fmaxf(amax, fabsf(u));
