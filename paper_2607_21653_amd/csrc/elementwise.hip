@@ -139,7 +139,7 @@ __global__ __launch_bounds__(kThreads) void residual_norm_kernel(
     uint32_t c[2] = {0u, 0u};
     if (sc > 0.f) {
 #pragma unroll
-      for (int e = 0; e < 8; ++e) c[e / 4] |= f32_to_fp8e4m3(v[r][e] / sc) << (8 * (e % 4));
+      for (int e = 0; e < 8; e += 2) c[e / 4] |= f32x2_to_fp8e4m3(v[r][e] / sc, v[r][e + 1] / sc) << (8 * (e % 4));
     }
     *reinterpret_cast<uint2*>(yq + tiled_offset(t, i, d)) = make_uint2(c[0], c[1]);
     if (yq_rows) *reinterpret_cast<uint2*>(yq_rows + long(t) * d + i) = make_uint2(c[0], c[1]);
@@ -150,8 +150,10 @@ __global__ __launch_bounds__(kThreads) void residual_norm_kernel(
 // Per-row fp8 quantisation of tiled bf16 rows into tiled e4m3 codes (s = amax / 448,
 // code = e4m3(v / s), zero row -> s = 0): the SwiGLU product of the grouped GEMMs (rows in
 // padded expert order, count on the device, padding rows with pair -1 get zero codes and
-// scale 0) or an input activation (all `rows` rows). One wavefront per row, 8 values per
-// lane step.
+// scale 0) or an input activation (all `rows` rows). One wavefront per row; lane l holds
+// the 4-column chunks l, l + 64, ... in registers from the amax to the codes (the row is
+// read once; rows past 64 * kQuantRegChunks * 4 columns re-read the rest).
+constexpr int kQuantRegChunks = 16;
 __global__ __launch_bounds__(kThreads) void quant_rows_tiled_kernel(
     const uint16_t* __restrict__ h, const int32_t* __restrict__ pperm,
     const int32_t* __restrict__ n_rows, long rows, int cols, uint8_t* __restrict__ q,
@@ -161,32 +163,40 @@ __global__ __launch_bounds__(kThreads) void quant_rows_tiled_kernel(
   if (r >= (n_rows ? long(*n_rows) : rows)) return;
   const bool pad = pperm && pperm[r] < 0;
   const long rb_in = 2L * cols, rb_out = cols;
+  const uint8_t* hb = reinterpret_cast<const uint8_t*>(h);
+  const int nch = cols / 4;                  // 4-column chunks of the row
+  auto load = [&](int ch) __attribute__((always_inline)) {
+    return *reinterpret_cast<const uint2*>(hb + tiled_offset(r, 8L * ch, rb_in));
+  };
+  uint2 reg[kQuantRegChunks];
   float amax = 0.f;
-  for (int c = lane * 8; c < cols; c += kWave * 8) {
-    const int4 v = *reinterpret_cast<const int4*>(
-        reinterpret_cast<const uint8_t*>(h) + tiled_offset(r, 2L * c, rb_in));
-    const uint32_t w[4] = {uint32_t(v.x), uint32_t(v.y), uint32_t(v.z), uint32_t(v.w)};
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-      amax = fmaxf(amax, fmaxf(fabsf(bf16_to_f32(uint16_t(w[i]))), fabsf(bf16_to_f32(uint16_t(w[i] >> 16)))));
+  for (int k = 0; k < kQuantRegChunks; ++k) {
+    const int ch = lane + kWave * k;
+    reg[k] = ch < nch ? load(ch) : make_uint2(0u, 0u);
   }
+  auto absmax = [&](uint2 v) __attribute__((always_inline)) {
+    return fmaxf(fmaxf(fabsf(bf16_to_f32(uint16_t(v.x))), fabsf(bf16_to_f32(uint16_t(v.x >> 16)))),
+                 fmaxf(fabsf(bf16_to_f32(uint16_t(v.y))), fabsf(bf16_to_f32(uint16_t(v.y >> 16)))));
+  };
+#pragma unroll
+  for (int k = 0; k < kQuantRegChunks; ++k) amax = fmaxf(amax, absmax(reg[k]));
+  for (int ch = lane + kWave * kQuantRegChunks; ch < nch; ch += kWave) amax = fmaxf(amax, absmax(load(ch)));
   amax = pad ? 0.f : wave_max(amax);
   const float s = amax / 448.0f;
-  for (int c = lane * 8; c < cols; c += kWave * 8) {
-    const int4 v = *reinterpret_cast<const int4*>(
-        reinterpret_cast<const uint8_t*>(h) + tiled_offset(r, 2L * c, rb_in));
-    const uint32_t w[4] = {uint32_t(v.x), uint32_t(v.y), uint32_t(v.z), uint32_t(v.w)};
-    uint32_t code[2] = {0u, 0u};
-    if (s > 0.f) {
+  auto encode = [&](int ch, uint2 v) __attribute__((always_inline)) {
+    uint32_t code = 0u;
+    if (s > 0.f)
+      code = f32x2_to_fp8e4m3(bf16_to_f32(uint16_t(v.x)) / s, bf16_to_f32(uint16_t(v.x >> 16)) / s) |
+             (f32x2_to_fp8e4m3(bf16_to_f32(uint16_t(v.y)) / s, bf16_to_f32(uint16_t(v.y >> 16)) / s) << 16);
+    *reinterpret_cast<uint32_t*>(q + tiled_offset(r, 4L * ch, rb_out)) = code;
+  };
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const uint32_t lo = f32_to_fp8e4m3(bf16_to_f32(uint16_t(w[i])) / s);
-        const uint32_t hi = f32_to_fp8e4m3(bf16_to_f32(uint16_t(w[i] >> 16)) / s);
-        code[i / 2] |= (lo | (hi << 8)) << (16 * (i % 2));
-      }
-    }
-    *reinterpret_cast<uint2*>(q + tiled_offset(r, c, rb_out)) = make_uint2(code[0], code[1]);
+  for (int k = 0; k < kQuantRegChunks; ++k) {
+    const int ch = lane + kWave * k;
+    if (ch < nch) encode(ch, reg[k]);
   }
+  for (int ch = lane + kWave * kQuantRegChunks; ch < nch; ch += kWave) encode(ch, load(ch));
   if (lane == 0) scale[r] = s;
 }
 
