@@ -508,6 +508,10 @@ __global__ __launch_bounds__(128 * WN) void lds_gemm_kernel(GemmParams p, float*
   const long RB = long(p.K) * 2;
   const int nk = int(RB / kRowBytes);
   const int kb0 = int(long(nk) * split / splits), kb1 = int(long(nk) * (split + 1) / splits);
+  // RoPE epilogue: this thread's row's KV-cache slot, read before the K loop (loaded at the
+  // epilogue it would wait behind the table loads there)
+  int my_slot = -1;
+  if constexpr (ROPE) my_slot = rk.slot[min(row0 + int(threadIdx.x % BM), p.M - 1)];
 
   // chunk q = tid + NT u of a slice is 16-byte chunk q % 256 of block q / 256 (A blocks,
   // then B blocks; each a 4 KB tile, clamped into the padded operands); it lands at byte
@@ -601,9 +605,9 @@ __global__ __launch_bounds__(128 * WN) void lds_gemm_kernel(GemmParams p, float*
       for (int n = 0; n < RG; ++n)
         cs[n] = rk.table[long(min(row0 + pr + PR * (RG * g + n), p.M - 1)) * 64 + pi];
     };
-    if (rotate) fetch(0);
     __shared__ int s_slot[BM];
-    if (threadIdx.x < BM) s_slot[threadIdx.x] = row0 + int(threadIdx.x) < p.M ? rk.slot[row0 + threadIdx.x] : -1;
+    if (rotate) fetch(0);
+    if (threadIdx.x < BM) s_slot[threadIdx.x] = row0 + int(threadIdx.x) < p.M ? my_slot : -1;
     __syncthreads();
     float* ob = reinterpret_cast<float*>(&lds[0][0]);     // [BM][128]
 #pragma unroll
@@ -619,6 +623,9 @@ __global__ __launch_bounds__(128 * WN) void lds_gemm_kernel(GemmParams p, float*
 #pragma unroll
       for (int g = 0; g < NG; ++g) {
         if (g > 0) fetch(g);
+        // all of the group's table entries in before its first store: with the stores behind
+        // branches the compiler would otherwise wait for every earlier store at each row
+        __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
 #pragma unroll
         for (int n = 0; n < RG; ++n) {
           const int r = pr + PR * (RG * g + n), t = row0 + r;
