@@ -71,6 +71,17 @@ MOLT_DEV uint32_t f32_to_fp8e4m3(float f) {
   return sign | code;
 }
 
+// v / s for the fp8 row quantisation, from r = 1 / s (IEEE) and one fma correction of
+// q0 = v * r, the sign copied from v (the correction turns -0 into +0). For s > 1e-30 and
+// bf16 values |v| <= 448 s (the quantisation's domain: v a bf16 entry of the row, s its
+// amax / 448) it gives the same e4m3 code as the IEEE quotient: compared on gfx950 for
+// every positive bf16 amax and every bf16 v with |v| <= amax, no code differs.
+MOLT_DEV float div_by_scale(float v, float s, float r) {
+  const float q0 = v * r;
+  return __builtin_copysignf(__builtin_fmaf(__builtin_fmaf(-q0, s, v), r, q0), v);
+}
+constexpr float kFastDivMinScale = 1.0e-30f;
+
 // Two codes at once on the hardware conversion (v_cvt_pk_fp8_f32: OCP e4m3, round to
 // nearest even), inputs clamped to +-448 first so that it saturates, NaN mapped to 0x7F:
 // the same code as f32_to_fp8e4m3 for every f32 (compared exhaustively on gfx950 over all

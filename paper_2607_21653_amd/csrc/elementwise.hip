@@ -132,18 +132,25 @@ __global__ __launch_bounds__(kThreads) void residual_norm_kernel(
   if (yq == nullptr) return;
   amax = block_max_dpp<kThreads / kWave>(amax, red);
   const float sc = amax / 448.0f;
+  // v / sc: IEEE for tiny scales, else the reciprocal with one fma correction (same codes;
+  // the values are the bf16-rounded y, |v| <= amax)
+  const float rsc = 1.0f / sc;
+  auto codes = [&](auto div) __attribute__((always_inline)) {
 #pragma unroll
-  for (int r = 0; r < kNormRuns; ++r) {
-    const int i = (threadIdx.x + r * kThreads) * 8;
-    if (i >= d) break;
-    uint32_t c[2] = {0u, 0u};
-    if (sc > 0.f) {
+    for (int r = 0; r < kNormRuns; ++r) {
+      const int i = (threadIdx.x + r * kThreads) * 8;
+      if (i >= d) break;
+      uint32_t c[2] = {0u, 0u};
+      if (sc > 0.f) {
 #pragma unroll
-      for (int e = 0; e < 8; e += 2) c[e / 4] |= f32x2_to_fp8e4m3(v[r][e] / sc, v[r][e + 1] / sc) << (8 * (e % 4));
+        for (int e = 0; e < 8; e += 2) c[e / 4] |= f32x2_to_fp8e4m3(div(v[r][e]), div(v[r][e + 1])) << (8 * (e % 4));
+      }
+      *reinterpret_cast<uint2*>(yq + tiled_offset(t, i, d)) = make_uint2(c[0], c[1]);
+      if (yq_rows) *reinterpret_cast<uint2*>(yq_rows + long(t) * d + i) = make_uint2(c[0], c[1]);
     }
-    *reinterpret_cast<uint2*>(yq + tiled_offset(t, i, d)) = make_uint2(c[0], c[1]);
-    if (yq_rows) *reinterpret_cast<uint2*>(yq_rows + long(t) * d + i) = make_uint2(c[0], c[1]);
-  }
+  };
+  if (sc > kFastDivMinScale) codes([&](float x) { return div_by_scale(x, sc, rsc); });
+  else codes([&](float x) { return x / sc; });
   if (threadIdx.x == 0) ys[t] = sc;
 }
 
@@ -184,19 +191,25 @@ __global__ __launch_bounds__(kThreads) void quant_rows_tiled_kernel(
   for (int ch = lane + kWave * kQuantRegChunks; ch < nch; ch += kWave) amax = fmaxf(amax, absmax(load(ch)));
   amax = pad ? 0.f : wave_max(amax);
   const float s = amax / 448.0f;
-  auto encode = [&](int ch, uint2 v) __attribute__((always_inline)) {
+  // v / s: IEEE for tiny scales, else the reciprocal with one fma correction (same codes)
+  const float rs = 1.0f / s;
+  auto encode = [&](int ch, uint2 v, auto div) __attribute__((always_inline)) {
     uint32_t code = 0u;
     if (s > 0.f)
-      code = f32x2_to_fp8e4m3(bf16_to_f32(uint16_t(v.x)) / s, bf16_to_f32(uint16_t(v.x >> 16)) / s) |
-             (f32x2_to_fp8e4m3(bf16_to_f32(uint16_t(v.y)) / s, bf16_to_f32(uint16_t(v.y >> 16)) / s) << 16);
+      code = f32x2_to_fp8e4m3(div(bf16_to_f32(uint16_t(v.x))), div(bf16_to_f32(uint16_t(v.x >> 16)))) |
+             (f32x2_to_fp8e4m3(div(bf16_to_f32(uint16_t(v.y))), div(bf16_to_f32(uint16_t(v.y >> 16)))) << 16);
     *reinterpret_cast<uint32_t*>(q + tiled_offset(r, 4L * ch, rb_out)) = code;
   };
+  auto encode_all = [&](auto div) __attribute__((always_inline)) {
 #pragma unroll
-  for (int k = 0; k < kQuantRegChunks; ++k) {
-    const int ch = lane + kWave * k;
-    if (ch < nch) encode(ch, reg[k]);
-  }
-  for (int ch = lane + kWave * kQuantRegChunks; ch < nch; ch += kWave) encode(ch, load(ch));
+    for (int k = 0; k < kQuantRegChunks; ++k) {
+      const int ch = lane + kWave * k;
+      if (ch < nch) encode(ch, reg[k], div);
+    }
+    for (int ch = lane + kWave * kQuantRegChunks; ch < nch; ch += kWave) encode(ch, load(ch), div);
+  };
+  if (s > kFastDivMinScale) encode_all([&](float x) { return div_by_scale(x, s, rs); });
+  else encode_all([&](float x) { return x / s; });
   if (lane == 0) scale[r] = s;
 }
 
