@@ -102,9 +102,20 @@ __global__ __launch_bounds__(64 * NW, NW == 8 ? 2 : 1) void attn_lds_kernel(Attn
   constexpr int kDepth = KS == 2 ? 1 : NW == 8 ? 3 : 6;
   __shared__ __attribute__((aligned(16))) uint8_t lds[2 * KS][PAIR];
 
-  const int split = blockIdx.x % p.splits;
-  const int qt = (blockIdx.x / p.splits) % p.qtiles;
-  const int bh = blockIdx.x / p.splits / p.qtiles;
+  // Workgroup i runs on XCD i % 8. With the work item equal to i and 8 splits, XCD x would
+  // take split x of every (b, h): the XCDs of the late splits, empty where a context is
+  // shorter than the longest, idled while the others set the kernel's time. With 4 or more
+  // splits the work item's low 3 bits are XORed with the group number j = i / 8 (a full
+  // group of 8 stays a permutation of itself), so every XCD takes every split index
+  // (long-context layer 318 -> 284 us; a hash that also mixed j's higher bits in: 306 us;
+  // with 1-2 splits, whose ranges are nearly equal, the mix measured 1-3% slower). Several
+  // query tiles of one (b, h) (prefill windows) keep the plain order: there an XCD takes
+  // one split's keys for many tiles, which then hit its L2.
+  int wi = blockIdx.x;
+  if (p.splits >= 4 && p.qtiles == 1 && (wi | 7) < int(gridDim.x)) wi = (wi & ~7) | ((wi ^ (wi >> 3)) & 7);
+  const int split = wi % p.splits;
+  const int qt = (wi / p.splits) % p.qtiles;
+  const int bh = wi / p.splits / p.qtiles;
   const int b = bh / p.Hkv, h = bh % p.Hkv;
   const int G = p.Hq / p.Hkv;
   const int kp1 = p.k + 1;
