@@ -282,7 +282,7 @@ MoeWs carve_moe(molt::Carver& c, int T, int d, int E, int K, int F, molt_dtype a
   m.pperm = c.take<int32_t>(R);
   m.n_padded = c.take<int32_t>(1);
   m.tiles = c.take<int32_t>(long(m.max_tiles) * 4);
-  m.n_tiles = c.take<int32_t>(1);
+  m.n_tiles = c.take<int32_t>(1 + 2 * molt::kTileQueues);   // + the GEMMs' tile queues
   if (w == MOLT_FP8_E4M3) {
     m.xq = c.take<uint8_t>(pad32(T) * d);
     m.xs = c.take<float>(pad32(T));

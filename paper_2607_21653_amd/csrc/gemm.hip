@@ -40,6 +40,7 @@ struct GemmParams {
   const float* b_scale;    // fp8: [E, b_scale_ld]
   int b_scale_ld;
   int accumulate;          // dense: C += result
+  int* queue;              // grouped, unchained: per-XCD tile queues (zero at launch)
 };
 
 MOLT_DEV floatx16_t mfma(const bf16x8_t& a, const bf16x8_t& b, const floatx16_t& c) {
@@ -88,7 +89,11 @@ template <int MODE>
 MOLT_DEV StreamTile stream_geometry(const GemmParams& p, int id, int nk, int wave) {
   StreamTile g;
   const int mt = id / p.n_ntiles, nt = id % p.n_ntiles;
-  const int4 t = p.tiles[mt];
+  // through the constant address space: a scalar load (the table is read-only here), which
+  // does not wait behind the vector stores of an epilogue
+  typedef const __attribute__((address_space(4))) int32x4_t* ConstTile;
+  const int32x4_t tv = *(ConstTile)(p.tiles + mt);
+  const int4 t = make_int4(tv[0], tv[1], tv[2], tv[3]);
   g.expert = t.x;
   g.row0 = t.y;                                       // a multiple of 32
   g.row1 = t.z;
@@ -189,6 +194,15 @@ void stream_gemm_kernel(GemmParams p) {
   StreamTile gn = g;
   bool more = false;
   bool primed = false;                               // g's first slices already loaded
+  // Unchained launches take tiles from their XCD's queue: a workgroup's first tile is k8 as
+  // in the static walk, each later one the next of the pool [stride, chunk), taken by
+  // thread 0 when the tile enters its last K steps and passed on through LDS in the
+  // epilogue, so workgroups that run faster take more tiles (with 2-3 tiles each, the
+  // static walk left the XCD's workgroups ending anywhere between half and all of the
+  // kernel's time).
+  const bool dyn = !CHAIN && p.queue != nullptr;
+  __shared__ int s_grab;
+  int grab = chunk;                                  // thread 0: the next tile (dyn)
   for (;;) {
     // down: the pair index of each of the tile's rows, loaded before the tile's own loads
     int pv = -1;
@@ -197,11 +211,10 @@ void stream_gemm_kernel(GemmParams p) {
     auto put_prow = [&]() __attribute__((always_inline)) {
       if (MODE == kDown && threadIdx.x < BM) prow[threadIdx.x] = pv;
     };
-    {
+    if (!dyn) {
       const int kn = k8 + stride;
       more = kn < chunk && first + kn < total;
-      // the next tile's table entry is read here, not after the epilogue: a load issued
-      // behind the epilogue's stores would have to wait for all of them
+      // the next tile's table entry is read here, not after the epilogue
       if (more) gn = stream_geometry<MODE>(p, first + kn, nk, wave);
     }
     if (ROWS) {
@@ -224,6 +237,7 @@ void stream_gemm_kernel(GemmParams p) {
       MOLT_GLOAD(st0, g, 2);
       lds_barrier();
     }
+
 #pragma unroll
     for (int i = 0; i < MS; ++i)
 #pragma unroll
@@ -277,6 +291,7 @@ void stream_gemm_kernel(GemmParams p) {
       if (primed) lds_barrier();           // barrier since the last tile's epilogue read prow
       put_prow();
     }
+    if (dyn && threadIdx.x == 0) grab = stride + atomicAdd(p.queue + blockIdx.x % 8, 1);
     // the last 1..7 slices (kb % 4 == 0, so the slot pattern continues)
     if (kb < nk) MOLT_STEP(0, st1, 0, kb, 1);
     if (kb + 1 < nk) MOLT_STEP(1, st0, 1, kb + 1, 1);
@@ -286,6 +301,8 @@ void stream_gemm_kernel(GemmParams p) {
     if (kb + 5 < nk) MOLT_STEP(1, st0, 1, kb + 5, 1);
     if (kb + 6 < nk) MOLT_STEP(0, st1, 2, kb + 6, 1);
 #undef MOLT_STEP
+    // published by the epilogue's first barrier, read after the tile
+    if (dyn && threadIdx.x == 0) s_grab = grab;
     // accumulator element e of lane (lcol, lgrp) in tile i: row 32 i + 8 (e / 4) + 4 lgrp + e % 4
     int lcol = lane % 32, lgrp = lane / 32;
     // opaque per tile: the epilogue's address arithmetic stays here instead of being hoisted
@@ -412,6 +429,12 @@ void stream_gemm_kernel(GemmParams p) {
         }
         if (pass + 1 < 128 / kEpCols) lds_barrier();
       }
+    }
+    if (dyn) {
+      k8 = s_grab;
+      if (k8 >= chunk || first + k8 >= total) break;
+      g = stream_geometry<MODE>(p, first + k8, nk, wave);
+      continue;
     }
     if (!more) break;
     k8 += stride;
@@ -1026,6 +1049,7 @@ hipError_t launch_moe_gate_up(const void* a, const void* a_rows, const float* a_
     return hipGetLastError();
   }
   p.n_ntiles = F / (kBN / 2);
+  p.queue = const_cast<int32_t*>(n_tiles) + 1;
   if (wdt == MOLT_FP8_E4M3) return run_stream<true, kGateUp>(p, tile_m, s, a_rows != nullptr);
   return run_stream<false, kGateUp>(p, tile_m, s, a_rows != nullptr);
 }
@@ -1047,6 +1071,7 @@ hipError_t launch_moe_down(const void* a, const float* a_scale, const int32_t* p
     return hipGetLastError();
   }
   p.n_ntiles = d / kBN;
+  p.queue = const_cast<int32_t*>(n_tiles) + 1 + kTileQueues;
   if (wdt == MOLT_FP8_E4M3) return run_stream<true, kDown>(p, tile_m, s);
   return run_stream<false, kDown>(p, tile_m, s);
 }

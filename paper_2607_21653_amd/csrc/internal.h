@@ -101,6 +101,9 @@ hipError_t launch_mtp_record(const int32_t* tok, int i, int B, int W, int k, con
 // top-K + softmax of router logits (the sum, in order, of nparts split-K partials
 // logits[s * T * E ..]; or replay ids); stable permutation perm (position -> pair) and its
 // padded copy (pperm: padded row -> pair or -1, n_padded rows); tile table in padded rows
+// n_tiles of launch_route is followed by 2 x kTileQueues ints: the per-XCD tile queues of the
+// gate_up and down GEMMs, which the permutation zeroes.
+constexpr int kTileQueues = 8;
 hipError_t launch_route(const float* logits, int nparts, const float* bias, const int32_t* replay,
                         int T, int E, int K, int32_t* ids, float* w, int32_t* counts,
                         int32_t* offsets, int32_t* perm, int32_t* pperm, int32_t* n_padded,

@@ -257,6 +257,8 @@ __global__ __launch_bounds__(kPermThreads) void permute_kernel(PermuteParams p) 
       *p.n_padded = poff[p.E];
       *p.n_tiles = nt;
     }
+    // the grouped GEMMs' per-XCD tile queues (gate_up, down) that follow n_tiles
+    if (tid < 2 * kTileQueues) p.n_tiles[1 + tid] = 0;
     for (int i = nt + tid; i < p.max_tiles; i += kPermThreads) p.tiles[i] = make_int4(-1, 0, 0, 0);
   }
   // the range's pairs: position = offset + earlier pairs of the expert + rank
