@@ -40,7 +40,7 @@ struct GemmParams {
   const float* b_scale;    // fp8: [E, b_scale_ld]
   int b_scale_ld;
   int accumulate;          // dense: C += result
-  int* queue;              // grouped, unchained: per-XCD tile queues (zero at launch)
+  int* queue;              // grouped fp8: per-XCD tile queues (zero at launch)
 };
 
 MOLT_DEV floatx16_t mfma(const bf16x8_t& a, const bf16x8_t& b, const floatx16_t& c) {
@@ -123,6 +123,7 @@ MOLT_DEV StreamTile stream_geometry(const GemmParams& p, int id, int nk, int wav
 // HBM once and then hits that XCD's L2. Launching one workgroup per pair left the chip
 // at 50-80% of its resident workgroups on average (dispatch gaps between short tiles).
 // CHAIN requires K slices in multiples of 4 (the slot pattern then lines up across tiles).
+// fp8 launches take each workgroup's later tiles from its XCD's queue instead (see below).
 template <int BM, bool FP8, int MODE, bool CHAIN, bool ROWS>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(BM <= 64 ? 3 : 2)))
 void stream_gemm_kernel(GemmParams p) {
@@ -194,13 +195,15 @@ void stream_gemm_kernel(GemmParams p) {
   StreamTile gn = g;
   bool more = false;
   bool primed = false;                               // g's first slices already loaded
-  // Unchained launches take tiles from their XCD's queue: a workgroup's first tile is k8 as
-  // in the static walk, each later one the next of the pool [stride, chunk), taken by
-  // thread 0 when the tile enters its last K steps and passed on through LDS in the
-  // epilogue, so workgroups that run faster take more tiles (with 2-3 tiles each, the
-  // static walk left the XCD's workgroups ending anywhere between half and all of the
-  // kernel's time).
-  const bool dyn = !CHAIN && p.queue != nullptr;
+  // fp8 launches take tiles from their XCD's queue: a workgroup's first tile is k8 as in the
+  // static walk, each later one the next of the pool [stride, chunk), taken by thread 0 when
+  // the tile enters its last K steps and passed on through LDS in the epilogue, so
+  // workgroups that run faster take more tiles (the static walk left an XCD's workgroups
+  // ending anywhere between half and all of the kernel's time). Their Zipf-hot tiles are
+  // bound by the MFMAs and differ in cost; the bf16 launches are bound by HBM, where the
+  // late workgroups still share the full bandwidth and the queue measured 0-5% slower.
+  constexpr bool kDyn = FP8 && !CHAIN;
+  const bool dyn = kDyn && p.queue != nullptr;
   __shared__ int s_grab;
   int grab = chunk;                                  // thread 0: the next tile (dyn)
   for (;;) {
