@@ -202,3 +202,18 @@ def test_fp8_zipf_many_tiles(molt_lib):
     print("experts with >= 256 pairs", big.tolist(), flush=True)
     assert len(big) >= 2 and (big % 128 != 0).all()
     _check(w, o, g, 2e-2)
+
+
+def test_fp8_tile_queue_deterministic(molt_lib):
+    """The fp8 expert GEMMs hand out their tiles from per-XCD queues at run time, so which
+    workgroup computes a tile changes from call to call; every tile is computed whole by one
+    workgroup, so the layer's output must not. Three calls at the fp8 Zipf layer's own shape
+    (2304 tokens) agree bit for bit."""
+    w = workloads.FP8_ZIPF
+    T = w.tokens_per_step
+    lw, x = _layer(w, 3, T)
+    print(f"case fp8 zipf T={T} x3", flush=True)
+    outs = [_gpu(molt_lib, lw, x, w.top_k)[0].cpu().numpy() for _ in range(3)]
+    assert np.isfinite(outs[0]).all()
+    for o in outs[1:]:
+        np.testing.assert_array_equal(o, outs[0])
