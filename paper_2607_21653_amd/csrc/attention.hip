@@ -410,33 +410,46 @@ __global__ __launch_bounds__(64 * NW, NW == 8 ? 2 : 1) void attn_lds_kernel(Attn
   }
 }
 
-// log-sum-exp merge over splits: one workgroup per (b, h, row), threads over dims
+// log-sum-exp merge over splits: one workgroup per (b, h, group of 1024 / D rows), each
+// thread finishing 4 consecutive dims of one row (16-byte partial loads, one 8-byte store;
+// one workgroup per row with a thread per dim had taken 12 us for the single layer's 10 MB
+// of partials)
 template <int D>
-__global__ __launch_bounds__(D) void attn_merge_kernel(AttnParams p, int out_f32) {
+__global__ __launch_bounds__(256) void attn_merge_kernel(AttnParams p) {
+  constexpr int TPR = D / 4;                 // threads per row
+  constexpr int RPW = 256 / TPR;             // rows per workgroup
   const int G = p.Hq / p.Hkv;
   const int kp1 = p.k + 1;
   const int R = G * kp1;
-  const int r = blockIdx.x % R;
-  const int bh = blockIdx.x / R;
+  const int groups = (R + RPW - 1) / RPW;
+  const int bh = blockIdx.x / groups;
+  const int r = (blockIdx.x % groups) * RPW + int(threadIdx.x) / TPR;
+  if (r >= R) return;
+  const int d4 = (int(threadIdx.x) % TPR) * 4;
   const int b = bh / p.Hkv, h = bh % p.Hkv;
   const int j_end = min(kp1, (r / G / p.tq + 1) * p.tq);      // end of the row's query tile
   const int nblk = (p.ctx[b] + j_end + 15) / 16;
   const int ns = min(p.splits, (nblk + p.blocks_per_split - 1) / p.blocks_per_split);
+  const long pr0 = long(bh) * p.splits * R + r;              // split s: pr0 + s R
   float M = kNegBig;
-  for (int s = 0; s < ns; ++s) M = fmaxf(M, p.part_ml[((long(bh) * p.splits + s) * R + r) * 2]);
-  float L = 0.f, acc = 0.f;
+  for (int s = 0; s < ns; ++s) M = fmaxf(M, p.part_ml[(pr0 + long(s) * R) * 2]);
+  float L = 0.f;
+  floatx4_t acc = {0.f, 0.f, 0.f, 0.f};
   for (int s = 0; s < ns; ++s) {
-    const long pr = (long(bh) * p.splits + s) * R + r;
-    const float m = p.part_ml[pr * 2];
-    const float f = exp2f(m - M);
+    const long pr = pr0 + long(s) * R;
+    const float f = exp2f(p.part_ml[pr * 2] - M);
     L += p.part_ml[pr * 2 + 1] * f;
-    acc += p.part_o[pr * D + threadIdx.x] * f;
+    const floatx4_t o = *reinterpret_cast<const floatx4_t*>(p.part_o + pr * D + d4);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) acc[e] += o[e] * f;
   }
   const int j = r / G, gi = r % G;
-  const float v = L > 0.f ? acc / L : 0.f;
-  const long t = long(b) * kp1 + j, c = (h * G + gi) * D + threadIdx.x;
-  if (out_f32) reinterpret_cast<float*>(p.out)[out_index(p, t, c, long(p.Hq) * D, 4)] = v;
-  else p.out[out_index(p, t, c, long(p.Hq) * D, 2)] = f32_to_bf16(v);
+  uint16_t v[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) v[e] = f32_to_bf16(L > 0.f ? acc[e] / L : 0.f);
+  const long t = long(b) * kp1 + j, c = (h * G + gi) * D + d4;   // 4 consecutive columns
+  *reinterpret_cast<uint2*>(p.out + out_index(p, t, c, long(p.Hq) * D, 2)) =
+      make_uint2(uint32_t(v[0]) | (uint32_t(v[1]) << 16), uint32_t(v[2]) | (uint32_t(v[3]) << 16));
 }
 
 // ---------------------------------------------------------------- f32 VALU path
@@ -514,7 +527,7 @@ hipError_t launch_d(const AttnParams& p, int B, int R, hipStream_t s) {
   // two key groups when a query tile's row tiles fit half the wavefronts
   if ((Rt + 15) / 16 <= 4) attn_lds_kernel<D, 8, 2><<<grid, 512, 0, s>>>(p);
   else attn_lds_kernel<D, 8, 1><<<grid, 512, 0, s>>>(p);
-  if (p.splits > 1) attn_merge_kernel<D><<<B * p.Hkv * R, D, 0, s>>>(p, 0);
+  if (p.splits > 1) attn_merge_kernel<D><<<B * p.Hkv * ((R + 1024 / D - 1) / (1024 / D)), 256, 0, s>>>(p);
   return hipGetLastError();
 }
 
