@@ -845,6 +845,19 @@ __global__ __launch_bounds__(kThreads) void bigtile_gemm_kernel(GemmParams p) {
   // acc[i][j][e]: row 32 i + 8 (e / 4) + 4 lgrp + e % 4, column 64 wave + 32 j + lcol
   const int lcol = lane % 32, lgrp = lane / 32;
   float* C = static_cast<float*>(p.C);
+  if (!p.accumulate && row0 + kBigBM <= p.M && n0 + kBigBN <= p.N) {
+    // whole tile (all but the last column tile): no bounds checks between the stores (the
+    // LM head: 451 -> 411 us; nontemporal stores measured 420 us; without any stores 370 us:
+    // the tiles of a round end together and their 40 MB of logits go out in one burst)
+    float* base = C + long(row0 + 4 * lgrp) * p.ldc + n0 + 64 * wave + lcol;
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int i = 0; i < kBigAB; ++i)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) base[long(32 * i + 8 * (e / 4) + (e % 4)) * p.ldc + 32 * j] = acc[i][j][e];
+    return;
+  }
 #pragma unroll
   for (int j = 0; j < 2; ++j) {
     const int col = n0 + 64 * wave + 32 * j + lcol;
