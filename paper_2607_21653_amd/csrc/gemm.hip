@@ -686,6 +686,17 @@ __global__ __launch_bounds__(128 * WN) void lds_gemm_kernel(GemmParams p, float*
     return;
   }
   float* out = splits > 1 ? part + long(split) * p.M * p.ldc : static_cast<float*>(p.C);
+  if (!(splits == 1 && p.accumulate) && row0 + BM <= p.M && n0 + kBN <= p.N) {
+    // whole tile: no bounds checks between the stores
+    float* base = out + long(row0 + wm * WROWS + 4 * lgrp) * p.ldc + n0 + wn * 32 * NJ + lcol;
+#pragma unroll
+    for (int j = 0; j < NJ; ++j)
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) base[long(32 * i + 8 * (e / 4) + (e % 4)) * p.ldc + 32 * j] = acc[i][j][e];
+    return;
+  }
 #pragma unroll
   for (int j = 0; j < NJ; ++j) {
     const int c = n0 + wn * 32 * NJ + 32 * j + lcol;
