@@ -391,17 +391,19 @@ __global__ __launch_bounds__(64 * NW, NW == 8 ? 2 : 1) void attn_lds_kernel(Attn
     if (p.splits == 1) {
       const float inv = lt > 0.f ? 1.f / lt : 0.f;
 #pragma unroll
-      for (int dt = 0; dt < DT; ++dt)
+      for (int dt = 0; dt < DT; ++dt) {
+        // the 4 consecutive columns of the lane's rows: one 8-byte store in either layout
+        uint16_t v[4];
 #pragma unroll
-        for (int e = 0; e < 4; ++e)
-          p.out[out_index(p, long(b) * kp1 + j, (h * G + gi) * D + 16 * dt + 4 * g4 + e, long(p.Hq) * D, 2)] =
-              f32_to_bf16(o[dt][i][e] * inv);
+        for (int e = 0; e < 4; ++e) v[e] = f32_to_bf16(o[dt][i][e] * inv);
+        *reinterpret_cast<uint2*>(p.out + out_index(p, long(b) * kp1 + j, (h * G + gi) * D + 16 * dt + 4 * g4,
+                                                     long(p.Hq) * D, 2)) =
+            make_uint2(uint32_t(v[0]) | (uint32_t(v[1]) << 16), uint32_t(v[2]) | (uint32_t(v[3]) << 16));
+      }
     } else {
       const long pr = (long(bh) * p.splits + split) * R + r0 + r;
 #pragma unroll
-      for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-        for (int e = 0; e < 4; ++e) p.part_o[pr * D + 16 * dt + 4 * g4 + e] = o[dt][i][e];
+      for (int dt = 0; dt < DT; ++dt) *reinterpret_cast<floatx4_t*>(p.part_o + pr * D + 16 * dt + 4 * g4) = o[dt][i];
       if (g4 == 0) {
         p.part_ml[pr * 2 + 0] = m_run[i];
         p.part_ml[pr * 2 + 1] = lt;
