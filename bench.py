@@ -744,11 +744,11 @@ def main():
                           "higher_is_better": True, "dtype": w.dtype, "data": "synthetic",
                           "config": {"workload": w.name}, "measurement": m}))
         return
-    configs = {}
+    other_workloads = {}
     if not a.no_configs:
         for cw in (workloads.TINY_FP32, workloads.LAYER_BF16, workloads.LONG_CTX_BF16, workloads.FP8_ZIPF):
             log(f"[bench] workload {cw.name}")
-            configs[cw.name] = (tiny_measure if cw.name == workloads.TINY_FP32.name else layer_measure)(
+            other_workloads[cw.name] = (tiny_measure if cw.name == workloads.TINY_FP32.name else layer_measure)(
                 cw, a.seed, molt, flush, cpu=not a.no_cpu_baseline)
     del flush
     torch.cuda.empty_cache()
@@ -867,7 +867,7 @@ def main():
         "mtp_draft": mtp,
         "replay_recompute": rep,
         "reprefill": rpf,
-        "configs": configs or None,
+        "configs": other_workloads or None,
     }
     if not a.no_cpu_baseline:
         log("[bench] timing the CPU oracle on a bounded sample")
