@@ -32,9 +32,10 @@ struct GemmParams {
   int M, N, K;             // N: output columns (gate_up: F)
   int ldc;
   const int4* tiles;       // grouped: {expert, row0, row1, -}
-  const int32_t* n_tiles_live;   // grouped (device): entries of `tiles` in use
+  const int32_t* n_tiles_live;   // grouped (device): entries of `tiles` in use; null: n_mtiles
   int n_mtiles, n_ntiles;
-  const int32_t* perm;     // grouped: padded row -> pair (token * ktop + slot), -1 = padding
+  const int32_t* perm;     // grouped: padded row -> pair (token * ktop + slot), -1 = padding;
+                           // null (dense down mode): row r -> output row r
   int ktop;
   const float* a_scale;    // fp8: per A row (token for gate_up, padded row for down)
   const float* b_scale;    // fp8: [E, b_scale_ld]
@@ -92,8 +93,11 @@ MOLT_DEV StreamTile stream_geometry(const GemmParams& p, int id, int nk, int wav
   // through the constant address space: a scalar load (the table is read-only here), which
   // does not wait behind the vector stores of an epilogue
   typedef const __attribute__((address_space(4))) int32x4_t* ConstTile;
-  const int32x4_t tv = *(ConstTile)(p.tiles + mt);
-  const int4 t = make_int4(tv[0], tv[1], tv[2], tv[3]);
+  int4 t = make_int4(0, 0, p.M, 0);                   // no table: one dense row tile
+  if (p.tiles != nullptr) {
+    const int32x4_t tv = *(ConstTile)(p.tiles + mt);
+    t = make_int4(tv[0], tv[1], tv[2], tv[3]);
+  }
   g.expert = t.x;
   g.row0 = t.y;                                       // a multiple of 32
   g.row1 = t.z;
@@ -142,7 +146,7 @@ void stream_gemm_kernel(GemmParams p) {
   // down epilogue: the tile's outputs (BM x 128 f32; 128-row tiles in two 64-column passes)
   constexpr int kEpCols = BM == 128 ? 64 : 128;
   __shared__ __attribute__((aligned(16))) float dep[MODE == kDown ? BM * kEpCols : 1];
-  const int total = *p.n_tiles_live * p.n_ntiles;
+  const int total = (p.n_tiles_live != nullptr ? *p.n_tiles_live : p.n_mtiles) * p.n_ntiles;
   const int chunk = (total + 7) / 8;
   const int stride = gridDim.x / 8;
   const int first = (blockIdx.x % 8) * chunk;
@@ -210,7 +214,7 @@ void stream_gemm_kernel(GemmParams p) {
     // down: the pair index of each of the tile's rows, loaded before the tile's own loads
     int pv = -1;
     if (MODE == kDown && threadIdx.x < BM && g.row0 + int(threadIdx.x) < g.row1)
-      pv = p.perm[g.row0 + threadIdx.x];
+      pv = p.perm != nullptr ? p.perm[g.row0 + threadIdx.x] : g.row0 + int(threadIdx.x);
     auto put_prow = [&]() __attribute__((always_inline)) {
       if (MODE == kDown && threadIdx.x < BM) prow[threadIdx.x] = pv;
     };
@@ -1016,6 +1020,17 @@ hipError_t launch_gemm(const void* A, const void* Bw, float* C, int M, int N, in
     p.n_ntiles = (N + 63) / 64;
     f32_gemm_kernel<kDense><<<p.n_mtiles * p.n_ntiles, kThreads, 0, s>>>(p);
     return hipGetLastError();
+  }
+  if (dt == MOLT_BF16 && !accumulate && M <= 128 && N >= 8192 && N % kBN == 0) {
+    // few rows and many columns (the draft head's LM head, one row per sequence): every
+    // weight element is used by one row tile only, so the grouped GEMM's weight-streaming
+    // kernel in down mode takes it as one "expert" holding all rows (no tile table: one row
+    // tile, output row = input row); the 128 x 128 LDS kernel read the weights at about
+    // half of HBM bandwidth
+    p.tiles = nullptr; p.n_tiles_live = nullptr; p.perm = nullptr;
+    p.n_mtiles = 1;
+    p.n_ntiles = N / kBN;
+    return run_stream<false, kDown>(p, M <= 32 ? 32 : M <= 64 ? 64 : 128, s);
   }
   if (M >= kBigBM && N >= 8192 && long((M + kBigBM - 1) / kBigBM) * ((N + kBigBN - 1) / kBigBN) >= 512 &&
       long(M + 31) * 2 * K < (1L << 31) && long(kBigBN) * 2 * K < (1L << 31)) {

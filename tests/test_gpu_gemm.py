@@ -16,6 +16,9 @@ pytestmark = pytest.mark.gpu
     (77, 128, 2048, torch.bfloat16, False),     # router, 64-row tiles
     (25, 256, 2048, torch.bfloat16, False),     # 32-row tiles
     (640, 151936, 2048, torch.bfloat16, False), # LM head
+    (128, 151936, 2048, torch.bfloat16, False), # the draft head's LM head: weight-streaming kernel
+    (100, 16384, 512, torch.bfloat16, False),   # streaming kernel, ragged last row block
+    (20, 8192, 1024, torch.bfloat16, False),    # streaming kernel, 32-row tile
     (2304, 5120, 2048, torch.bfloat16, False),  # QKV at 2304 rows: 128-row tiles
     (2304, 2048, 4096, torch.bfloat16, True),   # O at 2304 rows, accumulate
     (1100, 2048, 4096, torch.bfloat16, True),   # ragged rows, accumulate
